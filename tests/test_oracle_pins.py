@@ -1,0 +1,313 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+The oracle is the plain definition of the draw (Section 2): fp64 sequential
+prefix sums of exact products, then the smallest k with u*S < S_k, and K-1 if
+none (what the linear and binary searches of Algorithms 2 and 3 return).  The
+pins below do not re-type that formula: they use exact rational arithmetic,
+closed-form counts over the whole u grid, a chi-square test, and special cases
+with textbook answers.  ``MUTANTS`` plants plausible mistakes in copies of the
+definition and checks that every one of them fails at least one pin.
+"""
+from fractions import Fraction
+
+import numpy as np
+import pytest
+from scipy import stats
+
+import oracle
+from paper_1505_03851_amd.inputs import make_corpus, make_random
+
+TWO24 = 1 << 24
+
+
+# --------------------------------------------------------------------------
+# draw functions under test: (theta, phi, doc_id, word_id, u) -> z
+def c_oracle(theta, phi, d, w, u):
+    return oracle.draw(theta, phi, d, w, u, with_band=False)
+
+
+def np_twin(theta, phi, d, w, u):
+    return oracle.draw_np(theta, phi, d, w, u)[0]
+
+
+# Plausible mistakes, each in a copy of the definition (never in the oracle).
+def _mut_base(theta, phi, d, w, u, cmp="<", clamp=True, inclusive=True,
+              total_index=-1):
+    a = theta[d].astype(np.float64) * phi[w].astype(np.float64)
+    S = np.cumsum(a, axis=1)
+    if not inclusive:                        # exclusive prefix (index slip)
+        S = np.concatenate([np.zeros((S.shape[0], 1)), S[:, :-1]], axis=1)
+    stop = u.astype(np.float64) * S[:, max(total_index, -S.shape[1])]
+    hit = (stop[:, None] < S) if cmp == "<" else (stop[:, None] <= S)
+    K = S.shape[1]
+    miss = K - 1 if clamp else 0
+    return np.where(hit.any(axis=1), hit.argmax(axis=1), miss).astype(np.int32)
+
+
+def _mut_transposed(theta, phi, d, w, u):    # phi indexed [k][word]
+    K = theta.shape[1]
+    flat = phi.reshape(-1)
+    cols = np.arange(K)[None, :] * phi.shape[0] + w[:, None]
+    ph = flat[np.minimum(cols, flat.size - 1)]
+    a = theta[d].astype(np.float64) * ph.astype(np.float64)
+    S = np.cumsum(a, axis=1)
+    stop = u.astype(np.float64) * S[:, -1]
+    hit = stop[:, None] < S
+    return np.where(hit.any(axis=1), hit.argmax(axis=1), K - 1).astype(np.int32)
+
+
+def _mut_largest_index(theta, phi, d, w, u):  # ties resolved to largest index
+    a = theta[d].astype(np.float64) * phi[w].astype(np.float64)
+    S = np.cumsum(a, axis=1)
+    stop = u.astype(np.float64) * S[:, -1]
+    K = S.shape[1]
+    hit = stop[:, None] < S
+    z = np.where(hit.any(axis=1), hit.argmax(axis=1), K - 1)
+    # among the entries equal to S_z, take the last one
+    same = S == S[np.arange(S.shape[0]), z][:, None]
+    return (K - 1 - np.argmax(same[:, ::-1], axis=1)).astype(np.int32)
+
+
+MUTANTS = {
+    "le_instead_of_lt": lambda *x: _mut_base(*x, cmp="<="),
+    "no_clamp_zero": lambda *x: _mut_base(*x, clamp=False),
+    "exclusive_prefix": lambda *x: _mut_base(*x, inclusive=False),
+    "wrong_total": lambda *x: _mut_base(*x, total_index=-2),
+    "phi_transposed": _mut_transposed,
+    "largest_index_on_ties": _mut_largest_index,
+}
+
+
+# --------------------------------------------------------------------------
+# pin checks; each returns a list of failure descriptions
+def _rand_f32(rng, shape, zero_frac=0.25):
+    x = rng.random(shape).astype(np.float32)
+    x[rng.random(shape) < zero_frac] = 0.0
+    return x
+
+
+def _exact_z(th, ph, u):
+    """Brute force in exact rationals over every k."""
+    a = [Fraction(float(t)) * Fraction(float(p)) for t, p in zip(th, ph)]
+    S, run = [], Fraction(0)
+    for x in a:
+        run += x
+        S.append(run)
+    stop = Fraction(float(u)) * S[-1]
+    for k, s in enumerate(S):
+        if stop < s:
+            return k
+    return len(S) - 1
+
+
+def pin_bruteforce(draw_fn, trials=60, seed=1):
+    """Random K <= 8 instances (with zero weights and repeated values) against
+    exact rational arithmetic."""
+    rng = np.random.default_rng(seed)
+    fails = []
+    for t in range(trials):
+        K = int(rng.integers(1, 9))
+        M, V, N = 3, 4, 64
+        theta = _rand_f32(rng, (M, K))
+        phi = _rand_f32(rng, (V, K))
+        if t % 3 == 0:   # repeated weights make ties between products
+            phi[:] = np.float32(0.5)
+        d = rng.integers(0, M, N).astype(np.int32)
+        w = rng.integers(0, V, N).astype(np.int32)
+        u = (rng.integers(0, TWO24, N) * 2.0 ** -24).astype(np.float32)
+        u[:4] = [0.0, 0.5, 0.25, 1 - 2.0 ** -24]
+        z = draw_fn(theta, phi, d, w, u)
+        for n in range(N):
+            e = _exact_z(theta[d[n]], phi[w[n]], u[n])
+            if z[n] != e:
+                fails.append((t, n, int(z[n]), e))
+    return fails
+
+
+GRID_WEIGHTS = [
+    # integer weights: products and sums are exact, so fp64 is exact here
+    [3.0, 0.0, 5.0, 8.0, 0.0, 16.0, 32.0],   # S = 64: boundaries on grid points
+    [1.0, 0.0, 999.0],                        # S = 1000
+    [7.0, 0.0, 0.0, 100.0, 1.0, 892.0, 0.0, 0.0],  # S = 1000, trailing zeros
+]
+
+
+def pin_grid_counts(draw_fn, bits=20):
+    """Over all 2**bits grid values u = i/2**bits (exact in fp32 for bits <=
+    24) the number of u drawing topic k is
+    ceil(2**bits S_k / S) - ceil(2**bits S_{k-1} / S)."""
+    fails = []
+    G = 1 << bits
+    i = np.arange(G, dtype=np.int64)
+    u = (i * 2.0 ** -bits).astype(np.float32)
+    d = np.zeros(G, np.int32)
+    for weights in GRID_WEIGHTS:
+        K = len(weights)
+        theta = np.array([weights], np.float32)
+        phi = np.ones((1, K), np.float32)
+        z = draw_fn(theta, phi, d, d, u)
+        counts = np.bincount(z, minlength=K)
+        S = [Fraction(0)]
+        for x in weights:
+            S.append(S[-1] + Fraction(x))
+        total = S[-1]
+
+        def ceil(q):
+            return -((-q.numerator) // q.denominator)
+
+        expect = [ceil(G * S[k + 1] / total) - ceil(G * S[k] / total)
+                  for k in range(K)]
+        if list(counts) != expect:
+            fails.append((weights, list(counts), expect))
+    return fails
+
+
+def pin_special_cases(draw_fn):
+    """Cases with textbook answers."""
+    fails = []
+    rng = np.random.default_rng(5)
+    N = 4096
+    u = (rng.integers(0, TWO24, N) * 2.0 ** -24).astype(np.float32)
+    u[:3] = [0.0, 0.5, 1 - 2.0 ** -24]
+    zeros = np.zeros(N, np.int32)
+
+    def run(theta_row, phi_row):
+        return draw_fn(np.array([theta_row], np.float32),
+                       np.array([phi_row], np.float32), zeros, zeros, u)
+
+    # K = 1: always topic 0 (also with zero weight).
+    for wgt in (0.7, 0.0):
+        z = run([wgt], [1.0])
+        if (z != 0).any():
+            fails.append(("K=1", wgt))
+    # One-hot: the only weighted topic is drawn for every u.
+    for K in (1, 5, 8, 33):
+        for t in {0, K // 2, K - 1}:
+            row = np.zeros(K)
+            row[t] = 0.3
+            z = run(row, np.ones(K))
+            if (z != t).any():
+                fails.append(("one-hot", K, t))
+    # Equal power-of-two weights: every partial sum is exact, z = floor(u*K).
+    for K in (2, 8, 16, 64, 256):
+        z = run(np.full(K, 2.0 ** -3), np.ones(K))
+        expect = np.floor(u.astype(np.float64) * K).astype(np.int32)
+        if (z != expect).any():
+            fails.append(("uniform-pow2", K))
+    # All-zero weights: no entry exceeds stop = 0, so the search ends at K-1.
+    for K in (1, 3, 64):
+        z = run(np.zeros(K), np.ones(K))
+        if (z != K - 1).any():
+            fails.append(("all-zero", K))
+    # Leading zero weights and u = 0: the first weighted topic.
+    z = run([0.0, 0.0, 0.0, 2.0, 1.0], np.ones(5))
+    if z[0] != 3:
+        fails.append(("u=0 leading zeros", int(z[0])))
+    # u just below 1 with trailing zeros: the last weighted topic.
+    z = run([1.0, 2.0, 0.0, 0.0], np.ones(4))
+    if z[2] != 1:
+        fails.append(("u->1 trailing zeros", int(z[2])))
+    return fails
+
+
+PINS = {
+    "bruteforce": pin_bruteforce,
+    "grid_counts": pin_grid_counts,
+    "special_cases": pin_special_cases,
+}
+
+
+@pytest.mark.parametrize("pin", list(PINS))
+@pytest.mark.parametrize("impl", ["c_oracle", "np_twin"])
+def test_oracle_meets_pin(pin, impl):
+    fn = {"c_oracle": c_oracle, "np_twin": np_twin}[impl]
+    assert PINS[pin](fn) == []
+
+
+@pytest.mark.parametrize("name", list(MUTANTS))
+def test_every_planted_mistake_fails_a_pin(name):
+    fn = MUTANTS[name]
+    failed = [p for p, check in PINS.items() if check(fn)]
+    assert failed, f"mutant {name} passed every pin"
+
+
+def test_grid_counts_full_24bit_grid():
+    """The grid-count pin over every fp32 u of the form i/2**24."""
+    assert pin_grid_counts(c_oracle, bits=24) == []
+
+
+def test_chi_square_fixed_distribution():
+    """1e6 draws from one K=8 distribution with a zero-weight topic: the
+    counts fit the normalised weights (6 degrees of freedom) and the
+    zero-weight topic is never drawn."""
+    weights = np.array([0.05, 0.2, 0.0, 0.1, 0.3, 0.15, 0.12, 0.08], np.float32)
+    theta = weights[None, :]
+    phi = np.ones((1, 8), np.float32)
+    N = 1_000_000
+    rng = np.random.default_rng(20150513)
+    u = (rng.integers(0, TWO24, N) * 2.0 ** -24).astype(np.float32)
+    zeros = np.zeros(N, np.int32)
+    z = oracle.draw(theta, phi, zeros, zeros, u, with_band=False)
+    counts = np.bincount(z, minlength=8)
+    assert counts[2] == 0
+    nz = weights > 0
+    p = weights[nz].astype(np.float64) / weights.astype(np.float64).sum()
+    chi2, pval = stats.chisquare(counts[nz], N * p)
+    assert pval >= 1e-3, (chi2, pval, counts)
+
+
+def test_invariants_on_corpus():
+    """z in [0, K); the drawn topic has a positive product whenever S > 0;
+    partial sums never decrease and the last one is the total; fp64 products
+    of fp32 inputs are exact."""
+    c = make_random(3000, 40, 500, 97, seed=3, doc_order="shuffled")
+    z, band = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u)
+    assert z.min() >= 0 and z.max() < c.K
+    a = c.theta[c.doc_id].astype(np.float64) * c.phi[c.word_id].astype(np.float64)
+    S = a.sum(axis=1)
+    pos = S > 0
+    assert (a[np.arange(c.N), z][pos] > 0).all()
+    for n in range(0, c.N, 97):
+        P = oracle.prefix_np(c.theta[c.doc_id[n]], c.phi[c.word_id[n]])
+        assert (np.diff(P) >= 0).all()
+        th, ph = c.theta[c.doc_id[n]], c.phi[c.word_id[n]]
+        for k in range(0, c.K, 13):
+            assert Fraction(float(th[k])) * Fraction(float(ph[k])) == \
+                Fraction(float(th[k]) * float(ph[k]))
+        run = Fraction(0)
+        for k in range(c.K):
+            run += Fraction(float(th[k])) * Fraction(float(ph[k]))
+        assert abs(float(run) - P[-1]) <= 1e-14 * max(P[-1], 1e-300)
+
+
+@pytest.mark.parametrize("name", ["tiny-K32"])
+def test_c_oracle_equals_numpy_twin_on_config(name):
+    c = make_corpus(name)
+    z1, b1 = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u)
+    z2, b2 = oracle.draw_np(c.theta, c.phi, c.doc_id, c.word_id, c.u)
+    assert (z1 == z2).all() and (b1 == b2).all()
+
+
+@pytest.mark.parametrize("K", [1, 7, 19, 64, 65, 300])
+@pytest.mark.parametrize("order", ["sequential", "shuffled"])
+def test_c_oracle_equals_numpy_twin_random(K, order):
+    c = make_random(1500, 17, 300, K, seed=K, doc_order=order)
+    z1, b1 = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u)
+    z2, b2 = oracle.draw_np(c.theta, c.phi, c.doc_id, c.word_id, c.u)
+    assert (z1 == z2).all() and (b1 == b2).all()
+
+
+def test_band_flag_definition():
+    """in_band marks exactly the tokens with |u*S - S_k| <= 1e-5 * S."""
+    theta = np.array([[1.0, 1.0, 2.0]], np.float32)   # S = 4, S_k = 1, 2, 4
+    phi = np.ones((1, 3), np.float32)
+    u = np.array([0.25, 0.25 * (1 + 2e-5), 0.25 * (1 + 0.5e-5), 0.6, 0.0],
+                 np.float32)
+    zeros = np.zeros(u.size, np.int32)
+    z, band = oracle.draw(theta, phi, zeros, zeros, u)
+    stop = u.astype(np.float64) * 4.0
+    expect = np.array([min(abs(s - b) for b in (1.0, 2.0, 4.0)) <= 4e-5
+                       for s in stop])
+    assert (band == expect).all()
+    assert band[0] and not band[3]
+    assert list(z) == [1, 1, 1, 2, 0]
