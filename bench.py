@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Benchmark of the per-token LDA topic draw on one MI355X.
+
+One step = one launch of the draw over every token of the workload (all inputs
+resident in HBM).  The headline workload is the K=1024 corpus (N=16,777,216
+tokens, M=65,536 documents x 256, V=100,000 Zipf(1.05) words); the K=256
+corpus and the naive kernel are reported beside it.
+
+Prints ONE JSON line.  ``roofline.achieved`` is the algorithmic bytes of one
+launch divided by the launch's average duration (HIP events on the launch
+stream); ``roofline.traffic`` is the HBM traffic per launch taken from the
+committed rocprofv3 counter summary, or null when the kernel source changed
+since the counters were collected.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = ("z draws/sec and achieved HBM GB/s (% of peak) at K=256 and K=1024, "
+          "1 MI355X")
+PEAK_HBM_GBPS = 8000.0            # MI355X HBM3E, published
+HEADLINE = "corpus16M-K1024"
+SECOND = "corpus1M-K256"
+COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
+KERNEL_SOURCES = [os.path.join(ROOT, "paper_1505_03851_amd", "csrc", f)
+                  for f in ("lda_draw.hip", "butterfly.hpp")]
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha1()
+    for p in KERNEL_SOURCES:
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def algorithmic_bytes(c) -> int:
+    """Bytes the method must move: each token's phi row (4K), its doc id,
+    word id, u and z (16), and each run of one document's tokens its theta row
+    once (4K)."""
+    import numpy as np
+    runs = 1 + int(np.count_nonzero(np.diff(c.doc_id))) if c.N else 0
+    return c.N * (4 * c.K + 16) + runs * 4 * c.K
+
+
+def upload(c):
+    import torch
+    return {k: torch.from_numpy(getattr(c, k)).cuda()
+            for k in ("theta", "phi", "doc_id", "word_id", "u")}
+
+
+def time_kernel(kernel: str, dev, steps: int, warmup: int):
+    """Warm up, then time exactly ``steps`` launches.  Returns (wall seconds of
+    the timed region, per-launch milliseconds from HIP events, z)."""
+    import torch
+    import paper_1505_03851_amd as lda
+    fn = {"butterfly": lda.draw_butterfly, "naive": lda.draw_naive}[kernel]
+    stream = torch.cuda.current_stream()
+    z = torch.empty_like(dev["doc_id"])
+    args = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    for _ in range(warmup):
+        fn(*args, out=z, stream=stream)
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True),
+           torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    t0 = time.perf_counter()
+    for s, e in ev:
+        s.record(stream)
+        fn(*args, out=z, stream=stream)
+        e.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return wall, [s.elapsed_time(e) for s, e in ev], z
+
+
+def measure(name: str, c, dev, kernel: str, steps: int, warmup: int) -> dict:
+    wall, per_ms, z = time_kernel(kernel, dev, steps, warmup)
+    avg_ms = sum(per_ms) / len(per_ms)
+    b_alg = algorithmic_bytes(c)
+    gbps = b_alg / (avg_ms * 1e-3) / 1e9
+    print(f"[bench] {name} {kernel}: {avg_ms:.3f} ms/launch "
+          f"(min {min(per_ms):.3f}), {c.N / (avg_ms * 1e-3) / 1e9:.3f} G draws/s, "
+          f"{gbps:.0f} GB/s algorithmic ({100 * gbps / PEAK_HBM_GBPS:.1f}% of "
+          f"8 TB/s)", file=sys.stderr, flush=True)
+    return {
+        "workload": name, "kernel": kernel, "N": c.N, "K": c.K,
+        "steps": steps, "wall_s": wall,
+        "ms_per_launch": avg_ms, "ms_per_launch_min": min(per_ms),
+        "draws_per_s": c.N / (avg_ms * 1e-3),
+        "alg_bytes_per_launch": b_alg,
+        "alg_GBps": gbps, "frac_of_hbm_peak": gbps / PEAK_HBM_GBPS,
+        "z": z,
+    }
+
+
+def traffic_from_counters():
+    """HBM bytes per launch from the committed counter summary, if it was
+    taken on the current kernel source."""
+    try:
+        with open(COUNTERS) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_source_sha1") != kernel_source_hash():
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def cpu_baseline(c, z_gpu, sample: int) -> dict:
+    """The oracle, as it stands, on the first ``sample`` tokens."""
+    import numpy as np
+    import oracle
+    n = min(sample, c.N)
+    d, w, u = c.doc_id[:n], c.word_id[:n], c.u[:n]
+    oracle.draw(c.theta, c.phi, d[:1024], w[:1024], u[:1024], with_band=False)
+    t0 = time.perf_counter()
+    z_ref = oracle.draw(c.theta, c.phi, d, w, u, with_band=False)
+    dt = time.perf_counter() - t0
+    zg = z_gpu[:n].cpu().numpy()
+    return {
+        "value": n / dt, "unit": "draws/s", "cores": oracle.num_threads(),
+        "kind": "oracle",
+        "sample": f"first {n} tokens of {c.name} (K={c.K}), fp64 oracle, "
+                  f"draw only, {dt:.2f} s wall",
+        "sample_mismatches_vs_gpu": int(np.count_nonzero(zg != z_ref)),
+    }
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--cpu-sample", type=int, default=1 << 22,
+                    help="tokens of the headline workload the oracle draws")
+    ap.add_argument("--only", choices=["butterfly", "naive"], default=None,
+                    help="time one kernel on one workload (for profiling)")
+    ap.add_argument("--workload", default=HEADLINE)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "the draw has no multi-GPU path in this build.", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd.inputs import make_corpus
+
+    lda.load()
+    if not torch.cuda.is_available():
+        print("bench.py needs a GPU", file=sys.stderr)
+        return 1
+
+    if args.only:
+        c = make_corpus(args.workload)
+        dev = upload(c)
+        r = measure(args.workload, c, dev, args.only, args.steps, args.warmup)
+        r.pop("z")
+        print(json.dumps(r), flush=True)
+        return 0
+
+    results = []
+    c2 = make_corpus(SECOND)
+    dev2 = upload(c2)
+    for k in ("butterfly", "naive"):
+        r = measure(SECOND, c2, dev2, k, max(args.steps, 20), args.warmup)
+        r.pop("z")
+        results.append(r)
+    del dev2, c2
+    torch.cuda.empty_cache()
+
+    c = make_corpus(HEADLINE)
+    dev = upload(c)
+    naive = measure(HEADLINE, c, dev, "naive", max(3, args.steps // 4), 1)
+    naive.pop("z")
+    results.append(naive)
+    head = measure(HEADLINE, c, dev, "butterfly", args.steps, args.warmup)
+    z_head = head.pop("z")
+    results.append(head)
+
+    wall = head["wall_s"]
+    value = c.N * args.steps / wall
+    out = {
+        "metric": METRIC,
+        "value": value,
+        "unit": "draws/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": 1e3 * wall / args.steps,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": HEADLINE, "N": c.N, "M": c.M, "V": c.V,
+                   "K": c.K, "kernel": "butterfly"},
+        "roofline": {
+            "bound": "hbm",
+            "achieved": head["alg_GBps"],
+            "peak": PEAK_HBM_GBPS,
+            "unit": "GB/s",
+            "frac": head["alg_GBps"] / PEAK_HBM_GBPS,
+            "traffic": traffic_from_counters(),
+        },
+        "cpu_baseline": cpu_baseline(c, z_head, args.cpu_sample),
+        "results": results,
+        "kernel_source_sha1": kernel_source_hash(),
+    }
+    print(json.dumps(out), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

@@ -1,0 +1,130 @@
+/*
+ * lda_draw.h -- C ABI of the MI355X (gfx950) per-token LDA topic draw.
+ *
+ * Method: G. L. Steele Jr. and J.-B. Tristan, "Using Butterfly-Patterned
+ * Partial Sums to Optimize GPU Memory Accesses for Drawing from Discrete
+ * Distributions" (arXiv 1505.03851).
+ *
+ * The operation (Section 2, problem statement and Algorithm 1): for every
+ * token n with document d = doc_id[n] and word w = word_id[n], topic k has the
+ * relative weight a_k = theta[d][k] * phi[w][k].  With S_k = a_0 + ... + a_k
+ * and S = S_{K-1}, the draw is
+ *
+ *     z[n] = the smallest k with u[n] * S < S_k            (strict "<")
+ *
+ * and K - 1 when no k qualifies (S = 0, or u*S rounding up to S), which is
+ * what the linear and binary searches of Algorithms 2 and 3 return.  The
+ * arithmetic is fp32; a result may differ from exact arithmetic only for
+ * tokens whose u*S lies within fp32 rounding of some S_k.
+ *
+ * Layout (all arrays dense and row-major, as Section 3 assumes):
+ *   theta   float [M][K]  document-topic weights, a document's K topics
+ *                         contiguous; entries >= 0 and finite.
+ *   phi     float [V][K]  topic-word weights stored word-major: row w holds
+ *                         word w's weight in every topic, K contiguous floats
+ *                         (the paper's phi[V, K]); entries >= 0 and finite.
+ *   doc_id  int32 [N]     0 <= doc_id[n] < M; need not be sorted (tokens of one
+ *                         document stored contiguously run faster).
+ *   word_id int32 [N]     0 <= word_id[n] < V.
+ *   u       float [N]     the uniform variate of each draw, 0 <= u[n] < 1.  The
+ *                         paper draws it inside the procedure; here the caller
+ *                         supplies it.
+ *   z       int32 [N]     output topics, 0 <= z[n] < K.
+ *
+ * Ownership and memory: every pointer is a device pointer (hipMalloc'd, or
+ * memory that the caller's framework allocated on the current device),
+ * owned by the caller, 4-byte aligned.  The library keeps no state between
+ * calls and allocates no device memory; kernels use on-chip LDS only (and,
+ * in the naive kernel, the per-lane private segment the HIP runtime manages).
+ *
+ * Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls only
+ * enqueue work and return; the caller synchronises.  Calls that share the
+ * output buffer must be ordered by the caller.
+ *
+ * Errors: every entry point returns LDA_OK (0) or a negative status.  Argument
+ * checks happen before any HIP call, so a rejected call has no effect and
+ * touches no device.  N == 0 is a no-op returning LDA_OK.  Preconditions that
+ * are not checked (ids in range, finite non-negative weights, u in [0, 1))
+ * are the caller's: an out-of-range id reads outside theta or phi.
+ */
+#ifndef LDA_DRAW_H
+#define LDA_DRAW_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define LDA_OK 0
+#define LDA_ERR_NULL (-1)        /* a required pointer is NULL while N > 0   */
+#define LDA_ERR_SHAPE (-2)       /* N < 0, M <= 0, V <= 0 or K <= 0          */
+#define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K                            */
+#define LDA_ERR_HIP (-4)         /* the HIP runtime reported an error        */
+#define LDA_ERR_ALIGN (-5)       /* a pointer is not 4-byte aligned          */
+
+/* Largest number of topics the kernels accept. */
+#define LDA_MAX_K 4096
+
+/*
+ * Baseline draw: Algorithm 1 with the binary search of Algorithm 3.  One lane
+ * per token; each lane walks its own theta and phi rows (lanes of a wavefront
+ * read addresses 4*K bytes apart), keeps the full prefix table of its token in
+ * its private segment and binary-searches it.
+ */
+int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
+                   const int32_t *word_id, const float *u, int32_t *z,
+                   int64_t N, int32_t M, int32_t V, int32_t K, void *stream);
+
+/*
+ * Butterfly draw (Algorithm 7 with Algorithms 5, 8, 9 and 10, Sections 3-4).
+ * A wavefront takes 64 consecutive tokens, one per lane, and reads theta and
+ * phi cooperatively: each load instruction fetches W consecutive topics of one
+ * token (coalesced).  Per block of W topics the lanes combine their products
+ * in a butterfly pattern (log2 W exchange stages) instead of a full
+ * transposition.  A first sweep over the blocks gives every lane the full
+ * prefix at each block end; the block holding u*S is found by binary search
+ * over those (Algorithm 9), its butterfly table is rebuilt on chip, and the
+ * lane reconstructs the remaining partial sums from it while it searches
+ * (Algorithm 10).  W = 64 for K >= 64, W = 32 below; the first K mod W topics
+ * (the remnant) are summed per lane without transposition.
+ */
+int lda_draw_butterfly(const float *theta, const float *phi,
+                       const int32_t *doc_id, const int32_t *word_id,
+                       const float *u, int32_t *z, int64_t N, int32_t M,
+                       int32_t V, int32_t K, void *stream);
+
+/*
+ * The butterfly-patterned tables themselves (Section 4, Fig. 1 right), for
+ * inspection and tests.  table is a device float array [N][K]: row n is the
+ * table p[K] that token n's lane holds in Algorithm 7 -- the remnant's full
+ * prefix, then for each block of W topics the W-1 butterfly entries of that
+ * lane's column followed by the full prefix at the block's end.  Entries of a
+ * column sum products of the other tokens of the same group of W lanes (lane
+ * groups are tokens [g*W, g*W + W), the last group padded by repeating token
+ * N-1).  W is chosen from K as in lda_draw_butterfly.
+ */
+int lda_butterfly_table(const float *theta, const float *phi,
+                        const int32_t *doc_id, const int32_t *word_id,
+                        float *table, int64_t N, int32_t M, int32_t V,
+                        int32_t K, void *stream);
+
+/* The W (butterfly width) the library uses for K, or LDA_ERR_UNSUPPORTED /
+ * LDA_ERR_SHAPE for a K it rejects. */
+int lda_butterfly_width(int32_t K);
+
+/* A static, human-readable description of a status code. */
+const char *lda_status_string(int status);
+
+/* The HIP error string behind the last LDA_ERR_HIP returned on this host
+ * thread ("no error" if none). */
+const char *lda_last_hip_error(void);
+
+/* Library version, as major * 10000 + minor * 100 + patch. */
+int lda_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LDA_DRAW_H */

@@ -1,2 +1,20 @@
 """MI355X-native per-token LDA topic draw with butterfly-patterned partial
-sums (Steele and Tristan, arXiv 1505.03851)."""
+sums (Steele and Tristan, arXiv 1505.03851).
+
+``draw_naive``, ``draw_butterfly`` and ``butterfly_table`` call the HIP
+library through its C ABI (``include/lda_draw.h``).  The binding is imported
+on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
+"""
+
+_BINDING = ("draw_naive", "draw_butterfly", "butterfly_table",
+            "butterfly_width", "status_string", "version", "LdaError",
+            "load", "MAX_K", "STATUS")
+
+__all__ = list(_BINDING)
+
+
+def __getattr__(name):
+    if name in _BINDING:
+        from . import _lib
+        return getattr(_lib, name)
+    raise AttributeError(name)

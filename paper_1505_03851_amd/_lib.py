@@ -1,0 +1,192 @@
+"""ctypes binding of liblda_draw.so: argument marshalling only.
+
+torch supplies device memory and the current stream; every step of the draw
+runs in the HIP kernels.  There is no fallback: if the library is missing or
+fails to load, every entry point raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+
+import torch  # loaded first so the library binds to torch's HIP runtime
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "liblda_draw.so")
+HEADER = os.path.join(os.path.dirname(_PKG), "include", "lda_draw.h")
+
+_lib = None
+
+
+class LdaError(RuntimeError):
+    """A non-zero status returned by the C ABI."""
+
+    def __init__(self, status: int, message: str):
+        super().__init__(f"lda status {status}: {message}")
+        self.status = status
+
+
+def _status_codes() -> dict[str, int]:
+    codes = {}
+    with open(HEADER) as f:
+        for m in re.finditer(r"#define\s+(LDA_\w+)\s+\(?(-?\d+)\)?", f.read()):
+            codes[m.group(1)] = int(m.group(2))
+    return codes
+
+
+STATUS = _status_codes()
+MAX_K = STATUS["LDA_MAX_K"]
+
+
+def load() -> ctypes.CDLL:
+    """Load the library (once).  Raises if it has not been built."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(
+            f"{LIB_PATH} is missing: build it with "
+            "`python -c 'import __graft_entry__ as g; g.build()'` "
+            "(or python paper_1505_03851_amd/build.py)")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
+    draw_args = [P, P, P, P, P, P, I64, I32, I32, I32, P]
+    for name in ("lda_draw_naive", "lda_draw_butterfly"):
+        getattr(lib, name).argtypes = draw_args
+        getattr(lib, name).restype = ctypes.c_int
+    lib.lda_butterfly_table.argtypes = [P, P, P, P, P, I64, I32, I32, I32, P]
+    lib.lda_butterfly_table.restype = ctypes.c_int
+    lib.lda_butterfly_width.argtypes = [I32]
+    lib.lda_butterfly_width.restype = ctypes.c_int
+    lib.lda_status_string.argtypes = [ctypes.c_int]
+    lib.lda_status_string.restype = ctypes.c_char_p
+    lib.lda_last_hip_error.restype = ctypes.c_char_p
+    lib.lda_version.restype = ctypes.c_int
+    _lib = lib
+    return lib
+
+
+def status_string(status: int) -> str:
+    return load().lda_status_string(status).decode()
+
+
+def _check(status: int) -> None:
+    if status != 0:
+        msg = status_string(status)
+        if status == STATUS["LDA_ERR_HIP"]:
+            msg += ": " + load().lda_last_hip_error().decode()
+        raise LdaError(status, msg)
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream)
+
+
+def _require(t: torch.Tensor, name: str, dtype, ndim: int) -> None:
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if t.dim() != ndim:
+        raise ValueError(f"{name} must have {ndim} dimension(s)")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
+def _shapes(theta, phi, doc_id, word_id, u=None):
+    _require(theta, "theta", torch.float32, 2)
+    _require(phi, "phi", torch.float32, 2)
+    _require(doc_id, "doc_id", torch.int32, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    M, K = theta.shape
+    V, K2 = phi.shape
+    N = doc_id.shape[0]
+    if K2 != K:
+        raise ValueError(f"theta has K={K} topics but phi has {K2}")
+    if word_id.shape[0] != N:
+        raise ValueError("doc_id and word_id lengths differ")
+    if u is not None:
+        _require(u, "u", torch.float32, 1)
+        if u.shape[0] != N:
+            raise ValueError("u and doc_id lengths differ")
+    devs = {t.device for t in (theta, phi, doc_id, word_id) + ((u,) if u is not None else ())}
+    if len(devs) != 1:
+        raise ValueError("all tensors must be on one device")
+    return N, M, V, K
+
+
+def _validate_ids(doc_id, word_id, M, V) -> None:
+    if doc_id.numel():
+        if int(doc_id.min()) < 0 or int(doc_id.max()) >= M:
+            raise ValueError("doc_id out of range [0, M)")
+        if int(word_id.min()) < 0 or int(word_id.max()) >= V:
+            raise ValueError("word_id out of range [0, V)")
+
+
+def _draw(fn_name, theta, phi, doc_id, word_id, u, out, stream, validate):
+    N, M, V, K = _shapes(theta, phi, doc_id, word_id, u)
+    if validate:
+        _validate_ids(doc_id, word_id, M, V)
+    if out is None:
+        out = torch.empty(N, dtype=torch.int32, device=doc_id.device)
+    else:
+        _require(out, "out", torch.int32, 1)
+        if out.shape[0] != N or out.device != doc_id.device:
+            raise ValueError("out must be int32[N] on the tensors' device")
+    with torch.cuda.device(doc_id.device):
+        st = getattr(load(), fn_name)(
+            theta.data_ptr(), phi.data_ptr(), doc_id.data_ptr(),
+            word_id.data_ptr(), u.data_ptr(), out.data_ptr(), N, M, V, K,
+            _stream_handle(stream))
+    _check(st)
+    return out
+
+
+def draw_naive(theta, phi, doc_id, word_id, u, out=None, stream=None,
+               validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the one-lane-per-token kernel (Algorithms 1 + 3)."""
+    return _draw("lda_draw_naive", theta, phi, doc_id, word_id, u, out,
+                 stream, validate)
+
+
+def draw_butterfly(theta, phi, doc_id, word_id, u, out=None, stream=None,
+                   validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the butterfly kernel (Algorithms 7-10)."""
+    return _draw("lda_draw_butterfly", theta, phi, doc_id, word_id, u, out,
+                 stream, validate)
+
+
+def butterfly_table(theta, phi, doc_id, word_id, out=None, stream=None,
+                    validate: bool = False) -> torch.Tensor:
+    """The per-lane butterfly tables, float32 [N][K] (Fig. 1, right)."""
+    N, M, V, K = _shapes(theta, phi, doc_id, word_id)
+    if validate:
+        _validate_ids(doc_id, word_id, M, V)
+    if out is None:
+        out = torch.empty((N, K), dtype=torch.float32, device=doc_id.device)
+    else:
+        _require(out, "out", torch.float32, 2)
+        if tuple(out.shape) != (N, K) or out.device != doc_id.device:
+            raise ValueError("out must be float32[N][K] on the tensors' device")
+    with torch.cuda.device(doc_id.device):
+        st = load().lda_butterfly_table(
+            theta.data_ptr(), phi.data_ptr(), doc_id.data_ptr(),
+            word_id.data_ptr(), out.data_ptr(), N, M, V, K,
+            _stream_handle(stream))
+    _check(st)
+    return out
+
+
+def butterfly_width(K: int) -> int:
+    w = load().lda_butterfly_width(int(K))
+    _check(min(w, 0))
+    return w
+
+
+def version() -> int:
+    return int(load().lda_version())

@@ -1,0 +1,66 @@
+"""Shared helpers of the GPU parity tests: upload a corpus, run a kernel
+through the C ABI, and compare with the oracle under the band rule."""
+from __future__ import annotations
+
+import dataclasses
+
+import numpy as np
+
+import oracle
+
+BAND_REL = 1e-5          # |u*S - S_k| <= 1e-5 * S marks a token as in-band
+MAX_MISMATCH_RATE = 1e-4  # mismatches (all in-band) per token
+
+
+@dataclasses.dataclass
+class ParityReport:
+    n: int
+    mismatches: int
+    hard: int            # mismatches outside the band
+    in_band: int         # tokens inside the band (a property of the data)
+    first_hard: list
+
+    @property
+    def mismatch_rate(self) -> float:
+        return self.mismatches / max(self.n, 1)
+
+    def __str__(self):
+        return (f"n={self.n} mismatches={self.mismatches} "
+                f"({self.mismatch_rate:.2e}) hard={self.hard} "
+                f"in_band={self.in_band} ({self.in_band / max(self.n, 1):.2e})")
+
+
+def to_device(c, device="cuda"):
+    import torch
+    return dict(
+        theta=torch.from_numpy(c.theta).to(device),
+        phi=torch.from_numpy(c.phi).to(device),
+        doc_id=torch.from_numpy(c.doc_id).to(device),
+        word_id=torch.from_numpy(c.word_id).to(device),
+        u=torch.from_numpy(c.u).to(device),
+    )
+
+
+def run_kernel(kernel: str, dev: dict):
+    import torch
+    import paper_1505_03851_amd as lda
+    fn = {"naive": lda.draw_naive, "butterfly": lda.draw_butterfly}[kernel]
+    z = fn(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    torch.cuda.synchronize()
+    return z.cpu().numpy()
+
+
+def compare(c, z_gpu, idx=None) -> ParityReport:
+    """Oracle on tokens ``idx`` (all if None) against the GPU's z there."""
+    if idx is None:
+        d, w, u, zg = c.doc_id, c.word_id, c.u, z_gpu
+    else:
+        d, w, u, zg = c.doc_id[idx], c.word_id[idx], c.u[idx], z_gpu[idx]
+    z_ref, band = oracle.draw(c.theta, c.phi, d, w, u, band_rel=BAND_REL)
+    mis = zg != z_ref
+    hard = mis & ~band
+    where = np.nonzero(hard)[0][:5]
+    first = [(int(i if idx is None else idx[i]), int(zg[i]), int(z_ref[i]))
+             for i in where]
+    return ParityReport(int(zg.size), int(mis.sum()), int(hard.sum()),
+                        int(band.sum()), first)

@@ -1,0 +1,123 @@
+"""The C ABI on the CPU: the library loads, exports every function the header
+declares, and rejects bad arguments before touching HIP (no kernel is
+launched by these tests)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from conftest import ROOT
+
+HEADER_DIR = os.path.join(ROOT, "include")
+
+
+def declared_functions():
+    names = []
+    for fn in sorted(os.listdir(HEADER_DIR)):
+        if fn.endswith(".h"):
+            src = open(os.path.join(HEADER_DIR, fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names += re.findall(r"^[A-Za-z_][\w\s\*]*?\b(lda_\w+)\s*\(", src,
+                                flags=re.M)
+    return names
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_1505_03851_amd import _lib
+    return _lib.load()
+
+
+def test_header_declares_the_boundary():
+    names = declared_functions()
+    for must in ("lda_draw_naive", "lda_draw_butterfly", "lda_status_string"):
+        assert must in names
+
+
+def test_every_declared_symbol_is_exported(lib):
+    from paper_1505_03851_amd import _lib
+    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    exported = set(re.findall(r"\bT\s+(\w+)$", out, flags=re.M))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    from paper_1505_03851_amd import _lib
+    seen = set()
+    for k, v in _lib.STATUS.items():
+        if k == "LDA_MAX_K":
+            continue
+        s = lib.lda_status_string(v).decode()
+        assert s and s != "unknown status"
+        seen.add(s)
+    assert len(seen) == len(_lib.STATUS) - 1
+    assert lib.lda_status_string(12345).decode() == "unknown status"
+    assert lib.lda_version() >= 100
+
+
+# Fake, aligned, non-null addresses: every call below must be rejected (or be
+# a no-op) by the host-side checks, so none of them is dereferenced.
+A = 4096
+
+
+def call(lib, fn, **kw):
+    args = dict(theta=A, phi=A, doc=A, word=A, u=A, z=A, N=10, M=3, V=5, K=8)
+    args.update(kw)
+    f = getattr(lib, fn)
+    if fn == "lda_butterfly_table":
+        return f(args["theta"], args["phi"], args["doc"], args["word"],
+                 args["z"], args["N"], args["M"], args["V"], args["K"], None)
+    return f(args["theta"], args["phi"], args["doc"], args["word"], args["u"],
+             args["z"], args["N"], args["M"], args["V"], args["K"], None)
+
+
+FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_butterfly_table"]
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_shape_errors(lib, fn):
+    from paper_1505_03851_amd._lib import STATUS
+    for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0), dict(K=-5),
+               dict(M=-1)):
+        assert call(lib, fn, **kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert call(lib, fn, K=STATUS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_null_and_alignment_errors(lib, fn):
+    from paper_1505_03851_amd._lib import STATUS
+    keys = ["theta", "phi", "doc", "word", "z"] + (["u"] if fn != "lda_butterfly_table" else [])
+    for key in keys:
+        assert call(lib, fn, **{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert call(lib, fn, **{key: A + 2}) == STATUS["LDA_ERR_ALIGN"], key
+
+
+@pytest.mark.parametrize("fn", FNS)
+def test_empty_is_noop(lib, fn):
+    # N = 0: no launch, no pointer needed
+    assert call(lib, fn, N=0, theta=None, phi=None, doc=None, word=None,
+                u=None, z=None) == 0
+
+
+def test_width(lib):
+    from paper_1505_03851_amd._lib import STATUS
+    assert lib.lda_butterfly_width(1) == 32
+    assert lib.lda_butterfly_width(63) == 32
+    assert lib.lda_butterfly_width(64) == 64
+    assert lib.lda_butterfly_width(STATUS["LDA_MAX_K"]) == 64
+    assert lib.lda_butterfly_width(0) == STATUS["LDA_ERR_SHAPE"]
+    assert lib.lda_butterfly_width(STATUS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+
+
+def test_binding_rejects_cpu_tensors():
+    import torch
+    import paper_1505_03851_amd as lda
+    t = torch.zeros((2, 4))
+    i = torch.zeros(3, dtype=torch.int32)
+    with pytest.raises(ValueError):
+        lda.draw_butterfly(t, t, i, i, torch.zeros(3))
