@@ -144,6 +144,9 @@ def main() -> int:
     ap.add_argument("--only", choices=["butterfly", "naive"], default=None,
                     help="time one kernel on one workload (for profiling)")
     ap.add_argument("--workload", default=HEADLINE)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run plain 1 GiB device-to-device copies (the "
+                         "reference for scaling HBM counters)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
@@ -158,6 +161,17 @@ def main() -> int:
     if not torch.cuda.is_available():
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
+
+    if args.copy_calibration:
+        n = 1 << 28                      # 1 GiB of float32
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n,
+                          "dispatches": 3}), flush=True)
+        return 0
 
     if args.only:
         c = make_corpus(args.workload)

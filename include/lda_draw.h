@@ -59,12 +59,17 @@ extern "C" {
 #define LDA_OK 0
 #define LDA_ERR_NULL (-1)        /* a required pointer is NULL while N > 0   */
 #define LDA_ERR_SHAPE (-2)       /* N < 0, M <= 0, V <= 0 or K <= 0          */
-#define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K                            */
+#define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K, or a table too large      */
 #define LDA_ERR_HIP (-4)         /* the HIP runtime reported an error        */
 #define LDA_ERR_ALIGN (-5)       /* a pointer is not 4-byte aligned          */
 
 /* Largest number of topics the kernels accept. */
 #define LDA_MAX_K 4096
+
+/* Largest size in bytes of theta (4*M*K) or phi (4*V*K): the butterfly
+ * kernel addresses both through buffer resources with 31-bit byte offsets.
+ * Larger tables are rejected with LDA_ERR_UNSUPPORTED. */
+#define LDA_MAX_TABLE_BYTES 2147483647
 
 /*
  * Baseline draw: Algorithm 1 with the binary search of Algorithm 3.  One lane

@@ -8,7 +8,7 @@ on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 
 _BINDING = ("draw_naive", "draw_butterfly", "butterfly_table",
             "butterfly_width", "status_string", "version", "LdaError",
-            "load", "MAX_K", "STATUS")
+            "load", "MAX_K", "MAX_TABLE_BYTES", "STATUS")
 
 __all__ = list(_BINDING)
 

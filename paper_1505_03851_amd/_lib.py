@@ -27,16 +27,19 @@ class LdaError(RuntimeError):
         self.status = status
 
 
-def _status_codes() -> dict[str, int]:
-    codes = {}
+def _header_constants() -> dict[str, int]:
+    consts = {}
     with open(HEADER) as f:
         for m in re.finditer(r"#define\s+(LDA_\w+)\s+\(?(-?\d+)\)?", f.read()):
-            codes[m.group(1)] = int(m.group(2))
-    return codes
+            consts[m.group(1)] = int(m.group(2))
+    return consts
 
 
-STATUS = _status_codes()
-MAX_K = STATUS["LDA_MAX_K"]
+_CONSTS = _header_constants()
+# status codes (LDA_OK and LDA_ERR_*) and size limits from the header
+STATUS = {k: v for k, v in _CONSTS.items() if k == "LDA_OK" or k.startswith("LDA_ERR_")}
+MAX_K = _CONSTS["LDA_MAX_K"]
+MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
 
 
 def load() -> ctypes.CDLL:

@@ -16,13 +16,20 @@ constexpr int kWave = 64;
 
 __device__ __forceinline__ int lane_id() { return threadIdx.x & (kWave - 1); }
 
-// Value of `x` held by lane (lane xor BIT), BIT a power of two below 64.
-// xor 1 and 2 are DPP quad permutations, xor 4..16 ds_swizzle in bit-mask
-// mode (within 32 lanes), xor 32 a ds_bpermute.
+__device__ __forceinline__ int as_int(float x) { return __builtin_bit_cast(int, x); }
+__device__ __forceinline__ float as_float(int x) { return __builtin_bit_cast(float, x); }
+
+// ---------------------------------------------------------------------------
+// Cross-lane primitives.
+
+// Value of `x` held by lane (lane xor BIT), BIT a power of two below 64:
+// the paper's shuffleXor with a constant mask.  xor 1 and 2 are DPP quad
+// permutations, xor 4..16 ds_swizzle in bit-mask mode (within 32 lanes),
+// xor 32 a ds_bpermute.
 template <int BIT>
 __device__ __forceinline__ float xor_lane(float x) {
   static_assert(BIT > 0 && BIT < kWave && (BIT & (BIT - 1)) == 0, "bad BIT");
-  int v = __builtin_bit_cast(int, x);
+  int v = as_int(x);
   if constexpr (BIT == 1) {
     v = __builtin_amdgcn_mov_dpp(v, 0xB1, 0xF, 0xF, false);  // [1,0,3,2]
   } else if constexpr (BIT == 2) {
@@ -32,10 +39,83 @@ __device__ __forceinline__ float xor_lane(float x) {
   } else {
     v = __builtin_amdgcn_ds_bpermute((lane_id() ^ BIT) << 2, v);
   }
-  return __builtin_bit_cast(float, v);
+  return as_float(v);
 }
 
-// Store policies for the table rows a stage finishes.
+// The paper's shuffleXor with a per-lane mask: value of `x` in lane
+// (lane xor m), m < 64.
+__device__ __forceinline__ float xor_lane_var(float x, int m) {
+  return as_float(__builtin_amdgcn_ds_bpermute((lane_id() ^ m) << 2, as_int(x)));
+}
+
+// Half exchange between lanes l and l xor BIT of two registers x, y: lanes
+// with BIT clear keep x and receive the partner's x in y; lanes with BIT set
+// keep y and receive the partner's y in x.  Afterwards x + y is, in every
+// lane, the pair sum of one token (the lane's "kept" register).
+//   BIT 32, 16: one v_permlane32_swap / v_permlane16_swap (gfx950);
+//   BIT 8, 4:   two DPP row shifts whose bank masks pick the receiving lanes.
+template <int BIT>
+__device__ __forceinline__ void half_swap(float &x, float &y) {
+  if constexpr (BIT == 32) {
+    auto s = __builtin_amdgcn_permlane32_swap(as_int(x), as_int(y), false, false);
+    x = as_float(s[0]);
+    y = as_float(s[1]);
+  } else if constexpr (BIT == 16) {
+    auto s = __builtin_amdgcn_permlane16_swap(as_int(x), as_int(y), false, false);
+    x = as_float(s[0]);
+    y = as_float(s[1]);
+  } else {
+    static_assert(BIT == 8 || BIT == 4, "half_swap: BIT in {4, 8, 16, 32}");
+    // row_shr:BIT (lane i reads i - BIT) into the lanes with BIT set,
+    // row_shl:BIT (lane i reads i + BIT) into the lanes with BIT clear.
+    constexpr int hi_banks = BIT == 8 ? 0xC : 0xA;
+    constexpr int lo_banks = BIT == 8 ? 0x3 : 0x5;
+    const int xi = as_int(x), yi = as_int(y);
+    const int xn = __builtin_amdgcn_update_dpp(xi, yi, 0x110 + BIT, 0xF, hi_banks, false);
+    const int yn = __builtin_amdgcn_update_dpp(yi, xi, 0x100 + BIT, 0xF, lo_banks, false);
+    x = as_float(xn);
+    y = as_float(yn);
+  }
+}
+
+// Pair sum for BIT 1, 2 (within a DPP bank): lanes with BIT clear return
+// x + partner's x, lanes with BIT set return y + partner's y.
+template <int BIT>
+__device__ __forceinline__ float pair_sum(float x, float y) {
+  const bool hi = (lane_id() & BIT) != 0;
+  const float send = hi ? x : y;
+  const float keep = hi ? y : x;
+  return keep + xor_lane<BIT>(send);
+}
+
+// ---------------------------------------------------------------------------
+// Block totals for the sweep: a reduce-scatter of the W x W tile.  Stage BIT
+// pairs registers k and k + BIT (k < BIT) across lanes l and l xor BIT; after
+// the stages for BIT = W/2 .. 1 lane l holds the sum of its own token over the
+// block's W topics in a[0].  The tile registers are consumed from the top, so
+// the caller can refill a[BIT..2*BIT-1] as soon as stage BIT has finished.
+template <int W, int BIT>
+__device__ __forceinline__ void reduce_stage(float (&a)[W]) {
+  if constexpr (BIT >= 4) {
+#pragma unroll
+    for (int k = BIT - 1; k >= 0; --k) {
+      half_swap<BIT>(a[k], a[k + BIT]);
+      a[k] = a[k] + a[k + BIT];
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < BIT; ++k) a[k] = pair_sum<BIT>(a[k], a[k + BIT]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Algorithm 8's butterfly for one block (the paper's replacement rule, with
+// stages in the paper's order bit = 1, 2, ..., W/2).  Set for BIT: rows d and
+// d + BIT, d = 2*BIT*i + BIT - 1, lanes r and r xor BIT; [a b; c d] becomes
+// [a d; a+b c+d]: the lane with BIT set keeps its row-(d+BIT) value in row d,
+// and row d + BIT receives the kept value plus what the partner sends.
+// Afterwards a[0..W-2] hold lane r's column of the butterfly-patterned block
+// (row d in a[d]) and a[W-1] holds the sum of lane r's own token.
 struct NoStore {
   __device__ __forceinline__ void operator()(int, float) const {}
 };
@@ -50,10 +130,6 @@ struct RowStore {
   }
 };
 
-// One set of replacements (Section 4): rows d and d + BIT, d = 2*BIT*i + BIT-1,
-// lanes r and r xor BIT.  [a b; c d] -> [a d; a+b c+d]: the lane with BIT set
-// keeps its row-(d+BIT) value in row d, and row d + BIT receives the sum of
-// the kept value and the value the partner lane sends.
 template <int W, int BIT, class Store>
 __device__ __forceinline__ void butterfly_stages(float (&a)[W], int r,
                                                  const Store &store) {
@@ -73,13 +149,26 @@ __device__ __forceinline__ void butterfly_stages(float (&a)[W], int r,
   }
 }
 
-// Algorithm 8's butterfly for one block: afterwards a[0..W-2] hold lane r's
-// column of the butterfly-patterned block (row d in a[d]) and a[W-1] holds
-// the sum of lane r's own token over the block.
 template <int W, class Store>
 __device__ __forceinline__ void butterfly_block(float (&a)[W], int r,
                                                 const Store &store) {
   butterfly_stages<W, 1, Store>(a, r, store);
+}
+
+// ---------------------------------------------------------------------------
+// Memory access through buffer resources: a per-wave base and size in SGPRs,
+// a per-lane byte offset (VGPR) and a per-token byte offset (SGPR).
+using rsrc_t = __amdgpu_buffer_rsrc_t;
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void *base, uint32_t bytes) {
+  // dword3: 32-bit raw data (same value the CDNA3/CDNA4 libraries use)
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, bytes,
+                                           0x00020000);
+}
+
+// (the builtin returns the 32 loaded bits as an unsigned integer)
+__device__ __forceinline__ float load_f32(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
 // Value of `v` in lane (group base + k): uniform across the wave when W = 64.
@@ -95,39 +184,11 @@ __device__ __forceinline__ int group_value(int v, int k) {
   }
 }
 
-// Transposed tile of one block per token (Algorithm 8's product loop, with
-// Algorithm 5's transposed theta access): a[k] = theta[doc_k][c_k] *
-// phi[word_k][c_k] with c_k = R + blk_k * W + r, where doc_k, word_k, blk_k
-// are the document, word and block of token k of the group.  Each k is one
-// coalesced load of W consecutive floats per group.  With `one_doc` (every
-// token of the wave in document doc0) and `one_blk` (every token on the same
-// block) theta is one load per lane instead of W.
-template <int W>
-__device__ __forceinline__ void load_tile(float (&a)[W],
-                                          const float *__restrict__ theta,
-                                          const float *__restrict__ phi, int K,
-                                          int R, int doc, int word, int blk,
-                                          int r, bool one_doc, bool one_blk) {
-  if (one_doc && one_blk) {
-    const int doc0 = __builtin_amdgcn_readfirstlane(doc);
-    const int blk0 = __builtin_amdgcn_readfirstlane(blk);
-    const int col = R + blk0 * W + r;
-    const float th = theta[(int64_t)doc0 * K + col];
-#pragma unroll
-    for (int k = 0; k < W; ++k) {
-      const int wk = group_value<W>(word, k);
-      a[k] = th * phi[(int64_t)wk * K + col];
-    }
-  } else {
-#pragma unroll
-    for (int k = 0; k < W; ++k) {
-      const int wk = group_value<W>(word, k);
-      const int dk = group_value<W>(doc, k);
-      const int col = R + group_value<W>(blk, k) * W + r;
-      a[k] = theta[(int64_t)dk * K + col] * phi[(int64_t)wk * K + col];
-    }
-  }
-}
+// How a wavefront's tokens map to documents, for the theta factor of the
+// tile: one document (one theta value per lane per block), two documents in
+// two contiguous runs (two values and a per-token choice), or any mix (one
+// theta load per token).
+enum ThetaMode : int { kOneDoc = 0, kTwoDocs = 1, kAnyDocs = 2 };
 
 // One step of the untransposed running sum of the remnant (and of the naive
 // kernel): sum + theta * phi.  Written once so that every recomputation of a

@@ -10,6 +10,12 @@
 #include "butterfly.hpp"
 #include "lda_draw.h"
 
+// Largest block count K / W for which the rebuilt block's table is kept in
+// LDS (see lds_table_for).
+#ifndef LDA_LDS_TABLE_MAX_BLOCKS
+#define LDA_LDS_TABLE_MAX_BLOCKS 4
+#endif
+
 namespace lda {
 namespace {
 
@@ -47,11 +53,267 @@ __global__ __launch_bounds__(256) void naive_kernel(
   z[n] = j;
 }
 
-// LDS floats per wavefront of the butterfly kernel: the block-end prefixes
-// (NB rows of 64 lanes) during the sweep, then the rebuilt table of one block
-// (W - 1 rows of 64 lanes) during the search.
-__host__ __device__ constexpr int region_rows(int NB, int W) {
-  return NB > W - 1 ? NB : W - 1;
+// ---------------------------------------------------------------------------
+// Per-wavefront state of the butterfly kernel.  The wavefront's 64 tokens are
+// the window [t0, t0 + 64) of the token arrays; their word and document ids
+// are read with scalar loads straight from those arrays whenever a tile is
+// loaded (SMALL: the window is padded by repeating token N - 1).
+template <int W, bool SMALL>
+struct Wave {
+  rsrc_t th_rs, ph_rs;  // theta, phi
+  const int32_t *wp;    // word_id + t0
+  const int32_t *dp;    // doc_id + t0
+  int last;             // SMALL: index in the window of token N - 1
+  uint32_t row_bytes;   // 4 * K
+  int R;                // remnant topics (K mod W)
+  int r;                // lane within its group of W
+  int gbase;            // first lane of the group
+  int doc;              // this lane's document
+  int mode;             // ThetaMode, uniform
+  int kb;               // kTwoDocs: wave lanes below kb are in the first doc
+  uint32_t th_off0, th_off1;  // theta row offsets of the first / last doc
+};
+
+// Keep a uniform value opaque to the optimiser, so that work depending on it
+// is done where it is written instead of being hoisted out of the block loop
+// into (and spilling out of) scalar registers.  The readfirstlane marks the
+// result uniform again for the divergence analysis, which treats inline
+// assembly results as per-lane.
+__device__ __forceinline__ int launder_int(int v) {
+  asm volatile("" : "+s"(v));
+  return __builtin_amdgcn_readfirstlane(v);
+}
+
+// The same for a pointer into a read-only kernel argument: only a zero offset
+// is made opaque, so the pointer keeps its provenance (and its loads stay
+// scalar loads of memory the kernel never writes).
+__device__ __forceinline__ const int32_t *launder(const int32_t *p) {
+  return p + launder_int(0);
+}
+
+// Scalar read of entry k of a wave window (k uniform).
+template <bool SMALL>
+__device__ __forceinline__ int window_at(const int32_t *p, int last, int k) {
+  return SMALL ? p[k < last ? k : last] : p[k];
+}
+
+// Byte offset of the phi row of token k of this lane's group: uniform for
+// W = 64, one value per half-wave for W = 32.
+template <int W, bool SMALL>
+__device__ __forceinline__ uint32_t phi_row(const Wave<W, SMALL> &w, const int32_t *wp, int k) {
+  if constexpr (W == kWave) {
+    return (uint32_t)window_at<SMALL>(wp, w.last, k) * w.row_bytes;
+  } else {
+    const uint32_t lo = (uint32_t)window_at<SMALL>(wp, w.last, k) * w.row_bytes;
+    const uint32_t hi = (uint32_t)window_at<SMALL>(wp, w.last, 32 + k) * w.row_bytes;
+    return w.gbase ? hi : lo;
+  }
+}
+
+// Same for the theta row of token k's document.
+template <int W, bool SMALL>
+__device__ __forceinline__ uint32_t theta_row(const Wave<W, SMALL> &w, int k) {
+  if constexpr (W == kWave) {
+    return (uint32_t)window_at<SMALL>(w.dp, w.last, k) * w.row_bytes;
+  } else {
+    const uint32_t lo = (uint32_t)window_at<SMALL>(w.dp, w.last, k) * w.row_bytes;
+    const uint32_t hi = (uint32_t)window_at<SMALL>(w.dp, w.last, 32 + k) * w.row_bytes;
+    return w.gbase ? hi : lo;
+  }
+}
+
+// buffer load at a per-lane offset plus a row offset that is uniform for
+// W = 64 (scalar operand) and per half-wave for W = 32 (added per lane).
+template <int W>
+__device__ __forceinline__ float load_row(rsrc_t rs, uint32_t voff, uint32_t row) {
+  if constexpr (W == kWave)
+    return load_f32(rs, voff, row);
+  else
+    return load_f32(rs, voff + row, 0);
+}
+
+// Issue the phi loads of tokens [LO, HI) of block `blk` into a[LO..HI-1].
+template <int W, bool SMALL, int LO, int HI>
+__device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t *wp,
+                                          float (&a)[W], int blk) {
+  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+#pragma unroll
+  for (int k = LO; k < HI; ++k) a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
+}
+
+// Theta of block `blk` at this lane's topic, for the first and last document.
+template <int W, bool SMALL>
+__device__ __forceinline__ void issue_theta(const Wave<W, SMALL> &w, int blk, float &th0,
+                                            float &th1) {
+  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+  th0 = load_f32(w.th_rs, voff, w.th_off0);
+  if (w.mode == kTwoDocs) th1 = load_f32(w.th_rs, voff, w.th_off1);
+}
+
+// The stages of the block-total reduce-scatter from BIT down to 1.  With
+// PREFETCH, the registers each stage frees are refilled at once with the next
+// block's phi values, so those loads are in flight during the rest of the
+// reduction.
+template <int W, bool SMALL, int BIT, bool PREFETCH>
+__device__ __forceinline__ void reduce_rest(const Wave<W, SMALL> &w, const int32_t *wp,
+                                            float (&a)[W], int next) {
+  if constexpr (BIT >= 1) {
+    reduce_stage<W, BIT>(a);
+    if constexpr (PREFETCH && BIT > 1) issue_phi<W, SMALL, BIT, 2 * BIT>(w, wp, a, next);
+    reduce_rest<W, SMALL, BIT / 2, PREFETCH>(w, wp, a, next);
+  }
+}
+
+// Sweep step for one block whose phi values are in (or in flight to) a[] and
+// whose theta values are in th0/th1.  Returns this lane's token total over
+// the block.  With PREFETCH, block `next`'s loads are issued along the way
+// and left in a[], th0, th1.
+template <int W, bool SMALL, bool PREFETCH>
+__device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int32_t *wp,
+                                             float (&a)[W], float &th0, float &th1,
+                                             int next) {
+  constexpr int B = W / 2;
+  if (w.mode == kOneDoc) {
+    // First stage fused with the theta factor: after the half exchange the
+    // two values of a pair sit at topics of the lower and upper half-group,
+    // whose theta values one more exchange of th0 provides.
+    float tA = th0, tB = th0;
+    half_swap<B>(tA, tB);
+    if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
+#pragma unroll
+    for (int k = B - 1; k >= 0; --k) {
+      half_swap<B>(a[k], a[k + B]);
+      a[k] = __builtin_fmaf(a[k], tA, a[k + B] * tB);
+    }
+  } else {
+    // Two contiguous document runs: wave lanes below kb take th0.  (kb is
+    // laundered so that the per-token choices are made here, not hoisted out
+    // of the block loop into scalar registers.)
+    const int kb = launder_int(w.kb);
+#pragma unroll
+    for (int k = 0; k < W; ++k) a[k] *= (w.gbase + k < kb) ? th0 : th1;
+    if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
+    reduce_stage<W, B>(a);
+  }
+  if constexpr (PREFETCH) issue_phi<W, SMALL, B, W>(w, wp, a, next);
+  reduce_rest<W, SMALL, B / 2, PREFETCH>(w, wp, a, next);
+  const float total = a[0];
+  if constexpr (PREFETCH) issue_phi<W, SMALL, 0, 2>(w, wp, a, next);
+  return total;
+}
+
+// Sweep step for a wave whose tokens belong to many documents: one theta
+// load per token, no prefetch.
+template <int W, bool SMALL>
+__device__ __forceinline__ float sweep_block_any(const Wave<W, SMALL> &w, const int32_t *wp,
+                                                 int blk) {
+  float a[W];
+  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+#pragma unroll
+  for (int k = 0; k < W; ++k)
+    a[k] = load_row<W>(w.th_rs, voff, theta_row(w, k)) *
+           load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
+  reduce_stage<W, W / 2>(a);
+  reduce_rest<W, SMALL, W / 4, false>(w, wp, a, 0);
+  return a[0];
+}
+
+// Transposed tile in which token k of the group contributes block blk_k
+// (this lane's `blk` is its own token's block): a[k] = theta[doc_k][c_k] *
+// phi[word_k][c_k], c_k = R + blk_k * W + r.
+template <int W, bool SMALL>
+__device__ __forceinline__ void load_tile_blocks(const Wave<W, SMALL> &w, float (&a)[W],
+                                                 int blk) {
+  const uint32_t v0 = (uint32_t)(w.R + w.r) * 4u;
+#pragma unroll
+  for (int k = 0; k < W; ++k) {
+    const uint32_t boff = (uint32_t)group_value<W>(blk, k) * (W * 4u);
+    a[k] = load_row<W>(w.th_rs, v0, theta_row(w, k) + boff) *
+           load_row<W>(w.ph_rs, v0, phi_row(w, w.wp, k) + boff);
+  }
+}
+
+template <int W, bool SMALL>
+__device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
+                                          const float *phi, uint32_t theta_bytes,
+                                          uint32_t phi_bytes, const int32_t *doc_id,
+                                          const int32_t *word_id, int64_t t0, int last,
+                                          int K, int lane, int doc) {
+  w.th_rs = make_rsrc(theta, theta_bytes);
+  w.ph_rs = make_rsrc(phi, phi_bytes);
+  w.wp = word_id + t0;
+  w.dp = doc_id + t0;
+  w.last = last;
+  w.row_bytes = (uint32_t)K * 4u;
+  w.R = K & (W - 1);
+  w.r = lane & (W - 1);
+  w.gbase = lane & ~(W - 1);
+  w.doc = doc;
+  const int d0 = __builtin_amdgcn_readfirstlane(doc);
+  const int d1 = __builtin_amdgcn_readlane(doc, kWave - 1);
+  const uint64_t in0 = __builtin_amdgcn_ballot_w64(doc == d0);
+  const uint64_t in1 = __builtin_amdgcn_ballot_w64(doc == d1);
+  if (in0 == ~0ull) {
+    w.mode = kOneDoc;
+    w.kb = kWave;
+  } else if ((in0 | in1) == ~0ull && (in0 & (in0 + 1)) == 0) {
+    w.mode = kTwoDocs;  // lanes [0, kb) in d0, [kb, 64) in d1
+    w.kb = __builtin_popcountll(in0);
+  } else {
+    w.mode = kAnyDocs;
+    w.kb = 0;
+  }
+  w.th_off0 = (uint32_t)d0 * w.row_bytes;
+  w.th_off1 = (uint32_t)d1 * w.row_bytes;
+}
+
+
+// In-block search of Algorithm 10.  `low` and `high` are the full prefixes
+// before and at the end of the block; a[0..W-2] is this lane's column of the
+// rebuilt block (or, with LDS_TABLE, the rows are in `table`, row d at
+// table[d * 64 + lane]).  Returns the offset within the block.
+template <int W, bool LDS_TABLE>
+__device__ __forceinline__ int inblock_search(const float (&a)[W], const float *table,
+                                              int r, int gbase, float stop, float low,
+                                              float high) {
+  constexpr int LOG2W = (W == 64) ? 6 : 5;
+  int flip = 0;
+#pragma unroll
+  for (int lvl = 0; lvl < LOG2W; ++lvl) {
+    const int bit = (W / 2) >> lvl;
+    const int mask = ((W - 1) * (2 * bit)) & (W - 1);
+    float y;
+    if constexpr (LDS_TABLE) {
+      // The entry the search-assist loop would deliver: row (r & mask) |
+      // (bit - 1) of column r xor flip.
+      y = table[((r & mask) | (bit - 1)) * kWave + gbase + (r ^ flip)];
+    } else {
+      // Search-assist loop: every lane offers each candidate row in turn;
+      // the lane keeps the one whose high bits match its own.
+      y = 0.0f;
+#pragma unroll
+      for (int i = 0; i < W / (2 * bit); ++i) {
+        const int d = (bit - 1) + 2 * bit * i;
+        const float t = xor_lane_var(a[d], flip);
+        if ((r & mask) == (d & mask)) y = t;
+      }
+    }
+    const float cmp = (r & bit) ? high - y : low + y;
+    if (stop < cmp) {
+      high = cmp;
+      flip ^= bit & r;
+    } else {
+      low = cmp;
+      flip ^= bit & ~r;
+    }
+  }
+  return flip ^ r;
+}
+
+// LDS rows per wavefront: the block-end prefixes (NB rows of 64 lanes), and,
+// with an LDS table, the rebuilt block's W - 1 rows in the same space.
+__host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
+  return lds_table ? (NB > W - 1 ? NB : W - 1) : NB;
 }
 
 // ---------------------------------------------------------------------------
@@ -59,146 +321,166 @@ __host__ __device__ constexpr int region_rows(int NB, int W) {
 // repeat token N - 1 so that every lane takes part in every exchange (the
 // paper's "staying awake" rule) and skip the store.
 //
-// Sweep (Algorithm 8 without the table): per block, the transposed tile,
-// the butterfly, and the running prefix at the block's end, kept in LDS.
-// Search (Algorithm 9): binary search over the block ends for stop = S * u.
-// Rebuild: one tile in which every token contributes its own chosen block;
-// the butterfly's rows go to LDS.  In-block search (Algorithm 10): at level b
-// lane r reads row (r & mask) | (bit - 1) of column r xor flip directly from
-// LDS, which is the entry the search-assist loop of the paper delivers with
-// shuffles.  Remnant: Algorithm 9's linear fallback.
-template <int W>
-__global__ __launch_bounds__(kBlockThreads) void butterfly_kernel(
+// Remnant: untransposed running sum of the first K mod W topics.
+// Sweep (K / W >= 2): per block the transposed tile, a reduce-scatter giving
+//   every lane its token's block total, and the running prefix at the block's
+//   end, kept in LDS.
+// Block search (Algorithm 9): binary search over the block ends for S * u.
+// Rebuild: one tile in which every token contributes its own chosen block,
+//   combined by Algorithm 8's butterfly (with K / W == 1 this tile is the only
+//   pass over phi).
+// In-block search (Algorithm 10) and the remnant fallback of Algorithm 9.
+template <int W, bool LDS_TABLE, bool SMALL>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(3)))
+void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi,
     const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
-    const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K) {
+    const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
+    uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
   if (first >= N) return;  // whole wavefront past the end
-  const int64_t n = first + lane < N ? first + lane : N - 1;
-  const bool valid = first + lane < N;
-  const int r = lane & (W - 1);
+  // Window of 64 tokens: the wavefront's own, or for the last wavefront the
+  // final 64 tokens (re-drawing some of the previous wavefront's, which it
+  // does not store).  SMALL (N < 64): tokens past N repeat token N - 1, so
+  // that every lane takes part in every exchange (the paper's "staying
+  // awake" rule).
+  const int64_t t0 = SMALL ? 0 : (first + kWave <= N ? first : N - kWave);
+  const int last = SMALL ? (int)(N - 1) : kWave - 1;
+  const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
+  const bool store = SMALL ? lane < N : t0 + lane >= first;
 
   const int doc = doc_id[n];
   const int word = word_id[n];
   const float un = u[n];
-  const int R = K % W;
-  const int NB = K / W;
-  float *region = lds + wave * region_rows(NB, W) * kWave;
-  const int doc0 = __builtin_amdgcn_readfirstlane(doc);
-  const bool one_doc = __builtin_amdgcn_ballot_w64(doc == doc0) == ~0ull;
+  const int NB = K >> LOG2W;
+  Wave<W, SMALL> w;
+  init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+                      lane, doc);
+  const int R = w.R;
+  float *region = lds + wave * region_rows(NB, W, LDS_TABLE) * kWave;
 
-  // Remnant: untransposed running sum of the first R topics.
+  // Remnant.
   const float *th_row = theta + (int64_t)doc * K;
   const float *ph_row = phi + (int64_t)word * K;
   float sum = 0.0f;
   for (int j = 0; j < R; ++j) sum = prefix_step(sum, th_row[j], ph_row[j]);
   const float p_rem = sum;
 
-  // Sweep over the blocks.
-  for (int b = 0; b < NB; ++b) {
-    float a[W];
-    load_tile<W>(a, theta, phi, K, R, doc, word, b, r, one_doc, true);
-    butterfly_block<W>(a, r, NoStore{});
-    sum += a[W - 1];
-    region[b * kWave + lane] = sum;
-  }
-
-  const float stop = sum * un;
   int j;
   if (NB == 0) {
-    j = remnant_search(th_row, ph_row, R, stop, K - 1);
+    j = remnant_search(th_row, ph_row, R, sum * un, K - 1);
   } else {
-    // Algorithm 9: binary search over the last row of each block.
-    int lo = 0, hi = NB - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (stop < region[mid * kWave + lane])
-        hi = mid;
+    float a[W];
+    float stop, low, high;
+    int blk;
+    if (NB == 1) {
+      // One block: its table is built once and searched directly.
+      blk = 0;
+      load_tile_blocks(w, a, 0);
+      if constexpr (LDS_TABLE)
+        butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
       else
-        lo = mid + 1;
-    }
-    float low = lo > 0 ? region[(lo - 1) * kWave + lane] : p_rem;
-    float high = region[lo * kWave + lane];
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // Rebuild the chosen block of every token and keep its table in LDS.
-    {
-      float a[W];
-      const int blk0 = __builtin_amdgcn_readfirstlane(lo);
-      const bool one_blk = __builtin_amdgcn_ballot_w64(lo == blk0) == ~0ull;
-      load_tile<W>(a, theta, phi, K, R, doc, word, lo, r, one_doc, one_blk);
-      butterfly_block<W>(a, r, RowStore{region + lane, kWave, true});
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // Algorithm 10: butterfly search within the block.
-    const int gbase = lane & ~(W - 1);
-    int flip = 0;
-#pragma unroll
-    for (int lvl = 0; lvl < LOG2W; ++lvl) {
-      const int bit = (W / 2) >> lvl;
-      const int mask = ((W - 1) * (2 * bit)) & (W - 1);
-      const int d = (r & mask) | (bit - 1);
-      const float y = region[d * kWave + gbase + (r ^ flip)];
-      const float cmp = (r & bit) ? high - y : low + y;
-      if (stop < cmp) {
-        high = cmp;
-        flip ^= bit & r;
+        butterfly_block<W>(a, w.r, NoStore{});
+      sum += a[W - 1];
+      stop = sum * un;
+      low = p_rem;
+      high = sum;
+    } else {
+      // Sweep over the blocks.
+      if (w.mode == kAnyDocs) {
+        for (int b = 0; b < NB; ++b) {
+          sum += sweep_block_any(w, launder(w.wp), b);
+          region[b * kWave + lane] = sum;
+        }
       } else {
-        low = cmp;
-        flip ^= bit & ~r;
+        float th0 = 0.0f, th1 = 0.0f;
+        issue_theta(w, 0, th0, th1);
+        issue_phi<W, SMALL, 0, W>(w, w.wp, a, 0);
+        for (int b = 0; b < NB - 1; ++b) {
+          sum += sweep_block<W, SMALL, true>(w, launder(w.wp), a, th0, th1, b + 1);
+          region[b * kWave + lane] = sum;
+        }
+        sum += sweep_block<W, SMALL, false>(w, w.wp, a, th0, th1, 0);
+        region[(NB - 1) * kWave + lane] = sum;
       }
+      stop = sum * un;
+      // Algorithm 9: binary search over the last row of each block.
+      int lo = 0, hi = NB - 1;
+      while (lo < hi) {
+        const int mid = (lo + hi) >> 1;
+        if (stop < region[mid * kWave + lane])
+          hi = mid;
+        else
+          lo = mid + 1;
+      }
+      blk = lo;
+      low = lo > 0 ? region[(lo - 1) * kWave + lane] : p_rem;
+      high = region[lo * kWave + lane];
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      // Rebuild every token's chosen block.
+      load_tile_blocks(w, a, blk);
+      if constexpr (LDS_TABLE)
+        butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+      else
+        butterfly_block<W>(a, w.r, NoStore{});
     }
-    j = R + lo * W + (flip ^ r);
-    if (lo == 0 && R > 0 && stop < p_rem)
-      j = remnant_search(th_row, ph_row, R, stop, K - 1);
+    if constexpr (LDS_TABLE) {
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    }
+    j = R + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
+    if (blk == 0 && R > 0 && stop < p_rem) j = remnant_search(th_row, ph_row, R, stop, K - 1);
   }
-  if (valid) z[n] = j;
+  if (store) z[n] = j;
 }
 
 // ---------------------------------------------------------------------------
-// Table dump: the per-lane table p[K] of Algorithm 7 for every token.
-template <int W>
+// Table dump: the per-lane table p[K] of Algorithm 7 for every token, built
+// with the same tile loads and butterfly as the draw's rebuild step.
+template <int W, bool SMALL>
 __global__ __launch_bounds__(kBlockThreads) void table_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi,
     const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
-    float *__restrict__ table, int64_t N, int K) {
+    float *__restrict__ table, int64_t N, int K, uint32_t theta_bytes,
+    uint32_t phi_bytes) {
   const int lane = lane_id();
-  const int wave = threadIdx.x / kWave;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
   if (first >= N) return;
-  const int64_t n = first + lane < N ? first + lane : N - 1;
-  const bool valid = first + lane < N;
-  const int r = lane & (W - 1);
+  // Groups of W tokens start at multiples of W: pad the last window by
+  // repeating token N - 1 (tables of shifted windows would differ).
+  const int64_t t0 = first;
+  const int last = (int)(N - 1 - first < kWave - 1 ? N - 1 - first : kWave - 1);
+  const int64_t n = t0 + (lane < last ? lane : last);
+  const bool store = lane <= last;
   const int doc = doc_id[n];
-  const int word = word_id[n];
-  const int R = K % W;
+  Wave<W, true> w;
+  init_wave<W, true>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+                     lane, doc);
+  const int R = w.R;
   const int NB = K / W;
-  const int doc0 = __builtin_amdgcn_readfirstlane(doc);
-  const bool one_doc = __builtin_amdgcn_ballot_w64(doc == doc0) == ~0ull;
   float *out = table + n * (int64_t)K;
 
   const float *th_row = theta + (int64_t)doc * K;
-  const float *ph_row = phi + (int64_t)word * K;
+  const float *ph_row = phi + (int64_t)word_id[n] * K;
   float sum = 0.0f;
   for (int j = 0; j < R; ++j) {
     sum = prefix_step(sum, th_row[j], ph_row[j]);
-    if (valid) out[j] = sum;
+    if (store) out[j] = sum;
   }
   for (int b = 0; b < NB; ++b) {
     float a[W];
-    load_tile<W>(a, theta, phi, K, R, doc, word, b, r, one_doc, true);
-    butterfly_block<W>(a, r, RowStore{out + R + b * W, 1, valid});
+    load_tile_blocks(w, a, b);
+    butterfly_block<W>(a, w.r, RowStore{out + R + b * W, 1, store});
     sum += a[W - 1];
-    if (valid) out[R + b * W + W - 1] = sum;
+    if (store) out[R + b * W + W - 1] = sum;
   }
 }
 
@@ -210,6 +492,10 @@ int check_args(const void *theta, const void *phi, const void *doc_id,
                int32_t M, int32_t V, int32_t K) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
+  // theta and phi are addressed with 31-bit byte offsets
+  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
+    return LDA_ERR_UNSUPPORTED;
   if (N == 0) return LDA_OK;
   const void *ptrs[] = {theta, phi, doc_id, word_id, u, z};
   for (const void *p : ptrs) {
@@ -230,6 +516,11 @@ int finish_launch() {
 
 int width_for(int32_t K) { return K >= 64 ? 64 : 32; }
 
+// The rebuilt block's table goes to LDS when the block search is short
+// (few blocks); otherwise it stays in registers and the search-assist loop
+// moves it, which keeps the LDS footprint to the block-end prefixes.
+bool lds_table_for(int32_t K) { return K / width_for(K) <= LDA_LDS_TABLE_MAX_BLOCKS; }
+
 dim3 wave_grid(int64_t N) {
   const int64_t waves = (N + kWave - 1) / kWave;
   return dim3((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
@@ -241,6 +532,22 @@ void launch_naive(const float *theta, const float *phi, const int32_t *d,
                   int32_t K, hipStream_t s) {
   const dim3 grid((unsigned)((N + 255) / 256));
   naive_kernel<KMAX><<<grid, 256, 0, s>>>(theta, phi, d, w, u, z, N, K);
+}
+
+template <int W, bool LDS_TABLE>
+void launch_butterfly(const float *theta, const float *phi, const int32_t *d,
+                      const int32_t *wd, const float *u, int32_t *z, int64_t N,
+                      int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  const size_t lds = (size_t)kWavesPerBlock * region_rows(K / W, W, LDS_TABLE) *
+                     kWave * sizeof(float);
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  if (N < kWave)
+    butterfly_kernel<W, LDS_TABLE, true><<<wave_grid(N), kBlockThreads, lds, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+  else
+    butterfly_kernel<W, LDS_TABLE, false><<<wave_grid(N), kBlockThreads, lds, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
 }  // namespace
@@ -274,15 +581,18 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int W = width_for(K);
-  const size_t lds = (size_t)kWavesPerBlock * region_rows(K / W, W) * kWave *
-                     sizeof(float);
-  if (W == 64)
-    butterfly_kernel<64><<<wave_grid(N), kBlockThreads, lds, s>>>(
-        theta, phi, doc_id, word_id, u, z, N, K);
-  else
-    butterfly_kernel<32><<<wave_grid(N), kBlockThreads, lds, s>>>(
-        theta, phi, doc_id, word_id, u, z, N, K);
+  const bool lt = lds_table_for(K);
+  if (width_for(K) == 64) {
+    if (lt)
+      launch_butterfly<64, true>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
+    else
+      launch_butterfly<64, false>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
+  } else {
+    if (lt)
+      launch_butterfly<32, true>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
+    else
+      launch_butterfly<32, false>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
+  }
   return finish_launch();
 }
 
@@ -296,12 +606,14 @@ extern "C" int lda_butterfly_table(const float *theta, const float *phi,
                             K);
   if (st != LDA_OK || N == 0) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (width_for(K) == 64)
-    table_kernel<64><<<wave_grid(N), kBlockThreads, 0, s>>>(
-        theta, phi, doc_id, word_id, table, N, K);
+    table_kernel<64, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+        theta, phi, doc_id, word_id, table, N, K, tb, pb);
   else
-    table_kernel<32><<<wave_grid(N), kBlockThreads, 0, s>>>(
-        theta, phi, doc_id, word_id, table, N, K);
+    table_kernel<32, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+        theta, phi, doc_id, word_id, table, N, K, tb, pb);
   return finish_launch();
 }
 
@@ -316,7 +628,9 @@ extern "C" const char *lda_status_string(int status) {
     case LDA_OK: return "ok";
     case LDA_ERR_NULL: return "a required pointer is NULL";
     case LDA_ERR_SHAPE: return "invalid shape (N < 0, M <= 0, V <= 0 or K <= 0)";
-    case LDA_ERR_UNSUPPORTED: return "K exceeds LDA_MAX_K";
+    case LDA_ERR_UNSUPPORTED:
+      return "unsupported size (K > LDA_MAX_K, or theta or phi larger than "
+             "LDA_MAX_TABLE_BYTES)";
     case LDA_ERR_HIP: return "HIP runtime error";
     case LDA_ERR_ALIGN: return "a pointer is not 4-byte aligned";
     default: return "unknown status";
@@ -327,4 +641,4 @@ extern "C" const char *lda_last_hip_error(void) {
   return hipGetErrorString(g_last_hip);
 }
 
-extern "C" int lda_version(void) { return 100; }
+extern "C" int lda_version(void) { return 200; }

@@ -50,12 +50,10 @@ def test_status_strings(lib):
     from paper_1505_03851_amd import _lib
     seen = set()
     for k, v in _lib.STATUS.items():
-        if k == "LDA_MAX_K":
-            continue
         s = lib.lda_status_string(v).decode()
         assert s and s != "unknown status"
         seen.add(s)
-    assert len(seen) == len(_lib.STATUS) - 1
+    assert len(seen) == len(_lib.STATUS)
     assert lib.lda_status_string(12345).decode() == "unknown status"
     assert lib.lda_version() >= 100
 
@@ -85,7 +83,13 @@ def test_shape_errors(lib, fn):
     for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0), dict(K=-5),
                dict(M=-1)):
         assert call(lib, fn, **kw) == STATUS["LDA_ERR_SHAPE"], kw
-    assert call(lib, fn, K=STATUS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    from paper_1505_03851_amd._lib import MAX_K, MAX_TABLE_BYTES
+    assert call(lib, fn, K=MAX_K + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    # tables past the byte limit are rejected before any HIP call
+    big = MAX_TABLE_BYTES // (4 * 1024) + 1
+    assert call(lib, fn, K=1024, V=big) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert call(lib, fn, K=1024, M=big) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert call(lib, fn, K=1024, V=big - 1, M=big - 1, N=0) == 0
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -105,13 +109,13 @@ def test_empty_is_noop(lib, fn):
 
 
 def test_width(lib):
-    from paper_1505_03851_amd._lib import STATUS
+    from paper_1505_03851_amd._lib import MAX_K, STATUS
     assert lib.lda_butterfly_width(1) == 32
     assert lib.lda_butterfly_width(63) == 32
     assert lib.lda_butterfly_width(64) == 64
-    assert lib.lda_butterfly_width(STATUS["LDA_MAX_K"]) == 64
+    assert lib.lda_butterfly_width(MAX_K) == 64
     assert lib.lda_butterfly_width(0) == STATUS["LDA_ERR_SHAPE"]
-    assert lib.lda_butterfly_width(STATUS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert lib.lda_butterfly_width(MAX_K + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
 
 
 def test_binding_rejects_cpu_tensors():
