@@ -114,6 +114,57 @@ def traffic_from_counters():
     return rec.get("hbm_bytes_per_launch")
 
 
+def _counter_means(d: str, kernel_substr: str) -> dict:
+    """Mean per-dispatch value of each counter in a rocprofv3 --pmc csv
+    directory, over the dispatches whose kernel name contains
+    ``kernel_substr`` (per-dispatch values are summed over instances)."""
+    import csv
+    import glob
+    per = {}
+    for path in glob.glob(os.path.join(d, "*counter_collection.csv")):
+        with open(path) as f:
+            for row in csv.DictReader(f):
+                if kernel_substr not in row["Kernel_Name"]:
+                    continue
+                key = (row["Counter_Name"], row["Dispatch_Id"])
+                per[key] = per.get(key, 0.0) + float(row["Counter_Value"])
+    out = {}
+    for (name, _), v in per.items():
+        out.setdefault(name, []).append(v)
+    return {k: sum(v) / len(v) for k, v in out.items()}
+
+
+def counters_summary(args) -> int:
+    """Turn rocprofv3 counter runs of the butterfly kernel and of the 1 GiB
+    copy into the record ``traffic_from_counters`` reads."""
+    kname = "butterfly_kernel"
+    copy = "copyBuffer"
+    fetch = _counter_means(args.fetch, kname)["FETCH_SIZE"]
+    write = _counter_means(args.write, kname)["WRITE_SIZE"]
+    copy_fetch = _counter_means(args.copy_fetch, copy)["FETCH_SIZE"]
+    copy_write = _counter_means(args.copy_write, copy)["WRITE_SIZE"]
+    copy_kib = (1 << 30) / 1024
+    f_scale, w_scale = copy_kib / copy_fetch, copy_kib / copy_write
+    rec = {
+        "kernel": "butterfly_kernel<64>", "workload": HEADLINE,
+        "kernel_source_sha1": kernel_source_hash(),
+        "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
+        "copy_1GiB_fetch_kib": copy_fetch, "copy_1GiB_write_kib": copy_write,
+        "fetch_scale": f_scale, "write_scale": w_scale,
+        "hbm_bytes_per_launch": 1024 * (fetch * f_scale + write * w_scale),
+    }
+    if args.hitmiss:
+        hm = _counter_means(args.hitmiss, kname)
+        rec["tcc_hit_per_dispatch"] = hm["TCC_HIT_sum"]
+        rec["tcc_miss_per_dispatch"] = hm["TCC_MISS_sum"]
+        rec["tcc_hit_rate"] = hm["TCC_HIT_sum"] / (hm["TCC_HIT_sum"] + hm["TCC_MISS_sum"])
+    with open(args.out, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+    print(json.dumps(rec, indent=1))
+    return 0
+
+
 def cpu_baseline(c, z_gpu, sample: int) -> dict:
     """The oracle, as it stands, on the first ``sample`` tokens."""
     import numpy as np
@@ -139,7 +190,7 @@ def main() -> int:
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--cpu-sample", type=int, default=1 << 22,
+    ap.add_argument("--cpu-sample", type=int, default=1 << 24,
                     help="tokens of the headline workload the oracle draws")
     ap.add_argument("--only", choices=["butterfly", "naive"], default=None,
                     help="time one kernel on one workload (for profiling)")
@@ -147,7 +198,17 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run plain 1 GiB device-to-device copies (the "
                          "reference for scaling HBM counters)")
+    ap.add_argument("--counters-summary", action="store_true",
+                    help="write the HBM-traffic record from rocprofv3 csv "
+                         "directories (--fetch, --write, --copy-fetch, "
+                         "--copy-write, optional --hitmiss) to --out")
+    for opt in ("--fetch", "--write", "--copy-fetch", "--copy-write",
+                "--hitmiss"):
+        ap.add_argument(opt, default=None)
+    ap.add_argument("--out", default=COUNTERS)
     args = ap.parse_args()
+    if args.counters_summary:
+        return counters_summary(args)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the draw has no multi-GPU path in this build.", file=sys.stderr)
