@@ -171,6 +171,19 @@ __device__ __forceinline__ float load_f32(rsrc_t r, uint32_t voff, uint32_t soff
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
+// Four consecutive floats per lane (one 16-byte buffer load).
+using f4 = float __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ f4 load_f32x4(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Sum of the four theta-phi products of a leaf of four topics, in topic order
+// (the products of topics 1..3 are fused multiply-adds onto the running sum).
+__device__ __forceinline__ float dot4(f4 t, f4 x) {
+  return __builtin_fmaf(t.w, x.w, __builtin_fmaf(t.z, x.z, __builtin_fmaf(t.y, x.y, t.x * x.x)));
+}
+
 // Value of `v` in lane (group base + k): uniform across the wave when W = 64.
 template <int W>
 __device__ __forceinline__ int group_value(int v, int k) {

@@ -10,16 +10,39 @@
 #include "butterfly.hpp"
 #include "lda_draw.h"
 
-// Largest block count K / W for which the rebuilt block's table is kept in
-// LDS (see lds_table_for).
+// Build-time tuning of the butterfly kernel (chosen by measurement on MI355X):
+//   LDA_LDS_TABLE_MAX_BLOCKS  largest K / W whose rebuilt table goes to LDS
+//                             (see lds_table_for);
+//   LDA_WAVES_PER_EU          wavefronts per SIMD the register budget targets;
+//   LDA_WAVES_PER_BLOCK       wavefronts per workgroup.
 #ifndef LDA_LDS_TABLE_MAX_BLOCKS
-#define LDA_LDS_TABLE_MAX_BLOCKS 4
+#define LDA_LDS_TABLE_MAX_BLOCKS 0
+#endif
+#ifndef LDA_WAVES_PER_EU
+#define LDA_WAVES_PER_EU 3
+#endif
+#ifndef LDA_WAVES_PER_BLOCK
+#define LDA_WAVES_PER_BLOCK 2
+#endif
+//   LDA_LEAF4_MAX_BLOCKS      use the four-topic-leaf kernel when K is a
+//                             multiple of 256 with at most this many 256-topic
+//                             blocks (0: never);
+//   LDA_LEAF4_WINDOW          tokens whose leaf loads are in flight at once.
+#ifndef LDA_LEAF4_MAX_BLOCKS
+#define LDA_LEAF4_MAX_BLOCKS 1
+#endif
+#ifndef LDA_LEAF4_WINDOW
+#define LDA_LEAF4_WINDOW 8
+#endif
+//   LDA_LEAF4_WAVES_PER_EU    wavefronts per SIMD for the four-topic kernel.
+#ifndef LDA_LEAF4_WAVES_PER_EU
+#define LDA_LEAF4_WAVES_PER_EU 3
 #endif
 
 namespace lda {
 namespace {
 
-constexpr int kWavesPerBlock = 4;
+constexpr int kWavesPerBlock = LDA_WAVES_PER_BLOCK;
 constexpr int kBlockThreads = kWavesPerBlock * kWave;
 
 // ---------------------------------------------------------------------------
@@ -72,6 +95,8 @@ struct Wave {
   int mode;             // ThetaMode, uniform
   int kb;               // kTwoDocs: wave lanes below kb are in the first doc
   uint32_t th_off0, th_off1;  // theta row offsets of the first / last doc
+  uint32_t ph_lane;           // phi row offset of this lane's own token
+  uint32_t th_lane;           // theta row offset of this lane's own token
 };
 
 // Keep a uniform value opaque to the optimiser, so that work depending on it
@@ -227,9 +252,11 @@ __device__ __forceinline__ void load_tile_blocks(const Wave<W, SMALL> &w, float 
   const uint32_t v0 = (uint32_t)(w.R + w.r) * 4u;
 #pragma unroll
   for (int k = 0; k < W; ++k) {
+    // row offsets of token k from the lane that holds it
     const uint32_t boff = (uint32_t)group_value<W>(blk, k) * (W * 4u);
-    a[k] = load_row<W>(w.th_rs, v0, theta_row(w, k) + boff) *
-           load_row<W>(w.ph_rs, v0, phi_row(w, w.wp, k) + boff);
+    const uint32_t toff = (uint32_t)group_value<W>((int)w.th_lane, k);
+    const uint32_t poff = (uint32_t)group_value<W>((int)w.ph_lane, k);
+    a[k] = load_row<W>(w.th_rs, v0, toff + boff) * load_row<W>(w.ph_rs, v0, poff + boff);
   }
 }
 
@@ -238,7 +265,7 @@ __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
                                           const float *phi, uint32_t theta_bytes,
                                           uint32_t phi_bytes, const int32_t *doc_id,
                                           const int32_t *word_id, int64_t t0, int last,
-                                          int K, int lane, int doc) {
+                                          int K, int lane, int doc, int word) {
   w.th_rs = make_rsrc(theta, theta_bytes);
   w.ph_rs = make_rsrc(phi, phi_bytes);
   w.wp = word_id + t0;
@@ -265,17 +292,20 @@ __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
   }
   w.th_off0 = (uint32_t)d0 * w.row_bytes;
   w.th_off1 = (uint32_t)d1 * w.row_bytes;
+  w.ph_lane = (uint32_t)word * w.row_bytes;
+  w.th_lane = (uint32_t)doc * w.row_bytes;
 }
 
 
 // In-block search of Algorithm 10.  `low` and `high` are the full prefixes
 // before and at the end of the block; a[0..W-2] is this lane's column of the
 // rebuilt block (or, with LDS_TABLE, the rows are in `table`, row d at
-// table[d * 64 + lane]).  Returns the offset within the block.
+// table[d * 64 + lane]).  Returns the offset within the block and leaves in
+// low / high the prefixes before and after that entry.
 template <int W, bool LDS_TABLE>
 __device__ __forceinline__ int inblock_search(const float (&a)[W], const float *table,
-                                              int r, int gbase, float stop, float low,
-                                              float high) {
+                                              int r, int gbase, float stop, float &low,
+                                              float &high) {
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   int flip = 0;
 #pragma unroll
@@ -331,7 +361,7 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
 //   pass over phi).
 // In-block search (Algorithm 10) and the remnant fallback of Algorithm 9.
 template <int W, bool LDS_TABLE, bool SMALL>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(3)))
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi,
     const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
@@ -359,7 +389,7 @@ void butterfly_kernel(
   const int NB = K >> LOG2W;
   Wave<W, SMALL> w;
   init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
-                      lane, doc);
+                      lane, doc, word);
   const int R = w.R;
   float *region = lds + wave * region_rows(NB, W, LDS_TABLE) * kWave;
 
@@ -442,6 +472,217 @@ void butterfly_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Butterfly kernel with leaves of four topics (K a multiple of 256).
+//
+// Lane l of a wavefront reads topics [4l, 4l + 4) of a 256-topic block with
+// one 16-byte load per token, so a block takes 64 loads instead of 256.  The
+// lane first sums its four products (dot4); the 64 lanes then combine these
+// leaf sums exactly as the W = 64 kernel combines single products: a
+// reduce-scatter for the sweep's block totals, the paper's butterfly for the
+// chosen block, and Algorithm 10's search, which now finds the leaf.  The
+// final step scans the four products of that leaf (lane-private loads).
+// Loads go through a rolling window of C tokens: the load of token k + C is
+// issued as soon as token k's leaf sum is formed.
+constexpr int kLeaf = 4;
+constexpr int kBlock4 = kWave * kLeaf;  // topics per block
+
+// Tokens of a sweep block are taken in pair order 0, 32, 1, 33, ...: as soon
+// as tokens k and k + 32 have their leaf sums, the first reduce-scatter stage
+// (lanes l and l xor 32) combines them, so only 32 partial sums stay live.
+__device__ __host__ constexpr int pair_token(int i) { return (i >> 1) + ((i & 1) << 5); }
+
+// Sweep step for one 256-topic block in one- or two-document waves.  win[]
+// holds (or awaits) the phi leaves of the first C tokens in pair order of
+// block `blk`; th[] the theta leaves of the first / last document.  With
+// PREFETCH the window and thn[] are refilled with block `next` as the block
+// drains, and th[] takes thn[] at the end.  Returns this lane's token total
+// over the block.
+template <bool SMALL, int C, bool TWO, bool PREFETCH>
+__device__ __forceinline__ float sweep4_block(const Wave<kWave, SMALL> &w, const int32_t *wp,
+                                              f4 (&win)[C], f4 (&th)[2], f4 (&thn)[2],
+                                              int blk, int next) {
+  // the slot of token i is i % C in every block, so the refill for the next
+  // block's token i + C - 64 lands in the slot that token reads
+  static_assert(kWave % C == 0, "the window size must divide 64");
+  const uint32_t vcur = (uint32_t)(blk * kBlock4 + kLeaf * w.r) * 4u;
+  const uint32_t vnext = (uint32_t)(next * kBlock4 + kLeaf * w.r) * 4u;
+  const int kb = TWO ? launder_int(w.kb) : kWave;
+  float s[kWave / 2];
+  float lo = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kWave; ++i) {
+    const int k = pair_token(i);
+    const float v = dot4((!TWO || k < kb) ? th[0] : th[1], win[i % C]);
+    if (i & 1) {
+      float hi = v;
+      half_swap<32>(lo, hi);
+      s[k - 32] = lo + hi;
+    } else {
+      lo = v;
+    }
+    if (i + C < kWave) {
+      win[i % C] = load_f32x4(w.ph_rs, vcur, __builtin_amdgcn_readlane(w.ph_lane, pair_token(i + C)));
+    } else if constexpr (PREFETCH) {
+      if (i + C == kWave) {
+        thn[0] = load_f32x4(w.th_rs, vnext, w.th_off0);
+        if constexpr (TWO) thn[1] = load_f32x4(w.th_rs, vnext, w.th_off1);
+      }
+      win[i % C] = load_f32x4(w.ph_rs, vnext,
+                              __builtin_amdgcn_readlane(w.ph_lane, pair_token(i + C - kWave)));
+    }
+    // keep the window rolling: no load is hoisted past this point (hoisting
+    // them all would need 4 registers per token of the block)
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  reduce_stage<kWave / 2, 16>(s);
+  reduce_stage<kWave / 2, 8>(s);
+  reduce_stage<kWave / 2, 4>(s);
+  reduce_stage<kWave / 2, 2>(s);
+  reduce_stage<kWave / 2, 1>(s);
+  if constexpr (PREFETCH) {
+    th[0] = thn[0];
+    if constexpr (TWO) th[1] = thn[1];
+  }
+  return s[0];
+}
+
+// The whole sweep (NB >= 2 blocks) of a one- or two-document wave: prologue
+// loads, blocks 0..NB-2 with prefetch of the next block, the last block
+// without.  The running prefix at block b's end goes to prefix[b * 64].
+template <bool SMALL, int C, bool TWO>
+__device__ __forceinline__ float sweep4(const Wave<kWave, SMALL> &w, int NB, float *prefix) {
+  f4 win[C], th[2], thn[2];
+  const uint32_t v0 = (uint32_t)(kLeaf * w.r) * 4u;
+  th[0] = load_f32x4(w.th_rs, v0, w.th_off0);
+  th[1] = TWO ? load_f32x4(w.th_rs, v0, w.th_off1) : th[0];
+#pragma unroll
+  for (int i = 0; i < C; ++i)
+    win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, pair_token(i)));
+  float sum = 0.0f;
+  for (int b = 0; b < NB - 1; ++b) {
+    sum += sweep4_block<SMALL, C, TWO, true>(w, launder(w.wp), win, th, thn, b, b + 1);
+    prefix[b * kWave] = sum;
+  }
+  sum += sweep4_block<SMALL, C, TWO, false>(w, w.wp, win, th, thn, NB - 1, 0);
+  prefix[(NB - 1) * kWave] = sum;
+  return sum;
+}
+
+// Tile of leaf sums in which token k reads block blk_k of its own document and
+// word (this lane's `blk` is its own token's block; any documents).
+template <bool SMALL, int C>
+__device__ __forceinline__ void leaf_tile(const Wave<kWave, SMALL> &w, const int32_t *wp,
+                                          int blk, float (&s)[kWave]) {
+  const uint32_t v0 = (uint32_t)(kLeaf * w.r) * 4u;
+  f4 wt[C], wph[C];
+  // row offsets of token k come from lane k (readlane: no scalar-load wait)
+  auto issue = [&](int k, f4 &t, f4 &p) {
+    const uint32_t boff = (uint32_t)__builtin_amdgcn_readlane(blk, k) * (kBlock4 * 4u);
+    t = load_f32x4(w.th_rs, v0, __builtin_amdgcn_readlane(w.th_lane, k) + boff);
+    p = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, k) + boff);
+  };
+#pragma unroll
+  for (int k = 0; k < C; ++k) issue(k, wt[k], wph[k]);
+#pragma unroll
+  for (int k = 0; k < kWave; ++k) {
+    s[k] = dot4(wt[k % C], wph[k % C]);
+    if (k + C < kWave) issue(k + C, wt[k % C], wph[k % C]);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// Linear scan of a leaf: the first of its four topics whose prefix exceeds
+// stop, starting from `low`, the prefix before the leaf (3 if none does).
+__device__ __forceinline__ int leaf_scan(rsrc_t th_rs, rsrc_t ph_rs, uint32_t th_row,
+                                         uint32_t ph_row, int base, float low, float stop) {
+  const uint32_t voff = (uint32_t)base * 4u;
+  const f4 t = load_f32x4(th_rs, th_row + voff, 0);
+  const f4 x = load_f32x4(ph_rs, ph_row + voff, 0);
+  const float c0 = prefix_step(low, t.x, x.x);
+  const float c1 = prefix_step(c0, t.y, x.y);
+  const float c2 = prefix_step(c1, t.z, x.z);
+  return stop < c0 ? 0 : stop < c1 ? 1 : stop < c2 ? 2 : 3;
+}
+
+template <bool SMALL, int C>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_LEAF4_WAVES_PER_EU)))
+void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                       const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
+                       const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
+                       uint32_t theta_bytes, uint32_t phi_bytes) {
+  extern __shared__ float lds[];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
+  if (first >= N) return;  // whole wavefront past the end
+  // Token window as in butterfly_kernel.
+  const int64_t t0 = SMALL ? 0 : (first + kWave <= N ? first : N - kWave);
+  const int last = SMALL ? (int)(N - 1) : kWave - 1;
+  const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
+  const bool store = SMALL ? lane < N : t0 + lane >= first;
+
+  const int doc = doc_id[n];
+  const int word = word_id[n];
+  const float un = u[n];
+  const int NB = K / kBlock4;
+  Wave<kWave, SMALL> w;
+  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+                          lane, doc, word);
+  float *region = lds + wave * NB * kWave;
+
+  float s[kWave];
+  float sum = 0.0f, stop, low, high;
+  int blk;
+  if (NB == 1) {
+    blk = 0;
+    leaf_tile<SMALL, C / 2>(w, w.wp, 0, s);
+    butterfly_block<kWave>(s, w.r, NoStore{});
+    sum = s[kWave - 1];
+    stop = sum * un;
+    low = 0.0f;
+    high = sum;
+  } else {
+    // Sweep over the blocks.
+    if (w.mode == kAnyDocs) {
+      for (int b = 0; b < NB; ++b) {
+        leaf_tile<SMALL, C / 2>(w, launder(w.wp), b, s);
+        reduce_stage<kWave, 32>(s);
+        reduce_rest<kWave, SMALL, 16, false>(w, w.wp, s, 0);
+        sum += s[0];
+        region[b * kWave + lane] = sum;
+      }
+    } else if (w.mode == kOneDoc) {
+      sum = sweep4<SMALL, C, false>(w, NB, region + lane);
+    } else {
+      sum = sweep4<SMALL, C, true>(w, NB, region + lane);
+    }
+    stop = sum * un;
+    // Algorithm 9: binary search over the last row of each block.
+    int lo = 0, hi = NB - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (stop < region[mid * kWave + lane])
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    blk = lo;
+    low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
+    high = region[lo * kWave + lane];
+    // Rebuild every token's chosen block as leaf sums and combine them with
+    // the paper's butterfly.
+    leaf_tile<SMALL, C / 2>(w, w.wp, blk, s);
+    butterfly_block<kWave>(s, w.r, NoStore{});
+  }
+  // Algorithm 10 over the leaves, then the four topics of the chosen leaf.
+  const int leaf = inblock_search<kWave, false>(s, nullptr, w.r, 0, stop, low, high);
+  const int base = blk * kBlock4 + kLeaf * leaf;
+  const int j = base + leaf_scan(w.th_rs, w.ph_rs, (uint32_t)doc * w.row_bytes,
+                                 (uint32_t)word * w.row_bytes, base, low, stop);
+  if (store) z[n] = j;
+}
+
+// ---------------------------------------------------------------------------
 // Table dump: the per-lane table p[K] of Algorithm 7 for every token, built
 // with the same tile loads and butterfly as the draw's rebuild step.
 template <int W, bool SMALL>
@@ -463,7 +704,7 @@ __global__ __launch_bounds__(kBlockThreads) void table_kernel(
   const int doc = doc_id[n];
   Wave<W, true> w;
   init_wave<W, true>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
-                     lane, doc);
+                     lane, doc, word_id[n]);
   const int R = w.R;
   const int NB = K / W;
   float *out = table + n * (int64_t)K;
@@ -516,10 +757,15 @@ int finish_launch() {
 
 int width_for(int32_t K) { return K >= 64 ? 64 : 32; }
 
-// The rebuilt block's table goes to LDS when the block search is short
-// (few blocks); otherwise it stays in registers and the search-assist loop
-// moves it, which keeps the LDS footprint to the block-end prefixes.
-bool lds_table_for(int32_t K) { return K / width_for(K) <= LDA_LDS_TABLE_MAX_BLOCKS; }
+// The rebuilt block's table goes to LDS only for block counts up to
+// LDA_LDS_TABLE_MAX_BLOCKS.  Measured on MI355X, the register table searched
+// with the search-assist shuffle loop is faster at every K (the LDS table
+// costs 16 KiB per wavefront and with it occupancy), so the default is 0 and
+// the LDS variant is kept for comparison builds.
+bool lds_table_for(int32_t K) {
+  const int nb = K / width_for(K);
+  return nb >= 1 && nb <= LDA_LDS_TABLE_MAX_BLOCKS;
+}
 
 dim3 wave_grid(int64_t N) {
   const int64_t waves = (N + kWave - 1) / kWave;
@@ -532,6 +778,21 @@ void launch_naive(const float *theta, const float *phi, const int32_t *d,
                   int32_t K, hipStream_t s) {
   const dim3 grid((unsigned)((N + 255) / 256));
   naive_kernel<KMAX><<<grid, 256, 0, s>>>(theta, phi, d, w, u, z, N, K);
+}
+
+template <int C>
+void launch_butterfly4(const float *theta, const float *phi, const int32_t *d,
+                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
+                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  const size_t lds = (size_t)kWavesPerBlock * (K / kBlock4) * kWave * sizeof(float);
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  if (N < kWave)
+    butterfly4_kernel<true, C><<<wave_grid(N), kBlockThreads, lds, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+  else
+    butterfly4_kernel<false, C><<<wave_grid(N), kBlockThreads, lds, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
 template <int W, bool LDS_TABLE>
@@ -581,6 +842,10 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
+    launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
+    return finish_launch();
+  }
   const bool lt = lds_table_for(K);
   if (width_for(K) == 64) {
     if (lt)

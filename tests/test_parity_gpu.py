@@ -79,6 +79,13 @@ SHAPES = [
     (64 * 17 + 9, 60, 500, 1000, "sequential"),
     (64 * 17 + 9, 60, 500, 2047, "shuffled"),
     (64 * 5 + 3, 20, 200, 4096, "sequential"),
+    # K a multiple of 256: the four-topic-leaf kernel
+    (1, 1, 7, 256, "sequential"),
+    (63, 5, 50, 512, "shuffled"),
+    (65, 5, 50, 768, "sequential"),
+    (64 * 7 + 5, 3, 90, 1280, "sequential"),   # waves spanning two documents
+    (64 * 9, 9, 100, 2304, "single"),
+    (64 * 9 + 33, 40, 100, 512, "shuffled"),
 ]
 
 
