@@ -263,6 +263,7 @@ def main() -> int:
 
     wall = head["wall_s"]
     value = c.N * args.steps / wall
+    traffic = traffic_from_counters()
     out = {
         "metric": METRIC,
         "value": value,
@@ -284,8 +285,14 @@ def main() -> int:
             "peak": PEAK_HBM_GBPS,
             "unit": "GB/s",
             "frac": head["alg_GBps"] / PEAK_HBM_GBPS,
-            "traffic": traffic_from_counters(),
+            "traffic": traffic,
         },
+        # the counted bytes that leave L2 (FETCH_SIZE + WRITE_SIZE, scaled by
+        # a plain copy) per launch, over the measured launch time
+        "hbm_traffic_GBps": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9
+                             if traffic else None),
+        "hbm_traffic_frac": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9 /
+                             PEAK_HBM_GBPS if traffic else None),
         "cpu_baseline": cpu_baseline(c, z_head, args.cpu_sample),
         "results": results,
         "kernel_source_sha1": kernel_source_hash(),
