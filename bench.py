@@ -185,6 +185,26 @@ def cpu_baseline(c, z_gpu, sample: int) -> dict:
     }
 
 
+def k_sweep(args) -> int:
+    """Kernel time of the naive and butterfly draws at the paper's topic
+    counts, on the synthetic corpus shaped like its evaluation corpus."""
+    import torch
+    from paper_1505_03851_amd.inputs import WIKI_K, make_corpus, wiki_shaped
+    for K in WIKI_K:
+        c = make_corpus(wiki_shaped(K))
+        dev = upload(c)
+        rec = {"workload": c.name, "K": K, "N": c.N}
+        for kernel in ("naive", "butterfly"):
+            r = measure(c.name, c, dev, kernel, args.steps, args.warmup)
+            rec[kernel + "_ms"] = r["ms_per_launch"]
+            rec[kernel + "_draws_per_s"] = r["draws_per_s"]
+        rec["speedup"] = rec["naive_ms"] / rec["butterfly_ms"]
+        print(json.dumps(rec), flush=True)
+        del dev
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -198,6 +218,10 @@ def main() -> int:
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run plain 1 GiB device-to-device copies (the "
                          "reference for scaling HBM counters)")
+    ap.add_argument("--k-sweep", action="store_true",
+                    help="naive vs butterfly over K = 16, 48, ..., 240 on the "
+                         "corpus shaped like the paper's evaluation corpus; one "
+                         "JSON line per K")
     ap.add_argument("--counters-summary", action="store_true",
                     help="write the HBM-traffic record from rocprofv3 csv "
                          "directories (--fetch, --write, --copy-fetch, "
@@ -233,6 +257,9 @@ def main() -> int:
         print(json.dumps({"copy_bytes_read": 4 * n, "copy_bytes_written": 4 * n,
                           "dispatches": 3}), flush=True)
         return 0
+
+    if args.k_sweep:
+        return k_sweep(args)
 
     if args.only:
         c = make_corpus(args.workload)

@@ -203,25 +203,11 @@ __device__ __forceinline__ int group_value(int v, int k) {
 // theta load per token).
 enum ThetaMode : int { kOneDoc = 0, kTwoDocs = 1, kAnyDocs = 2 };
 
-// One step of the untransposed running sum of the remnant (and of the naive
-// kernel): sum + theta * phi.  Written once so that every recomputation of a
-// remnant prefix rounds identically.
+// One step of an untransposed running sum (the naive kernel, the remnant of
+// the table dump, the scan of a leaf): sum + theta * phi.
 __device__ __forceinline__ float prefix_step(float sum, float th, float ph) {
   return __builtin_fmaf(th, ph, sum);
 }
 
-// Linear search of the remnant (Algorithm 9's fallback, Algorithm 2's loop):
-// recompute the prefix of topics 0..R-1 and return the first j with
-// stop < prefix_j, or `none` if there is no such j.
-__device__ __forceinline__ int remnant_search(const float *__restrict__ th_row,
-                                              const float *__restrict__ ph_row,
-                                              int R, float stop, int none) {
-  float s = 0.0f;
-  for (int j = 0; j < R; ++j) {
-    s = prefix_step(s, th_row[j], ph_row[j]);
-    if (stop < s) return j;
-  }
-  return none;
-}
 
 }  // namespace lda

@@ -89,6 +89,9 @@ struct Wave {
   int last;             // SMALL: index in the window of token N - 1
   uint32_t row_bytes;   // 4 * K
   int R;                // remnant topics (K mod W)
+  int c0;               // first topic of block 0: R - W if R > 0 (the remnant is
+                        // block 0, padded at its front with W - R empty
+                        // topics), else 0
   int r;                // lane within its group of W
   int gbase;            // first lane of the group
   int doc;              // this lane's document
@@ -157,11 +160,24 @@ __device__ __forceinline__ float load_row(rsrc_t rs, uint32_t voff, uint32_t row
     return load_f32(rs, voff + row, 0);
 }
 
+// This lane's topic in block `blk` (negative in the padding of block 0), and
+// the byte offset used to load it (padding lanes read topic 0; their theta
+// factor is replaced by zero where it is used).
+template <int W, bool SMALL>
+__device__ __forceinline__ int topic_of(const Wave<W, SMALL> &w, int blk) {
+  return w.c0 + blk * W + w.r;
+}
+template <int W, bool SMALL>
+__device__ __forceinline__ uint32_t col_bytes(const Wave<W, SMALL> &w, int blk) {
+  const int t = topic_of(w, blk);
+  return (uint32_t)(t > 0 ? t : 0) * 4u;
+}
+
 // Issue the phi loads of tokens [LO, HI) of block `blk` into a[LO..HI-1].
 template <int W, bool SMALL, int LO, int HI>
 __device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t *wp,
                                           float (&a)[W], int blk) {
-  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+  const uint32_t voff = col_bytes(w, blk);
 #pragma unroll
   for (int k = LO; k < HI; ++k) a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
 }
@@ -170,7 +186,7 @@ __device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t
 template <int W, bool SMALL>
 __device__ __forceinline__ void issue_theta(const Wave<W, SMALL> &w, int blk, float &th0,
                                             float &th1) {
-  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+  const uint32_t voff = col_bytes(w, blk);
   th0 = load_f32(w.th_rs, voff, w.th_off0);
   if (w.mode == kTwoDocs) th1 = load_f32(w.th_rs, voff, w.th_off1);
 }
@@ -196,13 +212,15 @@ __device__ __forceinline__ void reduce_rest(const Wave<W, SMALL> &w, const int32
 template <int W, bool SMALL, bool PREFETCH>
 __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int32_t *wp,
                                              float (&a)[W], float &th0, float &th1,
-                                             int next) {
+                                             int cur, int next) {
   constexpr int B = W / 2;
+  // padding topics of block 0 weigh nothing
+  const bool real = topic_of(w, cur) >= 0;
   if (w.mode == kOneDoc) {
     // First stage fused with the theta factor: after the half exchange the
     // two values of a pair sit at topics of the lower and upper half-group,
     // whose theta values one more exchange of th0 provides.
-    float tA = th0, tB = th0;
+    float tA = real ? th0 : 0.0f, tB = tA;
     half_swap<B>(tA, tB);
     if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
 #pragma unroll
@@ -215,8 +233,9 @@ __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int3
     // laundered so that the per-token choices are made here, not hoisted out
     // of the block loop into scalar registers.)
     const int kb = launder_int(w.kb);
+    const float t0 = real ? th0 : 0.0f, t1 = real ? th1 : 0.0f;
 #pragma unroll
-    for (int k = 0; k < W; ++k) a[k] *= (w.gbase + k < kb) ? th0 : th1;
+    for (int k = 0; k < W; ++k) a[k] *= (w.gbase + k < kb) ? t0 : t1;
     if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
     reduce_stage<W, B>(a);
   }
@@ -233,10 +252,11 @@ template <int W, bool SMALL>
 __device__ __forceinline__ float sweep_block_any(const Wave<W, SMALL> &w, const int32_t *wp,
                                                  int blk) {
   float a[W];
-  const uint32_t voff = (uint32_t)(w.R + blk * W + w.r) * 4u;
+  const uint32_t voff = col_bytes(w, blk);
+  const bool real = topic_of(w, blk) >= 0;
 #pragma unroll
   for (int k = 0; k < W; ++k)
-    a[k] = load_row<W>(w.th_rs, voff, theta_row(w, k)) *
+    a[k] = (real ? load_row<W>(w.th_rs, voff, theta_row(w, k)) : 0.0f) *
            load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
   reduce_stage<W, W / 2>(a);
   reduce_rest<W, SMALL, W / 4, false>(w, wp, a, 0);
@@ -246,17 +266,21 @@ __device__ __forceinline__ float sweep_block_any(const Wave<W, SMALL> &w, const 
 // Transposed tile in which token k of the group contributes block blk_k
 // (this lane's `blk` is its own token's block): a[k] = theta[doc_k][c_k] *
 // phi[word_k][c_k], c_k = R + blk_k * W + r.
-template <int W, bool SMALL>
+// Topic of lane r for token k is first + blk_k * W + r; with PADDED, topics
+// below 0 (the front padding of block 0) contribute 0.
+template <int W, bool SMALL, bool PADDED>
 __device__ __forceinline__ void load_tile_blocks(const Wave<W, SMALL> &w, float (&a)[W],
-                                                 int blk) {
-  const uint32_t v0 = (uint32_t)(w.R + w.r) * 4u;
+                                                 int blk, int first) {
 #pragma unroll
   for (int k = 0; k < W; ++k) {
     // row offsets of token k from the lane that holds it
-    const uint32_t boff = (uint32_t)group_value<W>(blk, k) * (W * 4u);
+    const int bk = group_value<W>(blk, k);
+    const int t = first + bk * W + w.r;
+    const uint32_t voff = (uint32_t)(PADDED && t < 0 ? 0 : t) * 4u;
     const uint32_t toff = (uint32_t)group_value<W>((int)w.th_lane, k);
     const uint32_t poff = (uint32_t)group_value<W>((int)w.ph_lane, k);
-    a[k] = load_row<W>(w.th_rs, v0, toff + boff) * load_row<W>(w.ph_rs, v0, poff + boff);
+    const float th = load_row<W>(w.th_rs, voff, toff);
+    a[k] = (PADDED && t < 0 ? 0.0f : th) * load_row<W>(w.ph_rs, voff, poff);
   }
 }
 
@@ -273,6 +297,7 @@ __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
   w.last = last;
   w.row_bytes = (uint32_t)K * 4u;
   w.R = K & (W - 1);
+  w.c0 = w.R ? w.R - W : 0;
   w.r = lane & (W - 1);
   w.gbase = lane & ~(W - 1);
   w.doc = doc;
@@ -386,88 +411,81 @@ void butterfly_kernel(
   const int doc = doc_id[n];
   const int word = word_id[n];
   const float un = u[n];
-  const int NB = K >> LOG2W;
+  // blocks of W topics; a remnant of K mod W topics becomes block 0, padded
+  // at its front with empty topics
+  const int NB = (K + W - 1) >> LOG2W;
   Wave<W, SMALL> w;
   init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
                       lane, doc, word);
-  const int R = w.R;
   float *region = lds + wave * region_rows(NB, W, LDS_TABLE) * kWave;
 
-  // Remnant.
-  const float *th_row = theta + (int64_t)doc * K;
-  const float *ph_row = phi + (int64_t)word * K;
-  float sum = 0.0f;
-  for (int j = 0; j < R; ++j) sum = prefix_step(sum, th_row[j], ph_row[j]);
-  const float p_rem = sum;
-
-  int j;
-  if (NB == 0) {
-    j = remnant_search(th_row, ph_row, R, sum * un, K - 1);
+  float a[W];
+  float sum, stop, low, high;
+  int blk;
+  if (NB == 1) {
+    // One block: its table is built once and searched directly.
+    blk = 0;
+    load_tile_blocks<W, SMALL, true>(w, a, 0, w.c0);
+    if constexpr (LDS_TABLE)
+      butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+    else
+      butterfly_block<W>(a, w.r, NoStore{});
+    sum = a[W - 1];
+    stop = sum * un;
+    low = 0.0f;
+    high = sum;
   } else {
-    float a[W];
-    float stop, low, high;
-    int blk;
-    if (NB == 1) {
-      // One block: its table is built once and searched directly.
-      blk = 0;
-      load_tile_blocks(w, a, 0);
-      if constexpr (LDS_TABLE)
-        butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
-      else
-        butterfly_block<W>(a, w.r, NoStore{});
-      sum += a[W - 1];
-      stop = sum * un;
-      low = p_rem;
-      high = sum;
+    // Sweep over the blocks.
+    sum = 0.0f;
+    if (w.mode == kAnyDocs) {
+      for (int b = 0; b < NB; ++b) {
+        sum += sweep_block_any(w, launder(w.wp), b);
+        region[b * kWave + lane] = sum;
+      }
     } else {
-      // Sweep over the blocks.
-      if (w.mode == kAnyDocs) {
-        for (int b = 0; b < NB; ++b) {
-          sum += sweep_block_any(w, launder(w.wp), b);
-          region[b * kWave + lane] = sum;
-        }
-      } else {
-        float th0 = 0.0f, th1 = 0.0f;
-        issue_theta(w, 0, th0, th1);
-        issue_phi<W, SMALL, 0, W>(w, w.wp, a, 0);
-        for (int b = 0; b < NB - 1; ++b) {
-          sum += sweep_block<W, SMALL, true>(w, launder(w.wp), a, th0, th1, b + 1);
-          region[b * kWave + lane] = sum;
-        }
-        sum += sweep_block<W, SMALL, false>(w, w.wp, a, th0, th1, 0);
-        region[(NB - 1) * kWave + lane] = sum;
+      float th0 = 0.0f, th1 = 0.0f;
+      issue_theta(w, 0, th0, th1);
+      issue_phi<W, SMALL, 0, W>(w, w.wp, a, 0);
+      for (int b = 0; b < NB - 1; ++b) {
+        sum += sweep_block<W, SMALL, true>(w, launder(w.wp), a, th0, th1, b, b + 1);
+        region[b * kWave + lane] = sum;
       }
-      stop = sum * un;
-      // Algorithm 9: binary search over the last row of each block.
-      int lo = 0, hi = NB - 1;
-      while (lo < hi) {
-        const int mid = (lo + hi) >> 1;
-        if (stop < region[mid * kWave + lane])
-          hi = mid;
-        else
-          lo = mid + 1;
-      }
-      blk = lo;
-      low = lo > 0 ? region[(lo - 1) * kWave + lane] : p_rem;
-      high = region[lo * kWave + lane];
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-      // Rebuild every token's chosen block.
-      load_tile_blocks(w, a, blk);
-      if constexpr (LDS_TABLE)
-        butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+      sum += sweep_block<W, SMALL, false>(w, w.wp, a, th0, th1, NB - 1, 0);
+      region[(NB - 1) * kWave + lane] = sum;
+    }
+    stop = sum * un;
+    // Algorithm 9: binary search over the last row of each block.
+    int lo = 0, hi = NB - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (stop < region[mid * kWave + lane])
+        hi = mid;
       else
-        butterfly_block<W>(a, w.r, NoStore{});
+        lo = mid + 1;
     }
-    if constexpr (LDS_TABLE) {
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-      __builtin_amdgcn_wave_barrier();
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    }
-    j = R + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
-    if (blk == 0 && R > 0 && stop < p_rem) j = remnant_search(th_row, ph_row, R, stop, K - 1);
+    blk = lo;
+    low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
+    high = region[lo * kWave + lane];
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    // Rebuild every token's chosen block.
+    load_tile_blocks<W, SMALL, true>(w, a, blk, w.c0);
+    if constexpr (LDS_TABLE)
+      butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+    else
+      butterfly_block<W>(a, w.r, NoStore{});
   }
+  if constexpr (LDS_TABLE) {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // Algorithm 10.  Empty topics of block 0 are never chosen: their prefix
+  // equals the prefix before them, which is never above stop >= 0, except
+  // when S = 0, where every comparison fails and the result is K - 1.
+  const int j =
+      w.c0 + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
   if (store) z[n] = j;
 }
 
@@ -718,7 +736,7 @@ __global__ __launch_bounds__(kBlockThreads) void table_kernel(
   }
   for (int b = 0; b < NB; ++b) {
     float a[W];
-    load_tile_blocks(w, a, b);
+    load_tile_blocks<W, true, false>(w, a, b, R);
     butterfly_block<W>(a, w.r, RowStore{out + R + b * W, 1, store});
     sum += a[W - 1];
     if (store) out[R + b * W + W - 1] = sum;
@@ -763,8 +781,8 @@ int width_for(int32_t K) { return K >= 64 ? 64 : 32; }
 // costs 16 KiB per wavefront and with it occupancy), so the default is 0 and
 // the LDS variant is kept for comparison builds.
 bool lds_table_for(int32_t K) {
-  const int nb = K / width_for(K);
-  return nb >= 1 && nb <= LDA_LDS_TABLE_MAX_BLOCKS;
+  const int nb = (K + width_for(K) - 1) / width_for(K);
+  return nb <= LDA_LDS_TABLE_MAX_BLOCKS;
 }
 
 dim3 wave_grid(int64_t N) {
@@ -799,7 +817,8 @@ template <int W, bool LDS_TABLE>
 void launch_butterfly(const float *theta, const float *phi, const int32_t *d,
                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
-  const size_t lds = (size_t)kWavesPerBlock * region_rows(K / W, W, LDS_TABLE) *
+  const int nb = (K + W - 1) / W;  // blocks, the remnant included
+  const size_t lds = (size_t)kWavesPerBlock * region_rows(nb, W, LDS_TABLE) *
                      kWave * sizeof(float);
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);

@@ -48,11 +48,18 @@ class CorpusConfig:
     zipf_s: float
     doc_len: int | None = None
     poisson_mean: float | None = None
+    # lognormal document lengths rescaled to exactly `total_tokens` tokens and
+    # clipped to [1, max_doc_len] (used for the corpus shaped like the paper's)
+    lognormal_sigma: float | None = None
+    total_tokens: int | None = None
+    max_doc_len: int | None = None
 
     @property
     def nominal_tokens(self) -> int:
         if self.doc_len is not None:
             return self.M * self.doc_len
+        if self.total_tokens is not None:
+            return self.total_tokens
         return int(round(self.M * self.poisson_mean))
 
 
@@ -100,6 +107,47 @@ class Corpus:
     @property
     def K(self) -> int:
         return int(self.theta.shape[1])
+
+
+# Corpus shaped like the one the paper's evaluation (Section 5) describes:
+# 43,556 documents, 37,286 distinct words, 3,072,662 tokens, at most 307 tokens
+# per document.  Only these four counts come from the paper; the length
+# distribution (lognormal, sigma 0.8), the Zipf exponent and the Dirichlet
+# parameters are this generator's assumptions.  No text of any corpus is used.
+WIKI_SHAPE = dict(M=43_556, V=37_286, total_tokens=3_072_662, max_doc_len=307,
+                  lognormal_sigma=0.8, zipf_s=1.0, alpha=0.1, beta=0.01)
+# K = 32 k + 16, 0 <= k <= 7: the topic counts of the paper's measurements.
+WIKI_K = tuple(32 * k + 16 for k in range(8))
+
+
+def wiki_shaped(K: int) -> CorpusConfig:
+    """The paper-shaped corpus at K topics (index 100 + K selects its seeds)."""
+    return CorpusConfig(f"wiki-shaped-K{K}", 100 + K, K=K, **WIKI_SHAPE)
+
+
+for _K in WIKI_K:
+    CONFIGS[f"wiki-shaped-K{_K}"] = wiki_shaped(_K)
+
+
+def _lognormal_lengths(seed, M: int, sigma: float, total: int,
+                       max_len: int) -> np.ndarray:
+    """M lengths in [1, max_len] summing to exactly `total`: lognormal draws
+    scaled to the target mean, clipped, then adjusted one token at a time on
+    the documents with room (deterministic given the seed)."""
+    g = np.random.Generator(np.random.PCG64(seed))
+    x = g.lognormal(0.0, sigma, size=M)
+    x *= total / x.sum()
+    n = np.clip(np.rint(x), 1, max_len).astype(np.int64)
+    order = g.permutation(M)
+    i = 0
+    while n.sum() != total:
+        j = order[i % M]
+        if n.sum() < total and n[j] < max_len:
+            n[j] += 1
+        elif n.sum() > total and n[j] > 1:
+            n[j] -= 1
+        i += 1
+    return n
 
 
 def _threads() -> int:
@@ -183,6 +231,9 @@ def make_corpus(cfg: CorpusConfig | str) -> Corpus:
     s_theta, s_phi, s_word, s_u, s_len = ss.spawn(5)
     if cfg.doc_len is not None:
         lengths = np.full(cfg.M, cfg.doc_len, dtype=np.int64)
+    elif cfg.lognormal_sigma is not None:
+        lengths = _lognormal_lengths(s_len, cfg.M, cfg.lognormal_sigma,
+                                     cfg.total_tokens, cfg.max_doc_len)
     else:
         g = np.random.Generator(np.random.PCG64(s_len))
         lengths = g.poisson(cfg.poisson_mean, size=cfg.M).astype(np.int64)

@@ -58,6 +58,17 @@ def test_config_full_size_sampled(name, kernel):
     _check(c, kernel, idx=idx)
 
 
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("K", [16, 80, 144, 240])
+def test_wiki_shaped_every_token(K, kernel):
+    """The corpus shaped like the paper's evaluation corpus (3.07M tokens,
+    documents of 1..307 tokens), at topic counts of the paper's measurements;
+    every K here has a remnant (K mod 64 = 16 or 48)."""
+    from paper_1505_03851_amd.inputs import wiki_shaped
+    c = corpus(wiki_shaped(K).name)
+    _check(c, kernel)
+
+
 SHAPES = [
     # (N, M, V, K, doc order)
     (1, 1, 7, 64, "sequential"),
