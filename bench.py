@@ -62,7 +62,8 @@ def time_kernel(kernel: str, dev, steps: int, warmup: int):
     the timed region, per-launch milliseconds from HIP events, z)."""
     import torch
     import paper_1505_03851_amd as lda
-    fn = {"butterfly": lda.draw_butterfly, "naive": lda.draw_naive}[kernel]
+    fn = {"butterfly": lda.draw_butterfly, "naive": lda.draw_naive,
+          "transposed": lda.draw_transposed}[kernel]
     stream = torch.cuda.current_stream()
     z = torch.empty_like(dev["doc_id"])
     args = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
@@ -194,11 +195,12 @@ def k_sweep(args) -> int:
         c = make_corpus(wiki_shaped(K))
         dev = upload(c)
         rec = {"workload": c.name, "K": K, "N": c.N}
-        for kernel in ("naive", "butterfly"):
+        for kernel in ("naive", "transposed", "butterfly"):
             r = measure(c.name, c, dev, kernel, args.steps, args.warmup)
             rec[kernel + "_ms"] = r["ms_per_launch"]
             rec[kernel + "_draws_per_s"] = r["draws_per_s"]
         rec["speedup"] = rec["naive_ms"] / rec["butterfly_ms"]
+        rec["speedup_vs_transposed"] = rec["transposed_ms"] / rec["butterfly_ms"]
         print(json.dumps(rec), flush=True)
         del dev
         torch.cuda.empty_cache()
@@ -212,7 +214,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-sample", type=int, default=1 << 24,
                     help="tokens of the headline workload the oracle draws")
-    ap.add_argument("--only", choices=["butterfly", "naive"], default=None,
+    ap.add_argument("--only", choices=["butterfly", "naive", "transposed"], default=None,
                     help="time one kernel on one workload (for profiling)")
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -272,7 +274,7 @@ def main() -> int:
     results = []
     c2 = make_corpus(SECOND)
     dev2 = upload(c2)
-    for k in ("butterfly", "naive"):
+    for k in ("butterfly", "transposed", "naive"):
         r = measure(SECOND, c2, dev2, k, max(args.steps, 20), args.warmup)
         r.pop("z")
         results.append(r)
@@ -284,6 +286,9 @@ def main() -> int:
     naive = measure(HEADLINE, c, dev, "naive", max(3, args.steps // 4), 1)
     naive.pop("z")
     results.append(naive)
+    tr = measure(HEADLINE, c, dev, "transposed", args.steps, args.warmup)
+    tr.pop("z")
+    results.append(tr)
     head = measure(HEADLINE, c, dev, "butterfly", args.steps, args.warmup)
     z_head = head.pop("z")
     results.append(head)

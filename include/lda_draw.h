@@ -100,6 +100,20 @@ int lda_draw_butterfly(const float *theta, const float *phi,
                        int32_t V, int32_t K, void *stream);
 
 /*
+ * Transposed-access draw (Algorithms 4, 5 and 6 with a binary search over
+ * block ends and a linear search of the chosen block, Section 3): the
+ * paper's design before the butterfly, kept for comparison.  The tile of W =
+ * 64 topics x 64 tokens is read with the same coalesced loads as
+ * lda_draw_butterfly, then transposed through LDS so that each lane sums its
+ * own token's products in topic order (16.6 KiB of LDS per wavefront).  Same
+ * arguments, layout, errors and result as lda_draw_butterfly.
+ */
+int lda_draw_transposed(const float *theta, const float *phi,
+                        const int32_t *doc_id, const int32_t *word_id,
+                        const float *u, int32_t *z, int64_t N, int32_t M,
+                        int32_t V, int32_t K, void *stream);
+
+/*
  * The butterfly-patterned tables themselves (Section 4, Fig. 1 right), for
  * inspection and tests.  table is a device float array [N][K]: row n is the
  * table p[K] that token n's lane holds in Algorithm 7 -- the remnant's full

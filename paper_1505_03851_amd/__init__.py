@@ -6,7 +6,7 @@ library through its C ABI (``include/lda_draw.h``).  The binding is imported
 on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 """
 
-_BINDING = ("draw_naive", "draw_butterfly", "butterfly_table",
+_BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "butterfly_table",
             "butterfly_width", "status_string", "version", "LdaError",
             "load", "MAX_K", "MAX_TABLE_BYTES", "STATUS")
 

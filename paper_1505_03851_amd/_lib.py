@@ -55,7 +55,7 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     P, I32, I64 = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64
     draw_args = [P, P, P, P, P, P, I64, I32, I32, I32, P]
-    for name in ("lda_draw_naive", "lda_draw_butterfly"):
+    for name in ("lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed"):
         getattr(lib, name).argtypes = draw_args
         getattr(lib, name).restype = ctypes.c_int
     lib.lda_butterfly_table.argtypes = [P, P, P, P, P, I64, I32, I32, I32, P]
@@ -161,6 +161,14 @@ def draw_butterfly(theta, phi, doc_id, word_id, u, out=None, stream=None,
                    validate: bool = False) -> torch.Tensor:
     """z[N] (int32) by the butterfly kernel (Algorithms 7-10)."""
     return _draw("lda_draw_butterfly", theta, phi, doc_id, word_id, u, out,
+                 stream, validate)
+
+
+def draw_transposed(theta, phi, doc_id, word_id, u, out=None, stream=None,
+                    validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the transposed-access kernel (Algorithms 4-6), the
+    paper's design before the butterfly, for comparison."""
+    return _draw("lda_draw_transposed", theta, phi, doc_id, word_id, u, out,
                  stream, validate)
 
 

@@ -44,7 +44,8 @@ def to_device(c, device="cuda"):
 def run_kernel(kernel: str, dev: dict):
     import torch
     import paper_1505_03851_amd as lda
-    fn = {"naive": lda.draw_naive, "butterfly": lda.draw_butterfly}[kernel]
+    fn = {"naive": lda.draw_naive, "butterfly": lda.draw_butterfly,
+          "transposed": lda.draw_transposed}[kernel]
     z = fn(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
     torch.cuda.synchronize()
     return z.cpu().numpy()

@@ -74,7 +74,7 @@ def call(lib, fn, **kw):
              args["z"], args["N"], args["M"], args["V"], args["K"], None)
 
 
-FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_butterfly_table"]
+FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_butterfly_table"]
 
 
 @pytest.mark.parametrize("fn", FNS)

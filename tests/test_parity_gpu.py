@@ -15,7 +15,7 @@ from parity import MAX_MISMATCH_RATE, compare, run_kernel, to_device
 
 pytestmark = pytest.mark.gpu
 
-KERNELS = ["naive", "butterfly"]
+KERNELS = ["naive", "butterfly", "transposed"]
 
 
 def _check(c, kernel, idx=None, rate=True):
