@@ -100,6 +100,24 @@ int lda_draw_butterfly(const float *theta, const float *phi,
                        int32_t V, int32_t K, void *stream);
 
 /*
+ * Butterfly draw over documents given in the paper's ragged form (Section 2:
+ * document m holds N[m] tokens; Algorithm 7 draws document by document):
+ * doc_offsets is an int64 device array [M + 1], non-decreasing, with
+ * doc_offsets[0] = 0 and doc_offsets[M] = N; document m's tokens are
+ * word_id[doc_offsets[m] .. doc_offsets[m+1]), with their u and z at the same
+ * positions.  Empty documents are allowed.  The result equals
+ * lda_draw_butterfly with doc_id[n] = the document whose range holds n.
+ * Tokens are still drawn one per lane, 64 consecutive tokens per wavefront:
+ * each lane finds its document by binary search over doc_offsets.
+ * doc_offsets must be 8-byte aligned (LDA_ERR_ALIGN otherwise); its contents
+ * are not checked.
+ */
+int lda_draw_docs(const float *theta, const float *phi,
+                  const int64_t *doc_offsets, const int32_t *word_id,
+                  const float *u, int32_t *z, int64_t N, int32_t M, int32_t V,
+                  int32_t K, void *stream);
+
+/*
  * Transposed-access draw (Algorithms 4, 5 and 6 with a binary search over
  * block ends and a linear search of the chosen block, Section 3): the
  * paper's design before the butterfly, kept for comparison.  The tile of W =

@@ -1,12 +1,14 @@
 """MI355X-native per-token LDA topic draw with butterfly-patterned partial
 sums (Steele and Tristan, arXiv 1505.03851).
 
-``draw_naive``, ``draw_butterfly`` and ``butterfly_table`` call the HIP
+``draw_naive``, ``draw_butterfly``, ``draw_transposed``, ``draw_docs`` and
+``butterfly_table`` call the HIP
 library through its C ABI (``include/lda_draw.h``).  The binding is imported
 on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 """
 
-_BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "butterfly_table",
+_BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs",
+            "butterfly_table",
             "butterfly_width", "status_string", "version", "LdaError",
             "load", "MAX_K", "MAX_TABLE_BYTES", "STATUS")
 

@@ -58,6 +58,8 @@ def load() -> ctypes.CDLL:
     for name in ("lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed"):
         getattr(lib, name).argtypes = draw_args
         getattr(lib, name).restype = ctypes.c_int
+    lib.lda_draw_docs.argtypes = draw_args
+    lib.lda_draw_docs.restype = ctypes.c_int
     lib.lda_butterfly_table.argtypes = [P, P, P, P, P, I64, I32, I32, I32, P]
     lib.lda_butterfly_table.restype = ctypes.c_int
     lib.lda_butterfly_width.argtypes = [I32]
@@ -170,6 +172,50 @@ def draw_transposed(theta, phi, doc_id, word_id, u, out=None, stream=None,
     paper's design before the butterfly, for comparison."""
     return _draw("lda_draw_transposed", theta, phi, doc_id, word_id, u, out,
                  stream, validate)
+
+
+def draw_docs(theta, phi, doc_offsets, word_id, u, out=None, stream=None,
+              validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the butterfly kernel, documents given as offsets:
+    document m holds tokens doc_offsets[m] .. doc_offsets[m+1]-1 (int64
+    [M+1], doc_offsets[0] = 0, doc_offsets[M] = N, non-decreasing; empty
+    documents allowed), the paper's ragged corpus of Section 2."""
+    _require(theta, "theta", torch.float32, 2)
+    _require(phi, "phi", torch.float32, 2)
+    _require(doc_offsets, "doc_offsets", torch.int64, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    _require(u, "u", torch.float32, 1)
+    M, K = theta.shape
+    V, K2 = phi.shape
+    N = word_id.shape[0]
+    if K2 != K:
+        raise ValueError(f"theta has K={K} topics but phi has {K2}")
+    if doc_offsets.shape[0] != M + 1:
+        raise ValueError("doc_offsets must have M + 1 entries")
+    if u.shape[0] != N:
+        raise ValueError("u and word_id lengths differ")
+    devs = {t.device for t in (theta, phi, doc_offsets, word_id, u)}
+    if len(devs) != 1:
+        raise ValueError("all tensors must be on one device")
+    if validate:
+        off = doc_offsets.cpu()
+        if int(off[0]) != 0 or int(off[-1]) != N or bool((off[1:] < off[:-1]).any()):
+            raise ValueError("doc_offsets must rise from 0 to N")
+        if N and (int(word_id.min()) < 0 or int(word_id.max()) >= V):
+            raise ValueError("word_id out of range [0, V)")
+    if out is None:
+        out = torch.empty(N, dtype=torch.int32, device=word_id.device)
+    else:
+        _require(out, "out", torch.int32, 1)
+        if out.shape[0] != N or out.device != word_id.device:
+            raise ValueError("out must be int32[N] on the tensors' device")
+    with torch.cuda.device(word_id.device):
+        st = load().lda_draw_docs(
+            theta.data_ptr(), phi.data_ptr(), doc_offsets.data_ptr(),
+            word_id.data_ptr(), u.data_ptr(), out.data_ptr(), N, M, V, K,
+            _stream_handle(stream))
+    _check(st)
+    return out
 
 
 def butterfly_table(theta, phi, doc_id, word_id, out=None, stream=None,

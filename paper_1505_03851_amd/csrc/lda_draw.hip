@@ -45,18 +45,41 @@ namespace {
 constexpr int kWavesPerBlock = LDA_WAVES_PER_BLOCK;
 constexpr int kBlockThreads = kWavesPerBlock * kWave;
 
+// Where a token's document comes from: a per-token id array, or the paper's
+// ragged form (Section 2: document m holds N[m] tokens), given as offsets --
+// document m's tokens are [offsets[m], offsets[m + 1]).
+struct DocSource {
+  const int32_t *ids;      // doc_id[N], or null
+  const int64_t *offsets;  // doc_offsets[M + 1], used when ids is null
+  int M;
+  // Document of token n: ids[n], or the last m with offsets[m] <= n (this
+  // skips empty documents).
+  __device__ __forceinline__ int operator()(int64_t n) const {
+    if (ids) return ids[n];
+    int lo = 0, hi = M - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (offsets[mid] <= n)
+        lo = mid;
+      else
+        hi = mid - 1;
+    }
+    return lo;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Naive kernel (Algorithm 1 with Algorithm 3).  Lane n walks the K topics of
 // its own token, keeps the full prefix table p[K] in its private segment and
 // binary-searches it for the first entry above stop = S * u.
 template <int KMAX>
 __global__ __launch_bounds__(256) void naive_kernel(
-    const float *__restrict__ theta, const float *__restrict__ phi,
-    const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
-    const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K) {
+    const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
+    const int32_t *__restrict__ word_id, const float *__restrict__ u,
+    int32_t *__restrict__ z, int64_t N, int K) {
   const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= N) return;
-  const float *th = theta + (int64_t)doc_id[n] * K;
+  const float *th = theta + (int64_t)docs(n) * K;
   const float *ph = phi + (int64_t)word_id[n] * K;
   float p[KMAX];
   float sum = 0.0f;
@@ -85,7 +108,6 @@ template <int W, bool SMALL>
 struct Wave {
   rsrc_t th_rs, ph_rs;  // theta, phi
   const int32_t *wp;    // word_id + t0
-  const int32_t *dp;    // doc_id + t0
   int last;             // SMALL: index in the window of token N - 1
   uint32_t row_bytes;   // 4 * K
   int R;                // remnant topics (K mod W)
@@ -138,16 +160,11 @@ __device__ __forceinline__ uint32_t phi_row(const Wave<W, SMALL> &w, const int32
   }
 }
 
-// Same for the theta row of token k's document.
+// Byte offset of the theta row of token k's document, from the lane that
+// holds token k (uniform for W = 64, per half-wave for W = 32).
 template <int W, bool SMALL>
 __device__ __forceinline__ uint32_t theta_row(const Wave<W, SMALL> &w, int k) {
-  if constexpr (W == kWave) {
-    return (uint32_t)window_at<SMALL>(w.dp, w.last, k) * w.row_bytes;
-  } else {
-    const uint32_t lo = (uint32_t)window_at<SMALL>(w.dp, w.last, k) * w.row_bytes;
-    const uint32_t hi = (uint32_t)window_at<SMALL>(w.dp, w.last, 32 + k) * w.row_bytes;
-    return w.gbase ? hi : lo;
-  }
+  return (uint32_t)group_value<W>((int)w.th_lane, k);
 }
 
 // buffer load at a per-lane offset plus a row offset that is uniform for
@@ -287,13 +304,11 @@ __device__ __forceinline__ void load_tile_blocks(const Wave<W, SMALL> &w, float 
 template <int W, bool SMALL>
 __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
                                           const float *phi, uint32_t theta_bytes,
-                                          uint32_t phi_bytes, const int32_t *doc_id,
-                                          const int32_t *word_id, int64_t t0, int last,
+                                          uint32_t phi_bytes, const int32_t *word_id, int64_t t0, int last,
                                           int K, int lane, int doc, int word) {
   w.th_rs = make_rsrc(theta, theta_bytes);
   w.ph_rs = make_rsrc(phi, phi_bytes);
   w.wp = word_id + t0;
-  w.dp = doc_id + t0;
   w.last = last;
   w.row_bytes = (uint32_t)K * 4u;
   w.R = K & (W - 1);
@@ -388,10 +403,9 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
 template <int W, bool LDS_TABLE, bool SMALL>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
-    const float *__restrict__ theta, const float *__restrict__ phi,
-    const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
-    const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
-    uint32_t theta_bytes, uint32_t phi_bytes) {
+    const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
+    const int32_t *__restrict__ word_id, const float *__restrict__ u,
+    int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
@@ -408,14 +422,14 @@ void butterfly_kernel(
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = doc_id[n];
+  const int doc = docs(n);
   const int word = word_id[n];
   const float un = u[n];
   // blocks of W topics; a remnant of K mod W topics becomes block 0, padded
   // at its front with empty topics
   const int NB = (K + W - 1) >> LOG2W;
   Wave<W, SMALL> w;
-  init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+  init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                       lane, doc, word);
   float *region = lds + wave * region_rows(NB, W, LDS_TABLE) * kWave;
 
@@ -625,7 +639,7 @@ __device__ __forceinline__ int leaf_scan(rsrc_t th_rs, rsrc_t ph_rs, uint32_t th
 template <bool SMALL, int C>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_LEAF4_WAVES_PER_EU)))
 void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
-                       const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
+                       DocSource docs, const int32_t *__restrict__ word_id,
                        const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
@@ -639,12 +653,12 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = doc_id[n];
+  const int doc = docs(n);
   const int word = word_id[n];
   const float un = u[n];
   const int NB = K / kBlock4;
   Wave<kWave, SMALL> w;
-  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                           lane, doc, word);
   float *region = lds + wave * NB * kWave;
 
@@ -733,7 +747,7 @@ __device__ __forceinline__ float transpose_sum(float *tile, const float (&a)[kWa
 template <bool SMALL>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void transposed_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
-                       const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
+                       DocSource docs, const int32_t *__restrict__ word_id,
                        const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
@@ -746,12 +760,12 @@ void transposed_kernel(const float *__restrict__ theta, const float *__restrict_
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = doc_id[n];
+  const int doc = docs(n);
   const int word = word_id[n];
   const float un = u[n];
   const int NB = (K + kWave - 1) / kWave;  // the remnant is block 0, padded
   Wave<kWave, SMALL> w;
-  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                           lane, doc, word);
   float *tile = lds + wave * (kTileFloats + NB * kWave);
   float *region = tile + kTileFloats;
@@ -843,7 +857,7 @@ __global__ __launch_bounds__(kBlockThreads) void table_kernel(
   const bool store = lane <= last;
   const int doc = doc_id[n];
   Wave<W, true> w;
-  init_wave<W, true>(w, theta, phi, theta_bytes, phi_bytes, doc_id, word_id, t0, last, K,
+  init_wave<W, true>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                      lane, doc, word_id[n]);
   const int R = w.R;
   const int NB = K / W;
@@ -913,15 +927,14 @@ dim3 wave_grid(int64_t N) {
 }
 
 template <int KMAX>
-void launch_naive(const float *theta, const float *phi, const int32_t *d,
-                  const int32_t *w, const float *u, int32_t *z, int64_t N,
-                  int32_t K, hipStream_t s) {
+void launch_naive(const float *theta, const float *phi, DocSource d, const int32_t *w,
+                  const float *u, int32_t *z, int64_t N, int32_t K, hipStream_t s) {
   const dim3 grid((unsigned)((N + 255) / 256));
   naive_kernel<KMAX><<<grid, 256, 0, s>>>(theta, phi, d, w, u, z, N, K);
 }
 
 template <int C>
-void launch_butterfly4(const float *theta, const float *phi, const int32_t *d,
+void launch_butterfly4(const float *theta, const float *phi, DocSource d,
                        const int32_t *wd, const float *u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const size_t lds = (size_t)kWavesPerBlock * (K / kBlock4) * kWave * sizeof(float);
@@ -935,7 +948,7 @@ void launch_butterfly4(const float *theta, const float *phi, const int32_t *d,
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
-void launch_transposed(const float *theta, const float *phi, const int32_t *d,
+void launch_transposed(const float *theta, const float *phi, DocSource d,
                        const int32_t *wd, const float *u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + kWave - 1) / kWave;
@@ -951,7 +964,7 @@ void launch_transposed(const float *theta, const float *phi, const int32_t *d,
 }
 
 template <int W, bool LDS_TABLE>
-void launch_butterfly(const float *theta, const float *phi, const int32_t *d,
+void launch_butterfly(const float *theta, const float *phi, DocSource d,
                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + W - 1) / W;  // blocks, the remnant included
@@ -967,6 +980,28 @@ void launch_butterfly(const float *theta, const float *phi, const int32_t *d,
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
+// The butterfly draw for either document source (kernel choice by K).
+void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
+                        const int32_t *word_id, const float *u, int32_t *z, int64_t N,
+                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
+    launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    return;
+  }
+  const bool lt = lds_table_for(K);
+  if (width_for(K) == 64) {
+    if (lt)
+      launch_butterfly<64, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else
+      launch_butterfly<64, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  } else {
+    if (lt)
+      launch_butterfly<32, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else
+      launch_butterfly<32, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  }
+}
+
 }  // namespace
 }  // namespace lda
 
@@ -979,14 +1014,15 @@ extern "C" int lda_draw_naive(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  const DocSource d{doc_id, nullptr, M};
   if (K <= 64)
-    launch_naive<64>(theta, phi, doc_id, word_id, u, z, N, K, s);
+    launch_naive<64>(theta, phi, d, word_id, u, z, N, K, s);
   else if (K <= 256)
-    launch_naive<256>(theta, phi, doc_id, word_id, u, z, N, K, s);
+    launch_naive<256>(theta, phi, d, word_id, u, z, N, K, s);
   else if (K <= 1024)
-    launch_naive<1024>(theta, phi, doc_id, word_id, u, z, N, K, s);
+    launch_naive<1024>(theta, phi, d, word_id, u, z, N, K, s);
   else
-    launch_naive<LDA_MAX_K>(theta, phi, doc_id, word_id, u, z, N, K, s);
+    launch_naive<LDA_MAX_K>(theta, phi, d, word_id, u, z, N, K, s);
   return finish_launch();
 }
 
@@ -997,23 +1033,8 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
                                   void *stream) {
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
-    launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
-    return finish_launch();
-  }
-  const bool lt = lds_table_for(K);
-  if (width_for(K) == 64) {
-    if (lt)
-      launch_butterfly<64, true>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
-    else
-      launch_butterfly<64, false>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
-  } else {
-    if (lt)
-      launch_butterfly<32, true>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
-    else
-      launch_butterfly<32, false>(theta, phi, doc_id, word_id, u, z, N, M, V, K, s);
-  }
+  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, u, z, N, M, V, K,
+                     static_cast<hipStream_t>(stream));
   return finish_launch();
 }
 
@@ -1023,8 +1044,20 @@ extern "C" int lda_draw_transposed(const float *theta, const float *phi,
                                    int32_t V, int32_t K, void *stream) {
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
-  launch_transposed(theta, phi, doc_id, word_id, u, z, N, M, V, K,
+  launch_transposed(theta, phi, DocSource{doc_id, nullptr, M}, word_id, u, z, N, M, V, K,
                     static_cast<hipStream_t>(stream));
+  return finish_launch();
+}
+
+extern "C" int lda_draw_docs(const float *theta, const float *phi,
+                             const int64_t *doc_offsets, const int32_t *word_id,
+                             const float *u, int32_t *z, int64_t N, int32_t M,
+                             int32_t V, int32_t K, void *stream) {
+  int st = check_args(theta, phi, doc_offsets, word_id, u, z, N, M, V, K);
+  if (st != LDA_OK || N == 0) return st;
+  if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
+  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M}, word_id, u, z, N, M, V,
+                     K, static_cast<hipStream_t>(stream));
   return finish_launch();
 }
 

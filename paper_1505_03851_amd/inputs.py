@@ -256,17 +256,33 @@ def make_corpus(cfg: CorpusConfig | str) -> Corpus:
     return corpus
 
 
+def doc_offsets(doc_id: np.ndarray, M: int) -> np.ndarray:
+    """The ragged (CSR) form of a corpus whose documents are contiguous:
+    int64 [M + 1], document m holding tokens offsets[m] .. offsets[m+1]-1."""
+    doc_id = np.asarray(doc_id)
+    if doc_id.size and (np.diff(doc_id) < 0).any():
+        raise ValueError("documents are not contiguous (doc_id decreases)")
+    counts = np.bincount(doc_id, minlength=M).astype(np.int64)
+    return np.concatenate([[0], np.cumsum(counts)]).astype(np.int64)
+
+
 def make_random(N: int, M: int, V: int, K: int, seed: int, *, alpha=0.1,
                 beta=0.01, zipf_s=1.0, doc_order: str = "sequential") -> Corpus:
     """A small corpus of arbitrary shape for parity and edge-case tests.
 
     ``doc_order``: "sequential" (contiguous runs of near-equal length),
-    "shuffled" (random doc id per token) or "single" (every token in doc 0).
+    "ragged" (contiguous runs of Dirichlet-multinomial lengths, many of them
+    zero), "shuffled" (random doc id per token) or "single" (every token in
+    doc 0).
     """
     ss = np.random.SeedSequence([BASE_SEED, 7, seed, N, M, V, K])
     s_theta, s_phi, s_word, s_u, s_doc = ss.spawn(5)
     if doc_order == "sequential":
         doc_id = (np.arange(N, dtype=np.int64) * M // max(N, 1)).astype(np.int32)
+    elif doc_order == "ragged":
+        g = np.random.Generator(np.random.PCG64(s_doc))
+        lengths = g.multinomial(N, g.dirichlet(np.full(M, 0.3)))
+        doc_id = np.repeat(np.arange(M, dtype=np.int32), lengths)
     elif doc_order == "shuffled":
         g = np.random.Generator(np.random.PCG64(s_doc))
         doc_id = g.integers(0, M, size=N, dtype=np.int64).astype(np.int32)

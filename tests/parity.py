@@ -42,8 +42,18 @@ def to_device(c, device="cuda"):
 
 
 def run_kernel(kernel: str, dev: dict):
+    """z by ``kernel``; "docs" hands the documents over as offsets (the
+    corpus's documents must be contiguous)."""
     import torch
     import paper_1505_03851_amd as lda
+    if kernel == "docs":
+        from paper_1505_03851_amd.inputs import doc_offsets
+        off = doc_offsets(dev["doc_id"].cpu().numpy(), dev["theta"].shape[0])
+        z = lda.draw_docs(dev["theta"], dev["phi"],
+                          torch.from_numpy(off).to(dev["theta"].device),
+                          dev["word_id"], dev["u"], validate=True)
+        torch.cuda.synchronize()
+        return z.cpu().numpy()
     fn = {"naive": lda.draw_naive, "butterfly": lda.draw_butterfly,
           "transposed": lda.draw_transposed}[kernel]
     z = fn(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])

@@ -74,7 +74,8 @@ def call(lib, fn, **kw):
              args["z"], args["N"], args["M"], args["V"], args["K"], None)
 
 
-FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_butterfly_table"]
+FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_draw_docs",
+       "lda_butterfly_table"]
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -106,6 +107,12 @@ def test_empty_is_noop(lib, fn):
     # N = 0: no launch, no pointer needed
     assert call(lib, fn, N=0, theta=None, phi=None, doc=None, word=None,
                 u=None, z=None) == 0
+
+
+def test_docs_offsets_need_8_byte_alignment(lib):
+    # doc_offsets is int64: 4-byte aligned is not enough
+    from paper_1505_03851_amd._lib import STATUS
+    assert call(lib, "lda_draw_docs", doc=A + 4) == STATUS["LDA_ERR_ALIGN"]
 
 
 def test_width(lib):

@@ -289,12 +289,27 @@ def test_c_oracle_equals_numpy_twin_on_config(name):
 
 
 @pytest.mark.parametrize("K", [1, 7, 19, 64, 65, 300])
-@pytest.mark.parametrize("order", ["sequential", "shuffled"])
+@pytest.mark.parametrize("order", ["sequential", "shuffled", "ragged"])
 def test_c_oracle_equals_numpy_twin_random(K, order):
     c = make_random(1500, 17, 300, K, seed=K, doc_order=order)
     z1, b1 = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u)
     z2, b2 = oracle.draw_np(c.theta, c.phi, c.doc_id, c.word_id, c.u)
     assert (z1 == z2).all() and (b1 == b2).all()
+
+
+def test_ragged_documents_and_offsets():
+    """The ragged generator keeps documents contiguous and leaves some
+    empty; the offsets form round-trips to the doc ids."""
+    from paper_1505_03851_amd.inputs import doc_offsets
+    c = make_random(64 * 21 + 5, 2000, 300, 64, seed=7, doc_order="ragged")
+    off = doc_offsets(c.doc_id, c.M)
+    assert off.dtype == np.int64 and off.shape == (c.M + 1,)
+    assert off[0] == 0 and off[-1] == c.N and (np.diff(off) >= 0).all()
+    assert (np.diff(off) == 0).sum() > c.M // 2        # many empty documents
+    back = np.repeat(np.arange(c.M), np.diff(off))
+    assert (back == c.doc_id).all()
+    with pytest.raises(ValueError):
+        doc_offsets(np.array([0, 2, 1], np.int32), 3)
 
 
 def test_band_flag_definition():

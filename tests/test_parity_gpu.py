@@ -162,6 +162,103 @@ def test_degenerate_weights(K, kernel):
     assert rep.hard == 0
 
 
+# ---------------------------------------------------------------------------
+# Documents as offsets (the ragged corpus of Section 2): same kernels, each
+# lane finds its document in the offsets.
+
+@pytest.mark.parametrize("name", ["tiny-K32", "corpus1M-K64", "corpus1M-K256"])
+def test_docs_config_every_token(name):
+    c = corpus(name)
+    _check(c, "docs", rate=c.N >= 1 << 20)
+
+
+@pytest.mark.parametrize("K", [16, 240])
+def test_docs_wiki_shaped_every_token(K):
+    from paper_1505_03851_amd.inputs import wiki_shaped
+    _check(corpus(wiki_shaped(K).name), "docs")
+
+
+def test_docs_full_size_equals_doc_ids():
+    """At full size the offsets form gives the same z as the doc-id form,
+    token for token (same kernel, same arithmetic), and a sample matches
+    the oracle."""
+    c = corpus("corpus16M-K1024")
+    dev = to_device(c)
+    print(f"[case] {c.name} docs vs butterfly", flush=True)
+    z_docs = run_kernel("docs", dev)
+    z_ids = run_kernel("butterfly", dev)
+    assert (z_docs == z_ids).all(), np.nonzero(z_docs != z_ids)[0][:10]
+    rng = np.random.default_rng(12)
+    idx = np.unique(np.concatenate([rng.choice(c.N, 1 << 18, replace=False),
+                                    np.arange(c.N - 300, c.N)]))
+    rep = compare(c, z_docs, idx)
+    assert rep.hard == 0, rep.first_hard
+
+
+RAGGED = [
+    # (N, M, V, K): Dirichlet(0.3) lengths, many documents empty
+    (1, 3, 7, 64),
+    (63, 40, 50, 5),
+    (64 * 9 + 17, 200, 300, 19),
+    (64 * 21 + 5, 2000, 300, 64),     # more documents than tokens
+    (64 * 21 + 5, 40, 300, 65),
+    (64 * 33 + 63, 60, 500, 200),
+    (64 * 9 + 33, 40, 100, 256),      # four-topic-leaf kernel
+    (64 * 7 + 5, 300, 90, 1280),
+    (64 * 17 + 9, 60, 500, 2047),
+    (64 * 5 + 3, 20, 200, 4096),
+]
+
+
+@pytest.mark.parametrize("shape", RAGGED, ids=lambda s: "N{}-M{}-K{}".format(s[0], s[1], s[3]))
+def test_docs_ragged(shape):
+    N, M, V, K = shape
+    c = make_random(N, M, V, K, seed=N + M + K, doc_order="ragged")
+    z_docs = run_kernel("docs", to_device(c))
+    _check(c, "butterfly", rate=False)
+    rep = compare(c, z_docs)
+    print(f"[parity] {c.name} docs: {rep}", flush=True)
+    assert rep.hard == 0, rep.first_hard
+    z_ids = run_kernel("butterfly", to_device(c))
+    assert (z_docs == z_ids).all()
+
+
+def test_docs_empty_corpus_and_empty_documents():
+    """N = 0 is a no-op; documents before, between and after the tokens
+    may be empty."""
+    import torch
+    import paper_1505_03851_amd as lda
+    K, V = 48, 30
+    rng = np.random.default_rng(5)
+    theta = torch.from_numpy(rng.random((6, K), dtype=np.float32)).cuda()
+    phi = torch.from_numpy(rng.random((V, K), dtype=np.float32)).cuda()
+    off = torch.tensor([0, 0, 0, 0, 0, 0, 0], dtype=torch.int64, device="cuda")
+    empty_i = torch.empty(0, dtype=torch.int32, device="cuda")
+    empty_f = torch.empty(0, dtype=torch.float32, device="cuda")
+    assert lda.draw_docs(theta, phi, off, empty_i, empty_f, validate=True).numel() == 0
+    N = 100
+    doc = np.repeat(np.arange(6), [0, 0, 37, 0, 63, 0]).astype(np.int32)
+    word = rng.integers(0, V, N).astype(np.int32)
+    u = _grid_u(N, 3)
+    c = _corpus(theta.cpu().numpy(), phi.cpu().numpy(), doc, word, u, "empty-docs")
+    _check(c, "docs", rate=False)
+
+
+def test_docs_rejects_bad_offsets():
+    import torch
+    import paper_1505_03851_amd as lda
+    theta = torch.ones((3, 8), device="cuda")
+    phi = torch.ones((4, 8), device="cuda")
+    w = torch.zeros(5, dtype=torch.int32, device="cuda")
+    u = torch.zeros(5, device="cuda")
+    for bad in ([0, 2, 1, 5], [1, 2, 3, 5], [0, 1, 2, 4]):
+        off = torch.tensor(bad, dtype=torch.int64, device="cuda")
+        with pytest.raises(ValueError):
+            lda.draw_docs(theta, phi, off, w, u, validate=True)
+    with pytest.raises(ValueError):   # M + 1 entries
+        lda.draw_docs(theta, phi, torch.zeros(3, dtype=torch.int64, device="cuda"), w, u)
+
+
 @pytest.mark.parametrize("K", [32, 50, 64, 83, 200, 1024])
 def test_butterfly_table_matches_closed_form(K):
     """The tables the kernel builds (Fig. 1, right) equal the oracle's closed
