@@ -52,30 +52,55 @@ def algorithmic_bytes(c) -> int:
 
 
 def upload(c):
+    """The corpus on the GPU; documents also as offsets when they are
+    contiguous (the form lda_draw_docs takes)."""
+    import numpy as np
     import torch
-    return {k: torch.from_numpy(getattr(c, k)).cuda()
-            for k in ("theta", "phi", "doc_id", "word_id", "u")}
+    from paper_1505_03851_amd.inputs import doc_offsets
+    dev = {k: torch.from_numpy(getattr(c, k)).cuda()
+           for k in ("theta", "phi", "doc_id", "word_id", "u")}
+    if c.N == 0 or (np.diff(c.doc_id) >= 0).all():
+        dev["doc_offsets"] = torch.from_numpy(doc_offsets(c.doc_id, c.M)).cuda()
+    return dev
+
+
+# kernels bench.py can time: name -> entry point of the binding
+KERNELS = ("butterfly", "naive", "transposed", "docs",
+           "variant-register", "variant-lds", "variant-lds_alt")
+
+
+def launcher(kernel: str, dev):
+    """A function (out, stream) that launches ``kernel`` once over ``dev``."""
+    import paper_1505_03851_amd as lda
+    th, ph, d, w, u = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    if kernel == "docs":
+        off = dev["doc_offsets"]
+        return lambda out, stream: lda.draw_docs(th, ph, off, w, u, out=out, stream=stream)
+    if kernel.startswith("variant-"):
+        v = kernel[len("variant-"):]
+        return lambda out, stream: lda.draw_variant(th, ph, d, w, u, variant=v, out=out,
+                                                    stream=stream)
+    fn = {"butterfly": lda.draw_butterfly, "naive": lda.draw_naive,
+          "transposed": lda.draw_transposed}[kernel]
+    return lambda out, stream: fn(th, ph, d, w, u, out=out, stream=stream)
 
 
 def time_kernel(kernel: str, dev, steps: int, warmup: int):
     """Warm up, then time exactly ``steps`` launches.  Returns (wall seconds of
     the timed region, per-launch milliseconds from HIP events, z)."""
     import torch
-    import paper_1505_03851_amd as lda
-    fn = {"butterfly": lda.draw_butterfly, "naive": lda.draw_naive,
-          "transposed": lda.draw_transposed}[kernel]
+    launch = launcher(kernel, dev)
     stream = torch.cuda.current_stream()
     z = torch.empty_like(dev["doc_id"])
-    args = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
     for _ in range(warmup):
-        fn(*args, out=z, stream=stream)
+        launch(z, stream)
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True),
            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
     for s, e in ev:
         s.record(stream)
-        fn(*args, out=z, stream=stream)
+        launch(z, stream)
         e.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -217,6 +242,35 @@ def k_sweep(args) -> int:
     return 0
 
 
+def ablation(args) -> int:
+    """The table variants of Section 4 (the paper's rule with the table in
+    registers or LDS, the alternative rule in LDS), the offsets form of the
+    documents and the default dispatch, on the two corpora and the corpus
+    shaped like the paper's at K = 80 and 240; one JSON line per workload.
+    z of every variant is compared with the default kernel's (identical
+    unless a token lies in the fp32 rounding band)."""
+    import torch
+    from paper_1505_03851_amd.inputs import make_corpus, wiki_shaped
+    names = [SECOND, HEADLINE, wiki_shaped(80).name, wiki_shaped(240).name]
+    for name in names:
+        c = make_corpus(name)
+        dev = upload(c)
+        rec = {"workload": name, "N": c.N, "K": c.K}
+        z_ref = None
+        for kernel in ("butterfly", "variant-register", "variant-lds",
+                       "variant-lds_alt", "docs"):
+            r = measure(name, c, dev, kernel, args.steps, args.warmup)
+            z = r.pop("z")
+            if z_ref is None:
+                z_ref = z
+            rec[kernel + "_ms"] = r["ms_per_launch"]
+            rec[kernel + "_differs"] = int((z != z_ref).sum())
+        print(json.dumps(rec), flush=True)
+        del dev
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -224,7 +278,7 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--cpu-sample", type=int, default=1 << 24,
                     help="tokens of the headline workload the oracle draws")
-    ap.add_argument("--only", choices=["butterfly", "naive", "transposed"], default=None,
+    ap.add_argument("--only", choices=KERNELS, default=None,
                     help="time one kernel on one workload (for profiling)")
     ap.add_argument("--workload", default=HEADLINE)
     ap.add_argument("--copy-calibration", action="store_true",
@@ -234,6 +288,9 @@ def main() -> int:
                     help="naive vs butterfly over K = 16, 48, ..., 240 on the "
                          "corpus shaped like the paper's evaluation corpus; one "
                          "JSON line per K")
+    ap.add_argument("--ablation", action="store_true",
+                    help="time the block-table variants and the offsets form "
+                         "of the documents; one JSON line per workload")
     ap.add_argument("--counters-summary", action="store_true",
                     help="write the HBM-traffic record from rocprofv3 csv "
                          "directories (--fetch, --write, --copy-fetch, "
@@ -272,6 +329,8 @@ def main() -> int:
 
     if args.k_sweep:
         return k_sweep(args)
+    if args.ablation:
+        return ablation(args)
 
     if args.only:
         c = make_corpus(args.workload)

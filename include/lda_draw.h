@@ -118,6 +118,32 @@ int lda_draw_docs(const float *theta, const float *phi,
                   int32_t K, void *stream);
 
 /*
+ * Butterfly draw with a chosen per-block table, for measuring the table's
+ * design choices (Section 4).  Same arguments, layout and errors as
+ * lda_draw_butterfly, plus `variant`:
+ *   LDA_VARIANT_REGISTER_TABLE  the paper's replacement [a b; c d] ->
+ *                               [a d; a+b c+d]; the table stays in registers
+ *                               and Algorithm 10's search-assist loop fetches
+ *                               each level's entry with cross-lane reads;
+ *   LDA_VARIANT_LDS_TABLE       the same table written to LDS; each search
+ *                               level reads its entry directly;
+ *   LDA_VARIANT_LDS_TABLE_ALT   the alternative rule the paper mentions,
+ *                               [a b; c d] -> [a c; a+b c+d], whose table
+ *                               holds left-half sums of aligned topic ranges,
+ *                               searched in LDS by a descent from the whole
+ *                               block.
+ * Every variant uses the one-topic-per-lane kernel for all K (W = 64 for
+ * K >= 64, else 32).  Any other `variant` returns LDA_ERR_UNSUPPORTED.
+ */
+#define LDA_VARIANT_REGISTER_TABLE 0
+#define LDA_VARIANT_LDS_TABLE 1
+#define LDA_VARIANT_LDS_TABLE_ALT 2
+int lda_draw_butterfly_variant(const float *theta, const float *phi,
+                               const int32_t *doc_id, const int32_t *word_id,
+                               const float *u, int32_t *z, int64_t N, int32_t M,
+                               int32_t V, int32_t K, int32_t variant, void *stream);
+
+/*
  * Transposed-access draw (Algorithms 4, 5 and 6 with a binary search over
  * block ends and a linear search of the chosen block, Section 3): the
  * paper's design before the butterfly, kept for comparison.  The tile of W =

@@ -19,6 +19,12 @@ schedule and the search tree of thread 5):
   search_sim(...)          the search of Algorithms 9 and 10 over that table,
                            with all W lanes as one numpy vector (shuffle and
                            shuffleXor are gathers across the vector).
+
+The alternative replacement the paper mentions in Section 4, [a b; c d] ->
+[a c; a+b c+d], has its own closed form (closed_form_alt), table
+(table_alt_fp64) and search (search_alt_sim): every entry of its table is the
+sum over the left half of an aligned range of topics, so the search is a
+descent from the whole block down a binary tree.
 """
 from __future__ import annotations
 
@@ -86,12 +92,35 @@ def apply_replacement(tab, i, j, k, l) -> None:
     tab[j][k], tab[j][l] = a + b, c + d
 
 
-def apply_replacements(tab, schedule, upto: int | None = None):
-    """Apply the first ``upto`` sets (all if None) in order; returns ``tab``."""
+def apply_replacement_alt(tab, i, j, k, l) -> None:
+    """The alternative rule: [a b; c d] at rows (i, j), columns (k, l)
+    becomes [a c; a+b c+d]."""
+    a, b, c, d = tab[i][k], tab[i][l], tab[j][k], tab[j][l]
+    tab[i][k], tab[i][l] = a, c
+    tab[j][k], tab[j][l] = a + b, c + d
+
+
+def apply_replacements(tab, schedule, upto: int | None = None, alt: bool = False):
+    """Apply the first ``upto`` sets (all if None) in order, with the paper's
+    rule or (``alt``) the alternative one; returns ``tab``."""
+    rule = apply_replacement_alt if alt else apply_replacement
     for s in schedule[:upto]:
         for (i, j, k, l) in s:
-            apply_replacement(tab, i, j, k, l)
+            rule(tab, i, j, k, l)
     return tab
+
+
+def closed_form_alt(i: int, j: int) -> tuple[int, int, int]:
+    """(thread, first, last) of the entry at block row i, column j of the
+    alternative table: with m = i xor (i+1) and k = floor(m/2), the thread is
+    (i & ~m) + (j & m), as in the paper's table, and the range is
+    (j & ~m) .. (j & ~m) + k: the left half of the aligned range of m + 1
+    topics that holds topic j."""
+    m = i ^ (i + 1)
+    k = m >> 1
+    thread = (i & ~m) + (j & m)
+    v = j & ~m
+    return thread, v, v + k
 
 
 def transposed_products(W: int) -> list[list[Z]]:
@@ -122,6 +151,68 @@ def table_fp64(a: np.ndarray, W: int) -> np.ndarray:
                 p[j, base + i] = a[t, base + v: base + w + 1].sum()
         p[:, base + W - 1] = S[:, base + W - 1]
     return p
+
+
+def table_alt_fp64(a: np.ndarray, W: int) -> np.ndarray:
+    """As table_fp64, with the alternative table in rows 0..W-2 of each
+    block."""
+    a = np.asarray(a, np.float64)
+    Wt, K = a.shape
+    assert Wt == W
+    R = K % W
+    S = np.cumsum(a, axis=1)
+    p = np.empty((W, K), np.float64)
+    p[:, :R] = S[:, :R]
+    for base in range(R, K, W):
+        for i in range(W - 1):
+            for j in range(W):
+                t, v, w = closed_form_alt(i, j)
+                p[j, base + i] = a[t, base + v: base + w + 1].sum()
+        p[:, base + W - 1] = S[:, base + W - 1]
+    return p
+
+
+def search_alt_sim(p: np.ndarray, u: np.ndarray, W: int) -> np.ndarray:
+    """z of each lane over the alternative table ``p`` ([W][K]): the block
+    search of Algorithm 9, then a descent inside the block.  Lane r, at the
+    node of 2**(s+1) topics starting at b, reads the sum over the left half,
+    which the table keeps at row (r & ~(2**(s+1)-1)) + 2**s - 1 of column
+    (r & (2**(s+1)-1)) + b; it goes left if stop < low + that sum, else right
+    with low increased by it.  A lane that finds no entry above its stop value
+    gets K - 1."""
+    p = np.asarray(p, np.float64)
+    Wl, K = p.shape
+    assert Wl == W
+    lg = log2_exact(W)
+    r = np.arange(W)
+    R, NB = K % W, K // W
+    stop = p[:, K - 1] * np.asarray(u, np.float64)
+    j = np.full(W, K - 1, np.int64)
+    if K >= W:
+        ends = p[:, R + W - 1::W]                       # [W][NB] block ends
+        blk = np.minimum((ends <= stop[:, None]).sum(axis=1), NB - 1)
+        base = R + blk * W
+        low = np.where(base > 0, p[r, np.maximum(base - 1, 0)], 0.0)
+        b = np.zeros(W, np.int64)
+        for s in range(lg - 1, -1, -1):
+            span, node = 1 << s, 2 << s
+            row = (r & ~(node - 1)) + span - 1
+            col = (r & (node - 1)) + b
+            # column col of the table holds, in lane r's block, r's own sum
+            cmp = low + p[col, base + row]
+            left = stop < cmp
+            low = np.where(left, low, cmp)
+            b = np.where(left, b, b + span)
+        j = base + b
+        in_rem = (base > 0) & (stop < p[r, np.maximum(base - 1, 0)])
+    else:
+        in_rem = np.ones(W, bool)
+    for lane in np.nonzero(in_rem)[0]:
+        for i in range(R):
+            if stop[lane] < p[lane, i]:
+                j[lane] = i
+                break
+    return j.astype(np.int32)
 
 
 def search_sim(p: np.ndarray, u: np.ndarray, W: int) -> np.ndarray:

@@ -40,6 +40,10 @@ _CONSTS = _header_constants()
 STATUS = {k: v for k, v in _CONSTS.items() if k == "LDA_OK" or k.startswith("LDA_ERR_")}
 MAX_K = _CONSTS["LDA_MAX_K"]
 MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
+# table variants of lda_draw_butterfly_variant, by name
+VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
+            "lds": _CONSTS["LDA_VARIANT_LDS_TABLE"],
+            "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"]}
 
 
 def load() -> ctypes.CDLL:
@@ -58,6 +62,8 @@ def load() -> ctypes.CDLL:
     for name in ("lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed"):
         getattr(lib, name).argtypes = draw_args
         getattr(lib, name).restype = ctypes.c_int
+    lib.lda_draw_butterfly_variant.argtypes = draw_args[:-1] + [I32, P]
+    lib.lda_draw_butterfly_variant.restype = ctypes.c_int
     lib.lda_draw_docs.argtypes = draw_args
     lib.lda_draw_docs.restype = ctypes.c_int
     lib.lda_butterfly_table.argtypes = [P, P, P, P, P, I64, I32, I32, I32, P]
@@ -133,7 +139,7 @@ def _validate_ids(doc_id, word_id, M, V) -> None:
             raise ValueError("word_id out of range [0, V)")
 
 
-def _draw(fn_name, theta, phi, doc_id, word_id, u, out, stream, validate):
+def _draw(fn_name, theta, phi, doc_id, word_id, u, out, stream, validate, extra=()):
     N, M, V, K = _shapes(theta, phi, doc_id, word_id, u)
     if validate:
         _validate_ids(doc_id, word_id, M, V)
@@ -147,7 +153,7 @@ def _draw(fn_name, theta, phi, doc_id, word_id, u, out, stream, validate):
         st = getattr(load(), fn_name)(
             theta.data_ptr(), phi.data_ptr(), doc_id.data_ptr(),
             word_id.data_ptr(), u.data_ptr(), out.data_ptr(), N, M, V, K,
-            _stream_handle(stream))
+            *extra, _stream_handle(stream))
     _check(st)
     return out
 
@@ -172,6 +178,18 @@ def draw_transposed(theta, phi, doc_id, word_id, u, out=None, stream=None,
     paper's design before the butterfly, for comparison."""
     return _draw("lda_draw_transposed", theta, phi, doc_id, word_id, u, out,
                  stream, validate)
+
+
+def draw_variant(theta, phi, doc_id, word_id, u, variant: str = "register",
+                 out=None, stream=None, validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the one-topic-per-lane butterfly kernel with a chosen
+    block table: "register" (the paper's rule, search-assist loop), "lds"
+    (the same table in LDS) or "lds_alt" (the alternative rule
+    [a b; c d] -> [a c; a+b c+d], Section 4)."""
+    if variant not in VARIANTS:
+        raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
+    return _draw("lda_draw_butterfly_variant", theta, phi, doc_id, word_id, u,
+                 out, stream, validate, extra=(VARIANTS[variant],))
 
 
 def draw_docs(theta, phi, doc_offsets, word_id, u, out=None, stream=None,

@@ -116,6 +116,12 @@ __device__ __forceinline__ void reduce_stage(float (&a)[W]) {
 // and row d + BIT receives the kept value plus what the partner sends.
 // Afterwards a[0..W-2] hold lane r's column of the butterfly-patterned block
 // (row d in a[d]) and a[W-1] holds the sum of lane r's own token.
+//
+// ALT applies the other rule the paper mentions, [a b; c d] -> [a c; a+b c+d]:
+// the lane with BIT set takes its partner's row-(d+BIT) value into row d, one
+// more select after the exchange.  Its row d (s trailing ones) then holds, in
+// column r, the sum of token (d & ~(2^(s+1)-1)) + (r & (2^(s+1)-1)) over the
+// left half of the aligned 2^(s+1) topics that contain topic r.
 struct NoStore {
   __device__ __forceinline__ void operator()(int, float) const {}
 };
@@ -130,7 +136,7 @@ struct RowStore {
   }
 };
 
-template <int W, int BIT, class Store>
+template <int W, int BIT, bool ALT, class Store>
 __device__ __forceinline__ void butterfly_stages(float (&a)[W], int r,
                                                  const Store &store) {
   if constexpr (BIT < W) {
@@ -141,18 +147,19 @@ __device__ __forceinline__ void butterfly_stages(float (&a)[W], int r,
       const float send = hi ? a[d] : a[d + BIT];
       const float recv = xor_lane<BIT>(send);
       const float keep = hi ? a[d + BIT] : a[d];
-      a[d] = keep;
+      const float row_d = ALT ? (hi ? recv : a[d]) : keep;
+      a[d] = row_d;
       a[d + BIT] = keep + recv;
-      store(d, keep);
+      store(d, row_d);
     }
-    butterfly_stages<W, BIT * 2, Store>(a, r, store);
+    butterfly_stages<W, BIT * 2, ALT, Store>(a, r, store);
   }
 }
 
-template <int W, class Store>
+template <int W, bool ALT = false, class Store>
 __device__ __forceinline__ void butterfly_block(float (&a)[W], int r,
                                                 const Store &store) {
-  butterfly_stages<W, 1, Store>(a, r, store);
+  butterfly_stages<W, 1, ALT, Store>(a, r, store);
 }
 
 // ---------------------------------------------------------------------------

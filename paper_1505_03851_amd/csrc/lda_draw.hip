@@ -380,6 +380,32 @@ __device__ __forceinline__ int inblock_search(const float (&a)[W], const float *
   return flip ^ r;
 }
 
+// In-block search over the table of the alternative rule (rows in `table`,
+// row d at table[d * 64 + lane]): a descent from the whole block.  At the
+// node of 2^(s+1) topics starting at b, lane r reads its own token's sum over
+// the node's left half, which the table keeps in row (r & ~(2^(s+1)-1)) +
+// 2^s - 1 of column (r & (2^(s+1)-1)) + b, and goes left when stop is below
+// low plus that sum.  Returns the offset within the block.
+template <int W>
+__device__ __forceinline__ int inblock_search_alt(const float *table, int r, int gbase,
+                                                  float stop, float &low, float &high) {
+  constexpr int LOG2W = (W == 64) ? 6 : 5;
+  int b = 0;
+#pragma unroll
+  for (int s = LOG2W - 1; s >= 0; --s) {
+    const int span = 1 << s, node = 2 << s;
+    const int row = (r & ~(node - 1)) + span - 1;
+    const float cmp = low + table[row * kWave + gbase + (r & (node - 1)) + b];
+    if (stop < cmp) {
+      high = cmp;
+    } else {
+      low = cmp;
+      b += span;
+    }
+  }
+  return b;
+}
+
 // LDS rows per wavefront: the block-end prefixes (NB rows of 64 lanes), and,
 // with an LDS table, the rebuilt block's W - 1 rows in the same space.
 __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
@@ -400,12 +426,15 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
 //   combined by Algorithm 8's butterfly (with K / W == 1 this tile is the only
 //   pass over phi).
 // In-block search (Algorithm 10) and the remnant fallback of Algorithm 9.
-template <int W, bool LDS_TABLE, bool SMALL>
+//
+// ALT (with LDS_TABLE only): the alternative replacement rule and its search.
+template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
     const int32_t *__restrict__ word_id, const float *__restrict__ u,
     int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_bytes, uint32_t phi_bytes) {
+  static_assert(!ALT || LDS_TABLE, "the alternative table is searched in LDS");
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
@@ -441,7 +470,7 @@ void butterfly_kernel(
     blk = 0;
     load_tile_blocks<W, SMALL, true>(w, a, 0, w.c0);
     if constexpr (LDS_TABLE)
-      butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+      butterfly_block<W, ALT>(a, w.r, RowStore{region + lane, kWave, true});
     else
       butterfly_block<W>(a, w.r, NoStore{});
     sum = a[W - 1];
@@ -486,7 +515,7 @@ void butterfly_kernel(
     // Rebuild every token's chosen block.
     load_tile_blocks<W, SMALL, true>(w, a, blk, w.c0);
     if constexpr (LDS_TABLE)
-      butterfly_block<W>(a, w.r, RowStore{region + lane, kWave, true});
+      butterfly_block<W, ALT>(a, w.r, RowStore{region + lane, kWave, true});
     else
       butterfly_block<W>(a, w.r, NoStore{});
   }
@@ -498,8 +527,12 @@ void butterfly_kernel(
   // Algorithm 10.  Empty topics of block 0 are never chosen: their prefix
   // equals the prefix before them, which is never above stop >= 0, except
   // when S = 0, where every comparison fails and the result is K - 1.
-  const int j =
-      w.c0 + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
+  int off;
+  if constexpr (ALT)
+    off = inblock_search_alt<W>(region, w.r, w.gbase, stop, low, high);
+  else
+    off = inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
+  const int j = w.c0 + blk * W + off;
   if (store) z[n] = j;
 }
 
@@ -963,7 +996,7 @@ void launch_transposed(const float *theta, const float *phi, DocSource d,
                                                                        N, K, tb, pb);
 }
 
-template <int W, bool LDS_TABLE>
+template <int W, bool LDS_TABLE, bool ALT = false>
 void launch_butterfly(const float *theta, const float *phi, DocSource d,
                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
@@ -973,11 +1006,24 @@ void launch_butterfly(const float *theta, const float *phi, DocSource d,
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (N < kWave)
-    butterfly_kernel<W, LDS_TABLE, true><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, true, ALT><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    butterfly_kernel<W, LDS_TABLE, false><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, false, ALT><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
+}
+
+// The W = 32 / 64 butterfly kernel with a chosen table: in registers with the
+// paper's search-assist loop, in LDS with direct reads, or the alternative
+// rule's table in LDS.
+template <bool LDS_TABLE, bool ALT>
+void launch_table_variant(const float *theta, const float *phi, DocSource d,
+                          const int32_t *word_id, const float *u, int32_t *z, int64_t N,
+                          int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  if (width_for(K) == 64)
+    launch_butterfly<64, LDS_TABLE, ALT>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else
+    launch_butterfly<32, LDS_TABLE, ALT>(theta, phi, d, word_id, u, z, N, M, V, K, s);
 }
 
 // The butterfly draw for either document source (kernel choice by K).
@@ -1046,6 +1092,27 @@ extern "C" int lda_draw_transposed(const float *theta, const float *phi,
   if (st != LDA_OK || N == 0) return st;
   launch_transposed(theta, phi, DocSource{doc_id, nullptr, M}, word_id, u, z, N, M, V, K,
                     static_cast<hipStream_t>(stream));
+  return finish_launch();
+}
+
+extern "C" int lda_draw_butterfly_variant(const float *theta, const float *phi,
+                                          const int32_t *doc_id, const int32_t *word_id,
+                                          const float *u, int32_t *z, int64_t N, int32_t M,
+                                          int32_t V, int32_t K, int32_t variant,
+                                          void *stream) {
+  if (variant != LDA_VARIANT_REGISTER_TABLE && variant != LDA_VARIANT_LDS_TABLE &&
+      variant != LDA_VARIANT_LDS_TABLE_ALT)
+    return LDA_ERR_UNSUPPORTED;
+  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
+  if (st != LDA_OK || N == 0) return st;
+  const DocSource d{doc_id, nullptr, M};
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (variant == LDA_VARIANT_REGISTER_TABLE)
+    launch_table_variant<false, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else if (variant == LDA_VARIANT_LDS_TABLE)
+    launch_table_variant<true, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else
+    launch_table_variant<true, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
   return finish_launch();
 }
 

@@ -43,7 +43,8 @@ def to_device(c, device="cuda"):
 
 def run_kernel(kernel: str, dev: dict):
     """z by ``kernel``; "docs" hands the documents over as offsets (the
-    corpus's documents must be contiguous)."""
+    corpus's documents must be contiguous); "variant-<name>" is the
+    butterfly kernel with the named block table."""
     import torch
     import paper_1505_03851_amd as lda
     if kernel == "docs":
@@ -52,6 +53,11 @@ def run_kernel(kernel: str, dev: dict):
         z = lda.draw_docs(dev["theta"], dev["phi"],
                           torch.from_numpy(off).to(dev["theta"].device),
                           dev["word_id"], dev["u"], validate=True)
+        torch.cuda.synchronize()
+        return z.cpu().numpy()
+    if kernel.startswith("variant-"):
+        z = lda.draw_variant(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"],
+                             dev["u"], variant=kernel[len("variant-"):])
         torch.cuda.synchronize()
         return z.cpu().numpy()
     fn = {"naive": lda.draw_naive, "butterfly": lda.draw_butterfly,

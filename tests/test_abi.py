@@ -67,6 +67,10 @@ def call(lib, fn, **kw):
     args = dict(theta=A, phi=A, doc=A, word=A, u=A, z=A, N=10, M=3, V=5, K=8)
     args.update(kw)
     f = getattr(lib, fn)
+    if fn == "lda_draw_butterfly_variant":
+        return f(args["theta"], args["phi"], args["doc"], args["word"], args["u"],
+                 args["z"], args["N"], args["M"], args["V"], args["K"],
+                 args.get("variant", 2), None)
     if fn == "lda_butterfly_table":
         return f(args["theta"], args["phi"], args["doc"], args["word"],
                  args["z"], args["N"], args["M"], args["V"], args["K"], None)
@@ -75,7 +79,7 @@ def call(lib, fn, **kw):
 
 
 FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_draw_docs",
-       "lda_butterfly_table"]
+       "lda_draw_butterfly_variant", "lda_butterfly_table"]
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -107,6 +111,16 @@ def test_empty_is_noop(lib, fn):
     # N = 0: no launch, no pointer needed
     assert call(lib, fn, N=0, theta=None, phi=None, doc=None, word=None,
                 u=None, z=None) == 0
+
+
+def test_variant_codes(lib):
+    from paper_1505_03851_amd._lib import STATUS, VARIANTS
+    assert sorted(VARIANTS.values()) == [0, 1, 2]
+    for bad in (-1, 3, 99):
+        assert call(lib, "lda_draw_butterfly_variant", variant=bad) == \
+            STATUS["LDA_ERR_UNSUPPORTED"]
+    # a known variant still goes through the argument checks
+    assert call(lib, "lda_draw_butterfly_variant", variant=0, K=0) == STATUS["LDA_ERR_SHAPE"]
 
 
 def test_docs_offsets_need_8_byte_alignment(lib):

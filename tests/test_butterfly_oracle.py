@@ -119,3 +119,98 @@ def test_search_over_butterfly_table_equals_definition(W):
             ids = np.arange(W, dtype=np.int32)
             z_def, band = oracle.draw_np(th, ph, ids, ids, u, band_rel=1e-12)
             assert ((z_sim == z_def) | band).all(), (W, K, z_sim, z_def)
+
+
+# ---------------------------------------------------------------------------
+# The alternative replacement [a b; c d] -> [a c; a+b c+d] (Section 4, the
+# rule the paper says also works but costs more instructions on its GPU).
+
+@pytest.mark.parametrize("W", [2, 4, 8, 16, 32, 64])
+def test_alt_closed_form_equals_replacement_process(W):
+    tab = bf.apply_replacements(bf.transposed_products(W),
+                                bf.replacement_schedule(W), alt=True)
+    for i in range(W):
+        for j in range(W):
+            z = tab[i][j]
+            assert (z.thread, z.lo, z.hi) == bf.closed_form_alt(i, j)
+    assert all(bf.closed_form_alt(W - 1, j) == (j, 0, W - 1) for j in range(W))
+
+
+@pytest.mark.parametrize("W", [2, 4, 8, 16, 32, 64])
+def test_alt_entries_are_left_halves_of_aligned_ranges(W):
+    """Every entry above the last row sums the left half of an aligned range
+    of 2**(s+1) topics (s = trailing ones of the row), and every thread finds
+    each left half it can descend through exactly once."""
+    seen = {}
+    for i in range(W - 1):
+        for j in range(W):
+            t, lo, hi = bf.closed_form_alt(i, j)
+            size = hi - lo + 1
+            assert size & (size - 1) == 0 and lo % (2 * size) == 0
+            assert ((i + 1) & ~i) == size      # row i has s trailing ones
+            seen.setdefault(t, []).append((lo, hi))
+    for t in range(W):
+        want = sorted((lo, lo + size - 1) for size in (1 << s for s in range(W.bit_length() - 1))
+                      for lo in range(0, W, 2 * size))
+        assert sorted(seen[t]) == want
+
+
+def test_alt_w2_holds_each_lanes_own_prefix():
+    """With two lanes the alternative table is the untransposed prefix table:
+    column j holds thread j's sums over topics 0..0 and 0..1."""
+    for j in range(2):
+        assert [bf.closed_form_alt(i, j) for i in range(2)] == [(j, 0, 0), (j, 0, 1)]
+    assert bf.closed_form(0, 1) == (1, 1, 1)        # the paper's rule does not
+
+
+@pytest.mark.parametrize("W", [8, 16, 64])
+@pytest.mark.parametrize("K_extra", [0, 3])
+def test_alt_numeric_table_equals_replacement(W, K_extra):
+    rng = np.random.default_rng(7 * W + K_extra)
+    K = 3 * W + K_extra
+    a = rng.random((W, K))
+    p = bf.table_alt_fp64(a, W)
+    R = K % W
+    for base in range(R, K, W):
+        blk = [[a[t, base + c] for c in range(W)] for t in range(W)]
+        tab = bf.apply_replacements(blk, bf.replacement_schedule(W), alt=True)
+        for i in range(W - 1):
+            for j in range(W):
+                assert abs(tab[i][j] - p[j, base + i]) <= 1e-12 * (1 + abs(p[j, base + i]))
+
+
+@pytest.mark.parametrize("W", [2, 4, 8, 16, 32, 64])
+def test_alt_search_equals_definition(W):
+    rng = np.random.default_rng(300 + W)
+    for K in sorted({1, 3, max(1, W - 1), W, W + 1, 19, 2 * W, 2 * W + 3, 5 * W + 7}):
+        for rep in range(3):
+            th = rng.random((W, K)).astype(np.float32)
+            ph = rng.random((W, K)).astype(np.float32)
+            th[rng.random((W, K)) < 0.3] = 0
+            if rep == 2:
+                th[0] = 0
+            u = (rng.integers(0, 1 << 24, W) * 2.0 ** -24).astype(np.float32)
+            a = th.astype(np.float64) * ph.astype(np.float64)
+            z_alt = bf.search_alt_sim(bf.table_alt_fp64(a, W), u, W)
+            ids = np.arange(W, dtype=np.int32)
+            z_def, band = oracle.draw_np(th, ph, ids, ids, u, band_rel=1e-12)
+            assert ((z_alt == z_def) | band).all(), (W, K, z_alt, z_def)
+
+
+def test_alt_search_needs_the_alt_table():
+    """Run over the paper's table, the descent draws wrong topics: the two
+    tables differ, so the pins above are not vacuous."""
+    W, K = 8, 24
+    rng = np.random.default_rng(1)
+    a = rng.random((W, K))
+    u = rng.random(W)
+    ids = np.arange(W, dtype=np.int32)
+    wrong = 0
+    for rep in range(20):
+        u = rng.random(W).astype(np.float32)
+        a32 = rng.random((W, K)).astype(np.float32)
+        a = a32.astype(np.float64)
+        z_def, _ = oracle.draw_np(a32, np.ones((W, K), np.float32), ids, ids, u)
+        wrong += (bf.search_alt_sim(bf.table_fp64(a, W), u, W) != z_def).sum()
+        assert (bf.search_alt_sim(bf.table_alt_fp64(a, W), u, W) == z_def).all()
+    assert wrong > 0

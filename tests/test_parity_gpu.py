@@ -1,4 +1,4 @@
-"""GPU parity: both kernels against the CPU oracle, through the C ABI.
+"""GPU parity: every kernel against the CPU oracle, through the C ABI.
 
 Rule: z equals the oracle's bit for bit except at tokens where
 |u*S - S_k| <= 1e-5 * S for some k (fp32 rounding may move such a draw to a
@@ -15,7 +15,8 @@ from parity import MAX_MISMATCH_RATE, compare, run_kernel, to_device
 
 pytestmark = pytest.mark.gpu
 
-KERNELS = ["naive", "butterfly", "transposed"]
+KERNELS = ["naive", "butterfly", "transposed",
+           "variant-register", "variant-lds", "variant-lds_alt"]
 
 
 def _check(c, kernel, idx=None, rate=True):
