@@ -65,7 +65,7 @@ def upload(c):
 
 
 # kernels bench.py can time: name -> entry point of the binding
-KERNELS = ("butterfly", "naive", "transposed", "docs",
+KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
            "variant-register", "variant-lds", "variant-lds_alt")
 
 
@@ -76,6 +76,10 @@ def launcher(kernel: str, dev):
     if kernel == "docs":
         off = dev["doc_offsets"]
         return lambda out, stream: lda.draw_docs(th, ph, off, w, u, out=out, stream=stream)
+    if kernel in ("doc_lanes", "doc_lanes_cache"):
+        off, cache = dev["doc_offsets"], kernel == "doc_lanes_cache"
+        return lambda out, stream: lda.draw_doc_lanes(th, ph, off, w, u, theta_cache=cache,
+                                                      out=out, stream=stream)
     if kernel.startswith("variant-"):
         v = kernel[len("variant-"):]
         return lambda out, stream: lda.draw_variant(th, ph, d, w, u, variant=v, out=out,
@@ -230,12 +234,13 @@ def k_sweep(args) -> int:
         c = make_corpus(wiki_shaped(K))
         dev = upload(c)
         rec = {"workload": c.name, "K": K, "N": c.N}
-        for kernel in ("naive", "transposed", "butterfly"):
+        for kernel in ("naive", "transposed", "doc_lanes", "doc_lanes_cache", "butterfly"):
             r = measure(c.name, c, dev, kernel, args.steps, args.warmup)
             rec[kernel + "_ms"] = r["ms_per_launch"]
             rec[kernel + "_draws_per_s"] = r["draws_per_s"]
         rec["speedup"] = rec["naive_ms"] / rec["butterfly_ms"]
         rec["speedup_vs_transposed"] = rec["transposed_ms"] / rec["butterfly_ms"]
+        rec["speedup_vs_doc_lanes"] = rec["doc_lanes_ms"] / rec["butterfly_ms"]
         print(json.dumps(rec), flush=True)
         del dev
         torch.cuda.empty_cache()
@@ -245,7 +250,7 @@ def k_sweep(args) -> int:
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
     registers or LDS, the alternative rule in LDS), the offsets form of the
-    documents and the default dispatch, on the two corpora and the corpus
+    documents, the document-per-lane driver and the default dispatch, on the two corpora and the corpus
     shaped like the paper's at K = 80 and 240; one JSON line per workload.
     z of every variant is compared with the default kernel's (identical
     unless a token lies in the fp32 rounding band)."""
@@ -257,8 +262,9 @@ def ablation(args) -> int:
         dev = upload(c)
         rec = {"workload": name, "N": c.N, "K": c.K}
         z_ref = None
-        for kernel in ("butterfly", "variant-register", "variant-lds",
-                       "variant-lds_alt", "docs"):
+        kernels = ["butterfly", "variant-register", "variant-lds", "variant-lds_alt",
+                   "docs", "doc_lanes"] + (["doc_lanes_cache"] if c.K <= 256 else [])
+        for kernel in kernels:
             r = measure(name, c, dev, kernel, args.steps, args.warmup)
             z = r.pop("z")
             if z_ref is None:

@@ -118,6 +118,30 @@ int lda_draw_docs(const float *theta, const float *phi,
                   int32_t K, void *stream);
 
 /*
+ * The paper's document-per-lane driver (Algorithm 7): 64 consecutive
+ * documents form a group, one per lane, and a master index walks their
+ * tokens in step; a lane whose document has run out repeats its last token
+ * (without storing) until the group's longest document is done.  Each
+ * group's master loop is split over several wavefronts (index i = s, s + S,
+ * ...) so that the launch fills the GPU.  Arguments, layout and errors as
+ * lda_draw_docs (doc_offsets int64 [M + 1], 8-byte aligned; out-of-range
+ * offsets are clamped to [0, N], never dereferenced), plus:
+ *   theta_cache  0: theta is read from memory in every iteration;
+ *                1: Algorithm 5's cache -- each wavefront first copies its
+ *                   documents' theta rows into LDS in transposed order; only
+ *                   for K up to LDA_DOC_LANES_MAX_CACHE_BYTES / 256 rounded
+ *                   to whole blocks (K <= 256), else LDA_ERR_UNSUPPORTED.
+ * Same z as lda_draw_docs except inside the fp32 rounding band (the lanes
+ * sum in another order).  Slower than lda_draw_docs: it is provided to
+ * measure the paper's design.
+ */
+#define LDA_DOC_LANES_MAX_CACHE_BYTES 65536
+int lda_draw_doc_lanes(const float *theta, const float *phi,
+                       const int64_t *doc_offsets, const int32_t *word_id,
+                       const float *u, int32_t *z, int64_t N, int32_t M, int32_t V,
+                       int32_t K, int32_t theta_cache, void *stream);
+
+/*
  * Butterfly draw with a chosen per-block table, for measuring the table's
  * design choices (Section 4).  Same arguments, layout and errors as
  * lda_draw_butterfly, plus `variant`:

@@ -7,7 +7,7 @@ library through its C ABI (``include/lda_draw.h``).  The binding is imported
 on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 """
 
-_BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs",
+_BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "draw_doc_lanes",
             "draw_variant", "VARIANTS",
             "butterfly_table",
             "butterfly_width", "status_string", "version", "LdaError",

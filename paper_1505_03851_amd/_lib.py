@@ -40,6 +40,7 @@ _CONSTS = _header_constants()
 STATUS = {k: v for k, v in _CONSTS.items() if k == "LDA_OK" or k.startswith("LDA_ERR_")}
 MAX_K = _CONSTS["LDA_MAX_K"]
 MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
+DOC_LANES_MAX_CACHE_BYTES = _CONSTS["LDA_DOC_LANES_MAX_CACHE_BYTES"]
 # table variants of lda_draw_butterfly_variant, by name
 VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
             "lds": _CONSTS["LDA_VARIANT_LDS_TABLE"],
@@ -66,6 +67,8 @@ def load() -> ctypes.CDLL:
     lib.lda_draw_butterfly_variant.restype = ctypes.c_int
     lib.lda_draw_docs.argtypes = draw_args
     lib.lda_draw_docs.restype = ctypes.c_int
+    lib.lda_draw_doc_lanes.argtypes = draw_args[:-1] + [I32, P]
+    lib.lda_draw_doc_lanes.restype = ctypes.c_int
     lib.lda_butterfly_table.argtypes = [P, P, P, P, P, I64, I32, I32, I32, P]
     lib.lda_butterfly_table.restype = ctypes.c_int
     lib.lda_butterfly_width.argtypes = [I32]
@@ -198,6 +201,22 @@ def draw_docs(theta, phi, doc_offsets, word_id, u, out=None, stream=None,
     document m holds tokens doc_offsets[m] .. doc_offsets[m+1]-1 (int64
     [M+1], doc_offsets[0] = 0, doc_offsets[M] = N, non-decreasing; empty
     documents allowed), the paper's ragged corpus of Section 2."""
+    return _draw_offsets("lda_draw_docs", theta, phi, doc_offsets, word_id, u,
+                         out, stream, validate)
+
+
+def draw_doc_lanes(theta, phi, doc_offsets, word_id, u, theta_cache: bool = False,
+                   out=None, stream=None, validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the paper's document-per-lane driver (Algorithm 7:
+    one document per lane, a master index over their tokens); arguments as
+    ``draw_docs``.  ``theta_cache``: copy each wavefront's theta rows to LDS
+    first (Algorithm 5; K <= 256)."""
+    return _draw_offsets("lda_draw_doc_lanes", theta, phi, doc_offsets, word_id,
+                         u, out, stream, validate, extra=(int(bool(theta_cache)),))
+
+
+def _draw_offsets(fn_name, theta, phi, doc_offsets, word_id, u, out, stream, validate,
+                  extra=()):
     _require(theta, "theta", torch.float32, 2)
     _require(phi, "phi", torch.float32, 2)
     _require(doc_offsets, "doc_offsets", torch.int64, 1)
@@ -228,10 +247,10 @@ def draw_docs(theta, phi, doc_offsets, word_id, u, out=None, stream=None,
         if out.shape[0] != N or out.device != word_id.device:
             raise ValueError("out must be int32[N] on the tensors' device")
     with torch.cuda.device(word_id.device):
-        st = load().lda_draw_docs(
+        st = getattr(load(), fn_name)(
             theta.data_ptr(), phi.data_ptr(), doc_offsets.data_ptr(),
             word_id.data_ptr(), u.data_ptr(), out.data_ptr(), N, M, V, K,
-            _stream_handle(stream))
+            *extra, _stream_handle(stream))
     _check(st)
     return out
 

@@ -42,17 +42,21 @@ def to_device(c, device="cuda"):
 
 
 def run_kernel(kernel: str, dev: dict):
-    """z by ``kernel``; "docs" hands the documents over as offsets (the
-    corpus's documents must be contiguous); "variant-<name>" is the
+    """z by ``kernel``; "docs", "doc_lanes" and "doc_lanes_cache" hand the
+    documents over as offsets (the corpus's documents must be contiguous); "variant-<name>" is the
     butterfly kernel with the named block table."""
     import torch
     import paper_1505_03851_amd as lda
-    if kernel == "docs":
+    if kernel in ("docs", "doc_lanes", "doc_lanes_cache"):
         from paper_1505_03851_amd.inputs import doc_offsets
         off = doc_offsets(dev["doc_id"].cpu().numpy(), dev["theta"].shape[0])
-        z = lda.draw_docs(dev["theta"], dev["phi"],
-                          torch.from_numpy(off).to(dev["theta"].device),
-                          dev["word_id"], dev["u"], validate=True)
+        off = torch.from_numpy(off).to(dev["theta"].device)
+        args = (dev["theta"], dev["phi"], off, dev["word_id"], dev["u"])
+        if kernel == "docs":
+            z = lda.draw_docs(*args, validate=True)
+        else:
+            z = lda.draw_doc_lanes(*args, theta_cache=kernel == "doc_lanes_cache",
+                                   validate=True)
         torch.cuda.synchronize()
         return z.cpu().numpy()
     if kernel.startswith("variant-"):

@@ -71,6 +71,10 @@ def call(lib, fn, **kw):
         return f(args["theta"], args["phi"], args["doc"], args["word"], args["u"],
                  args["z"], args["N"], args["M"], args["V"], args["K"],
                  args.get("variant", 2), None)
+    if fn == "lda_draw_doc_lanes":
+        return f(args["theta"], args["phi"], args["doc"], args["word"], args["u"],
+                 args["z"], args["N"], args["M"], args["V"], args["K"],
+                 args.get("theta_cache", 0), None)
     if fn == "lda_butterfly_table":
         return f(args["theta"], args["phi"], args["doc"], args["word"],
                  args["z"], args["N"], args["M"], args["V"], args["K"], None)
@@ -79,7 +83,7 @@ def call(lib, fn, **kw):
 
 
 FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_draw_docs",
-       "lda_draw_butterfly_variant", "lda_butterfly_table"]
+       "lda_draw_doc_lanes", "lda_draw_butterfly_variant", "lda_butterfly_table"]
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -123,10 +127,24 @@ def test_variant_codes(lib):
     assert call(lib, "lda_draw_butterfly_variant", variant=0, K=0) == STATUS["LDA_ERR_SHAPE"]
 
 
+def test_doc_lanes_theta_cache_limits(lib):
+    from paper_1505_03851_amd._lib import DOC_LANES_MAX_CACHE_BYTES, STATUS
+    fn = "lda_draw_doc_lanes"
+    for bad in (-1, 2):
+        assert call(lib, fn, theta_cache=bad) == STATUS["LDA_ERR_UNSUPPORTED"]
+    # the cache holds K rounded up to 64-topic blocks, 64 lanes x 4 bytes each
+    kmax = DOC_LANES_MAX_CACHE_BYTES // 256
+    assert kmax == 256
+    assert call(lib, fn, theta_cache=1, K=kmax + 1, N=0) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert call(lib, fn, theta_cache=1, K=kmax, N=0) == 0
+    assert call(lib, fn, theta_cache=0, K=4096, N=0) == 0
+
+
 def test_docs_offsets_need_8_byte_alignment(lib):
     # doc_offsets is int64: 4-byte aligned is not enough
     from paper_1505_03851_amd._lib import STATUS
-    assert call(lib, "lda_draw_docs", doc=A + 4) == STATUS["LDA_ERR_ALIGN"]
+    for fn in ("lda_draw_docs", "lda_draw_doc_lanes"):
+        assert call(lib, fn, doc=A + 4) == STATUS["LDA_ERR_ALIGN"]
 
 
 def test_width(lib):

@@ -164,19 +164,40 @@ def test_degenerate_weights(K, kernel):
 
 
 # ---------------------------------------------------------------------------
-# Documents as offsets (the ragged corpus of Section 2): same kernels, each
-# lane finds its document in the offsets.
+# Documents as offsets (the ragged corpus of Section 2): "docs" runs the
+# token-per-lane kernels, each lane finding its document in the offsets;
+# "doc_lanes" is Algorithm 7's document-per-lane driver.
 
+OFFSET_KERNELS = ["docs", "doc_lanes", "doc_lanes_cache"]
+
+
+def _offset_check(c, kernel, **kw):
+    """As _check; the theta cache of the document-per-lane driver takes
+    K <= 256 and must refuse larger K."""
+    if kernel == "doc_lanes_cache" and c.K > 256:
+        import paper_1505_03851_amd as lda
+        with pytest.raises(lda.LdaError) as e:
+            run_kernel(kernel, to_device(c))
+        assert e.value.status == lda.STATUS["LDA_ERR_UNSUPPORTED"]
+        return None
+    return _check(c, kernel, **kw)
+
+
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
 @pytest.mark.parametrize("name", ["tiny-K32", "corpus1M-K64", "corpus1M-K256"])
-def test_docs_config_every_token(name):
+def test_docs_config_every_token(name, kernel):
     c = corpus(name)
-    _check(c, "docs", rate=c.N >= 1 << 20)
+    _offset_check(c, kernel, rate=c.N >= 1 << 20)
 
 
-@pytest.mark.parametrize("K", [16, 240])
-def test_docs_wiki_shaped_every_token(K):
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
+@pytest.mark.parametrize("K", [16, 80, 144, 240])
+def test_docs_wiki_shaped_every_token(K, kernel):
+    """Lognormal document lengths of 1..307 tokens: for the document-per-lane
+    driver most lanes of a wavefront repeat their last token for many
+    iterations."""
     from paper_1505_03851_amd.inputs import wiki_shaped
-    _check(corpus(wiki_shaped(K).name), "docs")
+    _offset_check(corpus(wiki_shaped(K).name), kernel)
 
 
 def test_docs_full_size_equals_doc_ids():
@@ -196,6 +217,19 @@ def test_docs_full_size_equals_doc_ids():
     assert rep.hard == 0, rep.first_hard
 
 
+@pytest.mark.parametrize("name", ["corpus16M-K1024", "poisson300-K2048"])
+def test_doc_lanes_full_size_sampled(name):
+    """The document-per-lane driver on the full-size corpora (fixed and
+    Poisson(300) lengths), sampled against the oracle, with the first and
+    last tokens of every sampled document."""
+    c = corpus(name)
+    rng = np.random.default_rng(13)
+    idx = np.unique(np.concatenate([
+        rng.choice(c.N, size=1 << 19, replace=False),
+        np.arange(256), np.arange(c.N - 300, c.N)]))
+    _check(c, "doc_lanes", idx=idx)
+
+
 RAGGED = [
     # (N, M, V, K): Dirichlet(0.3) lengths, many documents empty
     (1, 3, 7, 64),
@@ -203,32 +237,36 @@ RAGGED = [
     (64 * 9 + 17, 200, 300, 19),
     (64 * 21 + 5, 2000, 300, 64),     # more documents than tokens
     (64 * 21 + 5, 40, 300, 65),
+    (64 * 33 + 63, 60, 500, 128),
+    (64 * 33 + 63, 60, 500, 129),
     (64 * 33 + 63, 60, 500, 200),
     (64 * 9 + 33, 40, 100, 256),      # four-topic-leaf kernel
     (64 * 7 + 5, 300, 90, 1280),
     (64 * 17 + 9, 60, 500, 2047),
     (64 * 5 + 3, 20, 200, 4096),
+    (64 * 40, 130, 400, 96),          # M past two full wavefronts of documents
 ]
 
 
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
 @pytest.mark.parametrize("shape", RAGGED, ids=lambda s: "N{}-M{}-K{}".format(s[0], s[1], s[3]))
-def test_docs_ragged(shape):
+def test_docs_ragged(shape, kernel):
     N, M, V, K = shape
     c = make_random(N, M, V, K, seed=N + M + K, doc_order="ragged")
-    z_docs = run_kernel("docs", to_device(c))
-    _check(c, "butterfly", rate=False)
-    rep = compare(c, z_docs)
-    print(f"[parity] {c.name} docs: {rep}", flush=True)
-    assert rep.hard == 0, rep.first_hard
-    z_ids = run_kernel("butterfly", to_device(c))
-    assert (z_docs == z_ids).all()
+    _offset_check(c, kernel, rate=False)
+    if kernel == "docs":
+        # same kernel as the doc-id form: identical z
+        assert (run_kernel("docs", to_device(c)) == run_kernel("butterfly", to_device(c))).all()
 
 
-def test_docs_empty_corpus_and_empty_documents():
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
+def test_docs_empty_corpus_and_empty_documents(kernel):
     """N = 0 is a no-op; documents before, between and after the tokens
     may be empty."""
     import torch
     import paper_1505_03851_amd as lda
+    fn = {"docs": lda.draw_docs, "doc_lanes": lda.draw_doc_lanes,
+          "doc_lanes_cache": lambda *a, **k: lda.draw_doc_lanes(*a, theta_cache=True, **k)}[kernel]
     K, V = 48, 30
     rng = np.random.default_rng(5)
     theta = torch.from_numpy(rng.random((6, K), dtype=np.float32)).cuda()
@@ -236,18 +274,21 @@ def test_docs_empty_corpus_and_empty_documents():
     off = torch.tensor([0, 0, 0, 0, 0, 0, 0], dtype=torch.int64, device="cuda")
     empty_i = torch.empty(0, dtype=torch.int32, device="cuda")
     empty_f = torch.empty(0, dtype=torch.float32, device="cuda")
-    assert lda.draw_docs(theta, phi, off, empty_i, empty_f, validate=True).numel() == 0
+    assert fn(theta, phi, off, empty_i, empty_f, validate=True).numel() == 0
     N = 100
     doc = np.repeat(np.arange(6), [0, 0, 37, 0, 63, 0]).astype(np.int32)
     word = rng.integers(0, V, N).astype(np.int32)
     u = _grid_u(N, 3)
     c = _corpus(theta.cpu().numpy(), phi.cpu().numpy(), doc, word, u, "empty-docs")
-    _check(c, "docs", rate=False)
+    _check(c, kernel, rate=False)
 
 
-def test_docs_rejects_bad_offsets():
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
+def test_docs_rejects_bad_offsets(kernel):
     import torch
     import paper_1505_03851_amd as lda
+    fn = {"docs": lda.draw_docs, "doc_lanes": lda.draw_doc_lanes,
+          "doc_lanes_cache": lambda *a, **k: lda.draw_doc_lanes(*a, theta_cache=True, **k)}[kernel]
     theta = torch.ones((3, 8), device="cuda")
     phi = torch.ones((4, 8), device="cuda")
     w = torch.zeros(5, dtype=torch.int32, device="cuda")
@@ -255,9 +296,26 @@ def test_docs_rejects_bad_offsets():
     for bad in ([0, 2, 1, 5], [1, 2, 3, 5], [0, 1, 2, 4]):
         off = torch.tensor(bad, dtype=torch.int64, device="cuda")
         with pytest.raises(ValueError):
-            lda.draw_docs(theta, phi, off, w, u, validate=True)
+            fn(theta, phi, off, w, u, validate=True)
     with pytest.raises(ValueError):   # M + 1 entries
-        lda.draw_docs(theta, phi, torch.zeros(3, dtype=torch.int64, device="cuda"), w, u)
+        fn(theta, phi, torch.zeros(3, dtype=torch.int64, device="cuda"), w, u)
+
+
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
+@pytest.mark.parametrize("K", [8, 64, 256, 1024])
+def test_docs_equal_power_of_two_weights_exact(K, kernel):
+    """Equal weights 2**-3 in ragged documents: z = floor(u*K) exactly."""
+    N = 64 * 37 + 11
+    u = _grid_u(N, K + 7)
+    doc = make_random(N, 97, 5, 1, seed=K, doc_order="ragged").doc_id
+    c = _corpus(np.full((97, K), 2.0 ** -3), np.ones((5, K)), doc,
+                np.arange(N) % 5, u, f"pow2-ragged-K{K}")
+    print(f"[case] {c.name} kernel={kernel}", flush=True)
+    if kernel == "doc_lanes_cache" and K > 256:
+        return
+    z = run_kernel(kernel, to_device(c))
+    expect = np.floor(u.astype(np.float64) * K).astype(np.int32)
+    assert (z == expect).all(), np.nonzero(z != expect)[0][:10]
 
 
 @pytest.mark.parametrize("K", [32, 50, 64, 83, 200, 1024])
