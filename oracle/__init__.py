@@ -14,7 +14,10 @@ Contents
   butterfly             the butterfly-patterned table of Section 4, three ways:
                         its closed form, the replacement process that builds it,
                         and a lane-vector simulation of the search over it
-                        (Algorithms 9 and 10).
+                        (Algorithms 9 and 10), and the table and descent search
+                        of the alternative replacement rule.
+  philox                Philox4x32-10 / 4x64-10 from their published definition
+                        and the per-token uniforms of the fused-RNG draw.
 """
 from __future__ import annotations
 
@@ -24,6 +27,7 @@ import os
 import numpy as np
 
 from . import butterfly  # noqa: F401  (re-exported)
+from . import philox  # noqa: F401  (re-exported)
 
 BAND_REL = 1e-5  # width of the rounding band, relative to the token's total
 
