@@ -66,13 +66,17 @@ def upload(c):
 
 # kernels bench.py can time: name -> entry point of the binding
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
-           "variant-register", "variant-lds", "variant-lds_alt")
+           "variant-register", "variant-lds", "variant-lds_alt", "philox")
+PHILOX_SEED = 0x5EED20150513
 
 
 def launcher(kernel: str, dev):
     """A function (out, stream) that launches ``kernel`` once over ``dev``."""
     import paper_1505_03851_amd as lda
     th, ph, d, w, u = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    if kernel == "philox":
+        return lambda out, stream: lda.draw_philox(th, ph, d, w, PHILOX_SEED, 0, out=out,
+                                                   stream=stream)
     if kernel == "docs":
         off = dev["doc_offsets"]
         return lambda out, stream: lda.draw_docs(th, ph, off, w, u, out=out, stream=stream)
@@ -250,7 +254,8 @@ def k_sweep(args) -> int:
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
     registers or LDS, the alternative rule in LDS), the offsets form of the
-    documents, the document-per-lane driver and the default dispatch, on the two corpora and the corpus
+    documents, the document-per-lane driver, the draw with in-kernel
+    uniforms and the default dispatch, on the two corpora and the corpus
     shaped like the paper's at K = 80 and 240; one JSON line per workload.
     z of every variant is compared with the default kernel's (identical
     unless a token lies in the fp32 rounding band)."""
@@ -263,14 +268,16 @@ def ablation(args) -> int:
         rec = {"workload": name, "N": c.N, "K": c.K}
         z_ref = None
         kernels = ["butterfly", "variant-register", "variant-lds", "variant-lds_alt",
-                   "docs", "doc_lanes"] + (["doc_lanes_cache"] if c.K <= 256 else [])
+                   "docs", "doc_lanes"] + (["doc_lanes_cache"] if c.K <= 256 else []) + \
+                  ["philox"]
         for kernel in kernels:
             r = measure(name, c, dev, kernel, args.steps, args.warmup)
             z = r.pop("z")
             if z_ref is None:
                 z_ref = z
             rec[kernel + "_ms"] = r["ms_per_launch"]
-            rec[kernel + "_differs"] = int((z != z_ref).sum())
+            if kernel != "philox":   # (other uniforms: z is not comparable)
+                rec[kernel + "_differs"] = int((z != z_ref).sum())
         print(json.dumps(rec), flush=True)
         del dev
         torch.cuda.empty_cache()

@@ -142,6 +142,30 @@ int lda_draw_doc_lanes(const float *theta, const float *phi,
                        int32_t K, int32_t theta_cache, void *stream);
 
 /*
+ * Butterfly draw with the uniforms generated in the kernel (Algorithm 1's
+ * draw of u inside the procedure; the paper names no generator): token n
+ * takes u = (y >> 8) * 2^-24, y the first output word of Philox4x32-10
+ * (Salmon, Moraes, Dror and Shaw, SC 2011) with key (seed mod 2^32,
+ * seed >> 32) and counter (n mod 2^32, n >> 32, sweep, 0).  Arguments,
+ * layout, dispatch and errors as lda_draw_butterfly without u; a caller
+ * passes a new `sweep` (or seed) for every pass over the corpus.  The
+ * result equals lda_draw_butterfly given u from lda_philox_uniforms.
+ */
+int lda_draw_butterfly_philox(const float *theta, const float *phi,
+                              const int32_t *doc_id, const int32_t *word_id,
+                              int32_t *z, int64_t N, int32_t M, int32_t V,
+                              int32_t K, uint64_t seed, uint32_t sweep, void *stream);
+
+/*
+ * The uniforms lda_draw_butterfly_philox uses, written out: u[i] (device,
+ * float32 [count], 4-byte aligned) = uniform of token first + i for `seed`
+ * and `sweep`.  count = 0 is a no-op; negative count or first, or
+ * first + count past INT64_MAX, is LDA_ERR_SHAPE.
+ */
+int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
+                        uint32_t sweep, void *stream);
+
+/*
  * Butterfly draw with a chosen per-block table, for measuring the table's
  * design choices (Section 4).  Same arguments, layout and errors as
  * lda_draw_butterfly, plus `variant`:

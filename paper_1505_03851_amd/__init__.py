@@ -8,6 +8,7 @@ on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 """
 
 _BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "draw_doc_lanes",
+            "draw_philox", "philox_uniforms",
             "draw_variant", "VARIANTS",
             "butterfly_table",
             "butterfly_width", "status_string", "version", "LdaError",

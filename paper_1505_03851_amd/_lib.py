@@ -65,6 +65,11 @@ def load() -> ctypes.CDLL:
         getattr(lib, name).restype = ctypes.c_int
     lib.lda_draw_butterfly_variant.argtypes = draw_args[:-1] + [I32, P]
     lib.lda_draw_butterfly_variant.restype = ctypes.c_int
+    lib.lda_draw_butterfly_philox.argtypes = [P, P, P, P, P, I64, I32, I32, I32,
+                                              ctypes.c_uint64, ctypes.c_uint32, P]
+    lib.lda_draw_butterfly_philox.restype = ctypes.c_int
+    lib.lda_philox_uniforms.argtypes = [P, I64, I64, ctypes.c_uint64, ctypes.c_uint32, P]
+    lib.lda_philox_uniforms.restype = ctypes.c_int
     lib.lda_draw_docs.argtypes = draw_args
     lib.lda_draw_docs.restype = ctypes.c_int
     lib.lda_draw_doc_lanes.argtypes = draw_args[:-1] + [I32, P]
@@ -193,6 +198,47 @@ def draw_variant(theta, phi, doc_id, word_id, u, variant: str = "register",
         raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
     return _draw("lda_draw_butterfly_variant", theta, phi, doc_id, word_id, u,
                  out, stream, validate, extra=(VARIANTS[variant],))
+
+
+def draw_philox(theta, phi, doc_id, word_id, seed: int, sweep: int = 0, out=None,
+                stream=None, validate: bool = False) -> torch.Tensor:
+    """z[N] (int32) by the butterfly kernel with the uniforms generated in the
+    kernel (Philox4x32-10 of token index, sweep and seed; see
+    ``philox_uniforms``)."""
+    N, M, V, K = _shapes(theta, phi, doc_id, word_id)
+    if validate:
+        _validate_ids(doc_id, word_id, M, V)
+    if out is None:
+        out = torch.empty(N, dtype=torch.int32, device=doc_id.device)
+    else:
+        _require(out, "out", torch.int32, 1)
+        if out.shape[0] != N or out.device != doc_id.device:
+            raise ValueError("out must be int32[N] on the tensors' device")
+    with torch.cuda.device(doc_id.device):
+        st = load().lda_draw_butterfly_philox(
+            theta.data_ptr(), phi.data_ptr(), doc_id.data_ptr(), word_id.data_ptr(),
+            out.data_ptr(), N, M, V, K, int(seed) & (2 ** 64 - 1),
+            int(sweep) & (2 ** 32 - 1), _stream_handle(stream))
+    _check(st)
+    return out
+
+
+def philox_uniforms(count: int, seed: int, sweep: int = 0, first: int = 0, out=None,
+                    device="cuda", stream=None) -> torch.Tensor:
+    """The uniforms of tokens first .. first + count - 1 that ``draw_philox``
+    uses (float32 [count] on the GPU)."""
+    if out is None:
+        out = torch.empty(int(count), dtype=torch.float32, device=device)
+    else:
+        _require(out, "out", torch.float32, 1)
+        if out.shape[0] != count:
+            raise ValueError("out must be float32[count]")
+    with torch.cuda.device(out.device):
+        st = load().lda_philox_uniforms(out.data_ptr(), int(count), int(first),
+                                        int(seed) & (2 ** 64 - 1),
+                                        int(sweep) & (2 ** 32 - 1), _stream_handle(stream))
+    _check(st)
+    return out
 
 
 def draw_docs(theta, phi, doc_offsets, word_id, u, out=None, stream=None,

@@ -6,6 +6,8 @@
 // lda_draw_doc_lanes  Algorithm 7's document-per-lane driver.
 // lda_draw_transposed Algorithms 4-6, for comparison.
 // lda_draw_butterfly_variant  the block-table variants of Section 4.
+// lda_draw_butterfly_philox   the butterfly draw with in-kernel uniforms.
+// lda_philox_uniforms         those uniforms, written out.
 // lda_butterfly_table the butterfly-patterned tables (Fig. 1, right).
 #include <hip/hip_runtime.h>
 
@@ -13,6 +15,7 @@
 
 #include "butterfly.hpp"
 #include "lda_draw.h"
+#include "philox.hpp"
 
 // Build-time tuning of the butterfly kernel (chosen by measurement on MI355X):
 //   LDA_LDS_TABLE_MAX_BLOCKS  largest K / W whose rebuilt table goes to LDS
@@ -77,6 +80,18 @@ struct DocSource {
   }
 };
 
+// Where a token's uniform comes from: the caller's array u[N], or (u null)
+// Philox4x32-10 with key (k0, k1) at counter (n mod 2^32, n / 2^32, sweep, 0),
+// whose first output word's top 24 bits, times 2^-24, give the uniform.
+struct UniformSource {
+  const float *u;
+  uint32_t k0, k1, sweep;
+  __device__ __forceinline__ float operator()(int64_t n) const {
+    if (u) return u[n];
+    return philox_uniform((uint64_t)n, sweep, k0, k1);
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Naive kernel (Algorithm 1 with Algorithm 3).  Lane n walks the K topics of
 // its own token, keeps the full prefix table p[K] in its private segment and
@@ -84,7 +99,7 @@ struct DocSource {
 template <int KMAX>
 __global__ __launch_bounds__(256) void naive_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
-    const int32_t *__restrict__ word_id, const float *__restrict__ u,
+    const int32_t *__restrict__ word_id, UniformSource u,
     int32_t *__restrict__ z, int64_t N, int K) {
   const int64_t n = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (n >= N) return;
@@ -96,7 +111,7 @@ __global__ __launch_bounds__(256) void naive_kernel(
     sum = prefix_step(sum, th[k], ph[k]);
     p[k] = sum;
   }
-  const float stop = sum * u[n];
+  const float stop = sum * u(n);
   int j = 0, hi = K - 1;
   while (j < hi) {
     const int mid = (j + hi) >> 1;
@@ -441,7 +456,7 @@ template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
-    const int32_t *__restrict__ word_id, const float *__restrict__ u,
+    const int32_t *__restrict__ word_id, UniformSource u,
     int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_bytes, uint32_t phi_bytes) {
   static_assert(!ALT || LDS_TABLE, "the alternative table is searched in LDS");
   extern __shared__ float lds[];
@@ -462,7 +477,7 @@ void butterfly_kernel(
 
   const int doc = docs(n);
   const int word = word_id[n];
-  const float un = u[n];
+  const float un = u(n);
   // blocks of W topics; a remnant of K mod W topics becomes block 0, padded
   // at its front with empty topics
   const int NB = (K + W - 1) >> LOG2W;
@@ -682,7 +697,7 @@ template <bool SMALL, int C>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_LEAF4_WAVES_PER_EU)))
 void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                        DocSource docs, const int32_t *__restrict__ word_id,
-                       const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
+                       UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
   const int lane = lane_id();
@@ -697,7 +712,7 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
 
   const int doc = docs(n);
   const int word = word_id[n];
-  const float un = u[n];
+  const float un = u(n);
   const int NB = K / kBlock4;
   Wave<kWave, SMALL> w;
   init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
@@ -790,7 +805,7 @@ template <bool SMALL>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void transposed_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                        DocSource docs, const int32_t *__restrict__ word_id,
-                       const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int K,
+                       UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
   const int lane = lane_id();
@@ -804,7 +819,7 @@ void transposed_kernel(const float *__restrict__ theta, const float *__restrict_
 
   const int doc = docs(n);
   const int word = word_id[n];
-  const float un = u[n];
+  const float un = u(n);
   const int NB = (K + kWave - 1) / kWave;  // the remnant is block 0, padded
   Wave<kWave, SMALL> w;
   init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
@@ -952,7 +967,7 @@ template <int W, bool THETA_LDS>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                       const int64_t *__restrict__ offsets, const int32_t *__restrict__ word_id,
-                      const float *__restrict__ u, int32_t *__restrict__ z, int64_t N, int M,
+                      UniformSource u, int32_t *__restrict__ z, int64_t N, int M,
                       int K, int S, uint32_t theta_bytes, uint32_t phi_bytes) {
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
@@ -1005,7 +1020,7 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
     const int64_t n = len > 0 ? start + (i < len ? i : len - 1) : 0;
     const bool store = i < len;
     w.ph_lane = (uint32_t)word_id[n] * w.row_bytes;
-    const float un = u[n];
+    const float un = u(n);
 
     float a[W];
     float sum = 0.0f, stop, low, high;
@@ -1057,6 +1072,15 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
 }
 
 // ---------------------------------------------------------------------------
+// The in-kernel uniforms written out: u[i] = uniform of token first + i.
+__global__ __launch_bounds__(256) void uniforms_kernel(float *__restrict__ u, int64_t count,
+                                                       int64_t first, UniformSource us) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    u[i] = us(first + i);
+}
+
+// ---------------------------------------------------------------------------
 thread_local hipError_t g_last_hip = hipSuccess;
 
 int check_args(const void *theta, const void *phi, const void *doc_id,
@@ -1105,14 +1129,14 @@ dim3 wave_grid(int64_t N) {
 
 template <int KMAX>
 void launch_naive(const float *theta, const float *phi, DocSource d, const int32_t *w,
-                  const float *u, int32_t *z, int64_t N, int32_t K, hipStream_t s) {
+                  UniformSource u, int32_t *z, int64_t N, int32_t K, hipStream_t s) {
   const dim3 grid((unsigned)((N + 255) / 256));
   naive_kernel<KMAX><<<grid, 256, 0, s>>>(theta, phi, d, w, u, z, N, K);
 }
 
 template <int C>
 void launch_butterfly4(const float *theta, const float *phi, DocSource d,
-                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
+                       const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const size_t lds = (size_t)kWavesPerBlock * (K / kBlock4) * kWave * sizeof(float);
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
@@ -1126,7 +1150,7 @@ void launch_butterfly4(const float *theta, const float *phi, DocSource d,
 }
 
 void launch_transposed(const float *theta, const float *phi, DocSource d,
-                       const int32_t *wd, const float *u, int32_t *z, int64_t N,
+                       const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + kWave - 1) / kWave;
   const size_t lds = (size_t)kWavesPerBlock * (kTileFloats + nb * kWave) * sizeof(float);
@@ -1142,7 +1166,7 @@ void launch_transposed(const float *theta, const float *phi, DocSource d,
 
 template <int W, bool LDS_TABLE, bool ALT = false>
 void launch_butterfly(const float *theta, const float *phi, DocSource d,
-                      const int32_t *wd, const float *u, int32_t *z, int64_t N,
+                      const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + W - 1) / W;  // blocks, the remnant included
   const size_t lds = (size_t)kWavesPerBlock * region_rows(nb, W, LDS_TABLE) *
@@ -1162,7 +1186,7 @@ void launch_butterfly(const float *theta, const float *phi, DocSource d,
 // rule's table in LDS.
 template <bool LDS_TABLE, bool ALT>
 void launch_table_variant(const float *theta, const float *phi, DocSource d,
-                          const int32_t *word_id, const float *u, int32_t *z, int64_t N,
+                          const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                           int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (width_for(K) == 64)
     launch_butterfly<64, LDS_TABLE, ALT>(theta, phi, d, word_id, u, z, N, M, V, K, s);
@@ -1197,7 +1221,7 @@ int doc_lanes_split(int64_t N, int32_t M) {
 
 template <int W, bool THETA_LDS>
 void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
-                      const int32_t *wd, const float *u, int32_t *z, int64_t N, int32_t M,
+                      const int32_t *wd, UniformSource u, int32_t *z, int64_t N, int32_t M,
                       int32_t V, int32_t K, hipStream_t s) {
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
@@ -1210,7 +1234,7 @@ void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
 
 // The butterfly draw for either document source (kernel choice by K).
 void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
-                        const int32_t *word_id, const float *u, int32_t *z, int64_t N,
+                        const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
     launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, d, word_id, u, z, N, M, V, K, s);
@@ -1241,16 +1265,17 @@ extern "C" int lda_draw_naive(const float *theta, const float *phi,
                               int32_t V, int32_t K, void *stream) {
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
+  const UniformSource us{u, 0, 0, 0};
   hipStream_t s = static_cast<hipStream_t>(stream);
   const DocSource d{doc_id, nullptr, M};
   if (K <= 64)
-    launch_naive<64>(theta, phi, d, word_id, u, z, N, K, s);
+    launch_naive<64>(theta, phi, d, word_id, us, z, N, K, s);
   else if (K <= 256)
-    launch_naive<256>(theta, phi, d, word_id, u, z, N, K, s);
+    launch_naive<256>(theta, phi, d, word_id, us, z, N, K, s);
   else if (K <= 1024)
-    launch_naive<1024>(theta, phi, d, word_id, u, z, N, K, s);
+    launch_naive<1024>(theta, phi, d, word_id, us, z, N, K, s);
   else
-    launch_naive<LDA_MAX_K>(theta, phi, d, word_id, u, z, N, K, s);
+    launch_naive<LDA_MAX_K>(theta, phi, d, word_id, us, z, N, K, s);
   return finish_launch();
 }
 
@@ -1261,7 +1286,8 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
                                   void *stream) {
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
-  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, u, z, N, M, V, K,
+  const UniformSource us{u, 0, 0, 0};
+  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
                      static_cast<hipStream_t>(stream));
   return finish_launch();
 }
@@ -1272,7 +1298,8 @@ extern "C" int lda_draw_transposed(const float *theta, const float *phi,
                                    int32_t V, int32_t K, void *stream) {
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
-  launch_transposed(theta, phi, DocSource{doc_id, nullptr, M}, word_id, u, z, N, M, V, K,
+  const UniformSource us{u, 0, 0, 0};
+  launch_transposed(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
                     static_cast<hipStream_t>(stream));
   return finish_launch();
 }
@@ -1287,14 +1314,15 @@ extern "C" int lda_draw_butterfly_variant(const float *theta, const float *phi,
     return LDA_ERR_UNSUPPORTED;
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
+  const UniformSource us{u, 0, 0, 0};
   const DocSource d{doc_id, nullptr, M};
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (variant == LDA_VARIANT_REGISTER_TABLE)
-    launch_table_variant<false, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    launch_table_variant<false, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);
   else if (variant == LDA_VARIANT_LDS_TABLE)
-    launch_table_variant<true, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    launch_table_variant<true, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);
   else
-    launch_table_variant<true, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    launch_table_variant<true, true>(theta, phi, d, word_id, us, z, N, M, V, K, s);
   return finish_launch();
 }
 
@@ -1310,19 +1338,47 @@ extern "C" int lda_draw_doc_lanes(const float *theta, const float *phi,
     return LDA_ERR_UNSUPPORTED;
   if (N == 0) return LDA_OK;
   if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
+  const UniformSource us{u, 0, 0, 0};
   hipStream_t s = static_cast<hipStream_t>(stream);
   const bool tl = theta_cache != 0;
   if (width_for(K) == 64) {
     if (tl)
-      launch_doc_lanes<64, true>(theta, phi, doc_offsets, word_id, u, z, N, M, V, K, s);
+      launch_doc_lanes<64, true>(theta, phi, doc_offsets, word_id, us, z, N, M, V, K, s);
     else
-      launch_doc_lanes<64, false>(theta, phi, doc_offsets, word_id, u, z, N, M, V, K, s);
+      launch_doc_lanes<64, false>(theta, phi, doc_offsets, word_id, us, z, N, M, V, K, s);
   } else {
     if (tl)
-      launch_doc_lanes<32, true>(theta, phi, doc_offsets, word_id, u, z, N, M, V, K, s);
+      launch_doc_lanes<32, true>(theta, phi, doc_offsets, word_id, us, z, N, M, V, K, s);
     else
-      launch_doc_lanes<32, false>(theta, phi, doc_offsets, word_id, u, z, N, M, V, K, s);
+      launch_doc_lanes<32, false>(theta, phi, doc_offsets, word_id, us, z, N, M, V, K, s);
   }
+  return finish_launch();
+}
+
+extern "C" int lda_draw_butterfly_philox(const float *theta, const float *phi,
+                                         const int32_t *doc_id, const int32_t *word_id,
+                                         int32_t *z, int64_t N, int32_t M, int32_t V,
+                                         int32_t K, uint64_t seed, uint32_t sweep,
+                                         void *stream) {
+  // (z stands in for the absent u in the pointer checks)
+  const int st = check_args(theta, phi, doc_id, word_id, z, z, N, M, V, K);
+  if (st != LDA_OK || N == 0) return st;
+  const UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
+  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
+                     static_cast<hipStream_t>(stream));
+  return finish_launch();
+}
+
+extern "C" int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
+                                   uint32_t sweep, void *stream) {
+  if (count < 0 || first < 0 || count > INT64_MAX - first) return LDA_ERR_SHAPE;
+  if (count == 0) return LDA_OK;
+  if (!u) return LDA_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(u) & 3u) return LDA_ERR_ALIGN;
+  const UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
+  const int64_t blocks = (count + 255) / 256;
+  uniforms_kernel<<<(unsigned)(blocks < 4096 ? blocks : 4096), 256, 0,
+                    static_cast<hipStream_t>(stream)>>>(u, count, first, us);
   return finish_launch();
 }
 
@@ -1333,7 +1389,8 @@ extern "C" int lda_draw_docs(const float *theta, const float *phi,
   int st = check_args(theta, phi, doc_offsets, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
-  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M}, word_id, u, z, N, M, V,
+  const UniformSource us{u, 0, 0, 0};
+  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M}, word_id, us, z, N, M, V,
                      K, static_cast<hipStream_t>(stream));
   return finish_launch();
 }

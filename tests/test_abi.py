@@ -164,3 +164,31 @@ def test_binding_rejects_cpu_tensors():
     i = torch.zeros(3, dtype=torch.int32)
     with pytest.raises(ValueError):
         lda.draw_butterfly(t, t, i, i, torch.zeros(3))
+
+
+def test_philox_draw_argument_errors(lib):
+    from paper_1505_03851_amd._lib import STATUS
+    f = lib.lda_draw_butterfly_philox
+    ok = dict(theta=A, phi=A, doc=A, word=A, z=A, N=10, M=3, V=5, K=8)
+
+    def run(**kw):
+        a = dict(ok, **kw)
+        return f(a["theta"], a["phi"], a["doc"], a["word"], a["z"], a["N"], a["M"],
+                 a["V"], a["K"], 123, 0, None)
+    for key in ("theta", "phi", "doc", "word", "z"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert run(**{key: A + 2}) == STATUS["LDA_ERR_ALIGN"], key
+    for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert run(N=0, theta=None, phi=None, doc=None, word=None, z=None) == 0
+
+
+def test_philox_uniforms_argument_errors(lib):
+    from paper_1505_03851_amd._lib import STATUS
+    f = lib.lda_philox_uniforms
+    assert f(None, 0, 0, 1, 0, None) == 0                     # no-op
+    assert f(A, -1, 0, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
+    assert f(A, 5, -1, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
+    assert f(A, 2, 2 ** 63 - 1, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
+    assert f(None, 5, 0, 1, 0, None) == STATUS["LDA_ERR_NULL"]
+    assert f(A + 1, 5, 0, 1, 0, None) == STATUS["LDA_ERR_ALIGN"]
