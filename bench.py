@@ -31,7 +31,7 @@ HEADLINE = "corpus16M-K1024"
 SECOND = "corpus1M-K256"
 COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1505_03851_amd", "csrc", f)
-                  for f in ("lda_draw.hip", "butterfly.hpp")]
+                  for f in ("lda_draw.hip", "butterfly.hpp", "philox.hpp")]
 
 
 def kernel_source_hash() -> str:
@@ -93,9 +93,11 @@ def launcher(kernel: str, dev):
     return lambda out, stream: fn(th, ph, d, w, u, out=out, stream=stream)
 
 
-def time_kernel(kernel: str, dev, steps: int, warmup: int):
+def time_kernel(kernel: str, dev, steps: int, warmup: int, flush=None):
     """Warm up, then time exactly ``steps`` launches.  Returns (wall seconds of
-    the timed region, per-launch milliseconds from HIP events, z)."""
+    the timed region, per-launch milliseconds from HIP events, z).  With
+    ``flush`` (a large device tensor), it is overwritten before every timed
+    launch, outside the launch's event pair: a cold-cache launch."""
     import torch
     launch = launcher(kernel, dev)
     stream = torch.cuda.current_stream()
@@ -107,6 +109,8 @@ def time_kernel(kernel: str, dev, steps: int, warmup: int):
            torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
     t0 = time.perf_counter()
     for s, e in ev:
+        if flush is not None:
+            flush.zero_()
         s.record(stream)
         launch(z, stream)
         e.record(stream)
@@ -115,19 +119,24 @@ def time_kernel(kernel: str, dev, steps: int, warmup: int):
     return wall, [s.elapsed_time(e) for s, e in ev], z
 
 
-def measure(name: str, c, dev, kernel: str, steps: int, warmup: int) -> dict:
-    wall, per_ms, z = time_kernel(kernel, dev, steps, warmup)
+def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None) -> dict:
+    wall, per_ms, z = time_kernel(kernel, dev, steps, warmup, flush)
     avg_ms = sum(per_ms) / len(per_ms)
+    srt = sorted(per_ms)
+    med_ms = srt[len(srt) // 2]
     b_alg = algorithmic_bytes(c)
     gbps = b_alg / (avg_ms * 1e-3) / 1e9
-    print(f"[bench] {name} {kernel}: {avg_ms:.3f} ms/launch "
-          f"(min {min(per_ms):.3f}), {c.N / (avg_ms * 1e-3) / 1e9:.3f} G draws/s, "
+    tag = " cold" if flush is not None else ""
+    print(f"[bench] {name} {kernel}{tag}: {avg_ms:.3f} ms/launch "
+          f"(median {med_ms:.3f}, min {srt[0]:.3f}, max {srt[-1]:.3f}), "
+          f"{c.N / (avg_ms * 1e-3) / 1e9:.3f} G draws/s, "
           f"{gbps:.0f} GB/s algorithmic ({100 * gbps / PEAK_HBM_GBPS:.1f}% of "
           f"8 TB/s)", file=sys.stderr, flush=True)
     return {
-        "workload": name, "kernel": kernel, "N": c.N, "K": c.K,
-        "steps": steps, "wall_s": wall,
-        "ms_per_launch": avg_ms, "ms_per_launch_min": min(per_ms),
+        "workload": name, "kernel": kernel + ("-cold" if flush is not None else ""),
+        "N": c.N, "K": c.K, "steps": steps, "wall_s": wall,
+        "ms_per_launch": avg_ms, "ms_per_launch_median": med_ms,
+        "ms_per_launch_min": srt[0], "ms_per_launch_max": srt[-1],
         "draws_per_s": c.N / (avg_ms * 1e-3),
         "alg_bytes_per_launch": b_alg,
         "alg_GBps": gbps, "frac_of_hbm_peak": gbps / PEAK_HBM_GBPS,
@@ -171,7 +180,7 @@ def _counter_means(d: str, kernel_substr: str) -> dict:
 def counters_summary(args) -> int:
     """Turn rocprofv3 counter runs of the butterfly kernel and of the 1 GiB
     copy into the record ``traffic_from_counters`` reads."""
-    kname = "butterfly_kernel"
+    kname = "butterfly"          # butterfly_kernel or butterfly4_kernel
     copy = "copyBuffer"
     fetch = _counter_means(args.fetch, kname)["FETCH_SIZE"]
     write = _counter_means(args.write, kname)["WRITE_SIZE"]
@@ -180,7 +189,7 @@ def counters_summary(args) -> int:
     copy_kib = (1 << 30) / 1024
     f_scale, w_scale = copy_kib / copy_fetch, copy_kib / copy_write
     rec = {
-        "kernel": "butterfly_kernel<64>", "workload": HEADLINE,
+        "kernel": "butterfly", "workload": args.workload,
         "kernel_source_sha1": kernel_source_hash(),
         "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
         "copy_1GiB_fetch_kib": copy_fetch, "copy_1GiB_write_kib": copy_write,
@@ -199,26 +208,48 @@ def counters_summary(args) -> int:
     return 0
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    return ln.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(c, z_gpu, sample: int) -> dict:
-    """The oracle, as it stands, on the first ``sample`` tokens."""
+    """The oracle, as it stands, on the first ``sample`` tokens with all its
+    OpenMP threads, and on the first ``sample // 16`` with one thread."""
     import numpy as np
     import oracle
     n = min(sample, c.N)
     d, w, u = c.doc_id[:n], c.word_id[:n], c.u[:n]
     oracle.draw(c.theta, c.phi, d[:1024], w[:1024], u[:1024], with_band=False)
+    threads = oracle.num_threads()
     t0 = time.perf_counter()
     z_ref = oracle.draw(c.theta, c.phi, d, w, u, with_band=False)
     dt = time.perf_counter() - t0
+    n1 = max(1, n // 16)
+    oracle.set_num_threads(1)
+    t1 = time.perf_counter()
+    oracle.draw(c.theta, c.phi, d[:n1], w[:n1], u[:n1], with_band=False)
+    dt1 = time.perf_counter() - t1
+    oracle.set_num_threads(threads)
     zg = z_gpu[:n].cpu().numpy()
     # parity on the same sample (outside the timed call): every mismatch must
     # lie in the rounding band |u*S - S_k| <= 1e-5 * S
     z_chk, band = oracle.draw(c.theta, c.phi, d, w, u, with_band=True)
     mism = zg != z_chk
     return {
-        "value": n / dt, "unit": "draws/s", "cores": oracle.num_threads(),
+        "value": n / dt, "unit": "draws/s", "cores": threads,
         "kind": "oracle",
         "sample": f"first {n} tokens of {c.name} (K={c.K}), fp64 oracle, "
                   f"draw only, {dt:.2f} s wall",
+        "cpu": cpu_model(), "host_cpus": os.cpu_count(),
+        "single_thread": {"value": n1 / dt1, "unit": "draws/s",
+                          "sample": f"first {n1} tokens, 1 thread, {dt1:.2f} s wall"},
         "parity": {
             "tokens": n,
             "mismatches": int(mism.sum()),
@@ -284,6 +315,32 @@ def ablation(args) -> int:
     return 0
 
 
+def all_configs(args) -> int:
+    """Every kernel on every workload of inputs.CONFIGS but the K sweep's, warm
+    and (butterfly) with a cold cache; one JSON line per workload."""
+    import torch
+    from paper_1505_03851_amd.inputs import CONFIGS, make_corpus
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")  # 1 GiB
+    for name in [n for n in CONFIGS if not n.startswith("wiki-shaped")]:
+        c = make_corpus(name)
+        dev = upload(c)
+        rec = {"workload": name, "N": c.N, "M": c.M, "V": c.V, "K": c.K,
+               "alg_bytes_per_launch": algorithmic_bytes(c)}
+        for kernel in ("naive", "transposed", "butterfly"):
+            steps = args.steps if kernel != "naive" or c.K <= 256 else max(3, args.steps // 4)
+            r = measure(name, c, dev, kernel, steps, args.warmup)
+            for key in ("ms_per_launch", "ms_per_launch_median", "ms_per_launch_min",
+                        "ms_per_launch_max", "draws_per_s", "alg_GBps"):
+                rec[f"{kernel}_{key}"] = r[key]
+        r = measure(name, c, dev, "butterfly", args.steps, args.warmup, flush=flush)
+        for key in ("ms_per_launch", "ms_per_launch_median", "draws_per_s", "alg_GBps"):
+            rec[f"butterfly_cold_{key}"] = r[key]
+        print(json.dumps(rec), flush=True)
+        del dev
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -301,6 +358,9 @@ def main() -> int:
                     help="naive vs butterfly over K = 16, 48, ..., 240 on the "
                          "corpus shaped like the paper's evaluation corpus; one "
                          "JSON line per K")
+    ap.add_argument("--all-configs", action="store_true",
+                    help="naive, transposed and butterfly (warm, and cold for the "
+                         "butterfly) on every workload; one JSON line each")
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
@@ -344,6 +404,8 @@ def main() -> int:
         return k_sweep(args)
     if args.ablation:
         return ablation(args)
+    if args.all_configs:
+        return all_configs(args)
 
     if args.only:
         c = make_corpus(args.workload)
@@ -374,6 +436,12 @@ def main() -> int:
     head = measure(HEADLINE, c, dev, "butterfly", args.steps, args.warmup)
     z_head = head.pop("z")
     results.append(head)
+    # the same launches with L2 and the MALL flushed before each (1 GiB fill)
+    flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
+    cold = measure(HEADLINE, c, dev, "butterfly", args.steps, 1, flush=flush)
+    cold.pop("z")
+    results.append(cold)
+    del flush
 
     wall = head["wall_s"]
     value = c.N * args.steps / wall

@@ -51,6 +51,8 @@ def _load():
                                 P, P, ctypes.c_double]
     lib.oracle_draw.restype = ctypes.c_int
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
+    lib.oracle_set_num_threads.restype = None
     _lib = lib
     return lib
 
@@ -58,6 +60,11 @@ def _load():
 def num_threads() -> int:
     """OpenMP threads the C oracle uses."""
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """OpenMP threads for the following draws (timing only)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def _as(a, dtype):

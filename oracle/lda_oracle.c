@@ -33,6 +33,17 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Threads for the following draws (n >= 1); the arithmetic is unchanged. */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n >= 1)
+        omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /* S[k] = sum_{i<=k} theta[d][i] * phi[w][i], sequential, fp64. */
 void oracle_prefix(const float *theta_row, const float *phi_row, int32_t K,
                    double *S)

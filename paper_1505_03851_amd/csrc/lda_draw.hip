@@ -59,24 +59,77 @@ constexpr int kBlockThreads = kWavesPerBlock * kWave;
 
 // Where a token's document comes from: a per-token id array, or the paper's
 // ragged form (Section 2: document m holds N[m] tokens), given as offsets --
-// document m's tokens are [offsets[m], offsets[m + 1]).
+// document m's tokens are [offsets[m], offsets[m + 1]).  With offsets, the
+// document of token n is the last m with offsets[m] <= n (which skips empty
+// documents); every search stays inside [0, M - 1] whatever the offsets hold.
 struct DocSource {
   const int32_t *ids;      // doc_id[N], or null
   const int64_t *offsets;  // doc_offsets[M + 1], used when ids is null
   int M;
-  // Document of token n: ids[n], or the last m with offsets[m] <= n (this
-  // skips empty documents).
-  __device__ __forceinline__ int operator()(int64_t n) const {
-    if (ids) return ids[n];
-    int lo = 0, hi = M - 1;
+  int64_t N;
+
+  // Last m in [lo, hi] with offsets[m] <= t, given offsets[lo] <= t and
+  // offsets[hi + 1] > t (bisection).
+  __device__ __forceinline__ int bisect(int64_t t, int lo, int hi) const {
     while (lo < hi) {
-      const int mid = (lo + hi + 1) >> 1;
-      if (offsets[mid] <= n)
+      const int mid = lo + ((hi - lo + 1) >> 1);
+      if (offsets[mid] <= t)
         lo = mid;
       else
         hi = mid - 1;
     }
     return lo;
+  }
+
+  // The same over [0, M - 1] from a guess g: steps of 1, 2, 4, ... away from g
+  // bracket the answer, then bisection (a few probes when g is close).
+  __device__ __forceinline__ int search_from(int64_t t, int g) const {
+    int lo, hi;
+    if (offsets[g] <= t) {
+      lo = g;
+      int step = 1;
+      while (lo + step <= M - 1 && offsets[lo + step] <= t) {
+        lo += step;
+        step *= 2;
+      }
+      hi = lo + step <= M - 1 ? lo + step - 1 : M - 1;
+    } else {
+      hi = g - 1;
+      int step = 1;
+      for (;;) {
+        const int m = hi - step + 1;
+        if (m <= 0) {
+          lo = 0;
+          break;
+        }
+        if (offsets[m] <= t) {
+          lo = m;
+          break;
+        }
+        hi = m - 1;
+        step *= 2;
+      }
+    }
+    return bisect(t, lo, hi);
+  }
+
+  // Document of token n, any lane layout (one bisection over all documents).
+  __device__ __forceinline__ int operator()(int64_t n) const {
+    if (ids) return ids[n];
+    return bisect(n, 0, M - 1);
+  }
+
+  // Document of token n for a wavefront whose tokens all lie in [first,
+  // last] (uniform): the documents of `first` and `last` are found once per
+  // wavefront, the first from the guess first * M / N, and each lane then
+  // bisects only the documents between them (usually one or two).
+  __device__ __forceinline__ int wave_doc(int64_t n, int64_t first, int64_t last) const {
+    if (ids) return ids[n];
+    int g = (int)((double)first * (double)M / (double)(N > 0 ? N : 1));
+    g = g < 0 ? 0 : (g > M - 1 ? M - 1 : g);
+    const int d0 = __builtin_amdgcn_readfirstlane(search_from(first, g));
+    const int d1 = __builtin_amdgcn_readfirstlane(search_from(last, d0));
+    return bisect(n, d0, d1 > d0 ? d1 : d0);
   }
 };
 
@@ -475,7 +528,7 @@ void butterfly_kernel(
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = docs(n);
+  const int doc = docs.wave_doc(n, t0, t0 + last);
   const int word = word_id[n];
   const float un = u(n);
   // blocks of W topics; a remnant of K mod W topics becomes block 0, padded
@@ -710,7 +763,7 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = docs(n);
+  const int doc = docs.wave_doc(n, t0, t0 + last);
   const int word = word_id[n];
   const float un = u(n);
   const int NB = K / kBlock4;
@@ -817,7 +870,7 @@ void transposed_kernel(const float *__restrict__ theta, const float *__restrict_
   const int64_t n = SMALL ? (lane < last ? lane : last) : t0 + lane;
   const bool store = SMALL ? lane < N : t0 + lane >= first;
 
-  const int doc = docs(n);
+  const int doc = docs.wave_doc(n, t0, t0 + last);
   const int word = word_id[n];
   const float un = u(n);
   const int NB = (K + kWave - 1) / kWave;  // the remnant is block 0, padded
@@ -1267,7 +1320,7 @@ extern "C" int lda_draw_naive(const float *theta, const float *phi,
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const DocSource d{doc_id, nullptr, M};
+  const DocSource d{doc_id, nullptr, M, N};
   if (K <= 64)
     launch_naive<64>(theta, phi, d, word_id, us, z, N, K, s);
   else if (K <= 256)
@@ -1287,7 +1340,7 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
-  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
+  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id, us, z, N, M, V, K,
                      static_cast<hipStream_t>(stream));
   return finish_launch();
 }
@@ -1299,7 +1352,7 @@ extern "C" int lda_draw_transposed(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
-  launch_transposed(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
+  launch_transposed(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id, us, z, N, M, V, K,
                     static_cast<hipStream_t>(stream));
   return finish_launch();
 }
@@ -1315,7 +1368,7 @@ extern "C" int lda_draw_butterfly_variant(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
-  const DocSource d{doc_id, nullptr, M};
+  const DocSource d{doc_id, nullptr, M, N};
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (variant == LDA_VARIANT_REGISTER_TABLE)
     launch_table_variant<false, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);
@@ -1364,7 +1417,7 @@ extern "C" int lda_draw_butterfly_philox(const float *theta, const float *phi,
   const int st = check_args(theta, phi, doc_id, word_id, z, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
-  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M}, word_id, us, z, N, M, V, K,
+  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id, us, z, N, M, V, K,
                      static_cast<hipStream_t>(stream));
   return finish_launch();
 }
@@ -1390,7 +1443,7 @@ extern "C" int lda_draw_docs(const float *theta, const float *phi,
   if (st != LDA_OK || N == 0) return st;
   if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
   const UniformSource us{u, 0, 0, 0};
-  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M}, word_id, us, z, N, M, V,
+  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M, N}, word_id, us, z, N, M, V,
                      K, static_cast<hipStream_t>(stream));
   return finish_launch();
 }

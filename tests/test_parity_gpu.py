@@ -260,6 +260,37 @@ def test_docs_ragged(shape, kernel):
 
 
 @pytest.mark.parametrize("kernel", OFFSET_KERNELS)
+@pytest.mark.parametrize("layout", ["huge-first", "huge-last", "huge-middle", "alternating"])
+def test_docs_skewed_lengths(layout, kernel):
+    """Document lengths far from uniform, so that a wavefront's guess of its
+    first document (token index * M / N) is far off in either direction."""
+    N, M, V, K = 64 * 50 + 13, 300, 400, 96
+    lengths = np.zeros(M, np.int64)
+    if layout == "huge-first":
+        lengths[0] = N - (M - 1)
+        lengths[1:] = 1
+    elif layout == "huge-last":
+        lengths[-1] = N - (M - 1)
+        lengths[:-1] = 1
+    elif layout == "huge-middle":
+        lengths[:] = 1
+        lengths[M // 2] = N - (M - 1)
+        lengths[M // 2 + 1: M // 2 + 40] = 0
+        lengths[M // 2] += 39
+    else:   # empty and long documents in turn
+        lengths[1::2] = 0
+        lengths[0::2] = N // (M // 2)
+        lengths[0] += N - lengths.sum()
+    assert lengths.sum() == N and (lengths >= 0).all()
+    base = make_random(N, M, V, K, seed=len(layout), doc_order="sequential")
+    doc = np.repeat(np.arange(M), lengths).astype(np.int32)
+    c = _corpus(base.theta, base.phi, doc, base.word_id, base.u, f"skewed-{layout}")
+    _offset_check(c, kernel, rate=False)
+    if kernel == "docs":
+        assert (run_kernel("docs", to_device(c)) == run_kernel("butterfly", to_device(c))).all()
+
+
+@pytest.mark.parametrize("kernel", OFFSET_KERNELS)
 def test_docs_empty_corpus_and_empty_documents(kernel):
     """N = 0 is a no-op; documents before, between and after the tokens
     may be empty."""
