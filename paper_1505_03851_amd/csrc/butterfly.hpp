@@ -90,22 +90,52 @@ __device__ __forceinline__ float pair_sum(float x, float y) {
 
 // ---------------------------------------------------------------------------
 // Block totals for the sweep: a reduce-scatter of the W x W tile.  Stage BIT
-// pairs registers k and k + BIT (k < BIT) across lanes l and l xor BIT; after
-// the stages for BIT = W/2 .. 1 lane l holds the sum of its own token over the
-// block's W topics in a[0].  The tile registers are consumed from the top, so
-// the caller can refill a[BIT..2*BIT-1] as soon as stage BIT has finished.
-template <int W, int BIT>
+// pairs registers k and k + BIT (k < BIT) across lanes l and l xor L, L the
+// stage's lane bit; after the stages for BIT = W/2 .. 1 lane l holds the sum
+// of its own token over the block's W topics in a[0].  The tile registers are
+// consumed from the top, so the caller can refill a[BIT..2*BIT-1] as soon as
+// stage BIT has finished.
+//
+// Lane bits: with HALF = false, L = BIT (lane bits W/2 .. 1).  With HALF
+// (W = 64), L = 16, 8, 4, 2, 1 and then 32: the lanes first sum over aligned
+// groups of topics inside each half of the block, so that just before the last
+// stage every lane holds its token's sum over each half.  Register k then
+// holds token reg_token(k), the register index with its bits moved to the
+// matching lane bits.
+template <int W, int BIT, bool HALF>
+__host__ __device__ constexpr int stage_lane_bit() {
+  return HALF ? (BIT == 1 ? W / 2 : BIT / 2) : BIT;
+}
+
+template <int W, bool HALF>
+__host__ __device__ constexpr int reg_token(int k) {
+  return HALF ? ((k >> 1) | ((k & 1) ? W / 2 : 0)) : k;
+}
+
+template <int W, int BIT, bool HALF = false>
 __device__ __forceinline__ void reduce_stage(float (&a)[W]) {
-  if constexpr (BIT >= 4) {
+  constexpr int L = stage_lane_bit<W, BIT, HALF>();
+  if constexpr (L >= 4) {
 #pragma unroll
     for (int k = BIT - 1; k >= 0; --k) {
-      half_swap<BIT>(a[k], a[k + BIT]);
+      half_swap<L>(a[k], a[k + BIT]);
       a[k] = a[k] + a[k + BIT];
     }
   } else {
 #pragma unroll
-    for (int k = 0; k < BIT; ++k) a[k] = pair_sum<BIT>(a[k], a[k + BIT]);
+    for (int k = 0; k < BIT; ++k) a[k] = pair_sum<L>(a[k], a[k + BIT]);
   }
+}
+
+// The last stage of the HALF order (lane bit W/2), which also returns the
+// lane's token sum over the lower half of the block: after the exchange a[0]
+// holds the lower half's sum and a[1] the upper half's, in every lane.
+template <int W>
+__device__ __forceinline__ float reduce_last_half(float (&a)[W]) {
+  half_swap<W / 2>(a[0], a[1]);
+  const float lower = a[0];
+  a[0] = a[0] + a[1];
+  return lower;
 }
 
 // ---------------------------------------------------------------------------

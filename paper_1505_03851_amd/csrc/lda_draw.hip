@@ -46,6 +46,13 @@
 #ifndef LDA_DOC_LANES_TARGET_WAVES
 #define LDA_DOC_LANES_TARGET_WAVES 16384
 #endif
+//   LDA_HALF_MAX_BLOCKS       largest K / 64 for which the W = 64 kernel
+//                             rebuilds only the chosen half-block (its 2 K/64
+//                             LDS rows per wavefront keep 12 wavefronts per CU
+//                             up to 26 blocks).
+#ifndef LDA_HALF_MAX_BLOCKS
+#define LDA_HALF_MAX_BLOCKS 24
+#endif
 //   LDA_LEAF4_WAVES_PER_EU    wavefronts per SIMD for the four-topic kernel.
 #ifndef LDA_LEAF4_WAVES_PER_EU
 #define LDA_LEAF4_WAVES_PER_EU 3
@@ -267,13 +274,15 @@ __device__ __forceinline__ uint32_t col_bytes(const Wave<W, SMALL> &w, int blk) 
   return (uint32_t)(t > 0 ? t : 0) * 4u;
 }
 
-// Issue the phi loads of tokens [LO, HI) of block `blk` into a[LO..HI-1].
-template <int W, bool SMALL, int LO, int HI>
+// Issue the phi loads of registers [LO, HI) of block `blk`: register k takes
+// the value of token reg_token(k) (token k unless HALF).
+template <int W, bool SMALL, int LO, int HI, bool HALF = false>
 __device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t *wp,
                                           float (&a)[W], int blk) {
   const uint32_t voff = col_bytes(w, blk);
 #pragma unroll
-  for (int k = LO; k < HI; ++k) a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
+  for (int k = LO; k < HI; ++k)
+    a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, reg_token<W, HALF>(k)));
 }
 
 // Theta of block `blk` at this lane's topic, for the first and last document.
@@ -288,38 +297,51 @@ __device__ __forceinline__ void issue_theta(const Wave<W, SMALL> &w, int blk, fl
 // The stages of the block-total reduce-scatter from BIT down to 1.  With
 // PREFETCH, the registers each stage frees are refilled at once with the next
 // block's phi values, so those loads are in flight during the rest of the
-// reduction.
+// reduction.  With HALF the last stage also leaves the lane's lower-half sum
+// in `lower`.
+template <int W, bool SMALL, int BIT, bool PREFETCH, bool HALF = false>
+__device__ __forceinline__ void reduce_rest(const Wave<W, SMALL> &w, const int32_t *wp,
+                                            float (&a)[W], int next, float &lower) {
+  if constexpr (BIT >= 1) {
+    if constexpr (HALF && BIT == 1)
+      lower = reduce_last_half<W>(a);
+    else
+      reduce_stage<W, BIT, HALF>(a);
+    if constexpr (PREFETCH && BIT > 1) issue_phi<W, SMALL, BIT, 2 * BIT, HALF>(w, wp, a, next);
+    reduce_rest<W, SMALL, BIT / 2, PREFETCH, HALF>(w, wp, a, next, lower);
+  }
+}
+
 template <int W, bool SMALL, int BIT, bool PREFETCH>
 __device__ __forceinline__ void reduce_rest(const Wave<W, SMALL> &w, const int32_t *wp,
                                             float (&a)[W], int next) {
-  if constexpr (BIT >= 1) {
-    reduce_stage<W, BIT>(a);
-    if constexpr (PREFETCH && BIT > 1) issue_phi<W, SMALL, BIT, 2 * BIT>(w, wp, a, next);
-    reduce_rest<W, SMALL, BIT / 2, PREFETCH>(w, wp, a, next);
-  }
+  float unused;
+  reduce_rest<W, SMALL, BIT, PREFETCH, false>(w, wp, a, next, unused);
 }
 
 // Sweep step for one block whose phi values are in (or in flight to) a[] and
 // whose theta values are in th0/th1.  Returns this lane's token total over
-// the block.  With PREFETCH, block `next`'s loads are issued along the way
-// and left in a[], th0, th1.
-template <int W, bool SMALL, bool PREFETCH>
+// the block (and with HALF its sum over the block's lower half in `lower`).
+// With PREFETCH, block `next`'s loads are issued along the way and left in
+// a[], th0, th1.
+template <int W, bool SMALL, bool PREFETCH, bool HALF = false>
 __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int32_t *wp,
                                              float (&a)[W], float &th0, float &th1,
-                                             int cur, int next) {
+                                             int cur, int next, float &lower) {
   constexpr int B = W / 2;
+  constexpr int L = stage_lane_bit<W, B, HALF>();  // lane bit of the first stage
   // padding topics of block 0 weigh nothing
   const bool real = topic_of(w, cur) >= 0;
   if (w.mode == kOneDoc) {
     // First stage fused with the theta factor: after the half exchange the
-    // two values of a pair sit at topics of the lower and upper half-group,
-    // whose theta values one more exchange of th0 provides.
+    // two values of a pair sit at the topics of lanes l and l xor L, whose
+    // theta values one more exchange of th0 provides.
     float tA = real ? th0 : 0.0f, tB = tA;
-    half_swap<B>(tA, tB);
+    half_swap<L>(tA, tB);
     if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
 #pragma unroll
     for (int k = B - 1; k >= 0; --k) {
-      half_swap<B>(a[k], a[k + B]);
+      half_swap<L>(a[k], a[k + B]);
       a[k] = __builtin_fmaf(a[k], tA, a[k + B] * tB);
     }
   } else {
@@ -329,31 +351,33 @@ __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int3
     const int kb = launder_int(w.kb);
     const float t0 = real ? th0 : 0.0f, t1 = real ? th1 : 0.0f;
 #pragma unroll
-    for (int k = 0; k < W; ++k) a[k] *= (w.gbase + k < kb) ? t0 : t1;
+    for (int k = 0; k < W; ++k) a[k] *= (w.gbase + reg_token<W, HALF>(k) < kb) ? t0 : t1;
     if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
-    reduce_stage<W, B>(a);
+    reduce_stage<W, B, HALF>(a);
   }
-  if constexpr (PREFETCH) issue_phi<W, SMALL, B, W>(w, wp, a, next);
-  reduce_rest<W, SMALL, B / 2, PREFETCH>(w, wp, a, next);
+  if constexpr (PREFETCH) issue_phi<W, SMALL, B, W, HALF>(w, wp, a, next);
+  reduce_rest<W, SMALL, B / 2, PREFETCH, HALF>(w, wp, a, next, lower);
   const float total = a[0];
-  if constexpr (PREFETCH) issue_phi<W, SMALL, 0, 2>(w, wp, a, next);
+  if constexpr (PREFETCH) issue_phi<W, SMALL, 0, 2, HALF>(w, wp, a, next);
   return total;
 }
 
 // Sweep step for a wave whose tokens belong to many documents: one theta
 // load per token, no prefetch.
-template <int W, bool SMALL>
+template <int W, bool SMALL, bool HALF = false>
 __device__ __forceinline__ float sweep_block_any(const Wave<W, SMALL> &w, const int32_t *wp,
-                                                 int blk) {
+                                                 int blk, float &lower) {
   float a[W];
   const uint32_t voff = col_bytes(w, blk);
   const bool real = topic_of(w, blk) >= 0;
 #pragma unroll
-  for (int k = 0; k < W; ++k)
-    a[k] = (real ? load_row<W>(w.th_rs, voff, theta_row(w, k)) : 0.0f) *
-           load_row<W>(w.ph_rs, voff, phi_row(w, wp, k));
-  reduce_stage<W, W / 2>(a);
-  reduce_rest<W, SMALL, W / 4, false>(w, wp, a, 0);
+  for (int k = 0; k < W; ++k) {
+    const int t = reg_token<W, HALF>(k);
+    a[k] = (real ? load_row<W>(w.th_rs, voff, theta_row(w, t)) : 0.0f) *
+           load_row<W>(w.ph_rs, voff, phi_row(w, wp, t));
+  }
+  reduce_stage<W, W / 2, HALF>(a);
+  reduce_rest<W, SMALL, W / 4, false, HALF>(w, wp, a, 0, lower);
   return a[0];
 }
 
@@ -483,10 +507,11 @@ __device__ __forceinline__ int inblock_search_alt(const float *table, int r, int
   return b;
 }
 
-// LDS rows per wavefront: the block-end prefixes (NB rows of 64 lanes), and,
-// with an LDS table, the rebuilt block's W - 1 rows in the same space.
-__host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
-  return lds_table ? (NB > W - 1 ? NB : W - 1) : NB;
+// LDS rows per wavefront: the block-end prefixes (NB rows of 64 lanes); with
+// the half-block tail also the prefixes at the block middles (2 NB rows); with
+// an LDS table, the rebuilt block's W - 1 rows in the same space.
+__host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table, bool half = false) {
+  return lds_table ? (NB > W - 1 ? NB : W - 1) : (half ? 2 * NB : NB);
 }
 
 // ---------------------------------------------------------------------------
@@ -505,13 +530,21 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table) {
 // In-block search (Algorithm 10) and the remnant fallback of Algorithm 9.
 //
 // ALT (with LDS_TABLE only): the alternative replacement rule and its search.
-template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false>
+//
+// HALF (W = 64, register table): the sweep's reduce-scatter ends with the
+// top lane bit, which leaves every lane its token's sums over both halves of
+// each block; the prefixes at block middles and ends go to LDS, Algorithm 9's
+// search runs over these 2 NB half-block ends, and the rebuild and Algorithm
+// 10 work on the chosen half: 32 topics per token, as the W = 32 groups do (two
+// tokens per load instruction, half the bytes, 31 exchanges in the search).
+template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false, bool HALF = false>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
     const int32_t *__restrict__ word_id, UniformSource u,
     int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_bytes, uint32_t phi_bytes) {
   static_assert(!ALT || LDS_TABLE, "the alternative table is searched in LDS");
+  static_assert(!HALF || (W == kWave && !LDS_TABLE), "half-block tail: W = 64, register table");
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
@@ -537,11 +570,13 @@ void butterfly_kernel(
   Wave<W, SMALL> w;
   init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                       lane, doc, word);
-  float *region = lds + wave * region_rows(NB, W, LDS_TABLE) * kWave;
+  float *region = lds + wave * region_rows(NB, W, LDS_TABLE, HALF) * kWave;
 
   float a[W];
+  float h[HALF ? W / 2 : 1];  // HALF: the chosen half-block's table
   float sum, stop, low, high;
-  int blk;
+  int blk;       // chosen block, or with HALF (NB > 1) chosen half-block
+  bool halves = false;
   if (NB == 1) {
     // One block: its table is built once and searched directly.
     blk = 0;
@@ -555,27 +590,38 @@ void butterfly_kernel(
     low = 0.0f;
     high = sum;
   } else {
-    // Sweep over the blocks.
+    // Sweep over the blocks: the running prefix at each block's end (row b),
+    // or with HALF at its middle (row 2b) and end (row 2b + 1).
     sum = 0.0f;
+    float lower = 0.0f;
     if (w.mode == kAnyDocs) {
       for (int b = 0; b < NB; ++b) {
-        sum += sweep_block_any(w, launder(w.wp), b);
-        region[b * kWave + lane] = sum;
+        const float total = sweep_block_any<W, SMALL, HALF>(w, launder(w.wp), b, lower);
+        if constexpr (HALF) region[(2 * b) * kWave + lane] = sum + lower;
+        sum += total;
+        region[(HALF ? 2 * b + 1 : b) * kWave + lane] = sum;
       }
     } else {
       float th0 = 0.0f, th1 = 0.0f;
       issue_theta(w, 0, th0, th1);
-      issue_phi<W, SMALL, 0, W>(w, w.wp, a, 0);
+      issue_phi<W, SMALL, 0, W, HALF>(w, w.wp, a, 0);
       for (int b = 0; b < NB - 1; ++b) {
-        sum += sweep_block<W, SMALL, true>(w, launder(w.wp), a, th0, th1, b, b + 1);
-        region[b * kWave + lane] = sum;
+        const float total = sweep_block<W, SMALL, true, HALF>(w, launder(w.wp), a, th0, th1, b,
+                                                              b + 1, lower);
+        if constexpr (HALF) region[(2 * b) * kWave + lane] = sum + lower;
+        sum += total;
+        region[(HALF ? 2 * b + 1 : b) * kWave + lane] = sum;
       }
-      sum += sweep_block<W, SMALL, false>(w, w.wp, a, th0, th1, NB - 1, 0);
-      region[(NB - 1) * kWave + lane] = sum;
+      const float total =
+          sweep_block<W, SMALL, false, HALF>(w, w.wp, a, th0, th1, NB - 1, 0, lower);
+      if constexpr (HALF) region[(2 * NB - 2) * kWave + lane] = sum + lower;
+      sum += total;
+      region[(HALF ? 2 * NB - 1 : NB - 1) * kWave + lane] = sum;
     }
     stop = sum * un;
-    // Algorithm 9: binary search over the last row of each block.
-    int lo = 0, hi = NB - 1;
+    // Algorithm 9: binary search over the last row of each block (with HALF,
+    // of each half-block).
+    int lo = 0, hi = (HALF ? 2 * NB : NB) - 1;
     while (lo < hi) {
       const int mid = (lo + hi) >> 1;
       if (stop < region[mid * kWave + lane])
@@ -589,12 +635,37 @@ void butterfly_kernel(
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    // Rebuild every token's chosen block.
-    load_tile_blocks<W, SMALL, true>(w, a, blk, w.c0);
-    if constexpr (LDS_TABLE)
-      butterfly_block<W, ALT>(a, w.r, RowStore{region + lane, kWave, true});
-    else
-      butterfly_block<W>(a, w.r, NoStore{});
+    if constexpr (HALF) {
+      // Rebuild every token's chosen half-block: lanes 32 g + r hold topic
+      // c0 + 32 blk_k + r of the tokens k of half-wave g.
+      halves = true;
+      Wave<W / 2, SMALL> wh;
+      wh.th_rs = w.th_rs;
+      wh.ph_rs = w.ph_rs;
+      wh.wp = w.wp;
+      wh.last = w.last;
+      wh.row_bytes = w.row_bytes;
+      wh.R = w.R;
+      wh.c0 = w.c0;
+      wh.r = lane & (W / 2 - 1);
+      wh.gbase = lane & (W / 2);
+      wh.doc = w.doc;
+      wh.mode = w.mode;
+      wh.kb = w.kb;
+      wh.th_off0 = w.th_off0;
+      wh.th_off1 = w.th_off1;
+      wh.ph_lane = w.ph_lane;
+      wh.th_lane = w.th_lane;
+      load_tile_blocks<W / 2, SMALL, true>(wh, h, blk, w.c0);
+      butterfly_block<W / 2>(h, wh.r, NoStore{});
+    } else {
+      // Rebuild every token's chosen block.
+      load_tile_blocks<W, SMALL, true>(w, a, blk, w.c0);
+      if constexpr (LDS_TABLE)
+        butterfly_block<W, ALT>(a, w.r, RowStore{region + lane, kWave, true});
+      else
+        butterfly_block<W>(a, w.r, NoStore{});
+    }
   }
   if constexpr (LDS_TABLE) {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -604,12 +675,19 @@ void butterfly_kernel(
   // Algorithm 10.  Empty topics of block 0 are never chosen: their prefix
   // equals the prefix before them, which is never above stop >= 0, except
   // when S = 0, where every comparison fails and the result is K - 1.
-  int off;
-  if constexpr (ALT)
-    off = inblock_search_alt<W>(region, w.r, w.gbase, stop, low, high);
-  else
-    off = inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
-  const int j = w.c0 + blk * W + off;
+  int j;
+  if constexpr (ALT) {
+    j = w.c0 + blk * W + inblock_search_alt<W>(region, w.r, w.gbase, stop, low, high);
+  } else if constexpr (HALF) {
+    if (halves)
+      j = w.c0 + blk * (W / 2) +
+          inblock_search<W / 2, false>(h, nullptr, lane & (W / 2 - 1), lane & (W / 2), stop,
+                                       low, high);
+    else
+      j = w.c0 + blk * W + inblock_search<W, false>(a, nullptr, w.r, w.gbase, stop, low, high);
+  } else {
+    j = w.c0 + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
+  }
   if (store) z[n] = j;
 }
 
@@ -1175,6 +1253,13 @@ bool lds_table_for(int32_t K) {
   return nb <= LDA_LDS_TABLE_MAX_BLOCKS;
 }
 
+// The half-block tail (W = 64) for block counts up to LDA_HALF_MAX_BLOCKS:
+// it doubles the LDS rows of the block prefixes.
+bool half_tail_for(int32_t K) {
+  const int nb = (K + 63) / 64;
+  return nb >= 2 && nb <= LDA_HALF_MAX_BLOCKS;
+}
+
 dim3 wave_grid(int64_t N) {
   const int64_t waves = (N + kWave - 1) / kWave;
   return dim3((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
@@ -1217,20 +1302,20 @@ void launch_transposed(const float *theta, const float *phi, DocSource d,
                                                                        N, K, tb, pb);
 }
 
-template <int W, bool LDS_TABLE, bool ALT = false>
+template <int W, bool LDS_TABLE, bool ALT = false, bool HALF = false>
 void launch_butterfly(const float *theta, const float *phi, DocSource d,
                       const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + W - 1) / W;  // blocks, the remnant included
-  const size_t lds = (size_t)kWavesPerBlock * region_rows(nb, W, LDS_TABLE) *
+  const size_t lds = (size_t)kWavesPerBlock * region_rows(nb, W, LDS_TABLE, HALF) *
                      kWave * sizeof(float);
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (N < kWave)
-    butterfly_kernel<W, LDS_TABLE, true, ALT><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, true, ALT, HALF><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    butterfly_kernel<W, LDS_TABLE, false, ALT><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, false, ALT, HALF><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
@@ -1297,6 +1382,8 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
   if (width_for(K) == 64) {
     if (lt)
       launch_butterfly<64, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (half_tail_for(K))
+      launch_butterfly<64, false, false, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     else
       launch_butterfly<64, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
   } else {
