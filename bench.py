@@ -341,6 +341,53 @@ def all_configs(args) -> int:
     return 0
 
 
+def graph_timing(args) -> int:
+    """Launch overhead: ``steps`` back-to-back draws launched one by one
+    against the same draws captured once in a HIP graph and replayed, on the
+    small workloads where a launch costs as much as the draw; one JSON line
+    per workload (per-draw time from events around all the draws)."""
+    import torch
+    from paper_1505_03851_amd.inputs import make_corpus
+    reps = max(args.steps, 50)
+    for name in ("tiny-K32", "corpus1M-K64", "corpus1M-K256"):
+        c = make_corpus(name)
+        dev = upload(c)
+        launch = launcher("butterfly", dev)
+        z = torch.empty_like(dev["doc_id"])
+        s = torch.cuda.Stream()
+        s.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(s):
+            for _ in range(3):
+                launch(z, s)
+        torch.cuda.current_stream().wait_stream(s)
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(reps):
+                launch(z, torch.cuda.current_stream())
+        stream = torch.cuda.current_stream()
+        e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+        g.replay()
+        torch.cuda.synchronize()
+        e0.record(stream)
+        for _ in range(reps):
+            launch(z, stream)
+        e1.record(stream)
+        g.replay()
+        e2.record(stream)
+        torch.cuda.synchronize()
+        eager_us = 1e3 * e0.elapsed_time(e1) / reps
+        graph_us = 1e3 * e1.elapsed_time(e2) / reps
+        print(f"[bench] {name} butterfly x{reps}: {eager_us:.2f} us/draw launched one by one, "
+              f"{graph_us:.2f} us/draw from one graph", file=sys.stderr, flush=True)
+        print(json.dumps({"workload": name, "N": c.N, "K": c.K, "draws": reps,
+                          "eager_us_per_draw": eager_us, "graph_us_per_draw": graph_us,
+                          "graph_draws_per_s": c.N / (graph_us * 1e-6)}), flush=True)
+        del g, dev
+        torch.cuda.empty_cache()
+    return 0
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -358,6 +405,9 @@ def main() -> int:
                     help="naive vs butterfly over K = 16, 48, ..., 240 on the "
                          "corpus shaped like the paper's evaluation corpus; one "
                          "JSON line per K")
+    ap.add_argument("--graph", action="store_true",
+                    help="launch overhead: draws launched one by one against the "
+                         "same draws replayed from one captured HIP graph")
     ap.add_argument("--all-configs", action="store_true",
                     help="naive, transposed and butterfly (warm, and cold for the "
                          "butterfly) on every workload; one JSON line each")
@@ -406,6 +456,8 @@ def main() -> int:
         return ablation(args)
     if args.all_configs:
         return all_configs(args)
+    if args.graph:
+        return graph_timing(args)
 
     if args.only:
         c = make_corpus(args.workload)
