@@ -49,9 +49,15 @@
 //   LDA_HALF_MAX_BLOCKS       largest K / 64 for which the W = 64 kernel
 //                             rebuilds only the chosen half-block (its 2 K/64
 //                             LDS rows per wavefront keep 12 wavefronts per CU
-//                             up to 26 blocks).
+//                             up to 26 blocks, 10 at 32 blocks).
 #ifndef LDA_HALF_MAX_BLOCKS
-#define LDA_HALF_MAX_BLOCKS 24
+#define LDA_HALF_MAX_BLOCKS 32
+#endif
+//   LDA_HALF_WAVES_PER_BLOCK  wavefronts per workgroup of the half-block-tail
+//                             kernel while three such workgroups fit in LDS
+//                             (else LDA_WAVES_PER_BLOCK).
+#ifndef LDA_HALF_WAVES_PER_BLOCK
+#define LDA_HALF_WAVES_PER_BLOCK 4
 #endif
 //   LDA_LEAF4_WAVES_PER_EU    wavefronts per SIMD for the four-topic kernel.
 #ifndef LDA_LEAF4_WAVES_PER_EU
@@ -285,13 +291,15 @@ __device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t
     a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, reg_token<W, HALF>(k)));
 }
 
-// Theta of block `blk` at this lane's topic, for the first and last document.
-template <int W, bool SMALL>
+// Theta of block `blk` at this lane's topic, for the first and last document
+// (MODE: the wave's ThetaMode when known at compile time, else -1).
+template <int W, bool SMALL, int MODE = -1>
 __device__ __forceinline__ void issue_theta(const Wave<W, SMALL> &w, int blk, float &th0,
                                             float &th1) {
   const uint32_t voff = col_bytes(w, blk);
   th0 = load_f32(w.th_rs, voff, w.th_off0);
-  if (w.mode == kTwoDocs) th1 = load_f32(w.th_rs, voff, w.th_off1);
+  if (MODE == kTwoDocs || (MODE < 0 && w.mode == kTwoDocs))
+    th1 = load_f32(w.th_rs, voff, w.th_off1);
 }
 
 // The stages of the block-total reduce-scatter from BIT down to 1.  With
@@ -324,21 +332,22 @@ __device__ __forceinline__ void reduce_rest(const Wave<W, SMALL> &w, const int32
 // the block (and with HALF its sum over the block's lower half in `lower`).
 // With PREFETCH, block `next`'s loads are issued along the way and left in
 // a[], th0, th1.
-template <int W, bool SMALL, bool PREFETCH, bool HALF = false>
+template <int W, bool SMALL, bool PREFETCH, bool HALF, int MODE>
 __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int32_t *wp,
                                              float (&a)[W], float &th0, float &th1,
                                              int cur, int next, float &lower) {
+  static_assert(MODE == kOneDoc || MODE == kTwoDocs, "sweep_block: one or two documents");
   constexpr int B = W / 2;
   constexpr int L = stage_lane_bit<W, B, HALF>();  // lane bit of the first stage
   // padding topics of block 0 weigh nothing
   const bool real = topic_of(w, cur) >= 0;
-  if (w.mode == kOneDoc) {
+  if constexpr (MODE == kOneDoc) {
     // First stage fused with the theta factor: after the half exchange the
     // two values of a pair sit at the topics of lanes l and l xor L, whose
     // theta values one more exchange of th0 provides.
     float tA = real ? th0 : 0.0f, tB = tA;
     half_swap<L>(tA, tB);
-    if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
+    if constexpr (PREFETCH) issue_theta<W, SMALL, MODE>(w, next, th0, th1);
 #pragma unroll
     for (int k = B - 1; k >= 0; --k) {
       half_swap<L>(a[k], a[k + B]);
@@ -352,7 +361,7 @@ __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int3
     const float t0 = real ? th0 : 0.0f, t1 = real ? th1 : 0.0f;
 #pragma unroll
     for (int k = 0; k < W; ++k) a[k] *= (w.gbase + reg_token<W, HALF>(k) < kb) ? t0 : t1;
-    if constexpr (PREFETCH) issue_theta(w, next, th0, th1);
+    if constexpr (PREFETCH) issue_theta<W, SMALL, MODE>(w, next, th0, th1);
     reduce_stage<W, B, HALF>(a);
   }
   if constexpr (PREFETCH) issue_phi<W, SMALL, B, W, HALF>(w, wp, a, next);
@@ -360,6 +369,33 @@ __device__ __forceinline__ float sweep_block(const Wave<W, SMALL> &w, const int3
   const float total = a[0];
   if constexpr (PREFETCH) issue_phi<W, SMALL, 0, 2, HALF>(w, wp, a, next);
   return total;
+}
+
+// The sweep over all NB blocks for a wave of one or two documents (MODE):
+// the running prefix at each block's end goes to row b of `region` (with
+// HALF, the prefixes at its middle and end to rows 2b and 2b + 1).  Returns
+// the lane's token total.  The loop is instantiated per mode so that its body
+// is branch-free.
+template <int W, bool SMALL, bool HALF, int MODE>
+__device__ __forceinline__ float sweep_blocks(const Wave<W, SMALL> &w, float (&a)[W],
+                                              float *region, int lane, int NB) {
+  float sum = 0.0f, lower = 0.0f;
+  float th0 = 0.0f, th1 = 0.0f;
+  issue_theta<W, SMALL, MODE>(w, 0, th0, th1);
+  issue_phi<W, SMALL, 0, W, HALF>(w, w.wp, a, 0);
+  for (int b = 0; b < NB - 1; ++b) {
+    const float total = sweep_block<W, SMALL, true, HALF, MODE>(w, launder(w.wp), a, th0, th1,
+                                                                b, b + 1, lower);
+    if constexpr (HALF) region[(2 * b) * kWave + lane] = sum + lower;
+    sum += total;
+    region[(HALF ? 2 * b + 1 : b) * kWave + lane] = sum;
+  }
+  const float total =
+      sweep_block<W, SMALL, false, HALF, MODE>(w, w.wp, a, th0, th1, NB - 1, 0, lower);
+  if constexpr (HALF) region[(2 * NB - 2) * kWave + lane] = sum + lower;
+  sum += total;
+  region[(HALF ? 2 * NB - 1 : NB - 1) * kWave + lane] = sum;
+  return sum;
 }
 
 // Sweep step for a wave whose tokens belong to many documents: one theta
@@ -537,8 +573,9 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table, boo
 // search runs over these 2 NB half-block ends, and the rebuild and Algorithm
 // 10 work on the chosen half: 32 topics per token, as the W = 32 groups do (two
 // tokens per load instruction, half the bytes, 31 exchanges in the search).
-template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false, bool HALF = false>
-__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
+template <int W, bool LDS_TABLE, bool SMALL, bool ALT = false, bool HALF = false,
+          int WPB = kWavesPerBlock>
+__global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(LDA_WAVES_PER_EU)))
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
     const int32_t *__restrict__ word_id, UniformSource u,
@@ -549,7 +586,7 @@ void butterfly_kernel(
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
+  const int64_t first = ((int64_t)blockIdx.x * WPB + wave) * kWave;
   if (first >= N) return;  // whole wavefront past the end
   // Window of 64 tokens: the wavefront's own, or for the last wavefront the
   // final 64 tokens (re-drawing some of the previous wavefront's, which it
@@ -601,22 +638,10 @@ void butterfly_kernel(
         sum += total;
         region[(HALF ? 2 * b + 1 : b) * kWave + lane] = sum;
       }
+    } else if (w.mode == kOneDoc) {
+      sum = sweep_blocks<W, SMALL, HALF, kOneDoc>(w, a, region, lane, NB);
     } else {
-      float th0 = 0.0f, th1 = 0.0f;
-      issue_theta(w, 0, th0, th1);
-      issue_phi<W, SMALL, 0, W, HALF>(w, w.wp, a, 0);
-      for (int b = 0; b < NB - 1; ++b) {
-        const float total = sweep_block<W, SMALL, true, HALF>(w, launder(w.wp), a, th0, th1, b,
-                                                              b + 1, lower);
-        if constexpr (HALF) region[(2 * b) * kWave + lane] = sum + lower;
-        sum += total;
-        region[(HALF ? 2 * b + 1 : b) * kWave + lane] = sum;
-      }
-      const float total =
-          sweep_block<W, SMALL, false, HALF>(w, w.wp, a, th0, th1, NB - 1, 0, lower);
-      if constexpr (HALF) region[(2 * NB - 2) * kWave + lane] = sum + lower;
-      sum += total;
-      region[(HALF ? 2 * NB - 1 : NB - 1) * kWave + lane] = sum;
+      sum = sweep_blocks<W, SMALL, HALF, kTwoDocs>(w, a, region, lane, NB);
     }
     stop = sum * un;
     // Algorithm 9: binary search over the last row of each block (with HALF,
@@ -1260,9 +1285,9 @@ bool half_tail_for(int32_t K) {
   return nb >= 2 && nb <= LDA_HALF_MAX_BLOCKS;
 }
 
-dim3 wave_grid(int64_t N) {
+dim3 wave_grid(int64_t N, int wpb = kWavesPerBlock) {
   const int64_t waves = (N + kWave - 1) / kWave;
-  return dim3((unsigned)((waves + kWavesPerBlock - 1) / kWavesPerBlock));
+  return dim3((unsigned)((waves + wpb - 1) / wpb));
 }
 
 template <int KMAX>
@@ -1302,21 +1327,31 @@ void launch_transposed(const float *theta, const float *phi, DocSource d,
                                                                        N, K, tb, pb);
 }
 
-template <int W, bool LDS_TABLE, bool ALT = false, bool HALF = false>
+template <int W, bool LDS_TABLE, bool ALT = false, bool HALF = false, int WPB = kWavesPerBlock>
 void launch_butterfly(const float *theta, const float *phi, DocSource d,
                       const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                       int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + W - 1) / W;  // blocks, the remnant included
-  const size_t lds = (size_t)kWavesPerBlock * region_rows(nb, W, LDS_TABLE, HALF) *
-                     kWave * sizeof(float);
+  const size_t lds = (size_t)WPB * region_rows(nb, W, LDS_TABLE, HALF) * kWave * sizeof(float);
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (N < kWave)
-    butterfly_kernel<W, LDS_TABLE, true, ALT, HALF><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, true, ALT, HALF, WPB><<<wave_grid(N, WPB), WPB * kWave, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    butterfly_kernel<W, LDS_TABLE, false, ALT, HALF><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly_kernel<W, LDS_TABLE, false, ALT, HALF, WPB><<<wave_grid(N, WPB), WPB * kWave, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
+}
+
+// Whether three workgroups of the half-block-tail kernel with
+// LDA_HALF_WAVES_PER_BLOCK wavefronts fit in a CU's 160 KiB of LDS (each
+// wavefront keeps 2 K/64 rows of 64 floats), so that the larger workgroups
+// cost no occupancy.  Measured on MI355X: 4 wavefronts per workgroup take
+// 1.3% off K = 1024 and cost 1% at K = 2048, where they would not fit.
+bool half_wide_groups(int32_t K) {
+  const int64_t bytes = 3LL * LDA_HALF_WAVES_PER_BLOCK *
+                        region_rows((K + 63) / 64, 64, false, true) * kWave * sizeof(float);
+  return bytes <= 160 * 1024;
 }
 
 // The W = 32 / 64 butterfly kernel with a chosen table: in registers with the
@@ -1382,6 +1417,9 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
   if (width_for(K) == 64) {
     if (lt)
       launch_butterfly<64, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (half_tail_for(K) && half_wide_groups(K))
+      launch_butterfly<64, false, false, true, LDA_HALF_WAVES_PER_BLOCK>(theta, phi, d, word_id, u,
+                                                                         z, N, M, V, K, s);
     else if (half_tail_for(K))
       launch_butterfly<64, false, false, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     else

@@ -90,6 +90,13 @@ SHAPES = [
     (64 * 33 + 63, 60, 500, 240, "single"),
     (64 * 17 + 9, 60, 500, 1000, "sequential"),
     (64 * 17 + 9, 60, 500, 2047, "shuffled"),
+    # half-block tail from 24 to 32 blocks: 4- and 2-wavefront workgroups,
+    # with and without a remnant, one, two and many documents per wave
+    (64 * 13 + 7, 30, 400, 1536, "sequential"),
+    (64 * 10 + 1, 30, 300, 1664, "shuffled"),
+    (64 * 9 + 40, 3, 100, 1792, "single"),
+    (64 * 11 + 3, 20, 300, 1900, "sequential"),
+    (64 * 8 + 63, 9, 200, 2048, "sequential"),
     (64 * 5 + 3, 20, 200, 4096, "sequential"),
     # K a multiple of 256: the four-topic-leaf kernel
     (1, 1, 7, 256, "sequential"),
