@@ -59,7 +59,33 @@
 #ifndef LDA_HALF_WAVES_PER_BLOCK
 #define LDA_HALF_WAVES_PER_BLOCK 4
 #endif
-//   LDA_LEAF4_WAVES_PER_EU    wavefronts per SIMD for the four-topic kernel.
+//   LDA_EIGHTHS_MAX_BLOCKS    largest K / 256 for which K a multiple of 256 is
+//                             drawn by the leaf kernel with 32-topic prefix
+//                             rows (8 K/256 LDS rows per wavefront; 0: never);
+//   LDA_EIGHTHS_SPLIT         largest K / 256 drawn with the first of its two
+//                             launch shapes;
+//   LDA_EIGHTHS_WINDOW{,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{,_LARGE}
+//                             tokens in flight per wavefront (16-byte loads)
+//                             and wavefronts per SIMD of the two shapes.
+#ifndef LDA_EIGHTHS_MAX_BLOCKS
+#define LDA_EIGHTHS_MAX_BLOCKS 8
+#endif
+#ifndef LDA_EIGHTHS_SPLIT
+#define LDA_EIGHTHS_SPLIT 4
+#endif
+#ifndef LDA_EIGHTHS_WINDOW
+#define LDA_EIGHTHS_WINDOW 16
+#endif
+#ifndef LDA_EIGHTHS_WAVES_PER_EU
+#define LDA_EIGHTHS_WAVES_PER_EU 2
+#endif
+#ifndef LDA_EIGHTHS_WINDOW_LARGE
+#define LDA_EIGHTHS_WINDOW_LARGE 4
+#endif
+#ifndef LDA_EIGHTHS_WAVES_PER_EU_LARGE
+#define LDA_EIGHTHS_WAVES_PER_EU_LARGE 4
+#endif
+//   LDA_LEAF4_WAVES_PER_EU    wavefronts per SIMD for the four-topic kernels.
 #ifndef LDA_LEAF4_WAVES_PER_EU
 #define LDA_LEAF4_WAVES_PER_EU 3
 #endif
@@ -474,6 +500,31 @@ __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
 }
 
 
+// The same wavefront seen as two groups of 32 lanes (W = 32): lanes 32 g + r
+// hold topic r of a 32-topic chunk for the tokens of half-wave g.
+template <bool SMALL>
+__device__ __forceinline__ Wave<kWave / 2, SMALL> half_wave(const Wave<kWave, SMALL> &w,
+                                                           int lane) {
+  Wave<kWave / 2, SMALL> h;
+  h.th_rs = w.th_rs;
+  h.ph_rs = w.ph_rs;
+  h.wp = w.wp;
+  h.last = w.last;
+  h.row_bytes = w.row_bytes;
+  h.R = w.R;
+  h.c0 = w.c0;
+  h.r = lane & (kWave / 2 - 1);
+  h.gbase = lane & (kWave / 2);
+  h.doc = w.doc;
+  h.mode = w.mode;
+  h.kb = w.kb;
+  h.th_off0 = w.th_off0;
+  h.th_off1 = w.th_off1;
+  h.ph_lane = w.ph_lane;
+  h.th_lane = w.th_lane;
+  return h;
+}
+
 // In-block search of Algorithm 10.  `low` and `high` are the full prefixes
 // before and at the end of the block; a[0..W-2] is this lane's column of the
 // rebuilt block (or, with LDS_TABLE, the rows are in `table`, row d at
@@ -664,23 +715,7 @@ void butterfly_kernel(
       // Rebuild every token's chosen half-block: lanes 32 g + r hold topic
       // c0 + 32 blk_k + r of the tokens k of half-wave g.
       halves = true;
-      Wave<W / 2, SMALL> wh;
-      wh.th_rs = w.th_rs;
-      wh.ph_rs = w.ph_rs;
-      wh.wp = w.wp;
-      wh.last = w.last;
-      wh.row_bytes = w.row_bytes;
-      wh.R = w.R;
-      wh.c0 = w.c0;
-      wh.r = lane & (W / 2 - 1);
-      wh.gbase = lane & (W / 2);
-      wh.doc = w.doc;
-      wh.mode = w.mode;
-      wh.kb = w.kb;
-      wh.th_off0 = w.th_off0;
-      wh.th_off1 = w.th_off1;
-      wh.ph_lane = w.ph_lane;
-      wh.th_lane = w.th_lane;
+      const Wave<W / 2, SMALL> wh = half_wave(w, lane);
       load_tile_blocks<W / 2, SMALL, true>(wh, h, blk, w.c0);
       butterfly_block<W / 2>(h, wh.r, NoStore{});
     } else {
@@ -924,6 +959,205 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
   const int base = blk * kBlock4 + kLeaf * leaf;
   const int j = base + leaf_scan(w.th_rs, w.ph_rs, (uint32_t)doc * w.row_bytes,
                                  (uint32_t)word * w.row_bytes, base, low, stop);
+  if (store) z[n] = j;
+}
+
+// ---------------------------------------------------------------------------
+// Leaf-4 kernel with 32-topic prefix rows (K a multiple of 256, from two to
+// LDA_EIGHTHS_MAX_BLOCKS 256-topic blocks, N >= 64).
+//
+// The sweep reads every token's phi row with 16-byte loads, lane l taking the
+// leaf of topics [4l, 4l + 4) of each 256-topic block, and forms the leaf
+// products' sums (dot4) as butterfly4_kernel does.  Its reduce-scatter first
+// sums over lane bits 2, 1, 0 (the eight lanes of a 32-topic "eighth" of the
+// block) and then only exchanges over lane bits 3, 4, 5, so that every lane
+// ends with its own token's eight eighth sums rather than their total.  The
+// running prefixes at the 8 NB eighth ends go to LDS; Algorithm 9's search
+// runs over them, and the chosen 32-topic chunk is rebuilt and searched with
+// the W = 32 machinery of the half-block tail (two tokens per load
+// instruction).  Against the dword sweep this reads the same bytes with four
+// times fewer load instructions, and the rebuild reads 128 B of phi per
+// token instead of a 256-topic block.
+//
+// Register slot s of the sweep holds token eighth_slot_token(s): with the
+// stage order above, lane l ends with slot (l5 l4 l3 l0 l1 l2) (bits listed
+// from bit 0 up), so slots are loaded with the inverse permutation and lane l
+// finishes with token l.  Afterwards eighth q of the lane's token is in
+// register bitrev3(q).
+__host__ __device__ constexpr int eighth_slot_token(int s) {
+  return ((s >> 3) & 1) | (((s >> 4) & 1) << 1) | (((s >> 5) & 1) << 2) |
+         (((s >> 2) & 1) << 3) | (((s >> 1) & 1) << 4) | ((s & 1) << 5);
+}
+__host__ __device__ constexpr int bitrev3(int q) { return ((q & 1) << 2) | (q & 2) | ((q >> 2) & 1); }
+
+// Sums registers k and k + BIT (k < BIT) across lanes l and l xor L: lanes
+// with L clear keep token k's sum, lanes with L set token k + BIT's.
+template <int L, int BIT, int N>
+__device__ __forceinline__ void pair_stage(float (&a)[N]) {
+#pragma unroll
+  for (int k = 0; k < BIT; ++k) {
+    if constexpr (L >= 4) {
+      half_swap<L>(a[k], a[k + BIT]);
+      a[k] = a[k] + a[k + BIT];
+    } else {
+      a[k] = pair_sum<L>(a[k], a[k + BIT]);
+    }
+  }
+}
+
+// Sweep step for one 256-topic block: win[] holds (or awaits) the phi leaves
+// of the first C slots in pair order, twin[] (any documents) their theta
+// leaves, th[] the theta leaves of the first / last document.  With PREFETCH
+// the windows and thn[] are refilled with block `next` as the block drains.
+// rows[q * 64] receives the running prefix at the end of eighth q; returns the
+// prefix at the block's end.
+template <int MODE, bool PREFETCH, int C, int CT>
+__device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&win)[C],
+                                              f4 (&twin)[CT], f4 (&th)[2], f4 (&thn)[2],
+                                              int blk, int next, float *rows, float prefix) {
+  static_assert(kWave % C == 0, "the window size must divide 64");
+  const uint32_t vcur = (uint32_t)(blk * kBlock4 + kLeaf * w.r) * 4u;
+  const uint32_t vnext = (uint32_t)(next * kBlock4 + kLeaf * w.r) * 4u;
+  const int kb = MODE == kTwoDocs ? launder_int(w.kb) : kWave;
+  float s[kWave / 2];
+  float lo = 0.0f;
+#pragma unroll
+  for (int i = 0; i < kWave; ++i) {
+    const int slot = pair_token(i);
+    const int t = eighth_slot_token(slot);
+    f4 tv;
+    if constexpr (MODE == kAnyDocs)
+      tv = twin[i % C];
+    else if constexpr (MODE == kTwoDocs)
+      tv = t < kb ? th[0] : th[1];
+    else
+      tv = th[0];
+    const float v = dot4(tv, win[i % C]);
+    if (i & 1) {
+      float hi = v;
+      half_swap<4>(lo, hi);
+      s[slot - 32] = lo + hi;
+    } else {
+      lo = v;
+    }
+    const bool refill = i + C < kWave;
+    if (refill || PREFETCH) {
+      const int tn = eighth_slot_token(pair_token(refill ? i + C : i + C - kWave));
+      const uint32_t voff = refill ? vcur : vnext;
+      if (!refill && MODE != kAnyDocs && i + C == kWave) {
+        thn[0] = load_f32x4(w.th_rs, vnext, w.th_off0);
+        if constexpr (MODE == kTwoDocs) thn[1] = load_f32x4(w.th_rs, vnext, w.th_off1);
+      }
+      win[i % C] = load_f32x4(w.ph_rs, voff, __builtin_amdgcn_readlane(w.ph_lane, tn));
+      if constexpr (MODE == kAnyDocs)
+        twin[i % C] = load_f32x4(w.th_rs, voff, __builtin_amdgcn_readlane(w.th_lane, tn));
+    }
+    // keep the window rolling (see sweep4_block)
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  pair_stage<2, 16>(s);
+  pair_stage<1, 8>(s);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) half_swap<8>(s[j], s[j + 4]);
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    half_swap<16>(s[j], s[j + 2]);
+    half_swap<16>(s[j + 4], s[j + 6]);
+  }
+#pragma unroll
+  for (int j = 0; j < 8; j += 2) half_swap<32>(s[j], s[j + 1]);
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    prefix += s[bitrev3(q)];
+    rows[q * kWave] = prefix;
+  }
+  if constexpr (PREFETCH && MODE != kAnyDocs) {
+    th[0] = thn[0];
+    if constexpr (MODE == kTwoDocs) th[1] = thn[1];
+  }
+  return prefix;
+}
+
+// The whole sweep over NB >= 2 blocks; rows[r * 64] receives the prefix at the
+// end of eighth r.  Returns the token's total.
+template <int MODE, int C>
+__device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, int NB, float *rows) {
+  constexpr int CT = MODE == kAnyDocs ? C : 1;
+  f4 win[C], twin[CT], th[2], thn[2];
+  const uint32_t v0 = (uint32_t)(kLeaf * w.r) * 4u;
+  if constexpr (MODE != kAnyDocs) {
+    th[0] = load_f32x4(w.th_rs, v0, w.th_off0);
+    th[1] = MODE == kTwoDocs ? load_f32x4(w.th_rs, v0, w.th_off1) : th[0];
+  }
+#pragma unroll
+  for (int i = 0; i < C; ++i) {
+    const int t = eighth_slot_token(pair_token(i));
+    win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, t));
+    if constexpr (MODE == kAnyDocs)
+      twin[i] = load_f32x4(w.th_rs, v0, __builtin_amdgcn_readlane(w.th_lane, t));
+  }
+  float prefix = 0.0f;
+  for (int b = 0; b < NB - 1; ++b)
+    prefix = sweep8_block<MODE, true, C, CT>(w, win, twin, th, thn, b, b + 1,
+                                             rows + 8 * b * kWave, prefix);
+  return sweep8_block<MODE, false, C, CT>(w, win, twin, th, thn, NB - 1, 0,
+                                          rows + 8 * (NB - 1) * kWave, prefix);
+}
+
+template <int C, int WPB, int WPEU>
+__global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
+void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                         DocSource docs, const int32_t *__restrict__ word_id,
+                         UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
+                         uint32_t theta_bytes, uint32_t phi_bytes) {
+  extern __shared__ float lds[];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t first = ((int64_t)blockIdx.x * WPB + wave) * kWave;
+  if (first >= N) return;  // whole wavefront past the end
+  // Window of 64 tokens as in butterfly_kernel (N >= 64 here).
+  const int64_t t0 = first + kWave <= N ? first : N - kWave;
+  const int64_t n = t0 + lane;
+  const bool store = n >= first;
+
+  const int doc = docs.wave_doc(n, t0, t0 + kWave - 1);
+  const int word = word_id[n];
+  const float un = u(n);
+  const int NB = K / kBlock4;
+  Wave<kWave, false> w;
+  init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, kWave - 1, K,
+                          lane, doc, word);
+  float *region = lds + wave * 8 * NB * kWave;
+
+  float sum;
+  if (w.mode == kOneDoc)
+    sum = sweep8<kOneDoc, C>(w, NB, region + lane);
+  else if (w.mode == kTwoDocs)
+    sum = sweep8<kTwoDocs, C>(w, NB, region + lane);
+  else
+    sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C)>(w, NB, region + lane);
+  const float stop = sum * un;
+  // Algorithm 9 over the ends of the 8 NB eighths.
+  int lo = 0, hi = 8 * NB - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (stop < region[mid * kWave + lane])
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  const int chunk = lo;
+  float low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
+  float high = region[lo * kWave + lane];
+  // Rebuild every token's chosen 32-topic chunk (W = 32 groups) and search it
+  // with Algorithm 10.  Empty topics are never chosen; with S = 0 every
+  // comparison fails and the result is K - 1.
+  const Wave<kWave / 2, false> wh = half_wave(w, lane);
+  float h[kWave / 2];
+  load_tile_blocks<kWave / 2, false, false>(wh, h, chunk, 0);
+  butterfly_block<kWave / 2>(h, wh.r, NoStore{});
+  const int j = chunk * (kWave / 2) +
+                inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
   if (store) z[n] = j;
 }
 
@@ -1312,6 +1546,32 @@ void launch_butterfly4(const float *theta, const float *phi, DocSource d,
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
+// Wavefronts per workgroup of the eighths kernel: 4 while three such
+// workgroups fit in a CU's LDS (8 K/256 rows of 64 floats per wavefront), else 2.
+bool eighths_wide_groups(int32_t K) {
+  return 3LL * 4 * 8 * (K / kBlock4) * kWave * (int64_t)sizeof(float) <= 160 * 1024;
+}
+
+template <int C, int WPEU>
+void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
+                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                    hipStream_t s) {
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const size_t rows = (size_t)8 * (K / kBlock4) * kWave * sizeof(float);
+  if (eighths_wide_groups(K))
+    leaf_eighths_kernel<C, 4, WPEU><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+  else
+    leaf_eighths_kernel<C, 2, WPEU><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+}
+
+bool eighths_for(int64_t N, int32_t K) {
+  return N >= kWave && K % kBlock4 == 0 && K / kBlock4 >= 2 &&
+         K / kBlock4 <= LDA_EIGHTHS_MAX_BLOCKS;
+}
+
 void launch_transposed(const float *theta, const float *phi, DocSource d,
                        const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
@@ -1409,6 +1669,18 @@ void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
 void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  if (eighths_for(N, K)) {
+    // launch shapes measured on MI355X: 16 tokens in flight per wavefront at
+    // 2 wavefronts per SIMD up to K = 1024 (1% faster there than 8 at 3), 4
+    // at 4 above (3% faster at K = 2048 than 8 at 3; 2 in flight: 30% slower)
+    if (K / kBlock4 <= LDA_EIGHTHS_SPLIT)
+      launch_eighths<LDA_EIGHTHS_WINDOW, LDA_EIGHTHS_WAVES_PER_EU>(theta, phi, d, word_id, u, z,
+                                                                   N, M, V, K, s);
+    else
+      launch_eighths<LDA_EIGHTHS_WINDOW_LARGE, LDA_EIGHTHS_WAVES_PER_EU_LARGE>(
+          theta, phi, d, word_id, u, z, N, M, V, K, s);
+    return;
+  }
   if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
     launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
