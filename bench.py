@@ -28,6 +28,8 @@ METRIC = ("z draws/sec and achieved HBM GB/s (% of peak) at K=256 and K=1024, "
           "1 MI355X")
 PEAK_HBM_GBPS = 8000.0            # MI355X HBM3E, published
 HEADLINE = "corpus16M-K1024"
+# the device kernel lda_draw_butterfly launches on the headline workload
+HEADLINE_KERNEL = "leaf_eighths_kernel"
 SECOND = "corpus1M-K256"
 COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1505_03851_amd", "csrc", f)
@@ -178,9 +180,10 @@ def _counter_means(d: str, kernel_substr: str) -> dict:
 
 
 def counters_summary(args) -> int:
-    """Turn rocprofv3 counter runs of the butterfly kernel and of the 1 GiB
-    copy into the record ``traffic_from_counters`` reads."""
-    kname = "butterfly"          # butterfly_kernel or butterfly4_kernel
+    """Turn rocprofv3 counter runs of the draw's kernel (dispatches whose name
+    contains ``--kernel-name``) and of the 1 GiB copy into the record
+    ``traffic_from_counters`` reads."""
+    kname = args.kernel_name
     copy = "copyBuffer"
     fetch = _counter_means(args.fetch, kname)["FETCH_SIZE"]
     write = _counter_means(args.write, kname)["WRITE_SIZE"]
@@ -189,7 +192,7 @@ def counters_summary(args) -> int:
     copy_kib = (1 << 30) / 1024
     f_scale, w_scale = copy_kib / copy_fetch, copy_kib / copy_write
     rec = {
-        "kernel": "butterfly", "workload": args.workload,
+        "kernel": "butterfly", "device_kernel": kname, "workload": args.workload,
         "kernel_source_sha1": kernel_source_hash(),
         "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
         "copy_1GiB_fetch_kib": copy_fetch, "copy_1GiB_write_kib": copy_write,
@@ -422,6 +425,9 @@ def main() -> int:
                 "--hitmiss"):
         ap.add_argument(opt, default=None)
     ap.add_argument("--out", default=COUNTERS)
+    ap.add_argument("--kernel-name", default=HEADLINE_KERNEL,
+                    help="substring of the device kernel's name in the counter "
+                         "csv files (--counters-summary)")
     args = ap.parse_args()
     if args.counters_summary:
         return counters_summary(args)

@@ -84,15 +84,17 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
 /*
  * Butterfly draw (Algorithm 7 with Algorithms 5, 8, 9 and 10, Sections 3-4).
  * A wavefront takes 64 consecutive tokens, one per lane, and reads theta and
- * phi cooperatively: each load instruction fetches W consecutive topics of one
- * token (coalesced).  Per block of W topics the lanes combine their products
- * in a butterfly pattern (log2 W exchange stages) instead of a full
- * transposition.  A first sweep over the blocks gives every lane the full
- * prefix at each block end; the block holding u*S is found by binary search
- * over those (Algorithm 9), its butterfly table is rebuilt on chip, and the
- * lane reconstructs the remaining partial sums from it while it searches
- * (Algorithm 10).  W = 64 for K >= 64, W = 32 below; the first K mod W topics
- * (the remnant) are summed per lane without transposition.
+ * phi cooperatively: each load instruction fetches consecutive topics of one
+ * token (coalesced) -- W topics, one per lane, or, when K is a multiple of
+ * 256, 256 topics as leaves of four per lane.  Per block the lanes combine
+ * their products in a butterfly pattern (log2 W exchange stages) instead of a
+ * full transposition.  A first sweep over the blocks gives every lane the full
+ * prefix at the end of each block (or of each 32-topic part of it); the part
+ * holding u*S is found by binary search over those (Algorithm 9), its
+ * butterfly table is rebuilt on chip, and the lane reconstructs the remaining
+ * partial sums from it while it searches (Algorithm 10).  W = 64 for K >= 64,
+ * W = 32 below; the first K mod W topics (the remnant) form a leading block
+ * padded with empty topics, which are never drawn.
  */
 int lda_draw_butterfly(const float *theta, const float *phi,
                        const int32_t *doc_id, const int32_t *word_id,

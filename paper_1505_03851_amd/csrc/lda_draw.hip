@@ -31,13 +31,8 @@
 #ifndef LDA_WAVES_PER_BLOCK
 #define LDA_WAVES_PER_BLOCK 2
 #endif
-//   LDA_LEAF4_MAX_BLOCKS      use the four-topic-leaf kernel when K is a
-//                             multiple of 256 with at most this many 256-topic
-//                             blocks (0: never);
-//   LDA_LEAF4_WINDOW          tokens whose leaf loads are in flight at once.
-#ifndef LDA_LEAF4_MAX_BLOCKS
-#define LDA_LEAF4_MAX_BLOCKS 1
-#endif
+//   LDA_LEAF4_WINDOW          tokens whose leaf loads are in flight at once in
+//                             the four-topic-leaf kernel for K = 256.
 #ifndef LDA_LEAF4_WINDOW
 #define LDA_LEAF4_WINDOW 8
 #endif
@@ -52,12 +47,6 @@
 //                             up to 26 blocks, 10 at 32 blocks).
 #ifndef LDA_HALF_MAX_BLOCKS
 #define LDA_HALF_MAX_BLOCKS 32
-#endif
-//   LDA_HALF_WAVES_PER_BLOCK  wavefronts per workgroup of the half-block-tail
-//                             kernel while three such workgroups fit in LDS
-//                             (else LDA_WAVES_PER_BLOCK).
-#ifndef LDA_HALF_WAVES_PER_BLOCK
-#define LDA_HALF_WAVES_PER_BLOCK 4
 #endif
 //   LDA_EIGHTHS_MAX_BLOCKS    largest K / 256 for which K a multiple of 256 is
 //                             drawn by the leaf kernel with 32-topic prefix
@@ -752,101 +741,19 @@ void butterfly_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Butterfly kernel with leaves of four topics (K a multiple of 256).
+// Butterfly kernel with leaves of four topics (K = 256: one block).
 //
-// Lane l of a wavefront reads topics [4l, 4l + 4) of a 256-topic block with
-// one 16-byte load per token, so a block takes 64 loads instead of 256.  The
+// Lane l of a wavefront reads topics [4l, 4l + 4) of the 256-topic block with
+// one 16-byte load per token, so the block takes 64 loads instead of 256.  The
 // lane first sums its four products (dot4); the 64 lanes then combine these
-// leaf sums exactly as the W = 64 kernel combines single products: a
-// reduce-scatter for the sweep's block totals, the paper's butterfly for the
-// chosen block, and Algorithm 10's search, which now finds the leaf.  The
-// final step scans the four products of that leaf (lane-private loads).
-// Loads go through a rolling window of C tokens: the load of token k + C is
-// issued as soon as token k's leaf sum is formed.
+// leaf sums exactly as the W = 64 kernel combines single products: the
+// paper's butterfly builds the block's table over leaves and Algorithm 10's
+// search finds the leaf.  The final step scans the four products of that leaf
+// (lane-private loads).  Loads go through a rolling window of C tokens: the
+// load of token k + C is issued as soon as token k's leaf sum is formed.
 constexpr int kLeaf = 4;
 constexpr int kBlock4 = kWave * kLeaf;  // topics per block
 
-// Tokens of a sweep block are taken in pair order 0, 32, 1, 33, ...: as soon
-// as tokens k and k + 32 have their leaf sums, the first reduce-scatter stage
-// (lanes l and l xor 32) combines them, so only 32 partial sums stay live.
-__device__ __host__ constexpr int pair_token(int i) { return (i >> 1) + ((i & 1) << 5); }
-
-// Sweep step for one 256-topic block in one- or two-document waves.  win[]
-// holds (or awaits) the phi leaves of the first C tokens in pair order of
-// block `blk`; th[] the theta leaves of the first / last document.  With
-// PREFETCH the window and thn[] are refilled with block `next` as the block
-// drains, and th[] takes thn[] at the end.  Returns this lane's token total
-// over the block.
-template <bool SMALL, int C, bool TWO, bool PREFETCH>
-__device__ __forceinline__ float sweep4_block(const Wave<kWave, SMALL> &w, const int32_t *wp,
-                                              f4 (&win)[C], f4 (&th)[2], f4 (&thn)[2],
-                                              int blk, int next) {
-  // the slot of token i is i % C in every block, so the refill for the next
-  // block's token i + C - 64 lands in the slot that token reads
-  static_assert(kWave % C == 0, "the window size must divide 64");
-  const uint32_t vcur = (uint32_t)(blk * kBlock4 + kLeaf * w.r) * 4u;
-  const uint32_t vnext = (uint32_t)(next * kBlock4 + kLeaf * w.r) * 4u;
-  const int kb = TWO ? launder_int(w.kb) : kWave;
-  float s[kWave / 2];
-  float lo = 0.0f;
-#pragma unroll
-  for (int i = 0; i < kWave; ++i) {
-    const int k = pair_token(i);
-    const float v = dot4((!TWO || k < kb) ? th[0] : th[1], win[i % C]);
-    if (i & 1) {
-      float hi = v;
-      half_swap<32>(lo, hi);
-      s[k - 32] = lo + hi;
-    } else {
-      lo = v;
-    }
-    if (i + C < kWave) {
-      win[i % C] = load_f32x4(w.ph_rs, vcur, __builtin_amdgcn_readlane(w.ph_lane, pair_token(i + C)));
-    } else if constexpr (PREFETCH) {
-      if (i + C == kWave) {
-        thn[0] = load_f32x4(w.th_rs, vnext, w.th_off0);
-        if constexpr (TWO) thn[1] = load_f32x4(w.th_rs, vnext, w.th_off1);
-      }
-      win[i % C] = load_f32x4(w.ph_rs, vnext,
-                              __builtin_amdgcn_readlane(w.ph_lane, pair_token(i + C - kWave)));
-    }
-    // keep the window rolling: no load is hoisted past this point (hoisting
-    // them all would need 4 registers per token of the block)
-    __builtin_amdgcn_sched_barrier(0);
-  }
-  reduce_stage<kWave / 2, 16>(s);
-  reduce_stage<kWave / 2, 8>(s);
-  reduce_stage<kWave / 2, 4>(s);
-  reduce_stage<kWave / 2, 2>(s);
-  reduce_stage<kWave / 2, 1>(s);
-  if constexpr (PREFETCH) {
-    th[0] = thn[0];
-    if constexpr (TWO) th[1] = thn[1];
-  }
-  return s[0];
-}
-
-// The whole sweep (NB >= 2 blocks) of a one- or two-document wave: prologue
-// loads, blocks 0..NB-2 with prefetch of the next block, the last block
-// without.  The running prefix at block b's end goes to prefix[b * 64].
-template <bool SMALL, int C, bool TWO>
-__device__ __forceinline__ float sweep4(const Wave<kWave, SMALL> &w, int NB, float *prefix) {
-  f4 win[C], th[2], thn[2];
-  const uint32_t v0 = (uint32_t)(kLeaf * w.r) * 4u;
-  th[0] = load_f32x4(w.th_rs, v0, w.th_off0);
-  th[1] = TWO ? load_f32x4(w.th_rs, v0, w.th_off1) : th[0];
-#pragma unroll
-  for (int i = 0; i < C; ++i)
-    win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, pair_token(i)));
-  float sum = 0.0f;
-  for (int b = 0; b < NB - 1; ++b) {
-    sum += sweep4_block<SMALL, C, TWO, true>(w, launder(w.wp), win, th, thn, b, b + 1);
-    prefix[b * kWave] = sum;
-  }
-  sum += sweep4_block<SMALL, C, TWO, false>(w, w.wp, win, th, thn, NB - 1, 0);
-  prefix[(NB - 1) * kWave] = sum;
-  return sum;
-}
 
 // Tile of leaf sums in which token k reads block blk_k of its own document and
 // word (this lane's `blk` is its own token's block; any documents).
@@ -890,7 +797,6 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
                        DocSource docs, const int32_t *__restrict__ word_id,
                        UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
-  extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
@@ -904,59 +810,20 @@ void butterfly4_kernel(const float *__restrict__ theta, const float *__restrict_
   const int doc = docs.wave_doc(n, t0, t0 + last);
   const int word = word_id[n];
   const float un = u(n);
-  const int NB = K / kBlock4;
   Wave<kWave, SMALL> w;
   init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
                           lane, doc, word);
-  float *region = lds + wave * NB * kWave;
 
+  // The block's table over leaves (any documents: a theta leaf per token).
   float s[kWave];
-  float sum = 0.0f, stop, low, high;
-  int blk;
-  if (NB == 1) {
-    blk = 0;
-    leaf_tile<SMALL, C / 2>(w, w.wp, 0, s);
-    butterfly_block<kWave>(s, w.r, NoStore{});
-    sum = s[kWave - 1];
-    stop = sum * un;
-    low = 0.0f;
-    high = sum;
-  } else {
-    // Sweep over the blocks.
-    if (w.mode == kAnyDocs) {
-      for (int b = 0; b < NB; ++b) {
-        leaf_tile<SMALL, C / 2>(w, launder(w.wp), b, s);
-        reduce_stage<kWave, 32>(s);
-        reduce_rest<kWave, SMALL, 16, false>(w, w.wp, s, 0);
-        sum += s[0];
-        region[b * kWave + lane] = sum;
-      }
-    } else if (w.mode == kOneDoc) {
-      sum = sweep4<SMALL, C, false>(w, NB, region + lane);
-    } else {
-      sum = sweep4<SMALL, C, true>(w, NB, region + lane);
-    }
-    stop = sum * un;
-    // Algorithm 9: binary search over the last row of each block.
-    int lo = 0, hi = NB - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (stop < region[mid * kWave + lane])
-        hi = mid;
-      else
-        lo = mid + 1;
-    }
-    blk = lo;
-    low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
-    high = region[lo * kWave + lane];
-    // Rebuild every token's chosen block as leaf sums and combine them with
-    // the paper's butterfly.
-    leaf_tile<SMALL, C / 2>(w, w.wp, blk, s);
-    butterfly_block<kWave>(s, w.r, NoStore{});
-  }
+  leaf_tile<SMALL, C / 2>(w, w.wp, 0, s);
+  butterfly_block<kWave>(s, w.r, NoStore{});
+  const float sum = s[kWave - 1];
+  const float stop = sum * un;
+  float low = 0.0f, high = sum;
   // Algorithm 10 over the leaves, then the four topics of the chosen leaf.
   const int leaf = inblock_search<kWave, false>(s, nullptr, w.r, 0, stop, low, high);
-  const int base = blk * kBlock4 + kLeaf * leaf;
+  const int base = kLeaf * leaf;
   const int j = base + leaf_scan(w.th_rs, w.ph_rs, (uint32_t)doc * w.row_bytes,
                                  (uint32_t)word * w.row_bytes, base, low, stop);
   if (store) z[n] = j;
@@ -989,6 +856,11 @@ __host__ __device__ constexpr int eighth_slot_token(int s) {
          (((s >> 2) & 1) << 3) | (((s >> 1) & 1) << 4) | ((s & 1) << 5);
 }
 __host__ __device__ constexpr int bitrev3(int q) { return ((q & 1) << 2) | (q & 2) | ((q >> 2) & 1); }
+
+// Slots of a sweep block are taken in pair order 0, 32, 1, 33, ...: as soon
+// as slots s and s + 32 have their leaf sums, the first reduce-scatter stage
+// combines them, so only 32 partial sums stay live.
+__device__ __host__ constexpr int pair_token(int i) { return (i >> 1) + ((i & 1) << 5); }
 
 // Sums registers k and k + BIT (k < BIT) across lanes l and l xor L: lanes
 // with L clear keep token k's sum, lanes with L set token k + BIT's.
@@ -1052,7 +924,8 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&
       if constexpr (MODE == kAnyDocs)
         twin[i % C] = load_f32x4(w.th_rs, voff, __builtin_amdgcn_readlane(w.th_lane, tn));
     }
-    // keep the window rolling (see sweep4_block)
+    // keep the window rolling: no load is hoisted past this point (hoisting
+    // them all would need 4 registers per token of the block)
     __builtin_amdgcn_sched_barrier(0);
   }
   pair_stage<2, 16>(s);
@@ -1535,14 +1408,13 @@ template <int C>
 void launch_butterfly4(const float *theta, const float *phi, DocSource d,
                        const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
-  const size_t lds = (size_t)kWavesPerBlock * (K / kBlock4) * kWave * sizeof(float);
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (N < kWave)
-    butterfly4_kernel<true, C><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly4_kernel<true, C><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    butterfly4_kernel<false, C><<<wave_grid(N), kBlockThreads, lds, s>>>(
+    butterfly4_kernel<false, C><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
@@ -1603,16 +1475,6 @@ void launch_butterfly(const float *theta, const float *phi, DocSource d,
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
-// Whether three workgroups of the half-block-tail kernel with
-// LDA_HALF_WAVES_PER_BLOCK wavefronts fit in a CU's 160 KiB of LDS (each
-// wavefront keeps 2 K/64 rows of 64 floats), so that the larger workgroups
-// cost no occupancy.  Measured on MI355X: 4 wavefronts per workgroup take
-// 1.3% off K = 1024 and cost 1% at K = 2048, where they would not fit.
-bool half_wide_groups(int32_t K) {
-  const int64_t bytes = 3LL * LDA_HALF_WAVES_PER_BLOCK *
-                        region_rows((K + 63) / 64, 64, false, true) * kWave * sizeof(float);
-  return bytes <= 160 * 1024;
-}
 
 // The W = 32 / 64 butterfly kernel with a chosen table: in registers with the
 // paper's search-assist loop, in LDS with direct reads, or the alternative
@@ -1681,7 +1543,7 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
           theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
   }
-  if (K % kBlock4 == 0 && K / kBlock4 <= LDA_LEAF4_MAX_BLOCKS) {
+  if (K == kBlock4) {
     launch_butterfly4<LDA_LEAF4_WINDOW>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
   }
@@ -1689,9 +1551,6 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
   if (width_for(K) == 64) {
     if (lt)
       launch_butterfly<64, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (half_tail_for(K) && half_wide_groups(K))
-      launch_butterfly<64, false, false, true, LDA_HALF_WAVES_PER_BLOCK>(theta, phi, d, word_id, u,
-                                                                         z, N, M, V, K, s);
     else if (half_tail_for(K))
       launch_butterfly<64, false, false, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     else
