@@ -241,7 +241,7 @@ __device__ __forceinline__ int group_value(int v, int k) {
 enum ThetaMode : int { kOneDoc = 0, kTwoDocs = 1, kAnyDocs = 2 };
 
 // One step of an untransposed running sum (the naive kernel, the remnant of
-// the table dump, the scan of a leaf): sum + theta * phi.
+// the table dump): sum + theta * phi.
 __device__ __forceinline__ float prefix_step(float sum, float th, float ph) {
   return __builtin_fmaf(th, ph, sum);
 }

@@ -97,8 +97,15 @@ SHAPES = [
     (64 * 9 + 40, 3, 100, 1792, "single"),
     (64 * 11 + 3, 20, 300, 1900, "sequential"),
     (64 * 8 + 63, 9, 200, 2048, "sequential"),
+    # K divisible by 4 but not by 256: the leaf kernel with empty topics in
+    # front of its first 256-topic block (one, two and many documents per wave)
+    (64 * 11 + 7, 13, 300, 1000, "sequential"),
+    (64 * 7 + 50, 9, 200, 516, "shuffled"),
+    (64 * 6 + 1, 4, 150, 2044, "single"),
+    (64 * 9 + 3, 30, 300, 1604, "sequential"),
+    (64 * 5 + 30, 3, 100, 772, "sequential"),
     (64 * 5 + 3, 20, 200, 4096, "sequential"),
-    # K a multiple of 256: the four-topic-leaf kernel
+    # K a multiple of 256 (the leaf kernel with 32-topic prefix rows up to 2048)
     (1, 1, 7, 256, "sequential"),
     (63, 5, 50, 512, "shuffled"),
     (65, 5, 50, 768, "sequential"),
@@ -148,7 +155,7 @@ def test_equal_power_of_two_weights_exact(K, kernel):
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("K", [1, 5, 32, 64, 100, 1024])
+@pytest.mark.parametrize("K", [1, 5, 32, 64, 100, 1000, 1024])
 def test_degenerate_weights(K, kernel):
     """All-zero documents draw K-1; a one-hot document draws its topic for
     every u (including u = 0 and u = 1 - 2**-24); mixed with normal rows."""
@@ -247,7 +254,7 @@ RAGGED = [
     (64 * 33 + 63, 60, 500, 128),
     (64 * 33 + 63, 60, 500, 129),
     (64 * 33 + 63, 60, 500, 200),
-    (64 * 9 + 33, 40, 100, 256),      # four-topic-leaf kernel
+    (64 * 9 + 33, 40, 100, 256),      # leaf kernel, one block
     (64 * 7 + 5, 300, 90, 1280),
     (64 * 17 + 9, 60, 500, 2047),
     (64 * 5 + 3, 20, 200, 4096),
