@@ -33,7 +33,7 @@ HEADLINE_KERNEL = "leaf_eighths_kernel"
 SECOND = "corpus1M-K256"
 COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
 KERNEL_SOURCES = [os.path.join(ROOT, "paper_1505_03851_amd", "csrc", f)
-                  for f in ("lda_draw.hip", "butterfly.hpp", "philox.hpp")]
+                  for f in ("lda_draw.hip", "butterfly.hpp", "philox.hpp", "route.hpp")]
 
 
 def kernel_source_hash() -> str:
@@ -42,6 +42,11 @@ def kernel_source_hash() -> str:
         with open(p, "rb") as f:
             h.update(f.read())
     return h.hexdigest()
+
+
+def routable(K: int) -> bool:
+    """K the routed draw takes (divisible by 4, 132 <= K <= 2048)."""
+    return K % 4 == 0 and 132 <= K <= 2048
 
 
 def algorithmic_bytes(c) -> int:
@@ -68,14 +73,32 @@ def upload(c):
 
 # kernels bench.py can time: name -> entry point of the binding
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
-           "variant-register", "variant-lds", "variant-lds_alt", "philox")
+           "variant-register", "variant-lds", "variant-lds_alt", "philox", "routed",
+           "routed+build")
 PHILOX_SEED = 0x5EED20150513
 
 
 def launcher(kernel: str, dev):
-    """A function (out, stream) that launches ``kernel`` once over ``dev``."""
+    """A function (out, stream) that launches ``kernel`` once over ``dev``.
+    "routed" draws the tokens routed to the XCDs with the routing built once
+    beforehand (as a sampler does once per corpus); "routed+build" builds the
+    routing again in every launch (one stream synchronisation inside)."""
     import paper_1505_03851_amd as lda
     th, ph, d, w, u = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    if kernel == "routed":
+        if "route" not in dev:
+            dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
+        route = dev["route"]
+        return lambda out, stream: lda.draw_routed(th, ph, route, u, out=out, stream=stream)
+    if kernel == "routed+build":
+        if "route" not in dev:
+            dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
+        ws = dev["route"].workspace
+
+        def build_and_draw(out, stream):
+            r = lda.route_build(d, w, th.shape[0], ph.shape[0], workspace=ws, stream=stream)
+            lda.draw_routed(th, ph, r, u, out=out, stream=stream)
+        return build_and_draw
     if kernel == "philox":
         return lambda out, stream: lda.draw_philox(th, ph, d, w, PHILOX_SEED, 0, out=out,
                                                    stream=stream)
@@ -338,6 +361,13 @@ def all_configs(args) -> int:
         r = measure(name, c, dev, "butterfly", args.steps, args.warmup, flush=flush)
         for key in ("ms_per_launch", "ms_per_launch_median", "draws_per_s", "alg_GBps"):
             rec[f"butterfly_cold_{key}"] = r[key]
+        if routable(c.K):
+            z_bf = measure(name, c, dev, "butterfly", 1, 0)["z"]
+            for kernel in ("routed", "routed+build"):
+                r = measure(name, c, dev, kernel, args.steps, args.warmup)
+                for key in ("ms_per_launch", "ms_per_launch_median", "draws_per_s", "alg_GBps"):
+                    rec[f"{kernel}_{key}"] = r[key]
+                rec[f"{kernel}_differs_from_butterfly"] = int((r["z"] != z_bf).sum())
         print(json.dumps(rec), flush=True)
         del dev
         torch.cuda.empty_cache()
@@ -494,6 +524,12 @@ def main() -> int:
     head = measure(HEADLINE, c, dev, "butterfly", args.steps, args.warmup)
     z_head = head.pop("z")
     results.append(head)
+    # the same draw over tokens routed to the XCDs by word: routing built once
+    # (as per corpus in a sampler), and built again in every step
+    for k in ("routed", "routed+build"):
+        r = measure(HEADLINE, c, dev, k, args.steps, args.warmup)
+        r["differs_from_butterfly"] = int((r.pop("z") != z_head).sum())
+        results.append(r)
     # the same launches with L2 and the MALL flushed before each (1 GiB fill)
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     cold = measure(HEADLINE, c, dev, "butterfly", args.steps, 1, flush=flush)

@@ -36,9 +36,11 @@
  * owned by the caller, 4-byte aligned.  The library keeps no state between
  * calls and allocates no device memory; kernels use on-chip LDS only (and,
  * in the naive kernel, the per-lane private segment the HIP runtime manages).
+ * The routed draw keeps its routing in a workspace the caller provides.
  *
  * Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls only
- * enqueue work and return; the caller synchronises.  Calls that share the
+ * enqueue work and return; the caller synchronises (lda_route_build alone
+ * waits for its own work, to read back the sizes of the routed lists).  Calls that share the
  * output buffer must be ordered by the caller.
  *
  * Errors: every entry point returns LDA_OK (0) or a negative status.  Argument
@@ -50,6 +52,7 @@
 #ifndef LDA_DRAW_H
 #define LDA_DRAW_H
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -62,6 +65,7 @@ extern "C" {
 #define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K, or a table too large      */
 #define LDA_ERR_HIP (-4)         /* the HIP runtime reported an error        */
 #define LDA_ERR_ALIGN (-5)       /* a pointer is not 4-byte aligned          */
+#define LDA_ERR_WORKSPACE (-6)   /* routing workspace too small or mismatched */
 
 /* Largest number of topics the kernels accept. */
 #define LDA_MAX_K 4096
@@ -221,6 +225,53 @@ int lda_butterfly_table(const float *theta, const float *phi,
                         const int32_t *doc_id, const int32_t *word_id,
                         float *table, int64_t N, int32_t M, int32_t V,
                         int32_t K, void *stream);
+
+/*
+ * Tokens routed to the GPU's XCDs by word.  The MI355X dispatches workgroups
+ * to its eight XCDs round robin, and each XCD has its own L2.  In token order
+ * every XCD reads phi rows from the whole vocabulary; routing gives every XCD
+ * the tokens of one eighth of the vocabulary, so its L2 serves more of them.
+ * The draw is the same per token (Algorithms 7-10 with 16-byte leaf loads);
+ * only the grouping of tokens into wavefronts changes.  Routing pays where
+ * phi is far larger than the caches (measured on MI355X: 19% at K = 2048 with
+ * a 390 MiB phi, 4% at K = 1024) and costs where it is not (K <= 256).
+ *
+ * lda_route_build: splits the words into 256 classes by a hash, assigns the
+ * classes to 8 lists with about equal token counts, and lays the tokens out
+ * in the caller's workspace as those 8 lists, each in the original token
+ * order and padded to a multiple of 64.  It depends on doc_id and word_id
+ * only, so a sampler builds it once per corpus and reuses it every sweep.
+ * It enqueues its kernels on `stream`, then synchronises `stream` once to
+ * copy the list sizes into *route (the one entry point that waits).
+ *   workspace        device memory, 8-byte aligned, at least
+ *                    lda_route_workspace_bytes(N) bytes (about 12 N), owned
+ *                    by the caller; it holds the routing and must stay
+ *                    unchanged until the last lda_draw_routed that uses it.
+ *   route            host struct filled on success.
+ * Errors as above; LDA_ERR_WORKSPACE if workspace_bytes is too small;
+ * LDA_ERR_UNSUPPORTED if N > LDA_ROUTE_MAX_N.
+ *
+ * lda_draw_routed: the draw of lda_draw_butterfly over routed tokens: z[n]
+ * and u[n] are indexed by the original token n.  theta, phi, M, V, K as for
+ * lda_draw_butterfly; K must be divisible by 4 with 132 <= K <= 2048, else
+ * LDA_ERR_UNSUPPORTED; `route` and `workspace` must come from one
+ * lda_route_build over these N tokens, else LDA_ERR_WORKSPACE.
+ */
+#define LDA_ROUTE_MAX_N 2147483135LL
+typedef struct lda_route {
+  int64_t N;          /* tokens routed */
+  int64_t tokens[8];  /* tokens in list x */
+  int64_t start[8];   /* first routed position of list x */
+  int64_t length[8];  /* positions of list x: tokens[x] rounded up to 64 */
+} lda_route;
+
+size_t lda_route_workspace_bytes(int64_t N);
+int lda_route_build(const int32_t *doc_id, const int32_t *word_id, int64_t N, int32_t M,
+                    int32_t V, void *workspace, size_t workspace_bytes, lda_route *route,
+                    void *stream);
+int lda_draw_routed(const float *theta, const float *phi, const void *workspace,
+                    size_t workspace_bytes, const lda_route *route, const float *u,
+                    int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K, void *stream);
 
 /* The W (butterfly width) the library uses for K, or LDA_ERR_UNSUPPORTED /
  * LDA_ERR_SHAPE for a K it rejects. */

@@ -47,6 +47,12 @@ VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
             "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"]}
 
 
+class RouteInfo(ctypes.Structure):
+    """struct lda_route: the sizes of the eight routed lists."""
+    _fields_ = [("N", ctypes.c_int64), ("tokens", ctypes.c_int64 * 8),
+                ("start", ctypes.c_int64 * 8), ("length", ctypes.c_int64 * 8)]
+
+
 def load() -> ctypes.CDLL:
     """Load the library (once).  Raises if it has not been built."""
     global _lib
@@ -82,6 +88,14 @@ def load() -> ctypes.CDLL:
     lib.lda_status_string.restype = ctypes.c_char_p
     lib.lda_last_hip_error.restype = ctypes.c_char_p
     lib.lda_version.restype = ctypes.c_int
+    lib.lda_route_workspace_bytes.argtypes = [I64]
+    lib.lda_route_workspace_bytes.restype = ctypes.c_size_t
+    lib.lda_route_build.argtypes = [P, P, I64, I32, I32, P, ctypes.c_size_t,
+                                    ctypes.POINTER(RouteInfo), P]
+    lib.lda_route_build.restype = ctypes.c_int
+    lib.lda_draw_routed.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(RouteInfo), P, P,
+                                    I64, I32, I32, I32, P]
+    lib.lda_draw_routed.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -330,3 +344,122 @@ def butterfly_width(K: int) -> int:
 
 def version() -> int:
     return int(load().lda_version())
+
+
+def route_workspace_bytes(N: int) -> int:
+    """Bytes of device workspace ``route_build`` needs for N tokens."""
+    return int(load().lda_route_workspace_bytes(int(N)))
+
+
+def route_layout(N: int) -> dict[str, int]:
+    """Byte offsets of the routing's sections in the workspace (the library's
+    layout: perm, rword, rdoc int32 [N + 512] each, then the builder's
+    tables, every section starting on a 256-byte boundary) and its size."""
+    Np = N + 8 * 64
+    nchunks = (N + 4095) // 4096
+    off, out = 0, {}
+    for name, nbytes in (("perm", 4 * Np), ("rword", 4 * Np), ("rdoc", 4 * Np),
+                         ("chunk_off", 32 * nchunks), ("counts", 1024), ("map", 1024),
+                         ("lists", 192)):
+        out[name] = off
+        off += (nbytes + 255) & ~255
+    out["bytes"] = off
+    return out
+
+
+class Route:
+    """Tokens routed to the GPU's XCDs by word (``route_build``): the device
+    workspace that holds the routing and the host copy of the list sizes.
+    It belongs to one corpus (its doc and word ids) and can be reused by
+    every ``draw_routed`` over that corpus."""
+
+    def __init__(self, workspace: torch.Tensor, info: RouteInfo, M: int, V: int):
+        self.workspace = workspace
+        self.info = info
+        self.M, self.V = M, V
+
+    @property
+    def N(self) -> int:
+        return int(self.info.N)
+
+    @property
+    def tokens(self) -> list[int]:
+        return list(self.info.tokens)
+
+    @property
+    def start(self) -> list[int]:
+        return list(self.info.start)
+
+    @property
+    def length(self) -> list[int]:
+        return list(self.info.length)
+
+    def arrays(self) -> dict[str, torch.Tensor]:
+        """Views of the routed arrays in the workspace: perm (token at each
+        routed position, -1 for padding), rword and rdoc (its word and
+        document), int32 [N + 512] each (positions past the lists unused)."""
+        lay = route_layout(self.N)
+        n = self.N + 8 * 64
+        return {k: self.workspace[lay[k]:lay[k] + 4 * n].view(torch.int32)
+                for k in ("perm", "rword", "rdoc")}
+
+
+def route_build(doc_id, word_id, M: int, V: int, workspace=None, stream=None,
+                validate: bool = False) -> Route:
+    """Route the tokens (doc_id, word_id: int32 [N] on the GPU) to the eight
+    XCDs by word.  ``workspace``: a uint8 tensor of at least
+    ``route_workspace_bytes(N)`` bytes on the same GPU, or None to allocate
+    one.  Synchronises ``stream`` once (to read back the list sizes)."""
+    _require(doc_id, "doc_id", torch.int32, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    N = doc_id.shape[0]
+    if word_id.shape[0] != N or word_id.device != doc_id.device:
+        raise ValueError("doc_id and word_id must have one length and device")
+    if validate:
+        _validate_ids(doc_id, word_id, M, V)
+    need = route_workspace_bytes(N)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=doc_id.device)
+    else:
+        _require(workspace, "workspace", torch.uint8, 1)
+        if workspace.device != doc_id.device:
+            raise ValueError("workspace must be on the tensors' device")
+    info = RouteInfo()
+    with torch.cuda.device(doc_id.device):
+        st = load().lda_route_build(doc_id.data_ptr(), word_id.data_ptr(), N, int(M), int(V),
+                                    workspace.data_ptr(), workspace.numel(),
+                                    ctypes.byref(info), _stream_handle(stream))
+    _check(st)
+    return Route(workspace, info, int(M), int(V))
+
+
+def draw_routed(theta, phi, route: Route, u, out=None, stream=None) -> torch.Tensor:
+    """z[N] (int32, indexed by the original token) by the leaf kernel over the
+    routed tokens; u float32 [N] indexed by the original token.  K must be
+    divisible by 4 with 132 <= K <= 2048."""
+    _require(theta, "theta", torch.float32, 2)
+    _require(phi, "phi", torch.float32, 2)
+    _require(u, "u", torch.float32, 1)
+    M, K = theta.shape
+    V, K2 = phi.shape
+    N = u.shape[0]
+    if K2 != K:
+        raise ValueError(f"theta has K={K} topics but phi has {K2}")
+    if (M, V, N) != (route.M, route.V, route.N):
+        raise ValueError("theta, phi and u do not match the routed corpus")
+    devs = {t.device for t in (theta, phi, u, route.workspace)}
+    if len(devs) != 1:
+        raise ValueError("all tensors must be on one device")
+    if out is None:
+        out = torch.empty(N, dtype=torch.int32, device=u.device)
+    else:
+        _require(out, "out", torch.int32, 1)
+        if out.shape[0] != N or out.device != u.device:
+            raise ValueError("out must be int32[N] on the tensors' device")
+    with torch.cuda.device(u.device):
+        st = load().lda_draw_routed(theta.data_ptr(), phi.data_ptr(), route.workspace.data_ptr(),
+                                    route.workspace.numel(), ctypes.byref(route.info),
+                                    u.data_ptr(), out.data_ptr(), N, M, V, K,
+                                    _stream_handle(stream))
+    _check(st)
+    return out

@@ -236,9 +236,10 @@ __device__ __forceinline__ int group_value(int v, int k) {
 
 // How a wavefront's tokens map to documents, for the theta factor of the
 // tile: one document (one theta value per lane per block), two documents in
-// two contiguous runs (two values and a per-token choice), or any mix (one
-// theta load per token).
-enum ThetaMode : int { kOneDoc = 0, kTwoDocs = 1, kAnyDocs = 2 };
+// two contiguous runs (two values and a per-token choice), any mix (one
+// theta load per token), or (leaf kernel on routed tokens) a few runs of
+// documents whose theta leaves are staged in LDS once per block.
+enum ThetaMode : int { kOneDoc = 0, kTwoDocs = 1, kAnyDocs = 2, kFewDocs = 3 };
 
 // One step of an untransposed running sum (the naive kernel, the remnant of
 // the table dump): sum + theta * phi.

@@ -9,6 +9,8 @@
 // lda_draw_butterfly_philox   the butterfly draw with in-kernel uniforms.
 // lda_philox_uniforms         those uniforms, written out.
 // lda_butterfly_table the butterfly-patterned tables (Fig. 1, right).
+// lda_route_build / lda_draw_routed  tokens routed to the XCDs by word, and
+//                     the leaf kernel drawing them.
 #include <hip/hip_runtime.h>
 
 #include <stdint.h>
@@ -16,6 +18,7 @@
 #include "butterfly.hpp"
 #include "lda_draw.h"
 #include "philox.hpp"
+#include "route.hpp"
 
 // Build-time tuning of the butterfly kernel (chosen by measurement on MI355X):
 //   LDA_LDS_TABLE_MAX_BLOCKS  largest K / W whose rebuilt table goes to LDS
@@ -816,6 +819,44 @@ __device__ __forceinline__ f4 theta_leaf(rsrc_t rs, int c0, int blk, int r, uint
   return t;
 }
 
+// Theta leaves of a wavefront whose tokens form D <= kFewMax runs of documents
+// (kFewDocs): per block, each run's leaf at this lane's topics is loaded once
+// and staged in LDS (lds[d * 64 + lane]); each token then reads its run's leaf
+// from LDS instead of from memory.
+constexpr int kFewMax = 4;
+struct FewDocs {
+  f4 *lds;                 // this wavefront's kFewMax x 64 leaves
+  int D;                   // runs of documents in the wavefront, uniform
+  uint32_t row[kFewMax];   // their theta row offsets, uniform
+  int slot;                // this lane's run
+};
+
+// Loads of block `blk`'s leaves of the wavefront's runs (to be staged later).
+template <bool PAD>
+__device__ __forceinline__ void few_load(const FewDocs &fd, rsrc_t th_rs, int c0, int blk, int r,
+                                         f4 (&st)[kFewMax]) {
+#pragma unroll
+  for (int d = 0; d < kFewMax; ++d)
+    if (d < fd.D) st[d] = theta_leaf<PAD>(th_rs, c0, blk, r, fd.row[d]);
+}
+
+// Stage the loaded leaves in LDS.  The wavefront's earlier LDS reads are
+// issued before these writes and LDS executes one wavefront's operations in
+// order, so the writes may replace leaves the wavefront has read already.
+__device__ __forceinline__ void few_stage(const FewDocs &fd, const f4 (&st)[kFewMax], int lane) {
+#pragma unroll
+  for (int d = 0; d < kFewMax; ++d)
+    if (d < fd.D) fd.lds[d * kWave + lane] = st[d];
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The staged leaf of token t's run.
+__device__ __forceinline__ f4 few_leaf(const FewDocs &fd, int t, int lane) {
+  return fd.lds[__builtin_amdgcn_readlane(fd.slot, t) * kWave + lane];
+}
+
 // Sweep step for one 256-topic block: win[] holds (or awaits) the phi leaves
 // of the first C slots in pair order, twin[] (any documents) their theta
 // leaves, th[] the theta leaves of the first / last document.  With PREFETCH
@@ -824,16 +865,21 @@ __device__ __forceinline__ f4 theta_leaf(rsrc_t rs, int c0, int blk, int r, uint
 // prefix at the block's end.  c0 is the first topic of block 0 (PAD: K is not
 // a multiple of 256 and block 0 begins with 256 - K mod 256 empty topics).
 template <int MODE, bool PREFETCH, int C, int CT, bool PAD>
-__device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&win)[C],
-                                              f4 (&twin)[CT], f4 (&th)[2], f4 (&thn)[2],
-                                              int c0, int blk, int next, float *rows,
-                                              float prefix) {
+__device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const FewDocs &fd,
+                                              f4 (&win)[C], f4 (&twin)[CT], f4 (&th)[2],
+                                              f4 (&thn)[2], int c0, int blk, int next,
+                                              float *rows, float prefix) {
   static_assert(kWave % C == 0, "the window size must divide 64");
   const uint32_t vcur = leaf_bytes(c0, blk, w.r);
   const uint32_t vnext = leaf_bytes(c0, next, w.r);
   // any documents: theta comes per token, so padding leaves are zeroed per product
   const bool real = !PAD || leaf_topic(c0, blk, w.r) >= 0;
   const int kb = MODE == kTwoDocs ? launder_int(w.kb) : kWave;
+  const int lane = lane_id();
+  // kFewDocs: the next block's run leaves, loaded now and staged in LDS once
+  // this block's last reads of the staged leaves have been issued
+  f4 st[kFewMax];
+  if constexpr (MODE == kFewDocs && PREFETCH) few_load<PAD>(fd, w.th_rs, c0, next, w.r, st);
   float s[kWave / 2];
   float lo = 0.0f;
 #pragma unroll
@@ -841,7 +887,7 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&
     const int slot = pair_token(i);
     const int t = eighth_slot_token(slot);
     f4 tv;
-    if constexpr (MODE == kAnyDocs)
+    if constexpr (MODE == kAnyDocs || MODE == kFewDocs)
       tv = twin[i % C];
     else if constexpr (MODE == kTwoDocs)
       tv = t < kb ? th[0] : th[1];
@@ -860,13 +906,16 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&
     if (refill || PREFETCH) {
       const int tn = eighth_slot_token(pair_token(refill ? i + C : i + C - kWave));
       const uint32_t voff = refill ? vcur : vnext;
-      if (!refill && MODE != kAnyDocs && i + C == kWave) {
+      if (!refill && (MODE == kOneDoc || MODE == kTwoDocs) && i + C == kWave) {
         thn[0] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off0);
         if constexpr (MODE == kTwoDocs) thn[1] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off1);
       }
+      if constexpr (MODE == kFewDocs)
+        if (!refill && i + C == kWave) few_stage(fd, st, lane);
       win[i % C] = load_f32x4(w.ph_rs, voff, __builtin_amdgcn_readlane(w.ph_lane, tn));
       if constexpr (MODE == kAnyDocs)
         twin[i % C] = load_f32x4(w.th_rs, voff, __builtin_amdgcn_readlane(w.th_lane, tn));
+      if constexpr (MODE == kFewDocs) twin[i % C] = few_leaf(fd, tn, lane);
     }
     // keep the window rolling: no load is hoisted past this point (hoisting
     // them all would need 4 registers per token of the block)
@@ -888,7 +937,7 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&
     prefix += s[bitrev3(q)];
     rows[q * kWave] = prefix;
   }
-  if constexpr (PREFETCH && MODE != kAnyDocs) {
+  if constexpr (PREFETCH && (MODE == kOneDoc || MODE == kTwoDocs)) {
     th[0] = thn[0];
     if constexpr (MODE == kTwoDocs) th[1] = thn[1];
   }
@@ -897,15 +946,25 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, f4 (&
 
 // The whole sweep over NB blocks; rows[r * 64] receives the prefix at the end
 // of eighth r.  Returns the token's total.
-template <int MODE, int C, bool PAD>
-__device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, int NB, int c0,
-                                        float *rows) {
-  constexpr int CT = MODE == kAnyDocs ? C : 1;
+// A sweep8 hook that does nothing.
+struct NoHook {
+  __device__ __forceinline__ void operator()() const {}
+};
+
+template <int MODE, int C, bool PAD, class Hook = NoHook>
+__device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDocs &fd, int NB,
+                                        int c0, float *rows, Hook hook = Hook{}) {
+  constexpr int CT = (MODE == kAnyDocs || MODE == kFewDocs) ? C : 1;
   f4 win[C], twin[CT], th[2], thn[2];
   const uint32_t v0 = leaf_bytes(c0, 0, w.r);
-  if constexpr (MODE != kAnyDocs) {
+  if constexpr (MODE == kOneDoc || MODE == kTwoDocs) {
     th[0] = theta_leaf<PAD>(w.th_rs, c0, 0, w.r, w.th_off0);
     th[1] = MODE == kTwoDocs ? theta_leaf<PAD>(w.th_rs, c0, 0, w.r, w.th_off1) : th[0];
+  }
+  if constexpr (MODE == kFewDocs) {
+    f4 st[kFewMax];
+    few_load<PAD>(fd, w.th_rs, c0, 0, w.r, st);
+    few_stage(fd, st, lane_id());
   }
 #pragma unroll
   for (int i = 0; i < C; ++i) {
@@ -913,13 +972,20 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, int NB, int
     win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, t));
     if constexpr (MODE == kAnyDocs)
       twin[i] = load_f32x4(w.th_rs, v0, __builtin_amdgcn_readlane(w.th_lane, t));
+    if constexpr (MODE == kFewDocs) twin[i] = few_leaf(fd, t, lane_id());
   }
+  // hook() runs once, after the first block's step (loads it issues are in
+  // flight during the other blocks)
   float prefix = 0.0f;
-  for (int b = 0; b < NB - 1; ++b)
-    prefix = sweep8_block<MODE, true, C, CT, PAD>(w, win, twin, th, thn, c0, b, b + 1,
+  for (int b = 0; b < NB - 1; ++b) {
+    prefix = sweep8_block<MODE, true, C, CT, PAD>(w, fd, win, twin, th, thn, c0, b, b + 1,
                                                   rows + 8 * b * kWave, prefix);
-  return sweep8_block<MODE, false, C, CT, PAD>(w, win, twin, th, thn, c0, NB - 1, 0,
-                                               rows + 8 * (NB - 1) * kWave, prefix);
+    if (b == 0) hook();
+  }
+  prefix = sweep8_block<MODE, false, C, CT, PAD>(w, fd, win, twin, th, thn, c0, NB - 1, 0,
+                                                 rows + 8 * (NB - 1) * kWave, prefix);
+  if (NB == 1) hook();
+  return prefix;
 }
 
 template <int C, int WPB, int WPEU, bool PAD>
@@ -950,13 +1016,14 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
                           lane, doc, word);
   float *region = lds + wave * 8 * NB * kWave;
 
+  const FewDocs none{};
   float sum;
   if (w.mode == kOneDoc)
-    sum = sweep8<kOneDoc, C, PAD>(w, NB, c0, region + lane);
+    sum = sweep8<kOneDoc, C, PAD>(w, none, NB, c0, region + lane);
   else if (w.mode == kTwoDocs)
-    sum = sweep8<kTwoDocs, C, PAD>(w, NB, c0, region + lane);
+    sum = sweep8<kTwoDocs, C, PAD>(w, none, NB, c0, region + lane);
   else
-    sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, NB, c0, region + lane);
+    sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, none, NB, c0, region + lane);
   const float stop = sum * un;
   // Algorithm 9 over the ends of the 8 NB eighths.
   int lo = 0, hi = 8 * NB - 1;
@@ -980,6 +1047,109 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   const int j = c0 + chunk * (kWave / 2) +
                 inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
   if (store) z[n] = j;
+}
+
+// ---------------------------------------------------------------------------
+// The leaf kernel on routed tokens.  Workgroups are dispatched to the GPU's
+// eight XCDs round robin (workgroup b on XCD b mod 8), and each XCD has its
+// own L2.  Routing gives list x of the tokens -- those whose word falls in the
+// word classes assigned to XCD x -- to the workgroups b with b mod 8 = x, so
+// that each L2 caches the phi rows of one eighth of the vocabulary.  Routed
+// position i holds token perm[i] (-1: padding, drawn but not stored) with
+// word rword[i] and document rdoc[i]; list x is [lists[x], lists[x] +
+// lists[8 + x]), a multiple of 64 long, in the original token order, so that
+// the documents of a wavefront form a few runs (kFewDocs).
+constexpr int kXcds = kRouteXcds;
+
+struct RoutedTokens {
+  const int32_t *perm, *rword, *rdoc;
+  int64_t base[kXcds], len[kXcds];  // list starts and lengths
+};
+
+// LDS floats per wavefront of the routed kernel: the prefix rows, then the
+// staged theta leaves of up to kFewMax runs.
+__host__ __device__ constexpr int routed_lds_floats(int NB) {
+  return 8 * NB * kWave + kFewMax * kWave * 4;
+}
+
+template <int C, int WPB, int WPEU, bool PAD>
+__global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
+void routed_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                           RoutedTokens rt, UniformSource u, int32_t *__restrict__ z, int K,
+                           uint32_t theta_bytes, uint32_t phi_bytes) {
+  extern __shared__ float lds[];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int x = blockIdx.x % kXcds;
+  const int64_t base = rt.base[x];
+  const int64_t len = rt.len[x];
+  const int NB = (K + kBlock4 - 1) / kBlock4;
+  const int c0 = K - NB * kBlock4;
+  float *region = lds + wave * routed_lds_floats(NB);
+  FewDocs fd;
+  fd.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
+  // One tile of WPB wavefronts of its list per workgroup (the grid holds as
+  // many tiles per list as the longest list needs).
+  {
+    const int64_t first = ((int64_t)(blockIdx.x / kXcds) * WPB + wave) * kWave;
+    if (first >= len) return;
+    const int64_t i = base + first + lane;
+    const int doc = rt.rdoc[i];
+    const int word = rt.rword[i];
+    const int n = rt.perm[i];
+    Wave<kWave, false> w;
+    init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, rt.rword + base, first,
+                            kWave - 1, K, lane, doc, word);
+    // runs of documents among the wavefront's tokens
+    const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
+    const uint64_t starts = __builtin_amdgcn_ballot_w64(lane == 0 || doc != prev);
+    fd.D = __builtin_amdgcn_readfirstlane(__builtin_popcountll(starts));
+    fd.slot = __builtin_popcountll(starts & ((2ull << lane) - 1ull)) - 1;
+    uint64_t m = starts;
+#pragma unroll
+    for (int d = 0; d < kFewMax; ++d) {
+      fd.row[d] = 0;
+      if (m) {
+        const int ln = __builtin_ctzll(m);
+        m &= m - 1;
+        fd.row[d] = (uint32_t)__builtin_amdgcn_readlane(doc, ln) * w.row_bytes;
+      }
+    }
+    // The uniform's load depends on the token index's; issued before the
+    // sweep it would hold up every in-order wait for the sweep's loads, so
+    // it is issued after the first block's step.
+    float un = 0.0f;
+    const auto load_u = [&]() { un = u(n >= 0 ? n : 0); };
+    float sum;
+    if (fd.D == 1)
+      sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region + lane, load_u);
+    else if (fd.D <= kFewMax)
+      sum = sweep8<kFewDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
+    else
+      sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
+    const float stop = sum * un;
+    // Algorithm 9 over the ends of the 8 NB eighths.
+    int lo = 0, hi = 8 * NB - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (stop < region[mid * kWave + lane])
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    const int chunk = lo;
+    float low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
+    float high = region[lo * kWave + lane];
+    // Rebuild and Algorithm 10 on the chosen 32-topic chunk, as in
+    // leaf_eighths_kernel.
+    const Wave<kWave / 2, false> wh = half_wave(w, lane);
+    float h[kWave / 2];
+    load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+    butterfly_block<kWave / 2>(h, wh.r, NoStore{});
+    const int j = c0 + chunk * (kWave / 2) +
+                  inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
+    if (n >= 0) z[n] = j;
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -1387,6 +1557,28 @@ void launch_eighths(const float *theta, const float *phi, DocSource d, const int
     launch_eighths<C, WPEU, true>(theta, phi, d, wd, u, z, N, M, V, K, s);
 }
 
+// Launch of the routed kernel over lists of at most max_len positions: 16
+// tokens in flight per wavefront at 2 wavefronts per SIMD for every K (the
+// few-documents path halves the window), 4 wavefronts per workgroup while
+// three workgroups fit in LDS.
+template <bool PAD>
+void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt, UniformSource u,
+                   int32_t *z, int64_t max_len, int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  constexpr int C = LDA_EIGHTHS_WINDOW, WPEU = LDA_EIGHTHS_WAVES_PER_EU;
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const size_t per_wave = (size_t)routed_lds_floats(eighths_blocks(K)) * sizeof(float);
+  if (3 * 4 * per_wave <= 160 * 1024) {
+    const int64_t tiles = (max_len + 4 * kWave - 1) / (4 * kWave);
+    routed_eighths_kernel<C, 4, WPEU, PAD><<<(unsigned)(kXcds * tiles), 4 * kWave, 4 * per_wave, s>>>(
+        theta, phi, rt, u, z, K, tb, pb);
+  } else {
+    const int64_t tiles = (max_len + 2 * kWave - 1) / (2 * kWave);
+    routed_eighths_kernel<C, 2, WPEU, PAD><<<(unsigned)(kXcds * tiles), 2 * kWave, 2 * per_wave, s>>>(
+        theta, phi, rt, u, z, K, tb, pb);
+  }
+}
+
 // The eighths kernel takes K divisible by 4 (16-byte leaves) from
 // LDA_EIGHTHS_MIN_K topics to LDA_EIGHTHS_MAX_BLOCKS 256-topic blocks, for
 // N >= 64.  Measured on MI355X against the one-topic kernel: 15-30% faster
@@ -1511,6 +1703,48 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
     else
       launch_butterfly<32, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
   }
+}
+
+// Workspace of the routing: the routed arrays and the builder's tables, each
+// section starting on a 256-byte boundary.
+struct RouteLayout {
+  int64_t Np, nchunks;
+  size_t perm, rword, rdoc, chunk_off, counts, map, lists, bytes;
+};
+
+RouteLayout route_layout(int64_t N) {
+  RouteLayout L;
+  L.Np = N + (int64_t)kRouteXcds * kRoutePad;  // a list pads fewer than 64 positions
+  L.nchunks = (N + kRouteChunk - 1) / kRouteChunk;
+  size_t off = 0;
+  auto take = [&](size_t b) {
+    const size_t o = off;
+    off += (b + 255) & ~(size_t)255;
+    return o;
+  };
+  L.perm = take(4 * (size_t)L.Np);
+  L.rword = take(4 * (size_t)L.Np);
+  L.rdoc = take(4 * (size_t)L.Np);
+  L.chunk_off = take(4 * (size_t)kRouteXcds * (size_t)L.nchunks);
+  L.counts = take(4 * kRouteClasses);
+  L.map = take(4 * kRouteClasses);
+  L.lists = take(8 * 3 * kRouteXcds);
+  L.bytes = off;
+  return L;
+}
+
+RoutePlan route_plan(void *ws, const RouteLayout &L) {
+  char *b = static_cast<char *>(ws);
+  return RoutePlan{reinterpret_cast<int32_t *>(b + L.perm), reinterpret_cast<int32_t *>(b + L.rword),
+                   reinterpret_cast<int32_t *>(b + L.rdoc), reinterpret_cast<int32_t *>(b + L.chunk_off),
+                   reinterpret_cast<int32_t *>(b + L.counts), reinterpret_cast<int32_t *>(b + L.map),
+                   reinterpret_cast<int64_t *>(b + L.lists)};
+}
+
+// K the routed draw takes: the leaf kernel's (K divisible by 4 from
+// LDA_EIGHTHS_MIN_K to LDA_EIGHTHS_MAX_BLOCKS blocks of 256).
+bool routed_for(int32_t K) {
+  return K % kLeaf == 0 && K >= LDA_EIGHTHS_MIN_K && eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
 }
 
 }  // namespace
@@ -1675,6 +1909,92 @@ extern "C" int lda_butterfly_table(const float *theta, const float *phi,
   return finish_launch();
 }
 
+extern "C" size_t lda_route_workspace_bytes(int64_t N) {
+  if (N < 0 || N > LDA_ROUTE_MAX_N) return 0;
+  return route_layout(N).bytes;
+}
+
+extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, int64_t N,
+                               int32_t M, int32_t V, void *workspace, size_t workspace_bytes,
+                               lda_route *route, void *stream) {
+  if (!route) return LDA_ERR_NULL;
+  if (N < 0 || M <= 0 || V <= 0) return LDA_ERR_SHAPE;
+  if (N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
+  *route = lda_route{};
+  if (N == 0) return LDA_OK;
+  if (!doc_id || !word_id || !workspace) return LDA_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(doc_id) | reinterpret_cast<uintptr_t>(word_id)) & 3u ||
+      reinterpret_cast<uintptr_t>(workspace) & 7u)
+    return LDA_ERR_ALIGN;
+  const RouteLayout L = route_layout(N);
+  if (workspace_bytes < L.bytes) return LDA_ERR_WORKSPACE;
+  const RoutePlan P = route_plan(workspace, L);
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  route_fill<<<1, kRouteClasses, 0, s>>>(P.counts, kRouteClasses, 0);
+  route_hist<<<(unsigned)(L.nchunks < 256 ? L.nchunks : 256), kRouteThreads, 0, s>>>(
+      word_id, N, L.nchunks, P.counts);
+  route_map<<<1, kRouteThreads, 0, s>>>(P.counts, P.map, P.lists);
+  route_count<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, N, P.map, P.chunk_off);
+  route_scan<<<kRouteXcds, kRouteThreads, 0, s>>>(P.chunk_off, L.nchunks);
+  route_scatter<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, doc_id, N, P.map,
+                                                              P.chunk_off, P.lists, P.perm,
+                                                              P.rword, P.rdoc);
+  route_pad<<<kRouteXcds, kRouteThreads, 0, s>>>(P.lists, P.perm, P.rword, P.rdoc);
+  int st = finish_launch();
+  if (st != LDA_OK) return st;
+  // the list sizes size the draw's grid: read them back once
+  int64_t lists[3 * kRouteXcds];
+  hipError_t e = hipMemcpyAsync(lists, P.lists, sizeof(lists), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    g_last_hip = e;
+    return LDA_ERR_HIP;
+  }
+  route->N = N;
+  for (int x = 0; x < kRouteXcds; ++x) {
+    route->tokens[x] = lists[x];
+    route->start[x] = lists[kRouteXcds + x];
+    route->length[x] = lists[2 * kRouteXcds + x];
+  }
+  return LDA_OK;
+}
+
+extern "C" int lda_draw_routed(const float *theta, const float *phi, const void *workspace,
+                               size_t workspace_bytes, const lda_route *route, const float *u,
+                               int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                               void *stream) {
+  if (!route) return LDA_ERR_NULL;
+  const int st = check_args(theta, phi, workspace, workspace, u, z, N, M, V, K);
+  if (st != LDA_OK) return st;
+  if (!routed_for(K) || N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
+  if (N == 0) return LDA_OK;
+  if (reinterpret_cast<uintptr_t>(workspace) & 7u) return LDA_ERR_ALIGN;
+  const RouteLayout L = route_layout(N);
+  if (route->N != N || workspace_bytes < L.bytes) return LDA_ERR_WORKSPACE;
+  int64_t max_len = 0, total = 0;
+  for (int x = 0; x < kRouteXcds; ++x) {
+    if (route->length[x] < 0 || route->start[x] < 0 || route->length[x] % kRoutePad ||
+        route->start[x] + route->length[x] > L.Np)
+      return LDA_ERR_WORKSPACE;
+    max_len = route->length[x] > max_len ? route->length[x] : max_len;
+    total += route->tokens[x];
+  }
+  if (total != N) return LDA_ERR_WORKSPACE;
+  const RoutePlan P = route_plan(const_cast<void *>(workspace), L);
+  RoutedTokens rt{P.perm, P.rword, P.rdoc, {}, {}};
+  for (int x = 0; x < kRouteXcds; ++x) {
+    rt.base[x] = route->start[x];
+    rt.len[x] = route->length[x];
+  }
+  const UniformSource us{u, 0, 0, 0};
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (K % kBlock4 == 0)
+    launch_routed<false>(theta, phi, rt, us, z, max_len, M, V, K, s);
+  else
+    launch_routed<true>(theta, phi, rt, us, z, max_len, M, V, K, s);
+  return finish_launch();
+}
+
 extern "C" int lda_butterfly_width(int32_t K) {
   if (K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
@@ -1690,7 +2010,9 @@ extern "C" const char *lda_status_string(int status) {
       return "unsupported size (K > LDA_MAX_K, or theta or phi larger than "
              "LDA_MAX_TABLE_BYTES)";
     case LDA_ERR_HIP: return "HIP runtime error";
-    case LDA_ERR_ALIGN: return "a pointer is not 4-byte aligned";
+    case LDA_ERR_ALIGN: return "a pointer is not aligned (4 bytes; 8 for offsets and workspaces)";
+    case LDA_ERR_WORKSPACE:
+      return "routing workspace too small, or the route does not belong to these tokens";
     default: return "unknown status";
   }
 }
@@ -1699,4 +2021,4 @@ extern "C" const char *lda_last_hip_error(void) {
   return hipGetErrorString(g_last_hip);
 }
 
-extern "C" int lda_version(void) { return 200; }
+extern "C" int lda_version(void) { return 300; }

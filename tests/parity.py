@@ -44,7 +44,8 @@ def to_device(c, device="cuda"):
 def run_kernel(kernel: str, dev: dict):
     """z by ``kernel``; "docs", "doc_lanes" and "doc_lanes_cache" hand the
     documents over as offsets (the corpus's documents must be contiguous); "variant-<name>" is the
-    butterfly kernel with the named block table."""
+    butterfly kernel with the named block table; "routed" routes the tokens to
+    the XCDs (route_build) and draws them with draw_routed."""
     import torch
     import paper_1505_03851_amd as lda
     if kernel in ("docs", "doc_lanes", "doc_lanes_cache"):
@@ -57,6 +58,12 @@ def run_kernel(kernel: str, dev: dict):
         else:
             z = lda.draw_doc_lanes(*args, theta_cache=kernel == "doc_lanes_cache",
                                    validate=True)
+        torch.cuda.synchronize()
+        return z.cpu().numpy()
+    if kernel == "routed":
+        M, V = dev["theta"].shape[0], dev["phi"].shape[0]
+        route = lda.route_build(dev["doc_id"], dev["word_id"], M, V, validate=True)
+        z = lda.draw_routed(dev["theta"], dev["phi"], route, dev["u"])
         torch.cuda.synchronize()
         return z.cpu().numpy()
     if kernel.startswith("variant-"):

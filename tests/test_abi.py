@@ -192,3 +192,81 @@ def test_philox_uniforms_argument_errors(lib):
     assert f(A, 2, 2 ** 63 - 1, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
     assert f(None, 5, 0, 1, 0, None) == STATUS["LDA_ERR_NULL"]
     assert f(A + 1, 5, 0, 1, 0, None) == STATUS["LDA_ERR_ALIGN"]
+
+
+# ---------------------------------------------------------------------------
+# Routing of tokens to the XCDs: argument checks (before any HIP call) and the
+# workspace size.
+
+def test_route_workspace_bytes(lib):
+    from paper_1505_03851_amd import _lib
+    f = lib.lda_route_workspace_bytes
+    assert f(-1) == 0
+    assert f(_lib._CONSTS["LDA_ROUTE_MAX_N"] + 1) == 0
+    prev = 0
+    for N in (0, 1, 63, 64, 4095, 4096, 4097, 10 ** 6, 16777216):
+        b = f(N)
+        assert b >= 12 * (N + 512) and b >= prev and b % 256 == 0
+        assert _lib.route_layout(N)["bytes"] == b   # the binding's mirror of the layout
+        prev = b
+
+
+def test_route_build_argument_errors(lib):
+    import ctypes
+    from paper_1505_03851_amd._lib import STATUS, RouteInfo
+    r = RouteInfo()
+    ws = lib.lda_route_workspace_bytes(10)
+
+    def run(doc=A, word=A, N=10, M=3, V=5, w=A, wb=ws, route=True):
+        return lib.lda_route_build(doc, word, N, M, V, w, wb,
+                                   ctypes.byref(r) if route else None, None)
+    assert run(route=False) == STATUS["LDA_ERR_NULL"]
+    for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(V=-2)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert run(N=2 ** 31) == STATUS["LDA_ERR_UNSUPPORTED"]
+    for key in ("doc", "word", "w"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+    assert run(doc=A + 2) == STATUS["LDA_ERR_ALIGN"]
+    assert run(word=A + 1) == STATUS["LDA_ERR_ALIGN"]
+    assert run(w=A + 4) == STATUS["LDA_ERR_ALIGN"]          # the workspace holds int64
+    assert run(wb=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
+    r.N = 77
+    assert run(N=0, doc=None, word=None, w=None) == 0        # no-op, route cleared
+    assert r.N == 0 and list(r.length) == [0] * 8
+
+
+def test_draw_routed_argument_errors(lib):
+    import ctypes
+    from paper_1505_03851_amd._lib import STATUS, RouteInfo
+    N = 1000
+    ws = lib.lda_route_workspace_bytes(N)
+    r = RouteInfo()
+    r.N = N
+    for x in range(8):          # a consistent (made-up) route of N tokens
+        r.tokens[x] = N // 8
+        r.length[x] = (N // 8 + 63) // 64 * 64
+        r.start[x] = x * r.length[0]
+
+    def run(theta=A, phi=A, w=A, wb=ws, route=True, u=A, z=A, n=N, M=3, V=5, K=1024):
+        return lib.lda_draw_routed(theta, phi, w, wb, ctypes.byref(r) if route else None,
+                                   u, z, n, M, V, K, None)
+    assert run(route=False) == STATUS["LDA_ERR_NULL"]
+    for key in ("theta", "phi", "w", "u", "z"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+    for kw in (dict(n=-1), dict(M=0), dict(V=0), dict(K=0)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    # K: divisible by 4, 132 <= K <= 2048
+    for K in (64, 128, 130, 1023, 2052, 4096):
+        assert run(K=K) == STATUS["LDA_ERR_UNSUPPORTED"], K
+    assert run(w=A + 4) == STATUS["LDA_ERR_ALIGN"]
+    assert run(wb=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
+    assert run(n=N - 1) == STATUS["LDA_ERR_WORKSPACE"]        # route of other tokens
+    r.length[3] += 1                                          # not whole wavefronts
+    assert run() == STATUS["LDA_ERR_WORKSPACE"]
+    r.length[3] -= 1
+    r.tokens[0] += 1                                          # token counts do not add up
+    assert run() == STATUS["LDA_ERR_WORKSPACE"]
+    r.tokens[0] -= 1
+    r.start[7] = 10 ** 9                                      # past the workspace
+    assert run() == STATUS["LDA_ERR_WORKSPACE"]
+    assert run(n=0, theta=None, phi=None, w=None, u=None, z=None) == 0
