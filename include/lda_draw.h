@@ -242,7 +242,8 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * order and padded to a multiple of 64.  It depends on doc_id and word_id
  * only, so a sampler builds it once per corpus and reuses it every sweep.
  * It enqueues its kernels on `stream`, then synchronises `stream` once to
- * copy the list sizes into *route (the one entry point that waits).
+ * copy the list sizes into *route (the one entry point that waits; it cannot
+ * be captured into a HIP graph, while lda_draw_routed can).
  *   workspace        device memory, 8-byte aligned, at least
  *                    lda_route_workspace_bytes(N) bytes (about 12 N), owned
  *                    by the caller; it holds the routing and must stay

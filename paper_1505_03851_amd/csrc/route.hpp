@@ -224,9 +224,9 @@ __global__ __launch_bounds__(kRouteThreads) void route_scatter(
     const int x = valid ? m[route_class(w)] : -1;
     int rank = 0;
     for (int y = 0; y < kRouteXcds; ++y) {
-      const uint64_t m = __ballot(x == y);
-      if (x == y) rank = __popcll(m & below);
-      if (lane == 0) wave_count[wave][y] = __popcll(m);
+      const uint64_t mask = __ballot(x == y);
+      if (x == y) rank = __popcll(mask & below);
+      if (lane == 0) wave_count[wave][y] = __popcll(mask);
     }
     __syncthreads();
     if (valid) {

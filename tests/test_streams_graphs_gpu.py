@@ -28,18 +28,21 @@ def test_side_stream_orders_with_events():
     assert (z.cpu() == ref.cpu()).all()
 
 
-@pytest.mark.parametrize("kernel", ["butterfly", "docs", "philox"])
+@pytest.mark.parametrize("kernel", ["butterfly", "docs", "philox", "routed"])
 def test_graph_capture_and_replay(kernel):
     """Capture one draw, then replay it three times with new uniforms (or a
     new seed in the captured seed's place: the philox draw's uniforms are
     fixed by the capture, so its replays must repeat); each replay equals an
-    eager draw on the same inputs, with eager work between the replays."""
+    eager draw on the same inputs, with eager work between the replays.  The
+    routed draw's routing is built before the capture (its build waits on
+    the stream and cannot be captured)."""
     import torch
     import paper_1505_03851_amd as lda
     from paper_1505_03851_amd.inputs import doc_offsets
     c = make_random(64 * 300 + 17, 200, 3000, 200, seed=5, doc_order="ragged")
     dev = to_device(c)
     off = torch.from_numpy(doc_offsets(c.doc_id, c.M)).cuda()
+    route = lda.route_build(dev["doc_id"], dev["word_id"], c.M, c.V) if kernel == "routed" else None
     z = torch.empty(c.N, dtype=torch.int32, device="cuda")
 
     def launch(out, stream=None):
@@ -49,6 +52,9 @@ def test_graph_capture_and_replay(kernel):
         if kernel == "docs":
             return lda.draw_docs(dev["theta"], dev["phi"], off, dev["word_id"], dev["u"],
                                  out=out, stream=stream)
+        if kernel == "routed":
+            return lda.draw_routed(dev["theta"], dev["phi"], route, dev["u"], out=out,
+                                   stream=stream)
         return lda.draw_philox(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"],
                                1234, 7, out=out, stream=stream)
 
