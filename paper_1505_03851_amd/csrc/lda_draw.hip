@@ -49,11 +49,12 @@
 //   LDA_EIGHTHS_MAX_BLOCKS    largest number of 256-topic blocks for which the
 //                             leaf kernel with 32-topic prefix rows draws
 //                             (8 rows of LDS per block and wavefront; 0: never);
-//   LDA_EIGHTHS_SPLIT         largest block count drawn with the first of its
-//                             two launch shapes;
-//   LDA_EIGHTHS_WINDOW{,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{,_LARGE}
+//   LDA_EIGHTHS_SPLIT         largest block count drawn with the middle of its
+//                             three launch shapes (one block: the first shape;
+//                             more than LDA_EIGHTHS_SPLIT: the last);
+//   LDA_EIGHTHS_WINDOW{_ONE,,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{_ONE,,_LARGE}
 //                             tokens in flight per wavefront (16-byte loads)
-//                             and wavefronts per SIMD of the two shapes.
+//                             and wavefronts per SIMD of the three shapes.
 #ifndef LDA_EIGHTHS_MAX_BLOCKS
 #define LDA_EIGHTHS_MAX_BLOCKS 8
 #endif
@@ -64,7 +65,13 @@
 #define LDA_EIGHTHS_MIN_K 132
 #endif
 #ifndef LDA_EIGHTHS_SPLIT
-#define LDA_EIGHTHS_SPLIT 4
+#define LDA_EIGHTHS_SPLIT 5
+#endif
+#ifndef LDA_EIGHTHS_WINDOW_ONE
+#define LDA_EIGHTHS_WINDOW_ONE 8
+#endif
+#ifndef LDA_EIGHTHS_WAVES_PER_EU_ONE
+#define LDA_EIGHTHS_WAVES_PER_EU_ONE 3
 #endif
 #ifndef LDA_EIGHTHS_WINDOW
 #define LDA_EIGHTHS_WINDOW 16
@@ -1678,10 +1685,15 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (eighths_for(N, K)) {
-    // launch shapes measured on MI355X: 16 tokens in flight per wavefront at
-    // 2 wavefronts per SIMD up to K = 1024 (1% faster there than 8 at 3), 4
-    // at 4 above (3% faster at K = 2048 than 8 at 3; 2 in flight: 30% slower)
-    if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
+    // launch shapes measured on MI355X: one block (K <= 256): 8 tokens in
+    // flight per wavefront at 3 wavefronts per SIMD (7-10% faster than 16 at
+    // 2); two to five blocks: 16 at 2 (1-2% faster than 8 at 3 or 4 at 4);
+    // six to eight: 4 at 4 (3-5% faster than 16 at 2 or 8 at 3; 2 in flight:
+    // 30% slower)
+    if (eighths_blocks(K) == 1)
+      launch_eighths<LDA_EIGHTHS_WINDOW_ONE, LDA_EIGHTHS_WAVES_PER_EU_ONE>(
+          theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
       launch_eighths<LDA_EIGHTHS_WINDOW, LDA_EIGHTHS_WAVES_PER_EU>(theta, phi, d, word_id, u, z,
                                                                    N, M, V, K, s);
     else
