@@ -995,7 +995,7 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
   return prefix;
 }
 
-template <int C, int WPB, int WPEU, bool PAD>
+template <int C, int WPB, int WPEU, bool PAD, bool ONE = false>
 __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                          DocSource docs, const int32_t *__restrict__ word_id,
@@ -1015,8 +1015,9 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   const int word = word_id[n];
   const float un = u(n);
   // 256-topic blocks; with PAD block 0 starts at topic c0 < 0 (a remnant of
-  // K mod 256 topics behind 256 - K mod 256 empty ones, as in butterfly_kernel)
-  const int NB = (K + kBlock4 - 1) / kBlock4;
+  // K mod 256 topics behind 256 - K mod 256 empty ones, as in butterfly_kernel).
+  // ONE: K <= 256, a single block (no prefetch of a next block is compiled).
+  const int NB = ONE ? 1 : (K + kBlock4 - 1) / kBlock4;
   const int c0 = K - NB * kBlock4;
   Wave<kWave, false> w;
   init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, kWave - 1, K,
@@ -1539,7 +1540,7 @@ bool eighths_wide_groups(int32_t K) {
   return 3LL * 4 * 8 * eighths_blocks(K) * kWave * (int64_t)sizeof(float) <= 160 * 1024;
 }
 
-template <int C, int WPEU, bool PAD>
+template <int C, int WPEU, bool PAD, bool ONE>
 void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                     hipStream_t s) {
@@ -1547,21 +1548,22 @@ void launch_eighths(const float *theta, const float *phi, DocSource d, const int
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   const size_t rows = (size_t)8 * eighths_blocks(K) * kWave * sizeof(float);
   if (eighths_wide_groups(K))
-    leaf_eighths_kernel<C, 4, WPEU, PAD><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
+    leaf_eighths_kernel<C, 4, WPEU, PAD, ONE><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_eighths_kernel<C, 2, WPEU, PAD><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
+    leaf_eighths_kernel<C, 2, WPEU, PAD, ONE><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
-template <int C, int WPEU>
+// ONE: the kernel compiled for a single block (K <= 256 only).
+template <int C, int WPEU, bool ONE = false>
 void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                     hipStream_t s) {
   if (K % kBlock4 == 0)
-    launch_eighths<C, WPEU, false>(theta, phi, d, wd, u, z, N, M, V, K, s);
+    launch_eighths<C, WPEU, false, ONE>(theta, phi, d, wd, u, z, N, M, V, K, s);
   else
-    launch_eighths<C, WPEU, true>(theta, phi, d, wd, u, z, N, M, V, K, s);
+    launch_eighths<C, WPEU, true, ONE>(theta, phi, d, wd, u, z, N, M, V, K, s);
 }
 
 // Launch of the routed kernel over lists of at most max_len positions: 16
@@ -1691,7 +1693,7 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
     // six to eight: 4 at 4 (3-5% faster than 16 at 2 or 8 at 3; 2 in flight:
     // 30% slower)
     if (eighths_blocks(K) == 1)
-      launch_eighths<LDA_EIGHTHS_WINDOW_ONE, LDA_EIGHTHS_WAVES_PER_EU_ONE>(
+      launch_eighths<LDA_EIGHTHS_WINDOW_ONE, LDA_EIGHTHS_WAVES_PER_EU_ONE, true>(
           theta, phi, d, word_id, u, z, N, M, V, K, s);
     else if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
       launch_eighths<LDA_EIGHTHS_WINDOW, LDA_EIGHTHS_WAVES_PER_EU>(theta, phi, d, word_id, u, z,
