@@ -89,16 +89,25 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
  * Butterfly draw (Algorithm 7 with Algorithms 5, 8, 9 and 10, Sections 3-4).
  * A wavefront takes 64 consecutive tokens, one per lane, and reads theta and
  * phi cooperatively: each load instruction fetches consecutive topics of one
- * token (coalesced) -- W topics, one per lane, or, when K is a multiple of
- * 256, 256 topics as leaves of four per lane.  Per block the lanes combine
- * their products in a butterfly pattern (log2 W exchange stages) instead of a
- * full transposition.  A first sweep over the blocks gives every lane the full
- * prefix at the end of each block (or of each 32-topic part of it); the part
- * holding u*S is found by binary search over those (Algorithm 9), its
- * butterfly table is rebuilt on chip, and the lane reconstructs the remaining
- * partial sums from it while it searches (Algorithm 10).  W = 64 for K >= 64,
- * W = 32 below; the first K mod W topics (the remnant) form a leading block
- * padded with empty topics, which are never drawn.
+ * token, or of a few tokens (coalesced), instead of one topic of 64 tokens.
+ * The lanes combine their products in a butterfly pattern (log2 W exchange
+ * stages) instead of a full transposition, and each lane reconstructs the
+ * partial sums it needs from the butterfly table while it searches for u*S
+ * (Algorithm 10).  The kernel depends on K:
+ *  - K divisible by 4 up to 256 (N >= 64): groups of W = 8, 16, 32 or 64
+ *    lanes, each lane one leaf of 4 topics; load k brings token k's whole
+ *    row into its group; the butterfly runs over the W leaf sums, Algorithm
+ *    10 finds the token's leaf and a scan of its 4 products the topic;
+ *  - K divisible by 4 from 260 to 2048: 256-topic blocks read as leaves of 4
+ *    topics per lane; a first sweep keeps every token's prefix at the end of
+ *    each 32-topic part of each block, Algorithm 9 finds the part holding
+ *    u*S, whose butterfly table is rebuilt on chip and searched;
+ *  - otherwise: blocks of W topics, one topic per lane (W = 64 for K >= 64,
+ *    32 below), the prefix at each block end, then Algorithm 9 and the
+ *    rebuilt block (or half-block) with Algorithm 10.
+ * Where K is not a multiple of the block (or of the group's 4 W topics), the
+ * first K mod block topics (the remnant) form a leading block padded with
+ * empty topics, which are never drawn.
  */
 int lda_draw_butterfly(const float *theta, const float *phi,
                        const int32_t *doc_id, const int32_t *word_id,

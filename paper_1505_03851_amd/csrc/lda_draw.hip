@@ -49,14 +49,26 @@
 //   LDA_EIGHTHS_MAX_BLOCKS    largest number of 256-topic blocks for which the
 //                             leaf kernel with 32-topic prefix rows draws
 //                             (8 rows of LDS per block and wavefront; 0: never);
-//   LDA_EIGHTHS_SPLIT         largest block count drawn with the middle of its
-//                             three launch shapes (one block: the first shape;
-//                             more than LDA_EIGHTHS_SPLIT: the last);
-//   LDA_EIGHTHS_WINDOW{_ONE,,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{_ONE,,_LARGE}
+//   LDA_EIGHTHS_SPLIT         largest block count drawn with the first of its
+//                             two launch shapes;
+//   LDA_EIGHTHS_WINDOW{,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{,_LARGE}
 //                             tokens in flight per wavefront (16-byte loads)
-//                             and wavefronts per SIMD of the three shapes.
+//                             and wavefronts per SIMD of the two shapes.
 #ifndef LDA_EIGHTHS_MAX_BLOCKS
 #define LDA_EIGHTHS_MAX_BLOCKS 8
+#endif
+//   LDA_GROUP_MAX_K           largest K drawn by the leaf-group kernel (K
+//                             divisible by 4, at most 256; 0: never), and its
+//                             tokens in flight per wavefront and wavefronts
+//                             per SIMD.
+#ifndef LDA_GROUP_MAX_K
+#define LDA_GROUP_MAX_K 256
+#endif
+#ifndef LDA_GROUP_WINDOW
+#define LDA_GROUP_WINDOW 8
+#endif
+#ifndef LDA_GROUP_WAVES_PER_EU
+#define LDA_GROUP_WAVES_PER_EU 3
 #endif
 //   LDA_EIGHTHS_MIN_K         smallest K it takes (K divisible by 4; the first
 //                             block is padded with empty topics up to a
@@ -66,12 +78,6 @@
 #endif
 #ifndef LDA_EIGHTHS_SPLIT
 #define LDA_EIGHTHS_SPLIT 5
-#endif
-#ifndef LDA_EIGHTHS_WINDOW_ONE
-#define LDA_EIGHTHS_WINDOW_ONE 8
-#endif
-#ifndef LDA_EIGHTHS_WAVES_PER_EU_ONE
-#define LDA_EIGHTHS_WAVES_PER_EU_ONE 3
 #endif
 #ifndef LDA_EIGHTHS_WINDOW
 #define LDA_EIGHTHS_WINDOW 16
@@ -530,7 +536,8 @@ template <int W, bool LDS_TABLE>
 __device__ __forceinline__ int inblock_search(const float (&a)[W], const float *table,
                                               int r, int gbase, float stop, float &low,
                                               float &high) {
-  constexpr int LOG2W = (W == 64) ? 6 : 5;
+  static_assert(W >= 2 && W <= kWave && (W & (W - 1)) == 0, "W: a power of two up to 64");
+  constexpr int LOG2W = __builtin_ctz(W);
   int flip = 0;
 #pragma unroll
   for (int lvl = 0; lvl < LOG2W; ++lvl) {
@@ -995,7 +1002,7 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
   return prefix;
 }
 
-template <int C, int WPB, int WPEU, bool PAD, bool ONE = false>
+template <int C, int WPB, int WPEU, bool PAD>
 __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                          DocSource docs, const int32_t *__restrict__ word_id,
@@ -1015,9 +1022,8 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   const int word = word_id[n];
   const float un = u(n);
   // 256-topic blocks; with PAD block 0 starts at topic c0 < 0 (a remnant of
-  // K mod 256 topics behind 256 - K mod 256 empty ones, as in butterfly_kernel).
-  // ONE: K <= 256, a single block (no prefetch of a next block is compiled).
-  const int NB = ONE ? 1 : (K + kBlock4 - 1) / kBlock4;
+  // K mod 256 topics behind 256 - K mod 256 empty ones, as in butterfly_kernel)
+  const int NB = (K + kBlock4 - 1) / kBlock4;
   const int c0 = K - NB * kBlock4;
   Wave<kWave, false> w;
   init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, kWave - 1, K,
@@ -1158,6 +1164,113 @@ void routed_eighths_kernel(const float *__restrict__ theta, const float *__restr
                   inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
     if (n >= 0) z[n] = j;
   }
+}
+
+// ---------------------------------------------------------------------------
+// Leaf groups for small K (K divisible by 4, at most 4 G topics for a group
+// size G of 8, 16 or 32 lanes; N >= 64).  Sections 3 and 4 with a 4-topic
+// leaf in the place of a topic: a wavefront holds 64 / G groups of G tokens,
+// lane r of a group owns token r of the group and, in the tile, leaf r (topics
+// c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K topics are
+// empty) of every token of its group.  Load k brings leaf r of token k of
+// every group into lane r of that group, so each load instruction reads the
+// whole rows (16 G bytes) of 64 / G tokens.  Register a[k] is the leaf sum
+// (dot4) of token k; Algorithm 8's butterfly over the G leaves leaves the
+// table and the lane's own token's total; Algorithm 10 finds the leaf whose
+// prefix range holds u * S, and the leaf's four products, reloaded for the
+// lane's own token, give the topic by a scan from the prefix before the leaf.
+// The theta leaf comes once per lane when each group's tokens share one
+// document (GROUP_DOCS), else with every phi leaf.
+template <int G, int C, bool PAD, bool GROUP_DOCS>
+__device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
+                                           uint32_t voff, bool real, uint32_t ph_lane,
+                                           uint32_t th_lane, int gbase) {
+  static_assert(G % C == 0, "the window size must divide G");
+  const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  f4 th = zero;
+  if constexpr (GROUP_DOCS) th = real ? load_f32x4(th_rs, voff + th_lane, 0) : zero;
+  // leaf of token k of the group at row offset `row` of that token (held by
+  // the lane that owns the token): with G = 64 the row is uniform and goes in
+  // the scalar offset, else it is fetched per lane
+  const auto leaf_of = [&](rsrc_t rs, uint32_t row, int k) {
+    if constexpr (G == kWave)
+      return load_f32x4(rs, voff, (uint32_t)__builtin_amdgcn_readlane((int)row, k));
+    else
+      return load_f32x4(
+          rs, voff + (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row), 0);
+  };
+  f4 win[C], twin[GROUP_DOCS ? 1 : C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    win[k] = leaf_of(ph_rs, ph_lane, k);
+    if constexpr (!GROUP_DOCS) twin[k] = leaf_of(th_rs, th_lane, k);
+  }
+#pragma unroll
+  for (int k = 0; k < G; ++k) {
+    const f4 tv = GROUP_DOCS ? th : twin[k % C];
+    const float v = dot4(tv, win[k % C]);
+    a[k] = GROUP_DOCS || real ? v : 0.0f;
+    if (k + C < G) {
+      win[k % C] = leaf_of(ph_rs, ph_lane, k + C);
+      if constexpr (!GROUP_DOCS) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int G, int C, int WPEU, bool PAD>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(WPEU)))
+void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                       DocSource docs, const int32_t *__restrict__ word_id,
+                       UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
+                       uint32_t theta_bytes, uint32_t phi_bytes) {
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
+  if (first >= N) return;  // whole wavefront past the end
+  // Window of 64 tokens as in butterfly_kernel (N >= 64 here).
+  const int64_t t0 = first + kWave <= N ? first : N - kWave;
+  const int64_t n = t0 + lane;
+  const bool store = n >= first;
+  const int doc = docs.wave_doc(n, t0, t0 + kWave - 1);
+  const int word = word_id[n];
+  const float un = u(n);
+
+  const rsrc_t th_rs = make_rsrc(theta, theta_bytes);
+  const rsrc_t ph_rs = make_rsrc(phi, phi_bytes);
+  const uint32_t row_bytes = (uint32_t)K * 4u;
+  const uint32_t ph_lane = (uint32_t)word * row_bytes;
+  const uint32_t th_lane = (uint32_t)doc * row_bytes;
+  const int r = lane & (G - 1), gbase = lane & ~(G - 1);
+  const int c0 = K - kLeaf * G;
+  const int leaf = c0 + kLeaf * r;
+  const bool real = !PAD || leaf >= 0;
+  const uint32_t voff = (uint32_t)(real ? leaf : 0) * 4u;
+  const int gdoc = __builtin_amdgcn_ds_bpermute(gbase << 2, doc);
+  const bool group_docs = __builtin_amdgcn_ballot_w64(doc == gdoc) == ~0ull;
+
+  float a[G];
+  if (group_docs)
+    group_tile<G, C, PAD, true>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+  else
+    group_tile<G, C, PAD, false>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+  butterfly_block<G>(a, r, NoStore{});
+  const float total = a[G - 1];
+  const float stop = total * un;
+  float low = 0.0f, high = total;
+  const int q = inblock_search<G, false>(a, nullptr, r, gbase, stop, low, high);
+  // Leaf q of the lane's own token (never a padding leaf: the prefix there is
+  // zero and stop < 0 never holds), scanned from the prefix before it; with
+  // S = 0 every comparison fails and the result is K - 1.
+  const int tq = c0 + kLeaf * q;
+  const uint32_t qoff = (uint32_t)(tq > 0 ? tq : 0) * 4u;
+  const f4 tl = load_f32x4(th_rs, qoff + th_lane, 0);
+  const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
+  const float s0 = __builtin_fmaf(tl.x, pl.x, low);
+  const float s1 = __builtin_fmaf(tl.y, pl.y, s0);
+  const float s2 = __builtin_fmaf(tl.z, pl.z, s1);
+  const int i = stop < s0 ? 0 : (stop < s1 ? 1 : (stop < s2 ? 2 : 3));
+  if (store) z[n] = tq + i;
 }
 
 // ---------------------------------------------------------------------------
@@ -1540,7 +1653,7 @@ bool eighths_wide_groups(int32_t K) {
   return 3LL * 4 * 8 * eighths_blocks(K) * kWave * (int64_t)sizeof(float) <= 160 * 1024;
 }
 
-template <int C, int WPEU, bool PAD, bool ONE>
+template <int C, int WPEU, bool PAD>
 void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                     hipStream_t s) {
@@ -1548,22 +1661,45 @@ void launch_eighths(const float *theta, const float *phi, DocSource d, const int
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   const size_t rows = (size_t)8 * eighths_blocks(K) * kWave * sizeof(float);
   if (eighths_wide_groups(K))
-    leaf_eighths_kernel<C, 4, WPEU, PAD, ONE><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
+    leaf_eighths_kernel<C, 4, WPEU, PAD><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_eighths_kernel<C, 2, WPEU, PAD, ONE><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
+    leaf_eighths_kernel<C, 2, WPEU, PAD><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
-// ONE: the kernel compiled for a single block (K <= 256 only).
-template <int C, int WPEU, bool ONE = false>
+template <int C, int WPEU>
 void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                     hipStream_t s) {
   if (K % kBlock4 == 0)
-    launch_eighths<C, WPEU, false, ONE>(theta, phi, d, wd, u, z, N, M, V, K, s);
+    launch_eighths<C, WPEU, false>(theta, phi, d, wd, u, z, N, M, V, K, s);
   else
-    launch_eighths<C, WPEU, true, ONE>(theta, phi, d, wd, u, z, N, M, V, K, s);
+    launch_eighths<C, WPEU, true>(theta, phi, d, wd, u, z, N, M, V, K, s);
+}
+
+// The leaf-group kernel: K divisible by 4, up to LDA_GROUP_MAX_K (at most
+// 256) topics, N >= 64; groups of 8, 16, 32 or 64 lanes for K up to 32, 64,
+// 128, 256.  Measured on MI355X against the kernels it replaces there: 2.0x to
+// 2.6x faster than the one-topic kernel for K = 16 ... 128, 5-8% faster than
+// the eighths kernel for K = 144 ... 256.
+bool groups_for(int64_t N, int32_t K) {
+  return N >= kWave && K % kLeaf == 0 && K <= LDA_GROUP_MAX_K && K <= kLeaf * kWave;
+}
+
+template <int G>
+void launch_groups(const float *theta, const float *phi, DocSource d, const int32_t *wd,
+                   UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                   hipStream_t s) {
+  constexpr int C = LDA_GROUP_WINDOW < G ? LDA_GROUP_WINDOW : G;
+  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
+  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  if (K == kLeaf * G)
+    leaf_group_kernel<G, C, LDA_GROUP_WAVES_PER_EU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+  else
+    leaf_group_kernel<G, C, LDA_GROUP_WAVES_PER_EU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
 // Launch of the routed kernel over lists of at most max_len positions: 16
@@ -1593,7 +1729,8 @@ void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt,
 // N >= 64.  Measured on MI355X against the one-topic kernel: 15-30% faster
 // from K = 144 (K = 144 ... 240 on the paper-shaped corpus), 7% at K = 256,
 // 4% at K = 1024, 5% at K = 2048; 3-4% slower at K = 80 and 112, whose
-// padding fills most of the block.
+// padding fills most of the block.  (The dispatch gives K up to 256 to the
+// leaf-group kernel first.)
 bool eighths_for(int64_t N, int32_t K) {
   return N >= kWave && K % kLeaf == 0 && K >= LDA_EIGHTHS_MIN_K &&
          eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
@@ -1686,16 +1823,23 @@ void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
 void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
+  if (groups_for(N, K)) {
+    if (K <= kLeaf * 8)
+      launch_groups<8>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (K <= kLeaf * 16)
+      launch_groups<16>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (K <= kLeaf * 32)
+      launch_groups<32>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else
+      launch_groups<64>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    return;
+  }
   if (eighths_for(N, K)) {
-    // launch shapes measured on MI355X: one block (K <= 256): 8 tokens in
-    // flight per wavefront at 3 wavefronts per SIMD (7-10% faster than 16 at
-    // 2); two to five blocks: 16 at 2 (1-2% faster than 8 at 3 or 4 at 4);
-    // six to eight: 4 at 4 (3-5% faster than 16 at 2 or 8 at 3; 2 in flight:
-    // 30% slower)
-    if (eighths_blocks(K) == 1)
-      launch_eighths<LDA_EIGHTHS_WINDOW_ONE, LDA_EIGHTHS_WAVES_PER_EU_ONE, true>(
-          theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
+    // launch shapes measured on MI355X: up to five blocks, 16 tokens in
+    // flight per wavefront at 2 wavefronts per SIMD (1-2% faster than 8 at 3
+    // or 4 at 4); six to eight, 4 at 4 (3-5% faster than 16 at 2 or 8 at 3;
+    // 2 in flight: 30% slower)
+    if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
       launch_eighths<LDA_EIGHTHS_WINDOW, LDA_EIGHTHS_WAVES_PER_EU>(theta, phi, d, word_id, u, z,
                                                                    N, M, V, K, s);
     else

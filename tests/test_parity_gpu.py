@@ -105,6 +105,18 @@ SHAPES = [
     (64 * 9 + 3, 30, 300, 1604, "sequential"),
     (64 * 5 + 30, 3, 100, 772, "sequential"),
     (64 * 5 + 3, 20, 200, 4096, "sequential"),
+    # K divisible by 4 up to 128: the leaf-group kernel (groups of 8, 16 or
+    # 32 lanes, empty leaves in front when K is below 32, 64 or 128), with
+    # every group inside one document (long documents) or not
+    (64 * 5 + 9, 2, 40, 4, "sequential"),
+    (64 * 6 + 1, 50, 90, 12, "shuffled"),
+    (64 * 9 + 30, 4, 120, 20, "sequential"),
+    (64 * 9 + 30, 90, 120, 36, "sequential"),
+    (64 * 7 + 2, 1, 300, 48, "single"),
+    (64 * 8 + 63, 70, 300, 84, "sequential"),
+    (64 * 8 + 5, 3, 300, 96, "sequential"),
+    (64 * 12 + 11, 40, 300, 124, "ragged"),
+    (64, 3, 64, 128, "shuffled"),
     # K a multiple of 256 (the leaf kernel with 32-topic prefix rows up to 2048)
     (1, 1, 7, 256, "sequential"),
     (63, 5, 50, 512, "shuffled"),
