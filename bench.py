@@ -15,6 +15,7 @@ since the counters were collected.
 from __future__ import annotations
 
 import argparse
+import glob
 import hashlib
 import json
 import os
@@ -32,8 +33,7 @@ HEADLINE = "corpus16M-K1024"
 HEADLINE_KERNEL = "leaf_eighths_kernel"
 SECOND = "corpus1M-K256"
 COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
-KERNEL_SOURCES = [os.path.join(ROOT, "paper_1505_03851_amd", "csrc", f)
-                  for f in ("lda_draw.hip", "butterfly.hpp", "philox.hpp", "route.hpp")]
+KERNEL_SOURCES = sorted(glob.glob(os.path.join(ROOT, "paper_1505_03851_amd", "csrc", "*.[hc]*")))
 
 
 def kernel_source_hash() -> str:
@@ -187,7 +187,6 @@ def _counter_means(d: str, kernel_substr: str) -> dict:
     directory, over the dispatches whose kernel name contains
     ``kernel_substr`` (per-dispatch values are summed over instances)."""
     import csv
-    import glob
     per = {}
     for path in glob.glob(os.path.join(d, "*counter_collection.csv")):
         with open(path) as f:

@@ -208,8 +208,10 @@ __device__ __forceinline__ float load_f32(rsrc_t r, uint32_t voff, uint32_t soff
   return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0));
 }
 
-// Four consecutive floats per lane (one 16-byte buffer load).
+// Four consecutive floats per lane (one 16-byte buffer load): a leaf of
+// kLeaf topics.
 using f4 = float __attribute__((ext_vector_type(4)));
+constexpr int kLeaf = 4;
 
 __device__ __forceinline__ f4 load_f32x4(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));

@@ -1,0 +1,116 @@
+// Leaf-group kernel for K up to 256 (gfx950).
+#pragma once
+
+#include "tile.hpp"
+
+namespace lda {
+namespace {
+
+// Leaf groups for small K (K divisible by 4, at most 4 G topics for a group
+// size G of 8, 16 or 32 lanes; N >= 64).  Sections 3 and 4 with a 4-topic
+// leaf in the place of a topic: a wavefront holds 64 / G groups of G tokens,
+// lane r of a group owns token r of the group and, in the tile, leaf r (topics
+// c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K topics are
+// empty) of every token of its group.  Load k brings leaf r of token k of
+// every group into lane r of that group, so each load instruction reads the
+// whole rows (16 G bytes) of 64 / G tokens.  Register a[k] is the leaf sum
+// (dot4) of token k; Algorithm 8's butterfly over the G leaves leaves the
+// table and the lane's own token's total; Algorithm 10 finds the leaf whose
+// prefix range holds u * S, and the leaf's four products, reloaded for the
+// lane's own token, give the topic by a scan from the prefix before the leaf.
+// The theta leaf comes once per lane when each group's tokens share one
+// document (GROUP_DOCS), else with every phi leaf.
+template <int G, int C, bool PAD, bool GROUP_DOCS>
+__device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
+                                           uint32_t voff, bool real, uint32_t ph_lane,
+                                           uint32_t th_lane, int gbase) {
+  static_assert(G % C == 0, "the window size must divide G");
+  const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
+  f4 th = zero;
+  if constexpr (GROUP_DOCS) th = real ? load_f32x4(th_rs, voff + th_lane, 0) : zero;
+  // leaf of token k of the group at row offset `row` of that token (held by
+  // the lane that owns the token): with G = 64 the row is uniform and goes in
+  // the scalar offset, else it is fetched per lane
+  const auto leaf_of = [&](rsrc_t rs, uint32_t row, int k) {
+    if constexpr (G == kWave)
+      return load_f32x4(rs, voff, (uint32_t)__builtin_amdgcn_readlane((int)row, k));
+    else
+      return load_f32x4(
+          rs, voff + (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row), 0);
+  };
+  f4 win[C], twin[GROUP_DOCS ? 1 : C];
+#pragma unroll
+  for (int k = 0; k < C; ++k) {
+    win[k] = leaf_of(ph_rs, ph_lane, k);
+    if constexpr (!GROUP_DOCS) twin[k] = leaf_of(th_rs, th_lane, k);
+  }
+#pragma unroll
+  for (int k = 0; k < G; ++k) {
+    const f4 tv = GROUP_DOCS ? th : twin[k % C];
+    const float v = dot4(tv, win[k % C]);
+    a[k] = GROUP_DOCS || real ? v : 0.0f;
+    if (k + C < G) {
+      win[k % C] = leaf_of(ph_rs, ph_lane, k + C);
+      if constexpr (!GROUP_DOCS) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+template <int G, int C, int WPEU, bool PAD>
+__global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(WPEU)))
+void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                       DocSource docs, const int32_t *__restrict__ word_id,
+                       UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
+                       uint32_t theta_bytes, uint32_t phi_bytes) {
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
+  if (first >= N) return;  // whole wavefront past the end
+  // Window of 64 tokens as in butterfly_kernel (N >= 64 here).
+  const int64_t t0 = first + kWave <= N ? first : N - kWave;
+  const int64_t n = t0 + lane;
+  const bool store = n >= first;
+  const int doc = docs.wave_doc(n, t0, t0 + kWave - 1);
+  const int word = word_id[n];
+  const float un = u(n);
+
+  const rsrc_t th_rs = make_rsrc(theta, theta_bytes);
+  const rsrc_t ph_rs = make_rsrc(phi, phi_bytes);
+  const uint32_t row_bytes = (uint32_t)K * 4u;
+  const uint32_t ph_lane = (uint32_t)word * row_bytes;
+  const uint32_t th_lane = (uint32_t)doc * row_bytes;
+  const int r = lane & (G - 1), gbase = lane & ~(G - 1);
+  const int c0 = K - kLeaf * G;
+  const int leaf = c0 + kLeaf * r;
+  const bool real = !PAD || leaf >= 0;
+  const uint32_t voff = (uint32_t)(real ? leaf : 0) * 4u;
+  const int gdoc = __builtin_amdgcn_ds_bpermute(gbase << 2, doc);
+  const bool group_docs = __builtin_amdgcn_ballot_w64(doc == gdoc) == ~0ull;
+
+  float a[G];
+  if (group_docs)
+    group_tile<G, C, PAD, true>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+  else
+    group_tile<G, C, PAD, false>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+  butterfly_block<G>(a, r, NoStore{});
+  const float total = a[G - 1];
+  const float stop = total * un;
+  float low = 0.0f, high = total;
+  const int q = inblock_search<G, false>(a, nullptr, r, gbase, stop, low, high);
+  // Leaf q of the lane's own token (never a padding leaf: the prefix there is
+  // zero and stop < 0 never holds), scanned from the prefix before it; with
+  // S = 0 every comparison fails and the result is K - 1.
+  const int tq = c0 + kLeaf * q;
+  const uint32_t qoff = (uint32_t)(tq > 0 ? tq : 0) * 4u;
+  const f4 tl = load_f32x4(th_rs, qoff + th_lane, 0);
+  const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
+  const float s0 = __builtin_fmaf(tl.x, pl.x, low);
+  const float s1 = __builtin_fmaf(tl.y, pl.y, s0);
+  const float s2 = __builtin_fmaf(tl.z, pl.z, s1);
+  const int i = stop < s0 ? 0 : (stop < s1 ? 1 : (stop < s2 ? 2 : 3));
+  if (store) z[n] = tq + i;
+}
+
+}  // namespace
+}  // namespace lda

@@ -1,0 +1,113 @@
+// Leaf kernel on tokens routed to the XCDs (gfx950).
+#pragma once
+
+#include "leaf_eighths.hpp"
+#include "route.hpp"
+
+namespace lda {
+namespace {
+
+// The leaf kernel on routed tokens.  Workgroups are dispatched to the GPU's
+// eight XCDs round robin (workgroup b on XCD b mod 8), and each XCD has its
+// own L2.  Routing gives list x of the tokens -- those whose word falls in the
+// word classes assigned to XCD x -- to the workgroups b with b mod 8 = x, so
+// that each L2 caches the phi rows of one eighth of the vocabulary.  Routed
+// position i holds token perm[i] (-1: padding, drawn but not stored) with
+// word rword[i] and document rdoc[i]; list x is [lists[x], lists[x] +
+// lists[8 + x]), a multiple of 64 long, in the original token order, so that
+// the documents of a wavefront form a few runs (kFewDocs).
+constexpr int kXcds = kRouteXcds;
+
+struct RoutedTokens {
+  const int32_t *perm, *rword, *rdoc;
+  int64_t base[kXcds], len[kXcds];  // list starts and lengths
+};
+
+// LDS floats per wavefront of the routed kernel: the prefix rows, then the
+// staged theta leaves of up to kFewMax runs.
+__host__ __device__ constexpr int routed_lds_floats(int NB) {
+  return 8 * NB * kWave + kFewMax * kWave * 4;
+}
+
+template <int C, int WPB, int WPEU, bool PAD>
+__global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
+void routed_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
+                           RoutedTokens rt, UniformSource u, int32_t *__restrict__ z, int K,
+                           uint32_t theta_bytes, uint32_t phi_bytes) {
+  extern __shared__ float lds[];
+  const int lane = lane_id();
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
+  const int x = blockIdx.x % kXcds;
+  const int64_t base = rt.base[x];
+  const int64_t len = rt.len[x];
+  const int NB = (K + kBlock4 - 1) / kBlock4;
+  const int c0 = K - NB * kBlock4;
+  float *region = lds + wave * routed_lds_floats(NB);
+  FewDocs fd;
+  fd.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
+  // One tile of WPB wavefronts of its list per workgroup (the grid holds as
+  // many tiles per list as the longest list needs).
+  {
+    const int64_t first = ((int64_t)(blockIdx.x / kXcds) * WPB + wave) * kWave;
+    if (first >= len) return;
+    const int64_t i = base + first + lane;
+    const int doc = rt.rdoc[i];
+    const int word = rt.rword[i];
+    const int n = rt.perm[i];
+    Wave<kWave, false> w;
+    init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, rt.rword + base, first,
+                            kWave - 1, K, lane, doc, word);
+    // runs of documents among the wavefront's tokens
+    const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
+    const uint64_t starts = __builtin_amdgcn_ballot_w64(lane == 0 || doc != prev);
+    fd.D = __builtin_amdgcn_readfirstlane(__builtin_popcountll(starts));
+    fd.slot = __builtin_popcountll(starts & ((2ull << lane) - 1ull)) - 1;
+    uint64_t m = starts;
+#pragma unroll
+    for (int d = 0; d < kFewMax; ++d) {
+      fd.row[d] = 0;
+      if (m) {
+        const int ln = __builtin_ctzll(m);
+        m &= m - 1;
+        fd.row[d] = (uint32_t)__builtin_amdgcn_readlane(doc, ln) * w.row_bytes;
+      }
+    }
+    // The uniform's load depends on the token index's; issued before the
+    // sweep it would hold up every in-order wait for the sweep's loads, so
+    // it is issued after the first block's step.
+    float un = 0.0f;
+    const auto load_u = [&]() { un = u(n >= 0 ? n : 0); };
+    float sum;
+    if (fd.D == 1)
+      sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region + lane, load_u);
+    else if (fd.D <= kFewMax)
+      sum = sweep8<kFewDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
+    else
+      sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
+    const float stop = sum * un;
+    // Algorithm 9 over the ends of the 8 NB eighths.
+    int lo = 0, hi = 8 * NB - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi) >> 1;
+      if (stop < region[mid * kWave + lane])
+        hi = mid;
+      else
+        lo = mid + 1;
+    }
+    const int chunk = lo;
+    float low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
+    float high = region[lo * kWave + lane];
+    // Rebuild and Algorithm 10 on the chosen 32-topic chunk, as in
+    // leaf_eighths_kernel.
+    const Wave<kWave / 2, false> wh = half_wave(w, lane);
+    float h[kWave / 2];
+    load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+    butterfly_block<kWave / 2>(h, wh.r, NoStore{});
+    const int j = c0 + chunk * (kWave / 2) +
+                  inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
+    if (n >= 0) z[n] = j;
+  }
+}
+
+}  // namespace
+}  // namespace lda

@@ -1,0 +1,73 @@
+// Build-time tuning of the draw kernels (chosen by measurement on MI355X).
+#pragma once
+
+//   LDA_LDS_TABLE_MAX_BLOCKS  largest K / W whose rebuilt table goes to LDS
+//                             (see lds_table_for);
+//   LDA_WAVES_PER_EU          wavefronts per SIMD the register budget targets;
+//   LDA_WAVES_PER_BLOCK       wavefronts per workgroup.
+#ifndef LDA_LDS_TABLE_MAX_BLOCKS
+#define LDA_LDS_TABLE_MAX_BLOCKS 0
+#endif
+#ifndef LDA_WAVES_PER_EU
+#define LDA_WAVES_PER_EU 3
+#endif
+#ifndef LDA_WAVES_PER_BLOCK
+#define LDA_WAVES_PER_BLOCK 2
+#endif
+//   LDA_DOC_LANES_TARGET_WAVES wavefronts the document-per-lane driver aims
+//                             for by splitting each group's master loop.
+#ifndef LDA_DOC_LANES_TARGET_WAVES
+#define LDA_DOC_LANES_TARGET_WAVES 16384
+#endif
+//   LDA_HALF_MAX_BLOCKS       largest K / 64 for which the W = 64 kernel
+//                             rebuilds only the chosen half-block (its 2 K/64
+//                             LDS rows per wavefront keep 12 wavefronts per CU
+//                             up to 26 blocks, 10 at 32 blocks).
+#ifndef LDA_HALF_MAX_BLOCKS
+#define LDA_HALF_MAX_BLOCKS 32
+#endif
+//   LDA_EIGHTHS_MAX_BLOCKS    largest number of 256-topic blocks for which the
+//                             leaf kernel with 32-topic prefix rows draws
+//                             (8 rows of LDS per block and wavefront; 0: never);
+//   LDA_EIGHTHS_SPLIT         largest block count drawn with the first of its
+//                             two launch shapes;
+//   LDA_EIGHTHS_WINDOW{,_LARGE}, LDA_EIGHTHS_WAVES_PER_EU{,_LARGE}
+//                             tokens in flight per wavefront (16-byte loads)
+//                             and wavefronts per SIMD of the two shapes.
+#ifndef LDA_EIGHTHS_MAX_BLOCKS
+#define LDA_EIGHTHS_MAX_BLOCKS 8
+#endif
+//   LDA_GROUP_MAX_K           largest K drawn by the leaf-group kernel (K
+//                             divisible by 4, at most 256; 0: never), and its
+//                             tokens in flight per wavefront and wavefronts
+//                             per SIMD.
+#ifndef LDA_GROUP_MAX_K
+#define LDA_GROUP_MAX_K 256
+#endif
+#ifndef LDA_GROUP_WINDOW
+#define LDA_GROUP_WINDOW 8
+#endif
+#ifndef LDA_GROUP_WAVES_PER_EU
+#define LDA_GROUP_WAVES_PER_EU 3
+#endif
+//   LDA_EIGHTHS_MIN_K         smallest K it takes (K divisible by 4; the first
+//                             block is padded with empty topics up to a
+//                             multiple of 256).
+#ifndef LDA_EIGHTHS_MIN_K
+#define LDA_EIGHTHS_MIN_K 132
+#endif
+#ifndef LDA_EIGHTHS_SPLIT
+#define LDA_EIGHTHS_SPLIT 5
+#endif
+#ifndef LDA_EIGHTHS_WINDOW
+#define LDA_EIGHTHS_WINDOW 16
+#endif
+#ifndef LDA_EIGHTHS_WAVES_PER_EU
+#define LDA_EIGHTHS_WAVES_PER_EU 2
+#endif
+#ifndef LDA_EIGHTHS_WINDOW_LARGE
+#define LDA_EIGHTHS_WINDOW_LARGE 4
+#endif
+#ifndef LDA_EIGHTHS_WAVES_PER_EU_LARGE
+#define LDA_EIGHTHS_WAVES_PER_EU_LARGE 4
+#endif
