@@ -169,6 +169,28 @@ def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None)
     }
 
 
+def device_copy_GBps(steps: int = 10) -> float:
+    """Bytes read plus bytes written per second by a plain 1 GiB device copy
+    (torch's copy kernel, HIP events): the practical HBM ceiling on the box."""
+    import torch
+    n = 1 << 28
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record()
+        dst.copy_(src)
+        b.record()
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[steps // 2]
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * 4 * n / (ms * 1e-3) / 1e9
+
+
 def traffic_from_counters():
     """HBM bytes per launch from the committed counter summary, if it was
     taken on the current kernel source."""
@@ -539,6 +561,7 @@ def main() -> int:
     wall = head["wall_s"]
     value = c.N * args.steps / wall
     traffic = traffic_from_counters()
+    copy_GBps = device_copy_GBps()
     out = {
         "metric": METRIC,
         "value": value,
@@ -568,6 +591,11 @@ def main() -> int:
                              if traffic else None),
         "hbm_traffic_frac": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9 /
                              PEAK_HBM_GBPS if traffic else None),
+        # a plain 1 GiB device copy on the same GPU (bytes read + written per
+        # second), and the counted L2 traffic of the draw against it
+        "device_copy_GBps": copy_GBps,
+        "hbm_traffic_frac_of_copy": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9 /
+                                     copy_GBps if traffic else None),
         "cpu_baseline": cpu_baseline(c, z_head, args.cpu_sample),
         "results": results,
         "kernel_source_sha1": kernel_source_hash(),

@@ -160,9 +160,9 @@ void launch_groups(const float *theta, const float *phi, DocSource d, const int3
 }
 
 // Launch of the routed kernel over lists of at most max_len positions: 16
-// tokens in flight per wavefront at 2 wavefronts per SIMD for every K (the
-// few-documents path halves the window), 4 wavefronts per workgroup while
-// three workgroups fit in LDS.
+// tokens in flight per wavefront at 2 wavefronts per SIMD for every K (in the
+// few-documents path too, with theta leaves read 4 tokens ahead from LDS), 4
+// wavefronts per workgroup while three workgroups fit in LDS.
 template <bool PAD>
 void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt, UniformSource u,
                    int32_t *z, int64_t max_len, int32_t M, int32_t V, int32_t K, hipStream_t s) {

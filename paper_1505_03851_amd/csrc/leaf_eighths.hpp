@@ -122,8 +122,9 @@ __device__ __forceinline__ f4 few_leaf(const FewDocs &fd, int t, int lane) {
 }
 
 // Sweep step for one 256-topic block: win[] holds (or awaits) the phi leaves
-// of the first C slots in pair order, twin[] (any documents) their theta
-// leaves, th[] the theta leaves of the first / last document.  With PREFETCH
+// of the first C slots in pair order, twin[] their theta leaves (any
+// documents; with a few documents, those of the first CT slots, read from
+// LDS), th[] the theta leaves of the first / last document.  With PREFETCH
 // the windows and thn[] are refilled with block `next` as the block drains.
 // rows[q * 64] receives the running prefix at the end of eighth q; returns the
 // prefix at the block's end.  c0 is the first topic of block 0 (PAD: K is not
@@ -141,7 +142,8 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
   const int kb = MODE == kTwoDocs ? launder_int(w.kb) : kWave;
   const int lane = lane_id();
   // kFewDocs: the next block's run leaves, loaded now and staged in LDS once
-  // this block's last reads of the staged leaves have been issued
+  // this block's last reads of the staged leaves have been issued (CT slots
+  // before the block's end)
   f4 st[kFewMax];
   if constexpr (MODE == kFewDocs && PREFETCH) few_load<PAD>(fd, w.th_rs, c0, next, w.r, st);
   float s[kWave / 2];
@@ -151,8 +153,10 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
     const int slot = pair_token(i);
     const int t = eighth_slot_token(slot);
     f4 tv;
-    if constexpr (MODE == kAnyDocs || MODE == kFewDocs)
+    if constexpr (MODE == kAnyDocs)
       tv = twin[i % C];
+    else if constexpr (MODE == kFewDocs)
+      tv = twin[i % CT];
     else if constexpr (MODE == kTwoDocs)
       tv = t < kb ? th[0] : th[1];
     else
@@ -174,12 +178,17 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
         thn[0] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off0);
         if constexpr (MODE == kTwoDocs) thn[1] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off1);
       }
-      if constexpr (MODE == kFewDocs)
-        if (!refill && i + C == kWave) few_stage(fd, st, lane);
       win[i % C] = load_f32x4(w.ph_rs, voff, __builtin_amdgcn_readlane(w.ph_lane, tn));
       if constexpr (MODE == kAnyDocs)
         twin[i % C] = load_f32x4(w.th_rs, voff, __builtin_amdgcn_readlane(w.th_lane, tn));
-      if constexpr (MODE == kFewDocs) twin[i % C] = few_leaf(fd, tn, lane);
+    }
+    if constexpr (MODE == kFewDocs) {
+      const bool trefill = i + CT < kWave;
+      if (trefill || PREFETCH) {
+        if (!trefill && i + CT == kWave) few_stage(fd, st, lane);
+        const int tt = eighth_slot_token(pair_token(trefill ? i + CT : i + CT - kWave));
+        twin[i % CT] = few_leaf(fd, tt, lane);
+      }
     }
     // keep the window rolling: no load is hoisted past this point (hoisting
     // them all would need 4 registers per token of the block)
@@ -215,10 +224,11 @@ struct NoHook {
   __device__ __forceinline__ void operator()() const {}
 };
 
-template <int MODE, int C, bool PAD, class Hook = NoHook>
+template <int MODE, int C, bool PAD, int CF = C, class Hook = NoHook>
 __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDocs &fd, int NB,
                                         int c0, float *rows, Hook hook = Hook{}) {
-  constexpr int CT = (MODE == kAnyDocs || MODE == kFewDocs) ? C : 1;
+  static_assert(CF <= C && kWave % CF == 0, "the theta window divides 64 and is at most C");
+  constexpr int CT = MODE == kAnyDocs ? C : (MODE == kFewDocs ? CF : 1);
   f4 win[C], twin[CT], th[2], thn[2];
   const uint32_t v0 = leaf_bytes(c0, 0, w.r);
   if constexpr (MODE == kOneDoc || MODE == kTwoDocs) {
@@ -236,7 +246,8 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
     win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, t));
     if constexpr (MODE == kAnyDocs)
       twin[i] = load_f32x4(w.th_rs, v0, __builtin_amdgcn_readlane(w.th_lane, t));
-    if constexpr (MODE == kFewDocs) twin[i] = few_leaf(fd, t, lane_id());
+    if constexpr (MODE == kFewDocs)
+      if (i < CT) twin[i % CT] = few_leaf(fd, t, lane_id());
   }
   // hook() runs once, after the first block's step (loads it issues are in
   // flight during the other blocks)

@@ -81,7 +81,8 @@ void routed_eighths_kernel(const float *__restrict__ theta, const float *__restr
     if (fd.D == 1)
       sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region + lane, load_u);
     else if (fd.D <= kFewMax)
-      sum = sweep8<kFewDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
+      sum = sweep8<kFewDocs, LDA_ROUTED_FEW_WINDOW, PAD, LDA_ROUTED_FEW_THETA>(w, fd, NB, c0,
+                                                                             region + lane, load_u);
     else
       sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
     const float stop = sum * un;

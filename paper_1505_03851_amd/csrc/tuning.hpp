@@ -71,3 +71,13 @@
 #ifndef LDA_EIGHTHS_WAVES_PER_EU_LARGE
 #define LDA_EIGHTHS_WAVES_PER_EU_LARGE 4
 #endif
+//   LDA_ROUTED_FEW_WINDOW, LDA_ROUTED_FEW_THETA  tokens in flight per
+//                             wavefront (phi loads) and theta leaves read
+//                             ahead from LDS when a routed wavefront's tokens
+//                             form a few runs of documents.
+#ifndef LDA_ROUTED_FEW_WINDOW
+#define LDA_ROUTED_FEW_WINDOW 16
+#endif
+#ifndef LDA_ROUTED_FEW_THETA
+#define LDA_ROUTED_FEW_THETA 4
+#endif
