@@ -62,13 +62,19 @@ extern "C" {
 #define LDA_OK 0
 #define LDA_ERR_NULL (-1)        /* a required pointer is NULL while N > 0   */
 #define LDA_ERR_SHAPE (-2)       /* N < 0, M <= 0, V <= 0 or K <= 0          */
-#define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K, or a table too large      */
+#define LDA_ERR_UNSUPPORTED (-3) /* K > LDA_MAX_K, N > LDA_MAX_N, or a table
+                                    too large                                */
 #define LDA_ERR_HIP (-4)         /* the HIP runtime reported an error        */
 #define LDA_ERR_ALIGN (-5)       /* a pointer is not 4-byte aligned          */
 #define LDA_ERR_WORKSPACE (-6)   /* routing workspace too small or mismatched */
 
 /* Largest number of topics the kernels accept. */
 #define LDA_MAX_K 4096
+
+/* Largest number of tokens: a launch holds about one work-item per token, and
+ * a dispatch counts its work-items in 32 bits (2^32 - 2^16).  Token indices
+ * are 64-bit throughout.  Larger N is rejected with LDA_ERR_UNSUPPORTED. */
+#define LDA_MAX_N 4294901760LL
 
 /* Largest size in bytes of theta (4*M*K) or phi (4*V*K): the butterfly
  * kernel addresses both through buffer resources with 31-bit byte offsets.

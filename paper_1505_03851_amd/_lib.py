@@ -39,6 +39,7 @@ _CONSTS = _header_constants()
 # status codes (LDA_OK and LDA_ERR_*) and size limits from the header
 STATUS = {k: v for k, v in _CONSTS.items() if k == "LDA_OK" or k.startswith("LDA_ERR_")}
 MAX_K = _CONSTS["LDA_MAX_K"]
+MAX_N = _CONSTS["LDA_MAX_N"]
 MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
 DOC_LANES_MAX_CACHE_BYTES = _CONSTS["LDA_DOC_LANES_MAX_CACHE_BYTES"]
 # table variants of lda_draw_butterfly_variant, by name

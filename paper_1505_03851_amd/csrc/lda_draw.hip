@@ -46,7 +46,7 @@ int check_args(const void *theta, const void *phi, const void *doc_id,
                const void *word_id, const void *u, const void *z, int64_t N,
                int32_t M, int32_t V, int32_t K) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
-  if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
+  if (K > LDA_MAX_K || N > LDA_MAX_N) return LDA_ERR_UNSUPPORTED;
   // theta and phi are addressed with 31-bit byte offsets
   if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES ||
       (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)

@@ -94,6 +94,11 @@ def test_shape_errors(lib, fn):
         assert call(lib, fn, **kw) == STATUS["LDA_ERR_SHAPE"], kw
     from paper_1505_03851_amd._lib import MAX_K, MAX_TABLE_BYTES
     assert call(lib, fn, K=MAX_K + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    # token counts past what one dispatch can hold
+    from paper_1505_03851_amd._lib import MAX_N
+    assert MAX_N >= 2 ** 32 - 2 ** 16
+    assert call(lib, fn, N=MAX_N + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert call(lib, fn, N=2 ** 40) == STATUS["LDA_ERR_UNSUPPORTED"]
     # tables past the byte limit are rejected before any HIP call
     big = MAX_TABLE_BYTES // (4 * 1024) + 1
     assert call(lib, fn, K=1024, V=big) == STATUS["LDA_ERR_UNSUPPORTED"]
