@@ -83,7 +83,8 @@ __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__res
 // out one after another, each padded to a multiple of 64 positions.
 __global__ __launch_bounds__(kRouteThreads) void route_map(const int32_t *__restrict__ counts,
                                                            int32_t *map, int64_t *lists) {
-  __shared__ int32_t cnt[kRouteClasses], order[kRouteClasses], xcd[kRouteClasses];
+  __shared__ int32_t cnt[kRouteClasses], order[kRouteClasses], sorted[kRouteClasses],
+      xcd[kRouteClasses];
   const int t = threadIdx.x;
   const int32_t c = counts[t];
   cnt[t] = c;
@@ -94,14 +95,19 @@ __global__ __launch_bounds__(kRouteThreads) void route_map(const int32_t *__rest
     rank += (cv > c) || (cv == c && v < t);
   }
   order[rank] = t;
+  sorted[rank] = c;
   __syncthreads();
   if (t == 0) {
-    // (fully unrolled, so that the loads stay in registers)
-    int64_t load[kRouteXcds] = {};
+    // The greedy pass: each step reads its class and count straight from LDS
+    // (no dependence on the earlier steps, so the reads run ahead), and the
+    // list loads stay in registers (at most N < 2^31 tokens).
+    int32_t load[kRouteXcds] = {};
+#pragma unroll 4
     for (int r = 0; r < kRouteClasses; ++r) {
       const int cls = order[r];
+      const int32_t cc = sorted[r];
       int best = 0;
-      int64_t least = load[0];
+      int32_t least = load[0];
 #pragma unroll
       for (int x = 1; x < kRouteXcds; ++x)
         if (load[x] < least) {
@@ -109,13 +115,12 @@ __global__ __launch_bounds__(kRouteThreads) void route_map(const int32_t *__rest
           best = x;
         }
       xcd[cls] = best;
-      const int32_t cc = cnt[cls];
 #pragma unroll
       for (int x = 0; x < kRouteXcds; ++x) load[x] += x == best ? cc : 0;
     }
     int64_t start = 0;
     for (int x = 0; x < kRouteXcds; ++x) {
-      const int64_t len = (load[x] + kRoutePad - 1) / kRoutePad * kRoutePad;
+      const int64_t len = ((int64_t)load[x] + kRoutePad - 1) / kRoutePad * kRoutePad;
       lists[x] = load[x];                   // tokens
       lists[kRouteXcds + x] = start;        // start
       lists[2 * kRouteXcds + x] = len;      // padded length
