@@ -74,7 +74,7 @@ def upload(c):
 # kernels bench.py can time: name -> entry point of the binding
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
            "variant-register", "variant-lds", "variant-lds_alt", "philox", "routed",
-           "routed+build")
+           "routed+build", "routed-philox")
 PHILOX_SEED = 0x5EED20150513
 
 
@@ -90,6 +90,12 @@ def launcher(kernel: str, dev):
             dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
         route = dev["route"]
         return lambda out, stream: lda.draw_routed(th, ph, route, u, out=out, stream=stream)
+    if kernel == "routed-philox":
+        if "route" not in dev:
+            dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
+        route = dev["route"]
+        return lambda out, stream: lda.draw_routed_philox(th, ph, route, PHILOX_SEED, 0,
+                                                          out=out, stream=stream)
     if kernel == "routed+build":
         if "route" not in dev:
             dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
@@ -384,11 +390,12 @@ def all_configs(args) -> int:
             rec[f"butterfly_cold_{key}"] = r[key]
         if routable(c.K):
             z_bf = measure(name, c, dev, "butterfly", 1, 0)["z"]
-            for kernel in ("routed", "routed+build"):
+            for kernel in ("routed", "routed+build", "routed-philox"):
                 r = measure(name, c, dev, kernel, args.steps, args.warmup)
                 for key in ("ms_per_launch", "ms_per_launch_median", "draws_per_s", "alg_GBps"):
                     rec[f"{kernel}_{key}"] = r[key]
-                rec[f"{kernel}_differs_from_butterfly"] = int((r["z"] != z_bf).sum())
+                if kernel != "routed-philox":   # (other uniforms: z is not comparable)
+                    rec[f"{kernel}_differs_from_butterfly"] = int((r["z"] != z_bf).sum())
         print(json.dumps(rec), flush=True)
         del dev
         torch.cuda.empty_cache()

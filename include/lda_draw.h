@@ -272,6 +272,11 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * lda_draw_butterfly; K must be divisible by 4 with 132 <= K <= 2048, else
  * LDA_ERR_UNSUPPORTED; `route` and `workspace` must come from one
  * lda_route_build over these N tokens, else LDA_ERR_WORKSPACE.
+ *
+ * lda_draw_routed_philox: lda_draw_routed with the uniforms generated in the
+ * kernel exactly as lda_draw_butterfly_philox does (Philox4x32-10 of the
+ * original token index, sweep and seed), so its z equals that entry point's
+ * z except inside the rounding band.
  */
 #define LDA_ROUTE_MAX_N 2147483135LL
 typedef struct lda_route {
@@ -288,6 +293,10 @@ int lda_route_build(const int32_t *doc_id, const int32_t *word_id, int64_t N, in
 int lda_draw_routed(const float *theta, const float *phi, const void *workspace,
                     size_t workspace_bytes, const lda_route *route, const float *u,
                     int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K, void *stream);
+int lda_draw_routed_philox(const float *theta, const float *phi, const void *workspace,
+                           size_t workspace_bytes, const lda_route *route, int32_t *z,
+                           int64_t N, int32_t M, int32_t V, int32_t K, uint64_t seed,
+                           uint32_t sweep, void *stream);
 
 /* The W (butterfly width) the library uses for K, or LDA_ERR_UNSUPPORTED /
  * LDA_ERR_SHAPE for a K it rejects. */

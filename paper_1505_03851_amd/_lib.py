@@ -97,6 +97,10 @@ def load() -> ctypes.CDLL:
     lib.lda_draw_routed.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(RouteInfo), P, P,
                                     I64, I32, I32, I32, P]
     lib.lda_draw_routed.restype = ctypes.c_int
+    lib.lda_draw_routed_philox.argtypes = [P, P, P, ctypes.c_size_t, ctypes.POINTER(RouteInfo),
+                                           P, I64, I32, I32, I32, ctypes.c_uint64,
+                                           ctypes.c_uint32, P]
+    lib.lda_draw_routed_philox.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -434,33 +438,53 @@ def route_build(doc_id, word_id, M: int, V: int, workspace=None, stream=None,
     return Route(workspace, info, int(M), int(V))
 
 
-def draw_routed(theta, phi, route: Route, u, out=None, stream=None) -> torch.Tensor:
-    """z[N] (int32, indexed by the original token) by the leaf kernel over the
-    routed tokens; u float32 [N] indexed by the original token.  K must be
-    divisible by 4 with 132 <= K <= 2048."""
+def _routed_args(theta, phi, route: "Route", N: int, device, out):
     _require(theta, "theta", torch.float32, 2)
     _require(phi, "phi", torch.float32, 2)
-    _require(u, "u", torch.float32, 1)
     M, K = theta.shape
     V, K2 = phi.shape
-    N = u.shape[0]
     if K2 != K:
         raise ValueError(f"theta has K={K} topics but phi has {K2}")
     if (M, V, N) != (route.M, route.V, route.N):
         raise ValueError("theta, phi and u do not match the routed corpus")
-    devs = {t.device for t in (theta, phi, u, route.workspace)}
+    devs = {t.device for t in (theta, phi, route.workspace)} | {device}
     if len(devs) != 1:
         raise ValueError("all tensors must be on one device")
     if out is None:
-        out = torch.empty(N, dtype=torch.int32, device=u.device)
+        out = torch.empty(N, dtype=torch.int32, device=device)
     else:
         _require(out, "out", torch.int32, 1)
-        if out.shape[0] != N or out.device != u.device:
+        if out.shape[0] != N or out.device != device:
             raise ValueError("out must be int32[N] on the tensors' device")
+    return M, V, K, out
+
+
+def draw_routed(theta, phi, route: Route, u, out=None, stream=None) -> torch.Tensor:
+    """z[N] (int32, indexed by the original token) by the leaf kernel over the
+    routed tokens; u float32 [N] indexed by the original token.  K must be
+    divisible by 4 with 132 <= K <= 2048."""
+    _require(u, "u", torch.float32, 1)
+    N = u.shape[0]
+    M, V, K, out = _routed_args(theta, phi, route, N, u.device, out)
     with torch.cuda.device(u.device):
         st = load().lda_draw_routed(theta.data_ptr(), phi.data_ptr(), route.workspace.data_ptr(),
                                     route.workspace.numel(), ctypes.byref(route.info),
                                     u.data_ptr(), out.data_ptr(), N, M, V, K,
                                     _stream_handle(stream))
+    _check(st)
+    return out
+
+
+def draw_routed_philox(theta, phi, route: Route, seed: int, sweep: int = 0, out=None,
+                       stream=None) -> torch.Tensor:
+    """``draw_routed`` with the uniforms of ``draw_philox`` (generated in the
+    kernel from the original token index, sweep and seed)."""
+    N = route.N
+    M, V, K, out = _routed_args(theta, phi, route, N, route.workspace.device, out)
+    with torch.cuda.device(route.workspace.device):
+        st = load().lda_draw_routed_philox(
+            theta.data_ptr(), phi.data_ptr(), route.workspace.data_ptr(),
+            route.workspace.numel(), ctypes.byref(route.info), out.data_ptr(), N, M, V, K,
+            int(seed) & (2 ** 64 - 1), int(sweep) & (2 ** 32 - 1), _stream_handle(stream))
     _check(st)
     return out

@@ -11,7 +11,8 @@
 // lda_philox_uniforms         those uniforms, written out.
 // lda_butterfly_table the butterfly-patterned tables (Fig. 1, right).
 // lda_route_build / lda_draw_routed  tokens routed to the XCDs by word, and
-//                     the leaf kernel drawing them.
+//                     the leaf kernel drawing them (lda_draw_routed_philox:
+//                     with in-kernel uniforms).
 //
 // Device code: butterfly.hpp (lane exchanges, the butterfly, buffer loads),
 // philox.hpp, sources.hpp (document and uniform sources), tile.hpp (the
@@ -574,12 +575,17 @@ extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, in
   return LDA_OK;
 }
 
-extern "C" int lda_draw_routed(const float *theta, const float *phi, const void *workspace,
-                               size_t workspace_bytes, const lda_route *route, const float *u,
-                               int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
-                               void *stream) {
+namespace lda {
+namespace {
+
+// The routed draw for either uniform source.  `u_check` stands in for u in
+// the pointer checks (z when the uniforms come from Philox).
+int draw_routed(const float *theta, const float *phi, const void *workspace,
+                size_t workspace_bytes, const lda_route *route, const void *u_check,
+                const UniformSource &us, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                void *stream) {
   if (!route) return LDA_ERR_NULL;
-  const int st = check_args(theta, phi, workspace, workspace, u, z, N, M, V, K);
+  const int st = check_args(theta, phi, workspace, workspace, u_check, z, N, M, V, K);
   if (st != LDA_OK) return st;
   if (!routed_for(K) || N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
   if (N == 0) return LDA_OK;
@@ -601,13 +607,33 @@ extern "C" int lda_draw_routed(const float *theta, const float *phi, const void 
     rt.base[x] = route->start[x];
     rt.len[x] = route->length[x];
   }
-  const UniformSource us{u, 0, 0, 0};
   const hipStream_t s = static_cast<hipStream_t>(stream);
   if (K % kBlock4 == 0)
     launch_routed<false>(theta, phi, rt, us, z, max_len, M, V, K, s);
   else
     launch_routed<true>(theta, phi, rt, us, z, max_len, M, V, K, s);
   return finish_launch();
+}
+
+}  // namespace
+}  // namespace lda
+
+extern "C" int lda_draw_routed(const float *theta, const float *phi, const void *workspace,
+                               size_t workspace_bytes, const lda_route *route, const float *u,
+                               int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                               void *stream) {
+  return lda::draw_routed(theta, phi, workspace, workspace_bytes, route, u,
+                          lda::UniformSource{u, 0, 0, 0}, z, N, M, V, K, stream);
+}
+
+extern "C" int lda_draw_routed_philox(const float *theta, const float *phi,
+                                      const void *workspace, size_t workspace_bytes,
+                                      const lda_route *route, int32_t *z, int64_t N, int32_t M,
+                                      int32_t V, int32_t K, uint64_t seed, uint32_t sweep,
+                                      void *stream) {
+  const lda::UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
+  return lda::draw_routed(theta, phi, workspace, workspace_bytes, route, z, us, z, N, M, V, K,
+                          stream);
 }
 
 extern "C" int lda_butterfly_width(int32_t K) {
@@ -622,8 +648,8 @@ extern "C" const char *lda_status_string(int status) {
     case LDA_ERR_NULL: return "a required pointer is NULL";
     case LDA_ERR_SHAPE: return "invalid shape (N < 0, M <= 0, V <= 0 or K <= 0)";
     case LDA_ERR_UNSUPPORTED:
-      return "unsupported size (K > LDA_MAX_K, or theta or phi larger than "
-             "LDA_MAX_TABLE_BYTES)";
+      return "unsupported size (K > LDA_MAX_K, N > LDA_MAX_N, theta or phi larger than "
+             "LDA_MAX_TABLE_BYTES, or a K or N the entry point does not take)";
     case LDA_ERR_HIP: return "HIP runtime error";
     case LDA_ERR_ALIGN: return "a pointer is not aligned (4 bytes; 8 for offsets and workspaces)";
     case LDA_ERR_WORKSPACE:

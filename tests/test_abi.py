@@ -240,7 +240,8 @@ def test_route_build_argument_errors(lib):
     assert r.N == 0 and list(r.length) == [0] * 8
 
 
-def test_draw_routed_argument_errors(lib):
+@pytest.mark.parametrize("philox", [False, True])
+def test_draw_routed_argument_errors(lib, philox):
     import ctypes
     from paper_1505_03851_amd._lib import STATUS, RouteInfo
     N = 1000
@@ -253,10 +254,13 @@ def test_draw_routed_argument_errors(lib):
         r.start[x] = x * r.length[0]
 
     def run(theta=A, phi=A, w=A, wb=ws, route=True, u=A, z=A, n=N, M=3, V=5, K=1024):
-        return lib.lda_draw_routed(theta, phi, w, wb, ctypes.byref(r) if route else None,
-                                   u, z, n, M, V, K, None)
+        rp = ctypes.byref(r) if route else None
+        if philox:              # no u: the uniforms come from the seed
+            return lib.lda_draw_routed_philox(theta, phi, w, wb, rp, z, n, M, V, K,
+                                              12345, 0, None)
+        return lib.lda_draw_routed(theta, phi, w, wb, rp, u, z, n, M, V, K, None)
     assert run(route=False) == STATUS["LDA_ERR_NULL"]
-    for key in ("theta", "phi", "w", "u", "z"):
+    for key in ("theta", "phi", "w", "z") + (() if philox else ("u",)):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
     for kw in (dict(n=-1), dict(M=0), dict(V=0), dict(K=0)):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw

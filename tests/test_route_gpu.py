@@ -173,3 +173,35 @@ def test_routed_rejects_unsupported_k():
     with pytest.raises(lda.LdaError) as e:
         lda.draw_routed(dev["theta"], dev["phi"], route, dev["u"])
     assert e.value.status == lda.STATUS["LDA_ERR_UNSUPPORTED"]
+
+
+@pytest.mark.parametrize("name,sampled", [("wiki-shaped-K240", False), ("corpus16M-K1024", True)])
+def test_routed_philox(name, sampled):
+    """The routed draw with in-kernel uniforms: against the oracle fed the
+    oracle's own Philox uniforms of the original token indices, and equal to
+    the unrouted draw_philox except inside the rounding band."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from oracle import philox as px
+    seed, sweep = 0x5EED_2015_0513_0002, 5
+    c = make_corpus(name)
+    c.u = px.token_uniforms(seed, sweep, 0, c.N)
+    print(f"[case] routed philox {name}", flush=True)
+    dev = to_device(c)
+    route = lda.route_build(dev["doc_id"], dev["word_id"], c.M, c.V)
+    z = lda.draw_routed_philox(dev["theta"], dev["phi"], route, seed, sweep)
+    z_plain = lda.draw_philox(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], seed, sweep)
+    torch.cuda.synchronize()
+    z, z_plain = z.cpu().numpy(), z_plain.cpu().numpy()
+    idx = None
+    if sampled:
+        rng = np.random.default_rng(8)
+        idx = np.unique(np.concatenate([rng.integers(0, c.N, 1 << 19), np.arange(c.N - 300, c.N)]))
+    rep = compare(c, z, idx)
+    print(f"[parity] {name} routed philox: {rep}", flush=True)
+    assert rep.hard == 0, rep.first_hard
+    assert rep.mismatch_rate < MAX_MISMATCH_RATE
+    differ = np.nonzero(z != z_plain)[0]
+    assert differ.size <= max(1, c.N // 10000), differ.size
+    if differ.size:
+        assert compare(c, z, differ).hard == 0
