@@ -40,8 +40,8 @@
  *
  * Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls only
  * enqueue work and return; the caller synchronises (lda_route_build alone
- * waits for its own work, to read back the sizes of the routed lists).  Calls that share the
- * output buffer must be ordered by the caller.
+ * waits for its own work, to read back the sizes of the routed lists).
+ * Calls that share the output buffer must be ordered by the caller.
  *
  * Errors: every entry point returns LDA_OK (0) or a negative status.  Argument
  * checks happen before any HIP call, so a rejected call has no effect and
