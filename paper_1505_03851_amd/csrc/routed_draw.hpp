@@ -29,6 +29,77 @@ __host__ __device__ constexpr int routed_lds_floats(int NB) {
   return 8 * NB * kWave + kFewMax * kWave * 4;
 }
 
+// One wavefront of the leaf kernel over 64 listed tokens: lane `lane` draws
+// token n (document doc, word word) and stores z[n] if `store`.  The tokens
+// need not be consecutive; their documents usually form a few runs
+// (kFewDocs).  region: the wavefront's routed_lds_floats(NB) floats of LDS.
+template <int C, bool PAD>
+__device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
+                                            const float *__restrict__ phi, uint32_t theta_bytes,
+                                            uint32_t phi_bytes, int K, const int32_t *wp,
+                                            int64_t first, int lane, float *region, int64_t n,
+                                            bool store, int doc, int word, const UniformSource &u,
+                                            int32_t *__restrict__ z) {
+  const int NB = (K + kBlock4 - 1) / kBlock4;
+  const int c0 = K - NB * kBlock4;
+  FewDocs fd;
+  fd.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
+  Wave<kWave, false> w;
+  init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, wp, first, kWave - 1, K, lane,
+                          doc, word);
+  // runs of documents among the wavefront's tokens
+  const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
+  const uint64_t starts = __builtin_amdgcn_ballot_w64(lane == 0 || doc != prev);
+  fd.D = __builtin_amdgcn_readfirstlane(__builtin_popcountll(starts));
+  fd.slot = __builtin_popcountll(starts & ((2ull << lane) - 1ull)) - 1;
+  uint64_t m = starts;
+#pragma unroll
+  for (int d = 0; d < kFewMax; ++d) {
+    fd.row[d] = 0;
+    if (m) {
+      const int ln = __builtin_ctzll(m);
+      m &= m - 1;
+      fd.row[d] = (uint32_t)__builtin_amdgcn_readlane(doc, ln) * w.row_bytes;
+    }
+  }
+  // The uniform's load depends on the token index's; issued before the
+  // sweep it would hold up every in-order wait for the sweep's loads, so
+  // it is issued after the first block's step.
+  float un = 0.0f;
+  const auto load_u = [&]() { un = u(n); };
+  region += lane;
+  float sum;
+  if (fd.D == 1)
+    sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region, load_u);
+  else if (fd.D <= kFewMax)
+    sum = sweep8<kFewDocs, LDA_ROUTED_FEW_WINDOW, PAD, LDA_ROUTED_FEW_THETA>(w, fd, NB, c0,
+                                                                           region, load_u);
+  else
+    sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region, load_u);
+  const float stop = sum * un;
+  // Algorithm 9 over the ends of the 8 NB eighths.
+  int lo = 0, hi = 8 * NB - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (stop < region[mid * kWave])
+      hi = mid;
+    else
+      lo = mid + 1;
+  }
+  const int chunk = lo;
+  float low = lo > 0 ? region[(lo - 1) * kWave] : 0.0f;
+  float high = region[lo * kWave];
+  // Rebuild and Algorithm 10 on the chosen 32-topic chunk, as in
+  // leaf_eighths_kernel.
+  const Wave<kWave / 2, false> wh = half_wave(w, lane);
+  float h[kWave / 2];
+  load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+  butterfly_block<kWave / 2>(h, wh.r, NoStore{});
+  const int j = c0 + chunk * (kWave / 2) +
+                inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
+  if (store) z[n] = j;
+}
+
 template <int C, int WPB, int WPEU, bool PAD>
 __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void routed_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
@@ -41,73 +112,15 @@ void routed_eighths_kernel(const float *__restrict__ theta, const float *__restr
   const int64_t base = rt.base[x];
   const int64_t len = rt.len[x];
   const int NB = (K + kBlock4 - 1) / kBlock4;
-  const int c0 = K - NB * kBlock4;
-  float *region = lds + wave * routed_lds_floats(NB);
-  FewDocs fd;
-  fd.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
   // One tile of WPB wavefronts of its list per workgroup (the grid holds as
   // many tiles per list as the longest list needs).
-  {
-    const int64_t first = ((int64_t)(blockIdx.x / kXcds) * WPB + wave) * kWave;
-    if (first >= len) return;
-    const int64_t i = base + first + lane;
-    const int doc = rt.rdoc[i];
-    const int word = rt.rword[i];
-    const int n = rt.perm[i];
-    Wave<kWave, false> w;
-    init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, rt.rword + base, first,
-                            kWave - 1, K, lane, doc, word);
-    // runs of documents among the wavefront's tokens
-    const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
-    const uint64_t starts = __builtin_amdgcn_ballot_w64(lane == 0 || doc != prev);
-    fd.D = __builtin_amdgcn_readfirstlane(__builtin_popcountll(starts));
-    fd.slot = __builtin_popcountll(starts & ((2ull << lane) - 1ull)) - 1;
-    uint64_t m = starts;
-#pragma unroll
-    for (int d = 0; d < kFewMax; ++d) {
-      fd.row[d] = 0;
-      if (m) {
-        const int ln = __builtin_ctzll(m);
-        m &= m - 1;
-        fd.row[d] = (uint32_t)__builtin_amdgcn_readlane(doc, ln) * w.row_bytes;
-      }
-    }
-    // The uniform's load depends on the token index's; issued before the
-    // sweep it would hold up every in-order wait for the sweep's loads, so
-    // it is issued after the first block's step.
-    float un = 0.0f;
-    const auto load_u = [&]() { un = u(n >= 0 ? n : 0); };
-    float sum;
-    if (fd.D == 1)
-      sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region + lane, load_u);
-    else if (fd.D <= kFewMax)
-      sum = sweep8<kFewDocs, LDA_ROUTED_FEW_WINDOW, PAD, LDA_ROUTED_FEW_THETA>(w, fd, NB, c0,
-                                                                             region + lane, load_u);
-    else
-      sum = sweep8<kAnyDocs, (C > 2 ? C / 2 : C), PAD>(w, fd, NB, c0, region + lane, load_u);
-    const float stop = sum * un;
-    // Algorithm 9 over the ends of the 8 NB eighths.
-    int lo = 0, hi = 8 * NB - 1;
-    while (lo < hi) {
-      const int mid = (lo + hi) >> 1;
-      if (stop < region[mid * kWave + lane])
-        hi = mid;
-      else
-        lo = mid + 1;
-    }
-    const int chunk = lo;
-    float low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
-    float high = region[lo * kWave + lane];
-    // Rebuild and Algorithm 10 on the chosen 32-topic chunk, as in
-    // leaf_eighths_kernel.
-    const Wave<kWave / 2, false> wh = half_wave(w, lane);
-    float h[kWave / 2];
-    load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
-    butterfly_block<kWave / 2>(h, wh.r, NoStore{});
-    const int j = c0 + chunk * (kWave / 2) +
-                  inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
-    if (n >= 0) z[n] = j;
-  }
+  const int64_t first = ((int64_t)(blockIdx.x / kXcds) * WPB + wave) * kWave;
+  if (first >= len) return;
+  const int64_t i = base + first + lane;
+  const int n = rt.perm[i];
+  draw_listed<C, PAD>(theta, phi, theta_bytes, phi_bytes, K, rt.rword + base, first, lane,
+                      lds + wave * routed_lds_floats(NB), n >= 0 ? n : 0, n >= 0, rt.rdoc[i],
+                      rt.rword[i], u, z);
 }
 
 }  // namespace
