@@ -6,8 +6,8 @@
 namespace lda {
 namespace {
 
-// Leaf groups for small K (K divisible by 4, at most 4 G topics for a group
-// size G of 8, 16 or 32 lanes; N >= 64).  Sections 3 and 4 with a 4-topic
+// Leaf groups for K up to 256 (K divisible by 4, at most 4 G topics for a
+// group size G of 8, 16, 32 or 64 lanes; N >= 64).  Sections 3 and 4 with a 4-topic
 // leaf in the place of a topic: a wavefront holds 64 / G groups of G tokens,
 // lane r of a group owns token r of the group and, in the tile, leaf r (topics
 // c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K topics are
