@@ -7,19 +7,19 @@ namespace lda {
 namespace {
 
 // Leaf groups for K up to 256 (K divisible by 4, at most 4 G topics for a
-// group size G of 8, 16, 32 or 64 lanes; N >= 64).  Sections 3 and 4 with a 4-topic
-// leaf in the place of a topic: a wavefront holds 64 / G groups of G tokens,
-// lane r of a group owns token r of the group and, in the tile, leaf r (topics
-// c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K topics are
-// empty) of every token of its group.  Load k brings leaf r of token k of
-// every group into lane r of that group, so each load instruction reads the
-// whole rows (16 G bytes) of 64 / G tokens.  Register a[k] is the leaf sum
-// (dot4) of token k; Algorithm 8's butterfly over the G leaves leaves the
-// table and the lane's own token's total; Algorithm 10 finds the leaf whose
-// prefix range holds u * S, and the leaf's four products, reloaded for the
-// lane's own token, give the topic by a scan from the prefix before the leaf.
-// The theta leaf comes once per lane when each group's tokens share one
-// document (GROUP_DOCS), else with every phi leaf.
+// group size G of 8, 16, 32 or 64 lanes; N >= 64).  Sections 3 and 4 with a
+// 4-topic leaf in the place of a topic: a wavefront holds 64 / G groups of G
+// tokens, lane r of a group owns token r of the group and, in the tile, leaf
+// r (topics c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K
+// topics are empty) of every token of its group.  Load k brings leaf r of
+// token k of every group into lane r of that group, so each load instruction
+// reads the whole rows (16 G bytes) of 64 / G tokens.  Register a[k] is the
+// leaf sum (dot4) of token k; Algorithm 8's butterfly over the G leaves
+// leaves the table and the lane's own token's total; Algorithm 10 finds the
+// leaf whose prefix range holds u * S, and the leaf's four products,
+// reloaded for the lane's own token, give the topic by a scan from the
+// prefix before the leaf. The theta leaf comes once per lane when each
+// group's tokens share one document (GROUP_DOCS), else with every phi leaf.
 template <int G, int C, bool PAD, bool GROUP_DOCS>
 __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
                                            uint32_t voff, bool real, uint32_t ph_lane,
