@@ -90,13 +90,24 @@ SHAPES = [
     (64 * 33 + 63, 60, 500, 240, "single"),
     (64 * 17 + 9, 60, 500, 1000, "sequential"),
     (64 * 17 + 9, 60, 500, 2047, "shuffled"),
-    # half-block tail from 24 to 32 blocks: 4- and 2-wavefront workgroups,
-    # with and without a remnant, one, two and many documents per wave
+    # K from 1536 to 2048 divisible by 4: the leaf kernel with six to eight
+    # 256-topic blocks (its second launch shape), with and without a padded
+    # first block, one, two and many documents per wave
     (64 * 13 + 7, 30, 400, 1536, "sequential"),
     (64 * 10 + 1, 30, 300, 1664, "shuffled"),
     (64 * 9 + 40, 3, 100, 1792, "single"),
     (64 * 11 + 3, 20, 300, 1900, "sequential"),
     (64 * 8 + 63, 9, 200, 2048, "sequential"),
+    # K not divisible by 4: the one-topic kernel, with the half-block tail
+    # from 2 to 32 blocks of 64 topics (a remnant in front), and the
+    # full-block rebuild above 32 blocks
+    (64 * 9 + 5, 30, 400, 130, "sequential"),
+    (64 * 7 + 40, 9, 300, 513, "shuffled"),
+    (64 * 6 + 3, 3, 200, 1023, "single"),
+    (64 * 8 + 17, 20, 300, 1535, "sequential"),
+    (64 * 5 + 60, 9, 200, 1901, "sequential"),
+    (64 * 4 + 9, 5, 100, 2111, "shuffled"),
+    (64 * 3 + 1, 4, 100, 3001, "sequential"),
     # K divisible by 4 but not by 256: the leaf kernel with empty topics in
     # front of its first 256-topic block (one, two and many documents per wave)
     (64 * 11 + 7, 13, 300, 1000, "sequential"),
