@@ -149,14 +149,16 @@ template <int G>
 void launch_groups(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                    hipStream_t s) {
-  constexpr int C = LDA_GROUP_WINDOW < G ? LDA_GROUP_WINDOW : G;
+  constexpr int CW = G == kWave ? LDA_GROUP64_WINDOW : LDA_GROUP_WINDOW;
+  constexpr int C = CW < G ? CW : G;
+  constexpr int WPEU = G == kWave ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
   if (K == kLeaf * G)
-    leaf_group_kernel<G, C, LDA_GROUP_WAVES_PER_EU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
+    leaf_group_kernel<G, C, WPEU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_group_kernel<G, C, LDA_GROUP_WAVES_PER_EU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+    leaf_group_kernel<G, C, WPEU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 

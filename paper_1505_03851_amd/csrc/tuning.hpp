@@ -50,6 +50,16 @@
 #ifndef LDA_GROUP_WAVES_PER_EU
 #define LDA_GROUP_WAVES_PER_EU 3
 #endif
+//   LDA_GROUP64_WINDOW, LDA_GROUP64_WAVES_PER_EU  the same for groups of 64
+//                             lanes (K from 132 to 256): 8 at 3 was 0-15%
+//                             faster than 4 at 4, 2 at 4, 16 at 2, 2 or 4 at
+//                             5 at K = 144 ... 256.
+#ifndef LDA_GROUP64_WINDOW
+#define LDA_GROUP64_WINDOW 8
+#endif
+#ifndef LDA_GROUP64_WAVES_PER_EU
+#define LDA_GROUP64_WAVES_PER_EU 3
+#endif
 //   LDA_EIGHTHS_MIN_K         smallest K it takes (K divisible by 4; the first
 //                             block is padded with empty topics up to a
 //                             multiple of 256).
