@@ -20,14 +20,21 @@ namespace {
 // reloaded for the lane's own token, give the topic by a scan from the
 // prefix before the leaf. The theta leaf comes once per lane when each
 // group's tokens share one document (GROUP_DOCS), else with every phi leaf.
-template <int G, int C, bool PAD, bool GROUP_DOCS>
+// How the theta leaves of a group's tokens are found: every group's tokens in
+// one document (one leaf per lane, loaded once), in at most kMaxGroupRuns<G> runs
+// of documents (each run's leaf loaded once per lane; token k takes the leaf
+// of its run), or any mix (a leaf per token, loaded with its phi leaf).
+enum GroupTheta : int { kGroupOne = 0, kGroupRuns = 1, kGroupAny = 2 };
+template <int G>
+constexpr int kMaxGroupRuns = G == kWave ? 4 : 2;
+
+template <int G, int C, bool PAD, int MODE>
 __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
                                            uint32_t voff, bool real, uint32_t ph_lane,
-                                           uint32_t th_lane, int gbase) {
+                                           uint32_t th_lane, int gbase, uint64_t gstarts) {
   static_assert(G % C == 0, "the window size must divide G");
+  constexpr int R = MODE == kGroupRuns ? kMaxGroupRuns<G> : 1;
   const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
-  f4 th = zero;
-  if constexpr (GROUP_DOCS) th = real ? load_f32x4(th_rs, voff + th_lane, 0) : zero;
   // leaf of token k of the group at row offset `row` of that token (held by
   // the lane that owns the token): with G = 64 the row is uniform and goes in
   // the scalar offset, else it is fetched per lane
@@ -38,20 +45,52 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
       return load_f32x4(
           rs, voff + (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row), 0);
   };
-  f4 win[C], twin[GROUP_DOCS ? 1 : C];
+  // kGroupRuns: gstarts bit p (0 < p < G) marks the group's token p as the
+  // first of a run; run j's leaf is that of the token opening it
+  f4 th[R];
+  if constexpr (MODE == kGroupOne) {
+    th[0] = real ? load_f32x4(th_rs, voff + th_lane, 0) : zero;
+  } else if constexpr (MODE == kGroupRuns) {
+    uint64_t m = gstarts;
+    th[0] = leaf_of(th_rs, th_lane, 0);
+#pragma unroll
+    for (int j = 1; j < R; ++j) {
+      const int p = m ? (int)__builtin_ctzll(m) : 0;
+      m &= m - 1;
+      th[j] = leaf_of(th_rs, th_lane, p);
+    }
+#pragma unroll
+    for (int j = 0; j < R; ++j) th[j] = real ? th[j] : zero;
+  }
+  const auto run_of = [&](int k) {
+    // runs opened at the group's tokens 1 .. k
+    const uint64_t upto = k == 63 ? ~0ull : ((2ull << k) - 1ull);
+    return __builtin_popcountll(gstarts & upto);
+  };
+  f4 win[C], twin[MODE == kGroupAny ? C : 1];
 #pragma unroll
   for (int k = 0; k < C; ++k) {
     win[k] = leaf_of(ph_rs, ph_lane, k);
-    if constexpr (!GROUP_DOCS) twin[k] = leaf_of(th_rs, th_lane, k);
+    if constexpr (MODE == kGroupAny) twin[k] = leaf_of(th_rs, th_lane, k);
   }
 #pragma unroll
   for (int k = 0; k < G; ++k) {
-    const f4 tv = GROUP_DOCS ? th : twin[k % C];
+    f4 tv;
+    if constexpr (MODE == kGroupAny) {
+      tv = twin[k % C];
+    } else if constexpr (MODE == kGroupRuns) {
+      const int j = run_of(k);
+      tv = th[0];
+#pragma unroll
+      for (int i = 1; i < R; ++i) tv = j == i ? th[i] : tv;
+    } else {
+      tv = th[0];
+    }
     const float v = dot4(tv, win[k % C]);
-    a[k] = GROUP_DOCS || real ? v : 0.0f;
+    a[k] = MODE != kGroupAny || real ? v : 0.0f;
     if (k + C < G) {
       win[k % C] = leaf_of(ph_rs, ph_lane, k + C);
-      if constexpr (!GROUP_DOCS) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
+      if constexpr (MODE == kGroupAny) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
     }
     __builtin_amdgcn_sched_barrier(0);
   }
@@ -85,14 +124,26 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   const int leaf = c0 + kLeaf * r;
   const bool real = !PAD || leaf >= 0;
   const uint32_t voff = (uint32_t)(real ? leaf : 0) * 4u;
-  const int gdoc = __builtin_amdgcn_ds_bpermute(gbase << 2, doc);
-  const bool group_docs = __builtin_amdgcn_ballot_w64(doc == gdoc) == ~0ull;
+  // runs of documents inside each group: bit l of `starts` marks lane l's
+  // token as the first of a run (not counting the group's first token)
+  const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
+  const uint64_t starts = __builtin_amdgcn_ballot_w64(r != 0 && doc != prev);
+  const uint64_t gmask = G == kWave ? ~0ull : ((1ull << G) - 1ull);
+  const uint64_t gstarts = (starts >> gbase) & gmask;  // this lane's group, bit p = token p
+  // the most runs in any group (groups of G lanes: at most 64 / G of them)
+  int most = 0;
+#pragma unroll
+  for (int g = 0; g < kWave / G; ++g)
+    most = max(most, __builtin_popcountll((starts >> (g * G)) & gmask));
 
   float a[G];
-  if (group_docs)
-    group_tile<G, C, PAD, true>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+  if (most == 0)
+    group_tile<G, C, PAD, kGroupOne>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
+  else if (most < kMaxGroupRuns<G>)
+    group_tile<G, C, PAD, kGroupRuns>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase,
+                                      gstarts);
   else
-    group_tile<G, C, PAD, false>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase);
+    group_tile<G, C, PAD, kGroupAny>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
   butterfly_block<G>(a, r, NoStore{});
   const float total = a[G - 1];
   const float stop = total * un;
