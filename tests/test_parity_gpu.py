@@ -128,6 +128,13 @@ SHAPES = [
     (64 * 8 + 5, 3, 300, 96, "sequential"),
     (64 * 12 + 11, 40, 300, 124, "ragged"),
     (64, 3, 64, 128, "shuffled"),
+    # documents of 17-40 tokens: groups spanning one, two or more runs of
+    # documents (the leaf-group kernel's theta leaf per run, up to 2 runs per
+    # group below 64 lanes and 4 for 64 lanes, else a leaf per token)
+    (64 * 20 + 7, 32, 300, 64, "sequential"),
+    (64 * 20 + 7, 64, 300, 128, "sequential"),
+    (64 * 30 + 5, 60, 300, 200, "sequential"),
+    (64 * 30 + 5, 110, 300, 256, "sequential"),
     # K a multiple of 256 (the leaf kernel with 32-topic prefix rows up to 2048)
     (1, 1, 7, 256, "sequential"),
     (63, 5, 50, 512, "shuffled"),
