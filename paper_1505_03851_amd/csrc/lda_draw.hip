@@ -145,7 +145,7 @@ bool groups_for(int64_t N, int32_t K) {
   return N >= kWave && K % kLeaf == 0 && K <= LDA_GROUP_MAX_K && K <= kLeaf * kWave;
 }
 
-template <int G>
+template <int G, int H>
 void launch_groups(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                    hipStream_t s) {
@@ -154,11 +154,11 @@ void launch_groups(const float *theta, const float *phi, DocSource d, const int3
   constexpr int WPEU = G == kWave ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  if (K == kLeaf * G)
-    leaf_group_kernel<G, C, WPEU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
+  if (K == kLeaf * H * G)
+    leaf_group_kernel<G, H, C, WPEU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_group_kernel<G, C, WPEU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+    leaf_group_kernel<G, H, C, WPEU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
@@ -284,14 +284,16 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (groups_for(N, K)) {
-    if (K <= kLeaf * 8)
-      launch_groups<8>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= kLeaf * 16)
-      launch_groups<16>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= kLeaf * 32)
-      launch_groups<32>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    constexpr int H = LDA_GROUP_LEAF / kLeaf;  // quads per lane
+    constexpr int L = kLeaf * H;
+    if (K <= L * 8 / H)
+      launch_groups<8 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (K <= L * 16 / H)
+      launch_groups<16 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    else if (K <= L * 32 / H)
+      launch_groups<32 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     else
-      launch_groups<64>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+      launch_groups<64 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
   }
   if (eighths_for(N, K)) {

@@ -21,17 +21,42 @@ namespace {
 // prefix before the leaf. The theta leaf comes once per lane when each
 // group's tokens share one document (GROUP_DOCS), else with every phi leaf.
 // How the theta leaves of a group's tokens are found: every group's tokens in
-// one document (one leaf per lane, loaded once), in at most kMaxGroupRuns<G> runs
-// of documents (each run's leaf loaded once per lane; token k takes the leaf
-// of its run), or any mix (a leaf per token, loaded with its phi leaf).
+// one document (one leaf per lane, loaded once), in at most kMaxGroupRuns<G>
+// runs of documents (each run's leaf loaded once per lane; token k takes the
+// leaf of its run), or any mix (a leaf per token, loaded with its phi leaf).
 enum GroupTheta : int { kGroupOne = 0, kGroupRuns = 1, kGroupAny = 2 };
 template <int G>
 constexpr int kMaxGroupRuns = G == kWave ? 4 : 2;
 
-template <int G, int C, bool PAD, int MODE>
+// A leaf of L = 4 H consecutive topics: H 16-byte quads.
+template <int H>
+struct Leaf {
+  f4 q[H];
+};
+
+// Sum of the leaf's L theta-phi products, in topic order (the first a
+// product, the others fused multiply-adds onto the running sum).
+template <int H>
+__device__ __forceinline__ float leaf_dot(const Leaf<H> &t, const Leaf<H> &p) {
+  float s = dot4(t.q[0], p.q[0]);
+#pragma unroll
+  for (int h = 1; h < H; ++h) {
+    s = __builtin_fmaf(t.q[h].x, p.q[h].x, s);
+    s = __builtin_fmaf(t.q[h].y, p.q[h].y, s);
+    s = __builtin_fmaf(t.q[h].z, p.q[h].z, s);
+    s = __builtin_fmaf(t.q[h].w, p.q[h].w, s);
+  }
+  return s;
+}
+
+// The tile of a group: a[k] = this lane's leaf sum of token k of its group.
+// voff[h]: byte offset of quad h of this lane's leaf in a row; real[h]: the
+// quad holds topics (false: front padding, its theta is zero).
+template <int G, int H, int C, int MODE>
 __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
-                                           uint32_t voff, bool real, uint32_t ph_lane,
-                                           uint32_t th_lane, int gbase, uint64_t gstarts) {
+                                           const uint32_t (&voff)[H], const bool (&real)[H],
+                                           uint32_t ph_lane, uint32_t th_lane, int gbase,
+                                           uint64_t gstarts) {
   static_assert(G % C == 0, "the window size must divide G");
   constexpr int R = MODE == kGroupRuns ? kMaxGroupRuns<G> : 1;
   const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -39,35 +64,47 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   // the lane that owns the token): with G = 64 the row is uniform and goes in
   // the scalar offset, else it is fetched per lane
   const auto leaf_of = [&](rsrc_t rs, uint32_t row, int k) {
-    if constexpr (G == kWave)
-      return load_f32x4(rs, voff, (uint32_t)__builtin_amdgcn_readlane((int)row, k));
-    else
-      return load_f32x4(
-          rs, voff + (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row), 0);
+    Leaf<H> l;
+    if constexpr (G == kWave) {
+      const uint32_t srow = (uint32_t)__builtin_amdgcn_readlane((int)row, k);
+#pragma unroll
+      for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(rs, voff[h], srow);
+    } else {
+      const uint32_t vrow = (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row);
+#pragma unroll
+      for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(rs, voff[h] + vrow, 0);
+    }
+    return l;
+  };
+  const auto mask = [&](Leaf<H> l) {
+#pragma unroll
+    for (int h = 0; h < H; ++h) l.q[h] = real[h] ? l.q[h] : zero;
+    return l;
   };
   // kGroupRuns: gstarts bit p (0 < p < G) marks the group's token p as the
   // first of a run; run j's leaf is that of the token opening it
-  f4 th[R];
+  Leaf<H> th[R];
   if constexpr (MODE == kGroupOne) {
-    th[0] = real ? load_f32x4(th_rs, voff + th_lane, 0) : zero;
+    Leaf<H> l;
+#pragma unroll
+    for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(th_rs, voff[h] + th_lane, 0);
+    th[0] = mask(l);
   } else if constexpr (MODE == kGroupRuns) {
     uint64_t m = gstarts;
-    th[0] = leaf_of(th_rs, th_lane, 0);
+    th[0] = mask(leaf_of(th_rs, th_lane, 0));
 #pragma unroll
     for (int j = 1; j < R; ++j) {
       const int p = m ? (int)__builtin_ctzll(m) : 0;
       m &= m - 1;
-      th[j] = leaf_of(th_rs, th_lane, p);
+      th[j] = mask(leaf_of(th_rs, th_lane, p));
     }
-#pragma unroll
-    for (int j = 0; j < R; ++j) th[j] = real ? th[j] : zero;
   }
   const auto run_of = [&](int k) {
     // runs opened at the group's tokens 1 .. k
     const uint64_t upto = k == 63 ? ~0ull : ((2ull << k) - 1ull);
     return __builtin_popcountll(gstarts & upto);
   };
-  f4 win[C], twin[MODE == kGroupAny ? C : 1];
+  Leaf<H> win[C], twin[MODE == kGroupAny ? C : 1];
 #pragma unroll
   for (int k = 0; k < C; ++k) {
     win[k] = leaf_of(ph_rs, ph_lane, k);
@@ -75,19 +112,20 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   }
 #pragma unroll
   for (int k = 0; k < G; ++k) {
-    f4 tv;
+    Leaf<H> tv;
     if constexpr (MODE == kGroupAny) {
-      tv = twin[k % C];
+      tv = mask(twin[k % C]);
     } else if constexpr (MODE == kGroupRuns) {
       const int j = run_of(k);
       tv = th[0];
 #pragma unroll
-      for (int i = 1; i < R; ++i) tv = j == i ? th[i] : tv;
+      for (int i = 1; i < R; ++i)
+#pragma unroll
+        for (int h = 0; h < H; ++h) tv.q[h] = j == i ? th[i].q[h] : tv.q[h];
     } else {
       tv = th[0];
     }
-    const float v = dot4(tv, win[k % C]);
-    a[k] = MODE != kGroupAny || real ? v : 0.0f;
+    a[k] = leaf_dot(tv, win[k % C]);
     if (k + C < G) {
       win[k % C] = leaf_of(ph_rs, ph_lane, k + C);
       if constexpr (MODE == kGroupAny) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
@@ -96,12 +134,14 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   }
 }
 
-template <int G, int C, int WPEU, bool PAD>
+// L = 4 H topics per lane: groups of G lanes cover 4 H G topics.
+template <int G, int H, int C, int WPEU, bool PAD>
 __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                        DocSource docs, const int32_t *__restrict__ word_id,
                        UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_bytes, uint32_t phi_bytes) {
+  constexpr int L = kLeaf * H;
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
@@ -120,13 +160,20 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   const uint32_t ph_lane = (uint32_t)word * row_bytes;
   const uint32_t th_lane = (uint32_t)doc * row_bytes;
   const int r = lane & (G - 1), gbase = lane & ~(G - 1);
-  const int c0 = K - kLeaf * G;
-  const int leaf = c0 + kLeaf * r;
-  const bool real = !PAD || leaf >= 0;
-  const uint32_t voff = (uint32_t)(real ? leaf : 0) * 4u;
+  const int c0 = K - L * G;  // first topic of leaf 0 (< 0: front padding)
+  uint32_t voff[H];
+  bool real[H];
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const int topic = c0 + L * r + kLeaf * h;
+    real[h] = !PAD || topic >= 0;
+    voff[h] = (uint32_t)(real[h] ? topic : 0) * 4u;
+  }
   // runs of documents inside each group: bit l of `starts` marks lane l's
   // token as the first of a run (not counting the group's first token)
-  const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
+  // (lane l's previous document by a DPP wavefront shift right by one lane:
+  // no LDS round trip before the first loads; lane 0 keeps its own)
+  const int prev = __builtin_amdgcn_update_dpp(doc, doc, 0x138, 0xF, 0xF, false);
   const uint64_t starts = __builtin_amdgcn_ballot_w64(r != 0 && doc != prev);
   const uint64_t gmask = G == kWave ? ~0ull : ((1ull << G) - 1ull);
   const uint64_t gstarts = (starts >> gbase) & gmask;  // this lane's group, bit p = token p
@@ -138,28 +185,40 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
 
   float a[G];
   if (most == 0)
-    group_tile<G, C, PAD, kGroupOne>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
+    group_tile<G, H, C, kGroupOne>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
   else if (most < kMaxGroupRuns<G>)
-    group_tile<G, C, PAD, kGroupRuns>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase,
-                                      gstarts);
+    group_tile<G, H, C, kGroupRuns>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase,
+                                    gstarts);
   else
-    group_tile<G, C, PAD, kGroupAny>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
+    group_tile<G, H, C, kGroupAny>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0);
   butterfly_block<G>(a, r, NoStore{});
   const float total = a[G - 1];
   const float stop = total * un;
   float low = 0.0f, high = total;
   const int q = inblock_search<G, false>(a, nullptr, r, gbase, stop, low, high);
-  // Leaf q of the lane's own token (never a padding leaf: the prefix there is
-  // zero and stop < 0 never holds), scanned from the prefix before it; with
-  // S = 0 every comparison fails and the result is K - 1.
-  const int tq = c0 + kLeaf * q;
-  const uint32_t qoff = (uint32_t)(tq > 0 ? tq : 0) * 4u;
-  const f4 tl = load_f32x4(th_rs, qoff + th_lane, 0);
-  const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
-  const float s0 = __builtin_fmaf(tl.x, pl.x, low);
-  const float s1 = __builtin_fmaf(tl.y, pl.y, s0);
-  const float s2 = __builtin_fmaf(tl.z, pl.z, s1);
-  const int i = stop < s0 ? 0 : (stop < s1 ? 1 : (stop < s2 ? 2 : 3));
+  // Leaf q of the lane's own token, scanned from the prefix before it: the
+  // first of its L topics whose running sum exceeds stop, else the last.
+  // Padding topics (front of leaf 0 when K < L G) have zero weight and are
+  // never chosen (their running sum is `low`, and stop < low never holds);
+  // with S = 0 every comparison fails and the result is K - 1.
+  const int tq = c0 + L * q;
+  float sum = low;
+  int i = L - 1;
+#pragma unroll
+  for (int h = 0; h < H; ++h) {
+    const int topic = tq + kLeaf * h;
+    const uint32_t qoff = (uint32_t)(topic > 0 ? topic : 0) * 4u;
+    f4 tl = load_f32x4(th_rs, qoff + th_lane, 0);
+    const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
+    if (PAD && topic < 0) tl = f4{0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+    for (int e = 0; e < kLeaf; ++e) {
+      const int idx = kLeaf * h + e;
+      if (idx == L - 1) break;  // the leaf's last topic needs no comparison
+      sum = __builtin_fmaf(tl[e], pl[e], sum);
+      if (i == L - 1 && stop < sum) i = idx;
+    }
+  }
   if (store) z[n] = tq + i;
 }
 

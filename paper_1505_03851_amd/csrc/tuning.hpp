@@ -54,6 +54,12 @@
 //                             lanes (K from 132 to 256): 8 at 3 was 0-15%
 //                             faster than 4 at 4, 2 at 4, 16 at 2, 2 or 4 at
 //                             5 at K = 144 ... 256.
+//   LDA_GROUP_LEAF            topics per lane of the leaf-group kernel (4 or
+//                             8: groups of K / 4 or K / 8 lanes, rounded up
+//                             to a power of two).
+#ifndef LDA_GROUP_LEAF
+#define LDA_GROUP_LEAF 4
+#endif
 #ifndef LDA_GROUP64_WINDOW
 #define LDA_GROUP64_WINDOW 8
 #endif
