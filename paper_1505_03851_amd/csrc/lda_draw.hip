@@ -154,11 +154,12 @@ void launch_groups(const float *theta, const float *phi, DocSource d, const int3
   constexpr int WPEU = G == kWave ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const size_t lds = (size_t)kWavesPerBlock * group_lds_bytes<G, H>();  // (0 below 64 lanes)
   if (K == kLeaf * H * G)
-    leaf_group_kernel<G, H, C, WPEU, false><<<wave_grid(N), kBlockThreads, 0, s>>>(
+    leaf_group_kernel<G, H, C, WPEU, false><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_group_kernel<G, H, C, WPEU, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
+    leaf_group_kernel<G, H, C, WPEU, true><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 

@@ -6,6 +6,13 @@
 namespace lda {
 namespace {
 
+// Order one wavefront's earlier LDS writes before its later LDS reads.
+__device__ __forceinline__ void lds_order() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
 // Per-wavefront state of the butterfly kernel.  The wavefront's 64 tokens are
 // the window [t0, t0 + 64) of the token arrays; their word and document ids
 // are read with scalar loads straight from those arrays whenever a tile is

@@ -17,11 +17,6 @@ namespace {
 constexpr int kTileStride = kWave + 1;  // row padding: conflict-free LDS access
 constexpr int kTileFloats = kWave * kTileStride;
 
-__device__ __forceinline__ void lds_order() {
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-  __builtin_amdgcn_wave_barrier();
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
 
 // Store the tile (row k = token k) and return this lane's token's sum over
 // the block's topics, added in topic order.
