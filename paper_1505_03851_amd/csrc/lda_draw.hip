@@ -285,13 +285,15 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (groups_for(N, K)) {
-    constexpr int H = LDA_GROUP_LEAF / kLeaf;  // quads per lane
-    constexpr int L = kLeaf * H;
-    if (K <= L * 8 / H)
+    // groups just wide enough for K: K up to 32, 64, 128, 256 topics take
+    // 8, 16, 32, 64 lanes with 4-topic leaves (H = 1), half as many with
+    // 8-topic leaves (H = 2)
+    constexpr int H = LDA_GROUP_LEAF / kLeaf;
+    if (K <= kLeaf * 8)
       launch_groups<8 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= L * 16 / H)
+    else if (K <= kLeaf * 16)
       launch_groups<16 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= L * 32 / H)
+    else if (K <= kLeaf * 32)
       launch_groups<32 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     else
       launch_groups<64 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
