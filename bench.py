@@ -73,7 +73,8 @@ def upload(c):
 
 # kernels bench.py can time: name -> entry point of the binding
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
-           "variant-register", "variant-lds", "variant-lds_alt", "philox", "routed",
+           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "philox",
+           "routed",
            "routed+build", "routed-philox")
 PHILOX_SEED = 0x5EED20150513
 
@@ -337,7 +338,7 @@ def k_sweep(args) -> int:
 
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
-    registers or LDS, the alternative rule in LDS), the offsets form of the
+    registers or LDS, the alternative rule in LDS), 8-topic leaves, the offsets form of the
     documents, the document-per-lane driver, the draw with in-kernel
     uniforms and the default dispatch, on the two corpora and the corpus
     shaped like the paper's at K = 80 and 240; one JSON line per workload.
@@ -352,8 +353,8 @@ def ablation(args) -> int:
         rec = {"workload": name, "N": c.N, "K": c.K}
         z_ref = None
         kernels = ["butterfly", "variant-register", "variant-lds", "variant-lds_alt",
-                   "docs", "doc_lanes"] + (["doc_lanes_cache"] if c.K <= 256 else []) + \
-                  ["philox"]
+                   "variant-leaf8", "docs", "doc_lanes"] + \
+                  (["doc_lanes_cache"] if c.K <= 256 else []) + ["philox"]
         for kernel in kernels:
             r = measure(name, c, dev, kernel, args.steps, args.warmup)
             z = r.pop("z")

@@ -200,13 +200,19 @@ int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
  *                               [a b; c d] -> [a c; a+b c+d], whose table
  *                               holds left-half sums of aligned topic ranges,
  *                               searched in LDS by a descent from the whole
- *                               block.
- * Every variant uses the one-topic-per-lane kernel for all K (W = 64 for
- * K >= 64, else 32).  Any other `variant` returns LDA_ERR_UNSUPPORTED.
+ *                               block;
+ *   LDA_VARIANT_LEAF8           where lda_draw_butterfly uses its leaf groups
+ *                               (K divisible by 4 up to 256, N >= 64), leaves
+ *                               of 8 topics per lane in groups half as wide;
+ *                               elsewhere the kernels of lda_draw_butterfly.
+ * The three table variants use the one-topic-per-lane kernel for all K
+ * (W = 64 for K >= 64, else 32).  Any other `variant` returns
+ * LDA_ERR_UNSUPPORTED.
  */
 #define LDA_VARIANT_REGISTER_TABLE 0
 #define LDA_VARIANT_LDS_TABLE 1
 #define LDA_VARIANT_LDS_TABLE_ALT 2
+#define LDA_VARIANT_LEAF8 3
 int lda_draw_butterfly_variant(const float *theta, const float *phi,
                                const int32_t *doc_id, const int32_t *word_id,
                                const float *u, int32_t *z, int64_t N, int32_t M,

@@ -45,7 +45,8 @@ DOC_LANES_MAX_CACHE_BYTES = _CONSTS["LDA_DOC_LANES_MAX_CACHE_BYTES"]
 # table variants of lda_draw_butterfly_variant, by name
 VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
             "lds": _CONSTS["LDA_VARIANT_LDS_TABLE"],
-            "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"]}
+            "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"],
+            "leaf8": _CONSTS["LDA_VARIANT_LEAF8"]}
 
 
 class RouteInfo(ctypes.Structure):
@@ -209,10 +210,11 @@ def draw_transposed(theta, phi, doc_id, word_id, u, out=None, stream=None,
 
 def draw_variant(theta, phi, doc_id, word_id, u, variant: str = "register",
                  out=None, stream=None, validate: bool = False) -> torch.Tensor:
-    """z[N] (int32) by the one-topic-per-lane butterfly kernel with a chosen
-    block table: "register" (the paper's rule, search-assist loop), "lds"
-    (the same table in LDS) or "lds_alt" (the alternative rule
-    [a b; c d] -> [a c; a+b c+d], Section 4)."""
+    """z[N] (int32) by a variant of the butterfly draw: the one-topic-per-lane
+    kernel with a chosen block table, "register" (the paper's rule,
+    search-assist loop), "lds" (the same table in LDS) or "lds_alt" (the
+    alternative rule [a b; c d] -> [a c; a+b c+d], Section 4); or "leaf8",
+    the default kernels with 8-topic leaves in the leaf groups."""
     if variant not in VARIANTS:
         raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
     return _draw("lda_draw_butterfly_variant", theta, phi, doc_id, word_id, u,

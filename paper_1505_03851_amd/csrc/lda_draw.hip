@@ -6,7 +6,8 @@
 // lda_draw_docs       the same, documents given as offsets.
 // lda_draw_doc_lanes  Algorithm 7's document-per-lane driver.
 // lda_draw_transposed Algorithms 4-6, for comparison.
-// lda_draw_butterfly_variant  the block-table variants of Section 4.
+// lda_draw_butterfly_variant  the block-table variants of Section 4, and
+//                     8-topic leaves.
 // lda_draw_butterfly_philox   the butterfly draw with in-kernel uniforms.
 // lda_philox_uniforms         those uniforms, written out.
 // lda_butterfly_table the butterfly-patterned tables (Fig. 1, right).
@@ -280,23 +281,31 @@ void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
           theta, phi, off, wd, u, z, N, M, K, S, tb, pb);
 }
 
-// The butterfly draw for either document source (kernel choice by K).
+// The leaf-group kernel with groups just wide enough for K: K up to 32, 64,
+// 128, 256 topics take 8, 16, 32, 64 lanes with 4-topic leaves (H = 1), half
+// as many with 8-topic leaves (H = 2).
+template <int H>
+void dispatch_groups(const float *theta, const float *phi, DocSource d, const int32_t *word_id,
+                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                     hipStream_t s) {
+  if (K <= kLeaf * 8)
+    launch_groups<8 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else if (K <= kLeaf * 16)
+    launch_groups<16 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else if (K <= kLeaf * 32)
+    launch_groups<32 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+  else
+    launch_groups<64 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+}
+
+// The butterfly draw for either document source (kernel choice by K); with
+// H = 2 the leaf groups take 8-topic leaves.
+template <int H = LDA_GROUP_LEAF / kLeaf>
 void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
                         const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
                         int32_t M, int32_t V, int32_t K, hipStream_t s) {
   if (groups_for(N, K)) {
-    // groups just wide enough for K: K up to 32, 64, 128, 256 topics take
-    // 8, 16, 32, 64 lanes with 4-topic leaves (H = 1), half as many with
-    // 8-topic leaves (H = 2)
-    constexpr int H = LDA_GROUP_LEAF / kLeaf;
-    if (K <= kLeaf * 8)
-      launch_groups<8 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= kLeaf * 16)
-      launch_groups<16 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (K <= kLeaf * 32)
-      launch_groups<32 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else
-      launch_groups<64 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
+    dispatch_groups<H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
   }
   if (eighths_for(N, K)) {
@@ -426,14 +435,16 @@ extern "C" int lda_draw_butterfly_variant(const float *theta, const float *phi,
                                           int32_t V, int32_t K, int32_t variant,
                                           void *stream) {
   if (variant != LDA_VARIANT_REGISTER_TABLE && variant != LDA_VARIANT_LDS_TABLE &&
-      variant != LDA_VARIANT_LDS_TABLE_ALT)
+      variant != LDA_VARIANT_LDS_TABLE_ALT && variant != LDA_VARIANT_LEAF8)
     return LDA_ERR_UNSUPPORTED;
   const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
   const DocSource d{doc_id, nullptr, M, N};
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (variant == LDA_VARIANT_REGISTER_TABLE)
+  if (variant == LDA_VARIANT_LEAF8)
+    dispatch_butterfly<2>(theta, phi, d, word_id, us, z, N, M, V, K, s);
+  else if (variant == LDA_VARIANT_REGISTER_TABLE)
     launch_table_variant<false, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);
   else if (variant == LDA_VARIANT_LDS_TABLE)
     launch_table_variant<true, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);

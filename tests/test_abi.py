@@ -124,8 +124,8 @@ def test_empty_is_noop(lib, fn):
 
 def test_variant_codes(lib):
     from paper_1505_03851_amd._lib import STATUS, VARIANTS
-    assert sorted(VARIANTS.values()) == [0, 1, 2]
-    for bad in (-1, 3, 99):
+    assert sorted(VARIANTS.values()) == [0, 1, 2, 3]
+    for bad in (-1, 4, 99):
         assert call(lib, "lda_draw_butterfly_variant", variant=bad) == \
             STATUS["LDA_ERR_UNSUPPORTED"]
     # a known variant still goes through the argument checks

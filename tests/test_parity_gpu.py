@@ -16,7 +16,7 @@ from parity import MAX_MISMATCH_RATE, compare, run_kernel, to_device
 pytestmark = pytest.mark.gpu
 
 KERNELS = ["naive", "butterfly", "transposed",
-           "variant-register", "variant-lds", "variant-lds_alt"]
+           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8"]
 
 
 def _check(c, kernel, idx=None, rate=True):
