@@ -305,10 +305,13 @@ def test_docs_ragged(shape, kernel):
 
 @pytest.mark.parametrize("kernel", OFFSET_KERNELS)
 @pytest.mark.parametrize("layout", ["huge-first", "huge-last", "huge-middle", "alternating"])
-def test_docs_skewed_lengths(layout, kernel):
+@pytest.mark.parametrize("NM", [(64 * 50 + 13, 300), (64 * 400 + 13, 6000)],
+                         ids=lambda s: f"N{s[0]}-M{s[1]}")
+def test_docs_skewed_lengths(layout, kernel, NM):
     """Document lengths far from uniform, so that a wavefront's guess of its
-    first document (token index * M / N) is far off in either direction."""
-    N, M, V, K = 64 * 50 + 13, 300, 400, 96
+    first document (token index * M / N) is far off in either direction (by
+    thousands of documents at M = 6000)."""
+    (N, M), V, K = NM, 400, 96
     lengths = np.zeros(M, np.int64)
     if layout == "huge-first":
         lengths[0] = N - (M - 1)
