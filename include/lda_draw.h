@@ -40,7 +40,7 @@
  *
  * Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls only
  * enqueue work and return; the caller synchronises (lda_route_build alone
- * waits for its own work, to read back the sizes of the routed lists).
+ * waits, once, for its first kernels, to read back the word class counts).
  * Calls that share the output buffer must be ordered by the caller.
  *
  * Errors: every entry point returns LDA_OK (0) or a negative status.  Argument
@@ -262,9 +262,12 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * in the caller's workspace as those 8 lists, each in the original token
  * order and padded to a multiple of 64.  It depends on doc_id and word_id
  * only, so a sampler builds it once per corpus and reuses it every sweep.
- * It enqueues its kernels on `stream`, then synchronises `stream` once to
- * copy the list sizes into *route (the one entry point that waits; it cannot
- * be captured into a HIP graph, while lda_draw_routed can).
+ * It enqueues the class count on `stream` and synchronises `stream` once to
+ * read the counts back (the one entry point that waits; it cannot be
+ * captured into a HIP graph, while lda_draw_routed can); the host then
+ * assigns the classes, fills *route and enqueues the layout's kernels, which
+ * a draw on the same stream follows (a draw on another stream needs the
+ * caller's synchronisation).
  *   workspace        device memory, 8-byte aligned, at least
  *                    lda_route_workspace_bytes(N) bytes (about 12 N), owned
  *                    by the caller; it holds the routing and must stay

@@ -416,7 +416,8 @@ def route_build(doc_id, word_id, M: int, V: int, workspace=None, stream=None,
     """Route the tokens (doc_id, word_id: int32 [N] on the GPU) to the eight
     XCDs by word.  ``workspace``: a uint8 tensor of at least
     ``route_workspace_bytes(N)`` bytes on the same GPU, or None to allocate
-    one.  Synchronises ``stream`` once (to read back the list sizes)."""
+    one.  Synchronises ``stream`` once (to read back the word class counts);
+    a draw on the same stream follows the rest of the build."""
     _require(doc_id, "doc_id", torch.int32, 1)
     _require(word_id, "word_id", torch.int32, 1)
     N = doc_id.shape[0]

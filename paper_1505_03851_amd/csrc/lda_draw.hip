@@ -567,23 +567,28 @@ extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, in
   route_fill<<<1, kRouteClasses, 0, s>>>(P.counts, kRouteClasses, 0);
   route_hist<<<(unsigned)(L.nchunks < 256 ? L.nchunks : 256), kRouteThreads, 0, s>>>(
       word_id, N, L.nchunks, P.counts);
-  route_map<<<1, kRouteThreads, 0, s>>>(P.counts, P.map, P.lists);
+  int st = finish_launch();
+  if (st != LDA_OK) return st;
+  // the class counts, read back once: the host assigns the classes and lays
+  // out the lists (whose sizes also size the draw's grid)
+  int32_t counts[kRouteClasses];
+  hipError_t e = hipMemcpyAsync(counts, P.counts, sizeof(counts), hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  if (e != hipSuccess) {
+    g_last_hip = e;
+    return LDA_ERR_HIP;
+  }
+  const RouteAssignment a = route_assign(counts);
+  route_set<<<1, kRouteThreads, 0, s>>>(a, P.map, P.lists);
   route_count<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, N, P.map, P.chunk_off);
   route_scan<<<kRouteXcds, kRouteThreads, 0, s>>>(P.chunk_off, L.nchunks);
   route_scatter<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, doc_id, N, P.map,
                                                               P.chunk_off, P.lists, P.perm,
                                                               P.rword, P.rdoc);
   route_pad<<<kRouteXcds, kRouteThreads, 0, s>>>(P.lists, P.perm, P.rword, P.rdoc);
-  int st = finish_launch();
+  st = finish_launch();
   if (st != LDA_OK) return st;
-  // the list sizes size the draw's grid: read them back once
-  int64_t lists[3 * kRouteXcds];
-  hipError_t e = hipMemcpyAsync(lists, P.lists, sizeof(lists), hipMemcpyDeviceToHost, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
-  if (e != hipSuccess) {
-    g_last_hip = e;
-    return LDA_ERR_HIP;
-  }
+  const int64_t *lists = a.lists;
   route->N = N;
   for (int x = 0; x < kRouteXcds; ++x) {
     route->tokens[x] = lists[x];

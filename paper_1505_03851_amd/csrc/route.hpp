@@ -77,58 +77,57 @@ __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__res
   if (h[threadIdx.x]) atomicAdd(&counts[threadIdx.x], h[threadIdx.x]);
 }
 
-// One workgroup of 256 threads: rank the classes by token count (largest
-// first, ties by class), then assign them in that order, each to the list
-// with the fewest tokens so far (ties: the lowest list), and lay the lists
-// out one after another, each padded to a multiple of 64 positions.
-__global__ __launch_bounds__(kRouteThreads) void route_map(const int32_t *__restrict__ counts,
-                                                           int32_t *map, int64_t *lists) {
-  __shared__ int32_t cnt[kRouteClasses], order[kRouteClasses], sorted[kRouteClasses],
-      xcd[kRouteClasses];
-  const int t = threadIdx.x;
-  const int32_t c = counts[t];
-  cnt[t] = c;
-  __syncthreads();
-  int rank = 0;
-  for (int v = 0; v < kRouteClasses; ++v) {
-    const int32_t cv = cnt[v];
-    rank += (cv > c) || (cv == c && v < t);
-  }
-  order[rank] = t;
-  sorted[rank] = c;
-  __syncthreads();
-  if (t == 0) {
-    // The greedy pass: each step reads its class and count straight from LDS
-    // (no dependence on the earlier steps, so the reads run ahead), and the
-    // list loads stay in registers (at most N < 2^31 tokens).
-    int32_t load[kRouteXcds] = {};
-#pragma unroll 4
-    for (int r = 0; r < kRouteClasses; ++r) {
-      const int cls = order[r];
-      const int32_t cc = sorted[r];
-      int best = 0;
-      int32_t least = load[0];
-#pragma unroll
-      for (int x = 1; x < kRouteXcds; ++x)
-        if (load[x] < least) {
-          least = load[x];
-          best = x;
-        }
-      xcd[cls] = best;
-#pragma unroll
-      for (int x = 0; x < kRouteXcds; ++x) load[x] += x == best ? cc : 0;
+// The class map and the list layout, computed on the host from the class
+// counts (route_assign) and handed to the device as kernel arguments.
+struct RouteAssignment {
+  int32_t map[kRouteClasses];    // XCD of each word class
+  int64_t lists[3 * kRouteXcds];  // tokens[8], start[8], padded length[8]
+};
+
+// Rank the classes by token count (largest first, ties by class), then assign
+// them in that order, each to the list with the fewest tokens so far (ties:
+// the lowest list), and lay the lists out one after another, each padded to
+// a multiple of 64 positions.  (A serial pass of 256 steps: a few
+// microseconds on the host, where one GPU thread took tens.)
+inline RouteAssignment route_assign(const int32_t (&counts)[kRouteClasses]) {
+  int order[kRouteClasses];
+  for (int c = 0; c < kRouteClasses; ++c) order[c] = c;
+  // insertion sort: 256 entries, stable, so equal counts keep class order
+  for (int i = 1; i < kRouteClasses; ++i) {
+    const int c = order[i];
+    int j = i;
+    while (j > 0 && counts[order[j - 1]] < counts[c]) {
+      order[j] = order[j - 1];
+      --j;
     }
-    int64_t start = 0;
-    for (int x = 0; x < kRouteXcds; ++x) {
-      const int64_t len = ((int64_t)load[x] + kRoutePad - 1) / kRoutePad * kRoutePad;
-      lists[x] = load[x];                   // tokens
-      lists[kRouteXcds + x] = start;        // start
-      lists[2 * kRouteXcds + x] = len;      // padded length
-      start += len;
-    }
+    order[j] = c;
   }
-  __syncthreads();
-  map[t] = xcd[t];
+  RouteAssignment a;
+  int64_t load[kRouteXcds] = {};
+  for (int r = 0; r < kRouteClasses; ++r) {
+    const int c = order[r];
+    int best = 0;
+    for (int x = 1; x < kRouteXcds; ++x)
+      if (load[x] < load[best]) best = x;
+    a.map[c] = best;
+    load[best] += counts[c];
+  }
+  int64_t start = 0;
+  for (int x = 0; x < kRouteXcds; ++x) {
+    const int64_t len = (load[x] + kRoutePad - 1) / kRoutePad * kRoutePad;
+    a.lists[x] = load[x];
+    a.lists[kRouteXcds + x] = start;
+    a.lists[2 * kRouteXcds + x] = len;
+    start += len;
+  }
+  return a;
+}
+
+// The assignment into the workspace (one workgroup of 256 threads).
+__global__ __launch_bounds__(kRouteThreads) void route_set(const RouteAssignment a, int32_t *map,
+                                                           int64_t *lists) {
+  map[threadIdx.x] = a.map[threadIdx.x];
+  if (threadIdx.x < 3 * kRouteXcds) lists[threadIdx.x] = a.lists[threadIdx.x];
 }
 
 // Tokens of each list in each chunk of kRouteChunk tokens (the class map in
