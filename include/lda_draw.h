@@ -269,7 +269,7 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * a draw on the same stream follows (a draw on another stream needs the
  * caller's synchronisation).
  *   workspace        device memory, 8-byte aligned, at least
- *                    lda_route_workspace_bytes(N) bytes (about 12 N), owned
+ *                    lda_route_workspace_bytes(N) bytes (about 12.25 N), owned
  *                    by the caller; it holds the routing and must stay
  *                    unchanged until the last lda_draw_routed that uses it.
  *   route            host struct filled on success.

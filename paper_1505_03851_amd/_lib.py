@@ -367,7 +367,7 @@ def route_layout(N: int) -> dict[str, int]:
     off, out = 0, {}
     for name, nbytes in (("perm", 4 * Np), ("rword", 4 * Np), ("rdoc", 4 * Np),
                          ("chunk_off", 32 * nchunks), ("counts", 1024), ("map", 1024),
-                         ("lists", 192)):
+                         ("lists", 192), ("chunk_hist", 1024 * nchunks)):
         out[name] = off
         off += (nbytes + 255) & ~255
     out["bytes"] = off

@@ -341,7 +341,7 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
 // section starting on a 256-byte boundary.
 struct RouteLayout {
   int64_t Np, nchunks;
-  size_t perm, rword, rdoc, chunk_off, counts, map, lists, bytes;
+  size_t perm, rword, rdoc, chunk_off, counts, map, lists, chunk_hist, bytes;
 };
 
 RouteLayout route_layout(int64_t N) {
@@ -361,6 +361,7 @@ RouteLayout route_layout(int64_t N) {
   L.counts = take(4 * kRouteClasses);
   L.map = take(4 * kRouteClasses);
   L.lists = take(8 * 3 * kRouteXcds);
+  L.chunk_hist = take(4 * (size_t)kRouteClasses * (size_t)L.nchunks);
   L.bytes = off;
   return L;
 }
@@ -370,7 +371,8 @@ RoutePlan route_plan(void *ws, const RouteLayout &L) {
   return RoutePlan{reinterpret_cast<int32_t *>(b + L.perm), reinterpret_cast<int32_t *>(b + L.rword),
                    reinterpret_cast<int32_t *>(b + L.rdoc), reinterpret_cast<int32_t *>(b + L.chunk_off),
                    reinterpret_cast<int32_t *>(b + L.counts), reinterpret_cast<int32_t *>(b + L.map),
-                   reinterpret_cast<int64_t *>(b + L.lists)};
+                   reinterpret_cast<int64_t *>(b + L.lists),
+                   reinterpret_cast<int32_t *>(b + L.chunk_hist)};
 }
 
 // K the routed draw takes: the leaf kernel's (K divisible by 4 from
@@ -566,7 +568,7 @@ extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, in
   const hipStream_t s = static_cast<hipStream_t>(stream);
   route_fill<<<1, kRouteClasses, 0, s>>>(P.counts, kRouteClasses, 0);
   route_hist<<<(unsigned)(L.nchunks < 256 ? L.nchunks : 256), kRouteThreads, 0, s>>>(
-      word_id, N, L.nchunks, P.counts);
+      word_id, N, L.nchunks, P.chunk_hist, P.counts);
   int st = finish_launch();
   if (st != LDA_OK) return st;
   // the class counts, read back once: the host assigns the classes and lays
@@ -580,7 +582,7 @@ extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, in
   }
   const RouteAssignment a = route_assign(counts);
   route_set<<<1, kRouteThreads, 0, s>>>(a, P.map, P.lists);
-  route_count<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, N, P.map, P.chunk_off);
+  route_count<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(P.chunk_hist, P.map, P.chunk_off);
   route_scan<<<kRouteXcds, kRouteThreads, 0, s>>>(P.chunk_off, L.nchunks);
   route_scatter<<<(unsigned)L.nchunks, kRouteThreads, 0, s>>>(word_id, doc_id, N, P.map,
                                                               P.chunk_off, P.lists, P.perm,

@@ -43,6 +43,7 @@ struct RoutePlan {
   int32_t *counts;               // [256] tokens per word class
   int32_t *map;                  // [256] XCD of each word class
   int64_t *lists;                // tokens[8], start[8], length[8]
+  int32_t *chunk_hist;           // [nchunks][256] tokens per word class in each chunk
 };
 
 // Fill n ints with v (used instead of a memset so the builder can be captured).
@@ -52,17 +53,21 @@ __global__ void route_fill(int32_t *p, int64_t n, int32_t v) {
     p[i] = v;
 }
 
-// Tokens per word class: each workgroup takes every gridDim.x-th chunk (each
-// thread's loads of a chunk issued before any is used) into an LDS
-// histogram, then adds it to the counts with one atomic per class.
+// Tokens per word class, in each chunk of kRouteChunk tokens and in all:
+// each workgroup takes every gridDim.x-th chunk (each thread's loads of a
+// chunk issued before any is used) into an LDS histogram, writes it out as
+// the chunk's and adds it to its own totals, which it then adds to the counts
+// with one atomic per class.
 __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__restrict__ word,
                                                             int64_t N, int64_t nchunks,
-                                                            int32_t *counts) {
+                                                            int32_t *chunk_hist, int32_t *counts) {
   __shared__ int32_t h[kRouteClasses];
-  h[threadIdx.x] = 0;
+  const int t = threadIdx.x;
+  h[t] = 0;
+  int32_t total = 0;
   __syncthreads();
   for (int64_t ch = blockIdx.x; ch < nchunks; ch += gridDim.x) {
-    const int64_t c0 = ch * kRouteChunk + threadIdx.x;
+    const int64_t c0 = ch * kRouteChunk + t;
     int32_t w[kRoutePer];
 #pragma unroll
     for (int k = 0; k < kRoutePer; ++k) {
@@ -72,9 +77,14 @@ __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__res
 #pragma unroll
     for (int k = 0; k < kRoutePer; ++k)
       if (w[k] >= 0) atomicAdd(&h[route_class(w[k])], 1);
+    __syncthreads();
+    const int32_t v = h[t];
+    chunk_hist[ch * kRouteClasses + t] = v;
+    total += v;
+    h[t] = 0;
+    __syncthreads();
   }
-  __syncthreads();
-  if (h[threadIdx.x]) atomicAdd(&counts[threadIdx.x], h[threadIdx.x]);
+  if (total) atomicAdd(&counts[t], total);
 }
 
 // The class map and the list layout, computed on the host from the class
@@ -130,29 +140,19 @@ __global__ __launch_bounds__(kRouteThreads) void route_set(const RouteAssignment
   if (threadIdx.x < 3 * kRouteXcds) lists[threadIdx.x] = a.lists[threadIdx.x];
 }
 
-// Tokens of each list in each chunk of kRouteChunk tokens (the class map in
-// LDS, every thread's loads issued before any is used).
-__global__ __launch_bounds__(kRouteThreads) void route_count(const int32_t *__restrict__ word,
-                                                             int64_t N,
+// Tokens of each list in each chunk, from the chunk's class histogram (one
+// workgroup per chunk).
+__global__ __launch_bounds__(kRouteThreads) void route_count(const int32_t *__restrict__ chunk_hist,
                                                              const int32_t *__restrict__ map,
                                                              int32_t *chunk_count) {
-  __shared__ int32_t m[kRouteClasses], c[kRouteXcds];
-  m[threadIdx.x] = map[threadIdx.x];
-  if (threadIdx.x < kRouteXcds) c[threadIdx.x] = 0;
-  const int64_t c0 = (int64_t)blockIdx.x * kRouteChunk + threadIdx.x;
-  int32_t w[kRoutePer];
-#pragma unroll
-  for (int k = 0; k < kRoutePer; ++k) {
-    const int64_t i = c0 + (int64_t)k * kRouteThreads;
-    w[k] = i < N ? word[i] : -1;
-  }
+  __shared__ int32_t c[kRouteXcds];
+  const int t = threadIdx.x;
+  if (t < kRouteXcds) c[t] = 0;
   __syncthreads();
-#pragma unroll
-  for (int k = 0; k < kRoutePer; ++k)
-    if (w[k] >= 0) atomicAdd(&c[m[route_class(w[k])]], 1);
+  const int32_t v = chunk_hist[(int64_t)blockIdx.x * kRouteClasses + t];
+  if (v) atomicAdd(&c[map[t]], v);
   __syncthreads();
-  if (threadIdx.x < kRouteXcds)
-    chunk_count[(int64_t)blockIdx.x * kRouteXcds + threadIdx.x] = c[threadIdx.x];
+  if (t < kRouteXcds) chunk_count[(int64_t)blockIdx.x * kRouteXcds + t] = c[t];
 }
 
 // Exclusive prefix over the chunks, in place: workgroup x scans list x.  Each
