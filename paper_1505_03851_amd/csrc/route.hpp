@@ -21,6 +21,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <algorithm>
+
 namespace lda {
 
 constexpr int kRouteXcds = 8;           // lists (XCDs of the MI355X)
@@ -100,22 +102,16 @@ struct RouteAssignment {
 // a multiple of 64 positions.  (A serial pass of 256 steps: a few
 // microseconds on the host, where one GPU thread took tens.)
 inline RouteAssignment route_assign(const int32_t (&counts)[kRouteClasses]) {
-  int order[kRouteClasses];
-  for (int c = 0; c < kRouteClasses; ++c) order[c] = c;
-  // insertion sort: 256 entries, stable, so equal counts keep class order
-  for (int i = 1; i < kRouteClasses; ++i) {
-    const int c = order[i];
-    int j = i;
-    while (j > 0 && counts[order[j - 1]] < counts[c]) {
-      order[j] = order[j - 1];
-      --j;
-    }
-    order[j] = c;
-  }
+  // one 64-bit key per class, (2^31 - 1 - count, class): ascending keys give
+  // the ranking (counts lie in [0, 2^31))
+  uint64_t key[kRouteClasses];
+  for (int c = 0; c < kRouteClasses; ++c)
+    key[c] = ((uint64_t)(uint32_t)(0x7fffffff - counts[c]) << 32) | (uint32_t)c;
+  std::sort(key, key + kRouteClasses);
   RouteAssignment a;
   int64_t load[kRouteXcds] = {};
   for (int r = 0; r < kRouteClasses; ++r) {
-    const int c = order[r];
+    const int c = (int)(key[r] & 0xffffffffu);
     int best = 0;
     for (int x = 1; x < kRouteXcds; ++x)
       if (load[x] < load[best]) best = x;
