@@ -11,6 +11,10 @@ Contents
                         twin for small inputs.
   prefix_np             the full table of partial sums of one token (Fig. 1,
                         left).
+  counts / counts_np    the per-document and per-word topic counts of a set of
+                        draws (the statistics the update of theta and phi
+                        consumes, Section 1), integer and exact; ``counts``
+                        runs the C file, ``counts_np`` is a numpy twin.
   butterfly             the butterfly-patterned table of Section 4, three ways:
                         its closed form, the replacement process that builds it,
                         and a lane-vector simulation of the search over it
@@ -53,6 +57,9 @@ def _load():
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_set_num_threads.restype = None
+    lib.oracle_counts.argtypes = [P, P, P, ctypes.c_int64, ctypes.c_int32,
+                                  ctypes.c_int32, ctypes.c_int32, P, P]
+    lib.oracle_counts.restype = ctypes.c_int64
     _lib = lib
     return lib
 
@@ -126,3 +133,34 @@ def draw_np(theta, phi, doc_id, word_id, u, band_rel: float = BAND_REL):
     z = np.where(hit.any(axis=1), hit.argmax(axis=1), K - 1).astype(np.int32)
     band = (np.abs(stop[:, None] - S) <= band_rel * total[:, None]).any(axis=1)
     return z, band
+
+
+def counts(doc_id, word_id, z, M: int, V: int, K: int):
+    """(ndk int32 [M][K], nwk int32 [V][K]): ndk[d][k] is the number of
+    tokens of document d drawn to topic k, nwk[w][k] the number of tokens of
+    word w drawn to topic k.  A token with an id or topic out of range is not
+    counted."""
+    doc_id = _as(doc_id, np.int32)
+    word_id = _as(word_id, np.int32)
+    z = _as(z, np.int32)
+    N = doc_id.shape[0]
+    assert word_id.shape[0] == N and z.shape[0] == N
+    assert M >= 1 and V >= 1 and K >= 1
+    ndk = np.empty((M, K), dtype=np.int32)
+    nwk = np.empty((V, K), dtype=np.int32)
+    _load().oracle_counts(doc_id.ctypes.data, word_id.ctypes.data, z.ctypes.data,
+                          N, M, V, K, ndk.ctypes.data, nwk.ctypes.data)
+    return ndk, nwk
+
+
+def counts_np(doc_id, word_id, z, M: int, V: int, K: int):
+    """Numpy twin of ``counts``: a histogram of the flat cell index of every
+    counted token."""
+    d = np.asarray(doc_id, np.int64)
+    w = np.asarray(word_id, np.int64)
+    k = np.asarray(z, np.int64)
+    ok = (d >= 0) & (d < M) & (w >= 0) & (w < V) & (k >= 0) & (k < K)
+    d, w, k = d[ok], w[ok], k[ok]
+    ndk = np.bincount(d * K + k, minlength=M * K).reshape(M, K).astype(np.int32)
+    nwk = np.bincount(w * K + k, minlength=V * K).reshape(V, K).astype(np.int32)
+    return ndk, nwk

@@ -15,6 +15,11 @@
  * in_band marks tokens where |stop - S_k| <= band_rel * S_{K-1} for some k:
  * there an fp32 evaluation of the same definition may legitimately land on a
  * neighbouring topic.
+ *
+ * It also counts a set of draws (oracle_counts): the per-document and
+ * per-word topic counts that the update of theta and phi consumes once every
+ * z has been drawn (Section 1: draw z for each word, then update theta and
+ * phi; Section 2: the uncollapsed sampler).  Integer work, exact.
  */
 #include <math.h>
 #include <stdint.h>
@@ -105,4 +110,30 @@ int oracle_draw(const float *theta, const float *phi, const int32_t *doc_id,
         free(S);
     }
     return failed ? -1 : 0;
+}
+
+/*
+ * Topic counts of the draws z[0..N): every token n with 0 <= doc_id[n] < M,
+ * 0 <= word_id[n] < V and 0 <= z[n] < K adds one to ndk[doc_id[n]][z[n]] and
+ * one to nwk[word_id[n]][z[n]]; tokens with an id or topic out of range are
+ * not counted.  ndk is [M][K] and nwk is [V][K] (word-major, the layout of
+ * phi), row-major int32, and are overwritten (zeroed first).  One sequential
+ * pass in token order.  Returns the number of tokens counted.
+ */
+int64_t oracle_counts(const int32_t *doc_id, const int32_t *word_id,
+                      const int32_t *z, int64_t N, int32_t M, int32_t V,
+                      int32_t K, int32_t *ndk, int32_t *nwk)
+{
+    memset(ndk, 0, sizeof(int32_t) * (size_t)M * (size_t)K);
+    memset(nwk, 0, sizeof(int32_t) * (size_t)V * (size_t)K);
+    int64_t counted = 0;
+    for (int64_t n = 0; n < N; ++n) {
+        const int32_t d = doc_id[n], w = word_id[n], k = z[n];
+        if (d < 0 || d >= M || w < 0 || w >= V || k < 0 || k >= K)
+            continue;
+        ndk[(int64_t)d * K + k] += 1;
+        nwk[(int64_t)w * K + k] += 1;
+        ++counted;
+    }
+    return counted;
 }
