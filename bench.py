@@ -45,8 +45,10 @@ def kernel_source_hash() -> str:
 
 
 def routable(K: int) -> bool:
-    """K the routed draw takes (divisible by 4, 132 <= K <= 2048)."""
-    return K % 4 == 0 and 132 <= K <= 2048
+    """K the routed draw takes (divisible by 4, 768 <= K <= 2048: below, the
+    routed draw is refused, being measured slower than the token-order
+    draw)."""
+    return K % 4 == 0 and 768 <= K <= 2048
 
 
 def algorithmic_bytes(c) -> int:
@@ -336,6 +338,34 @@ def k_sweep(args) -> int:
     return 0
 
 
+def route_sweep(args) -> int:
+    """Where routing the tokens to the XCDs pays: the plain draw against the
+    routed draw (routing built once, and rebuilt in every launch) on the
+    16.8M-token corpus at K = 256 ... 2048; one JSON line per K."""
+    import torch
+    from paper_1505_03851_amd.inputs import corpus16M_at, make_corpus
+    for K in (256, 512, 768, 1024, 1536, 2048):
+        c = make_corpus(corpus16M_at(K))
+        dev = upload(c)
+        rec = {"workload": c.name, "N": c.N, "V": c.V, "K": K,
+               "phi_MiB": 4 * c.V * K / 2 ** 20}
+        z_bf = None
+        for kernel in ("butterfly", "routed", "routed+build"):
+            r = measure(c.name, c, dev, kernel, args.steps, args.warmup)
+            z = r.pop("z")
+            if z_bf is None:
+                z_bf = z
+            else:
+                rec[kernel + "_differs_from_butterfly"] = int((z != z_bf).sum())
+            rec[kernel + "_ms"] = r["ms_per_launch"]
+        rec["routed_speedup"] = rec["butterfly_ms"] / rec["routed_ms"]
+        rec["routed_build_speedup"] = rec["butterfly_ms"] / rec["routed+build_ms"]
+        print(json.dumps(rec), flush=True)
+        del dev, c
+        torch.cuda.empty_cache()
+    return 0
+
+
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
     registers or LDS, the alternative rule in LDS), 8-topic leaves, the offsets form of the
@@ -473,6 +503,9 @@ def main() -> int:
     ap.add_argument("--all-configs", action="store_true",
                     help="naive, transposed and butterfly (warm, and cold for the "
                          "butterfly) on every workload; one JSON line each")
+    ap.add_argument("--route-sweep", action="store_true",
+                    help="plain against routed draw on the 16.8M-token corpus at "
+                         "K = 256 ... 2048; one JSON line per K")
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
@@ -519,6 +552,8 @@ def main() -> int:
         return k_sweep(args)
     if args.ablation:
         return ablation(args)
+    if args.route_sweep:
+        return route_sweep(args)
     if args.all_configs:
         return all_configs(args)
     if args.graph:

@@ -254,8 +254,12 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * the tokens of one eighth of the vocabulary, so its L2 serves more of them.
  * The draw is the same per token (Algorithms 7-10 with 16-byte leaf loads);
  * only the grouping of tokens into wavefronts changes.  Routing pays where
- * phi is far larger than the caches (measured on MI355X: 19% at K = 2048 with
- * a 390 MiB phi, 4% at K = 1024) and costs where it is not (K <= 256).
+ * phi is far larger than the caches and costs where phi fits the 256 MiB
+ * MALL.  Measured on MI355X over 16.8M Zipf tokens with V = 100,000 words:
+ * 28% slower than lda_draw_butterfly at K = 256, 3% slower at K = 512, 3%
+ * faster at K = 768, 6% at K = 1024, 11% at K = 2048 (25% on 9.8M tokens
+ * with V = 50,000 at K = 2048); so lda_draw_routed takes K >= LDA_ROUTE_MIN_K
+ * only.
  *
  * lda_route_build: splits the words into 256 classes by a hash, assigns the
  * classes to 8 lists with about equal token counts, and lays the tokens out
@@ -278,8 +282,8 @@ int lda_butterfly_table(const float *theta, const float *phi,
  *
  * lda_draw_routed: the draw of lda_draw_butterfly over routed tokens: z[n]
  * and u[n] are indexed by the original token n.  theta, phi, M, V, K as for
- * lda_draw_butterfly; K must be divisible by 4 with 132 <= K <= 2048, else
- * LDA_ERR_UNSUPPORTED; `route` and `workspace` must come from one
+ * lda_draw_butterfly; K must be divisible by 4 with LDA_ROUTE_MIN_K <= K <=
+ * 2048, else LDA_ERR_UNSUPPORTED (below, use lda_draw_butterfly); `route` and `workspace` must come from one
  * lda_route_build over these N tokens, else LDA_ERR_WORKSPACE.
  *
  * lda_draw_routed_philox: lda_draw_routed with the uniforms generated in the
@@ -288,6 +292,7 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * z except inside the rounding band.
  */
 #define LDA_ROUTE_MAX_N 2147483135LL
+#define LDA_ROUTE_MIN_K 768
 typedef struct lda_route {
   int64_t N;          /* tokens routed */
   int64_t tokens[8];  /* tokens in list x */
@@ -306,6 +311,30 @@ int lda_draw_routed_philox(const float *theta, const float *phi, const void *wor
                            size_t workspace_bytes, const lda_route *route, int32_t *z,
                            int64_t N, int32_t M, int32_t V, int32_t K, uint64_t seed,
                            uint32_t sweep, void *stream);
+
+/*
+ * Topic counts of a set of draws: the statistics the update of theta and
+ * phi consumes once every z has been drawn (Section 1: a topic is drawn for
+ * every word from theta and phi, then theta and phi are updated; Section 2:
+ * the uncollapsed sampler whose draw phase the other entry points perform).
+ *   ndk[d][k] = number of tokens n with doc_id[n] = d and z[n] = k
+ *   nwk[w][k] = number of tokens n with word_id[n] = w and z[n] = k
+ * ndk is int32 [M][K] and nwk int32 [V][K] (word-major, the layout of phi),
+ * row-major device arrays owned by the caller; both are overwritten (zeroed
+ * first, also when N = 0).  doc_id, word_id and z are int32 [N] device
+ * arrays (z typically the output of a draw on the same stream).  A token
+ * whose document, word or topic lies outside [0, M), [0, V) or [0, K) is not
+ * counted.  Integer work: the result is exact and does not depend on the
+ * order of the tokens.  Every pointer 4-byte aligned (LDA_ERR_ALIGN); ndk and
+ * nwk may not be NULL (LDA_ERR_NULL), nor the token arrays when N > 0;
+ * N above LDA_COUNT_MAX_N (counts are int32), K above LDA_MAX_K, or either
+ * table above LDA_MAX_TABLE_BYTES give LDA_ERR_UNSUPPORTED.  Enqueues two
+ * kernels that clear the tables, then one that counts; nothing is allocated.
+ */
+#define LDA_COUNT_MAX_N 2147483647LL
+int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_t *z,
+                     int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk, int32_t *nwk,
+                     void *stream);
 
 /* The W (butterfly width) the library uses for K, or LDA_ERR_UNSUPPORTED /
  * LDA_ERR_SHAPE for a K it rejects. */

@@ -2,7 +2,8 @@
 sums (Steele and Tristan, arXiv 1505.03851).
 
 ``draw_naive``, ``draw_butterfly``, ``draw_transposed``, ``draw_docs``,
-``route_build`` / ``draw_routed`` / ``draw_routed_philox`` and ``butterfly_table`` call the HIP
+``route_build`` / ``draw_routed`` / ``draw_routed_philox``, ``butterfly_table`` and
+``count_topics`` (the topic counts of the draws) call the HIP
 library through its C ABI (``include/lda_draw.h``).  The binding is imported
 on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 """
@@ -10,7 +11,7 @@ on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 _BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "draw_doc_lanes",
             "draw_philox", "philox_uniforms",
             "draw_variant", "VARIANTS",
-            "butterfly_table",
+            "butterfly_table", "count_topics",
             "route_build", "draw_routed", "draw_routed_philox", "route_workspace_bytes", "Route",
             "butterfly_width", "status_string", "version", "LdaError",
             "load", "MAX_K", "MAX_TABLE_BYTES", "STATUS")

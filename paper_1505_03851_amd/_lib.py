@@ -102,6 +102,8 @@ def load() -> ctypes.CDLL:
                                            P, I64, I32, I32, I32, ctypes.c_uint64,
                                            ctypes.c_uint32, P]
     lib.lda_draw_routed_philox.restype = ctypes.c_int
+    lib.lda_count_topics.argtypes = [P, P, P, I64, I32, I32, I32, P, P, P]
+    lib.lda_count_topics.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -341,6 +343,37 @@ def butterfly_table(theta, phi, doc_id, word_id, out=None, stream=None,
             _stream_handle(stream))
     _check(st)
     return out
+
+
+def count_topics(doc_id, word_id, z, M: int, V: int, K: int, ndk=None, nwk=None,
+                 stream=None) -> tuple[torch.Tensor, torch.Tensor]:
+    """(ndk int32 [M][K], nwk int32 [V][K]): the tokens of each document, and
+    of each word, drawn to each topic (lda_count_topics).  ``ndk`` / ``nwk``:
+    optional outputs to overwrite."""
+    _require(doc_id, "doc_id", torch.int32, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    _require(z, "z", torch.int32, 1)
+    N = doc_id.shape[0]
+    if word_id.shape[0] != N or z.shape[0] != N:
+        raise ValueError("doc_id, word_id and z lengths differ")
+    dev = doc_id.device
+    if word_id.device != dev or z.device != dev:
+        raise ValueError("all tensors must be on one device")
+    outs = []
+    for t, name, rows in ((ndk, "ndk", M), (nwk, "nwk", V)):
+        if t is None:
+            t = torch.empty((rows, K), dtype=torch.int32, device=dev)
+        else:
+            _require(t, name, torch.int32, 2)
+            if tuple(t.shape) != (rows, K) or t.device != dev:
+                raise ValueError(f"{name} must be int32[{rows}][{K}] on the tokens' device")
+        outs.append(t)
+    with torch.cuda.device(dev):
+        st = load().lda_count_topics(doc_id.data_ptr(), word_id.data_ptr(), z.data_ptr(), N,
+                                     int(M), int(V), int(K), outs[0].data_ptr(),
+                                     outs[1].data_ptr(), _stream_handle(stream))
+    _check(st)
+    return outs[0], outs[1]
 
 
 def butterfly_width(K: int) -> int:

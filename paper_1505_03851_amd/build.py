@@ -1,4 +1,6 @@
-"""Build the HIP library liblda_draw.so in-tree for gfx950."""
+"""Build the HIP libraries in-tree for gfx950: liblda_draw.so (the draw and
+its C ABI, include/lda_draw.h) and liblda_probe.so (the measurement probes,
+include/lda_probe.h)."""
 from __future__ import annotations
 
 import os
@@ -8,6 +10,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 SRC = os.path.join(PKG, "csrc", "lda_draw.hip")
 LIB = os.path.join(PKG, "liblda_draw.so")
+PROBE_SRC = os.path.join(PKG, "csrc", "probe.hip")
+PROBE_LIB = os.path.join(PKG, "liblda_probe.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [
@@ -27,13 +31,19 @@ FLAGS = [
 ]
 
 
-def build(verbose: bool = False, extra: list[str] | None = None) -> str:
-    cmd = [HIPCC, *FLAGS, *(extra or []), SRC, "-o", LIB + ".tmp"]
+def _compile(src: str, lib: str, verbose: bool, extra: list[str] | None) -> str:
+    cmd = [HIPCC, *FLAGS, *(extra or []), src, "-o", lib + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(LIB + ".tmp", LIB)
-    return LIB
+    os.replace(lib + ".tmp", lib)
+    return lib
+
+
+def build(verbose: bool = False, extra: list[str] | None = None) -> str:
+    """Both libraries; returns the draw library's path."""
+    _compile(PROBE_SRC, PROBE_LIB, verbose, extra)
+    return _compile(SRC, LIB, verbose, extra)
 
 
 if __name__ == "__main__":

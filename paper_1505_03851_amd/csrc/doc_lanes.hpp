@@ -136,7 +136,9 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
     }
     butterfly_block<W>(a, w.r, NoStore{});
     const int j = w.c0 + blk * W + inblock_search<W, false>(a, nullptr, w.r, w.gbase, stop, low, high);
-    if (store) z[n] = j;
+    // (a search ending among the empty topics of block 0, whose rebuilt
+    // prefixes may round above a stop of a few ulps: topic 0)
+    if (store) z[n] = j < 0 ? 0 : j;
   }
 }
 

@@ -14,6 +14,8 @@
 // lda_route_build / lda_draw_routed  tokens routed to the XCDs by word, and
 //                     the leaf kernel drawing them (lda_draw_routed_philox:
 //                     with in-kernel uniforms).
+// lda_count_topics    the per-document and per-word topic counts of a set of
+//                     draws (counts.hpp).
 //
 // Device code: butterfly.hpp (lane exchanges, the butterfly, buffer loads),
 // philox.hpp, sources.hpp (document and uniform sources), tile.hpp (the
@@ -38,6 +40,7 @@
 #include "transposed.hpp"
 #include "table.hpp"
 #include "doc_lanes.hpp"
+#include "counts.hpp"
 
 namespace lda {
 namespace {
@@ -377,8 +380,16 @@ RoutePlan route_plan(void *ws, const RouteLayout &L) {
 
 // K the routed draw takes: the leaf kernel's (K divisible by 4 from
 // LDA_EIGHTHS_MIN_K to LDA_EIGHTHS_MAX_BLOCKS blocks of 256).
+// K the routed draw takes: the eighths kernel's K from LDA_ROUTE_MIN_K up.
+// Routing pays only where phi is far larger than the caches: measured on
+// MI355X over 16.8M Zipf tokens with V = 100,000 words, the routed draw is
+// 28% slower than the token-order draw at K = 256 and 3% at K = 512 (phi of
+// 98 and 195 MiB: it fits the 256 MiB MALL, and the few-documents theta path
+// costs more than routing saves), and 2-11% faster from K = 768 (293 MiB) to
+// 2048 (25% on the Poisson corpus at K = 2048).  Smaller K are refused.
 bool routed_for(int32_t K) {
-  return K % kLeaf == 0 && K >= LDA_EIGHTHS_MIN_K && eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
+  return K % kLeaf == 0 && K >= LDA_ROUTE_MIN_K && K >= LDA_EIGHTHS_MIN_K &&
+         eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
 }
 
 }  // namespace
@@ -659,6 +670,34 @@ extern "C" int lda_draw_routed_philox(const float *theta, const float *phi,
   const lda::UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
   return lda::draw_routed(theta, phi, workspace, workspace_bytes, route, z, us, z, N, M, V, K,
                           stream);
+}
+
+extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_t *z,
+                                int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk,
+                                int32_t *nwk, void *stream) {
+  if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
+  if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
+  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
+    return LDA_ERR_UNSUPPORTED;
+  if (!ndk || !nwk) return LDA_ERR_NULL;
+  if (N > 0 && (!doc_id || !word_id || !z)) return LDA_ERR_NULL;
+  const void *ptrs[] = {ndk, nwk, doc_id, word_id, z};
+  for (const void *p : ptrs)
+    if (reinterpret_cast<uintptr_t>(p) & 3u) return LDA_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t cells[2] = {(int64_t)M * K, (int64_t)V * K};
+  int32_t *tables[2] = {ndk, nwk};
+  for (int t = 0; t < 2; ++t) {
+    const int64_t blocks = (cells[t] / 4 + 255) / 256;
+    count_clear<<<(unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), 256, 0, s>>>(
+        tables[t], cells[t]);
+  }
+  if (N > 0) {
+    const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
+    count_kernel<<<(unsigned)chunks, kCountThreads, 0, s>>>(doc_id, word_id, z, N, M, V, K, ndk,
+                                                            nwk);
+  }
+  return finish_launch();
 }
 
 extern "C" int lda_butterfly_width(int32_t K) {

@@ -313,15 +313,18 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   float low = lo > 0 ? region[(lo - 1) * kWave + lane] : 0.0f;
   float high = region[lo * kWave + lane];
   // Rebuild every token's chosen 32-topic chunk (W = 32 groups) and search it
-  // with Algorithm 10.  Empty topics are never chosen (their prefix equals the
-  // one before them); with S = 0 every comparison fails and the result is K - 1.
+  // with Algorithm 10.  Empty topics have the prefix 0 <= stop, but the
+  // search's rebuilt prefixes (high - y) may round to a tiny nonzero value
+  // there, so a stop of 0 (u = 0) or of a few ulps of S can end the search
+  // among them: the draw is then topic 0 (inside the rounding band).  With
+  // S = 0 every comparison fails and the result is K - 1.
   const Wave<kWave / 2, false> wh = half_wave(w, lane);
   float h[kWave / 2];
   load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
   butterfly_block<kWave / 2>(h, wh.r, NoStore{});
   const int j = c0 + chunk * (kWave / 2) +
                 inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
-  if (store) z[n] = j;
+  if (store) z[n] = j < 0 ? 0 : j;
 }
 
 }  // namespace

@@ -239,11 +239,24 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   const float total = a[G - 1];
   const float stop = total * un;
   float low = 0.0f, high = total;
-  const int q = inblock_search<G, false>(a, nullptr, r, gbase, stop, low, high);
+  int q = inblock_search<G, false>(a, nullptr, r, gbase, stop, low, high);
+  // The search rebuilds prefixes as low + y or high - y.  Where the true
+  // prefix is 0 (up to the first real topic) high - y may round to a tiny
+  // nonzero value, and a stop of 0 (u = 0) or of a few ulps of S may then
+  // end the search in a padding leaf.  The true prefix before the leaf
+  // holding topic 0 is exactly 0, so the search never ends before that leaf,
+  // and from there it scans from exactly 0.
+  if constexpr (PAD) {
+    const int qmin = (-c0) / L;  // leaf holding topic 0
+    if (q <= qmin) {
+      q = qmin;
+      low = 0.0f;
+    }
+  }
   // Leaf q of the lane's own token, scanned from the prefix before it: the
   // first of its L topics whose running sum exceeds stop, else the last.
-  // Padding topics (front of leaf 0 when K < L G) have zero weight and are
-  // never chosen (their running sum is `low`, and stop < low never holds);
+  // Padding topics (front of leaf qmin when L does not divide K) have zero
+  // weight and a running sum of exactly 0 <= stop, so they are never chosen;
   // with S = 0 every comparison fails and the result is K - 1.
   const int tq = c0 + L * q;
   float sum = low;

@@ -136,9 +136,13 @@ void butterfly_kernel(
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   }
-  // Algorithm 10.  Empty topics of block 0 are never chosen: their prefix
-  // equals the prefix before them, which is never above stop >= 0, except
-  // when S = 0, where every comparison fails and the result is K - 1.
+  // Algorithm 10.  Empty topics of block 0 have the prefix 0, which is never
+  // above stop >= 0; but the search rebuilds prefixes as low + y or high - y,
+  // and where the true prefix is 0 the rounding of high - y may leave a tiny
+  // nonzero value, so that a stop of 0 (u = 0) or of a few ulps of S can end
+  // the search among them: the draw is then topic 0 (a result inside the
+  // rounding band).  With S = 0 every comparison fails and the result is
+  // K - 1.
   int j;
   if constexpr (ALT) {
     j = w.c0 + blk * W + inblock_search_alt<W>(region, w.r, w.gbase, stop, low, high);
@@ -152,7 +156,7 @@ void butterfly_kernel(
   } else {
     j = w.c0 + blk * W + inblock_search<W, LDS_TABLE>(a, region, w.r, w.gbase, stop, low, high);
   }
-  if (store) z[n] = j;
+  if (store) z[n] = j < 0 ? 0 : j;
 }
 
 }  // namespace

@@ -59,7 +59,10 @@ __global__ void route_fill(int32_t *p, int64_t n, int32_t v) {
 // each workgroup takes every gridDim.x-th chunk (each thread's loads of a
 // chunk issued before any is used) into an LDS histogram, writes it out as
 // the chunk's and adds it to its own totals, which it then adds to the counts
-// with one atomic per class.
+// with one atomic per class.  A token counts when its index is below N,
+// whatever its word id, exactly as route_scatter places it: the two passes
+// must agree on the token set, or a list would receive more tokens than
+// its counted length.
 __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__restrict__ word,
                                                             int64_t N, int64_t nchunks,
                                                             int32_t *chunk_hist, int32_t *counts) {
@@ -74,11 +77,11 @@ __global__ __launch_bounds__(kRouteThreads) void route_hist(const int32_t *__res
 #pragma unroll
     for (int k = 0; k < kRoutePer; ++k) {
       const int64_t i = c0 + (int64_t)k * kRouteThreads;
-      w[k] = i < N ? word[i] : -1;
+      w[k] = i < N ? word[i] : 0;
     }
 #pragma unroll
     for (int k = 0; k < kRoutePer; ++k)
-      if (w[k] >= 0) atomicAdd(&h[route_class(w[k])], 1);
+      if (c0 + (int64_t)k * kRouteThreads < N) atomicAdd(&h[route_class(w[k])], 1);
     __syncthreads();
     const int32_t v = h[t];
     chunk_hist[ch * kRouteClasses + t] = v;

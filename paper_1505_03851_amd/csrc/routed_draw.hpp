@@ -97,7 +97,8 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
   butterfly_block<kWave / 2>(h, wh.r, NoStore{});
   const int j = c0 + chunk * (kWave / 2) +
                 inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
-  if (store) z[n] = j;
+  // (a search ending among the empty topics: topic 0, as in leaf_eighths_kernel)
+  if (store) z[n] = j < 0 ? 0 : j;
 }
 
 template <int C, int WPB, int WPEU, bool PAD>

@@ -129,6 +129,14 @@ for _K in WIKI_K:
     CONFIGS[f"wiki-shaped-K{_K}"] = wiki_shaped(_K)
 
 
+def corpus16M_at(K: int) -> CorpusConfig:
+    """The 16.8M-token corpus (65,536 documents of 256 tokens, V = 100,000,
+    Zipf s = 1.05) at another topic count K (index 200 + K selects its
+    seeds); used to measure where routing the tokens to the XCDs pays."""
+    base = CONFIGS["corpus16M-K1024"]
+    return dataclasses.replace(base, name=f"corpus16M-sweep-K{K}", index=200 + K, K=K)
+
+
 def _lognormal_lengths(seed, M: int, sigma: float, total: int,
                        max_len: int) -> np.ndarray:
     """M lengths in [1, max_len] summing to exactly `total`: lognormal draws

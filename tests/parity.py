@@ -78,13 +78,43 @@ def run_kernel(kernel: str, dev: dict):
     return z.cpu().numpy()
 
 
-def compare(c, z_gpu, idx=None) -> ParityReport:
-    """Oracle on tokens ``idx`` (all if None) against the GPU's z there."""
+_NAMED = {}
+
+
+def named_corpus(name):
+    """A named workload, kept (with its oracle result, see ``reference``)
+    until another name is asked for: one full-size corpus in memory at a
+    time."""
+    from paper_1505_03851_amd.inputs import make_corpus
+    if name not in _NAMED:
+        _NAMED.clear()
+        _NAMED[name] = {"corpus": make_corpus(name)}
+    return _NAMED[name]["corpus"]
+
+
+def reference(name):
+    """The oracle's z and band flags for every token of the named workload
+    (computed once, then reused by every kernel compared with it)."""
+    c = named_corpus(name)
+    ent = _NAMED[name]
+    if "ref" not in ent:
+        ent["ref"] = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u,
+                                 band_rel=BAND_REL)
+    return ent["ref"]
+
+
+def compare(c, z_gpu, idx=None, ref=None) -> ParityReport:
+    """Oracle on tokens ``idx`` (all if None) against the GPU's z there.
+    ``ref``: the oracle's (z, band) for every token of ``c``, if already
+    computed (``reference``)."""
     if idx is None:
         d, w, u, zg = c.doc_id, c.word_id, c.u, z_gpu
     else:
         d, w, u, zg = c.doc_id[idx], c.word_id[idx], c.u[idx], z_gpu[idx]
-    z_ref, band = oracle.draw(c.theta, c.phi, d, w, u, band_rel=BAND_REL)
+    if ref is not None:
+        z_ref, band = ref if idx is None else (ref[0][idx], ref[1][idx])
+    else:
+        z_ref, band = oracle.draw(c.theta, c.phi, d, w, u, band_rel=BAND_REL)
     mis = zg != z_ref
     hard = mis & ~band
     where = np.nonzero(hard)[0][:5]

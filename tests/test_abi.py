@@ -13,10 +13,14 @@ from conftest import ROOT
 HEADER_DIR = os.path.join(ROOT, "include")
 
 
-def declared_functions():
+# each header and the library that must export what it declares
+HEADER_LIBS = {"lda_draw.h": "liblda_draw.so", "lda_probe.h": "liblda_probe.so"}
+
+
+def declared_functions(header=None):
     names = []
     for fn in sorted(os.listdir(HEADER_DIR)):
-        if fn.endswith(".h"):
+        if fn.endswith(".h") and (header is None or fn == header):
             src = open(os.path.join(HEADER_DIR, fn)).read()
             src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
             names += re.findall(r"^[A-Za-z_][\w\s\*]*?\b(lda_\w+)\s*\(", src,
@@ -36,14 +40,23 @@ def test_header_declares_the_boundary():
         assert must in names
 
 
-def test_every_declared_symbol_is_exported(lib):
-    from paper_1505_03851_amd import _lib
-    out = subprocess.run(["nm", "-D", "--defined-only", _lib.LIB_PATH],
+def test_every_header_has_its_library():
+    assert sorted(f for f in os.listdir(HEADER_DIR) if f.endswith(".h")) == sorted(HEADER_LIBS)
+
+
+@pytest.mark.parametrize("header", sorted(HEADER_LIBS))
+def test_every_declared_symbol_is_exported(header):
+    from paper_1505_03851_amd import _lib, probe
+    loaded = {"lda_draw.h": _lib.load, "lda_probe.h": probe.load}[header]()
+    path = os.path.join(ROOT, "paper_1505_03851_amd", HEADER_LIBS[header])
+    out = subprocess.run(["nm", "-D", "--defined-only", path],
                          capture_output=True, text=True, check=True).stdout
     exported = set(re.findall(r"\bT\s+(\w+)$", out, flags=re.M))
-    for name in declared_functions():
+    names = declared_functions(header)
+    assert names
+    for name in names:
         assert name in exported, name
-        assert getattr(lib, name) is not None
+        assert getattr(loaded, name) is not None
 
 
 def test_status_strings(lib):
@@ -264,8 +277,8 @@ def test_draw_routed_argument_errors(lib, philox):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
     for kw in (dict(n=-1), dict(M=0), dict(V=0), dict(K=0)):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
-    # K: divisible by 4, 132 <= K <= 2048
-    for K in (64, 128, 130, 1023, 2052, 4096):
+    # K: divisible by 4, 768 <= K <= 2048 (routing measured slower below)
+    for K in (64, 128, 130, 256, 512, 764, 766, 1023, 2052, 4096):
         assert run(K=K) == STATUS["LDA_ERR_UNSUPPORTED"], K
     assert run(w=A + 4) == STATUS["LDA_ERR_ALIGN"]
     assert run(wb=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
@@ -279,3 +292,53 @@ def test_draw_routed_argument_errors(lib, philox):
     r.start[7] = 10 ** 9                                      # past the workspace
     assert run() == STATUS["LDA_ERR_WORKSPACE"]
     assert run(n=0, theta=None, phi=None, w=None, u=None, z=None) == 0
+
+
+def test_count_topics_argument_errors(lib):
+    """lda_count_topics rejects bad arguments before any HIP call (calls that
+    pass every check would launch kernels, so none is made here)."""
+    from paper_1505_03851_amd._lib import STATUS, _CONSTS
+
+    def run(d=A, w=A, z=A, N=100, M=3, V=5, K=7, ndk=A, nwk=A):
+        return lib.lda_count_topics(d, w, z, N, M, V, K, ndk, nwk, None)
+    for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert run(K=_CONSTS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert run(N=_CONSTS["LDA_COUNT_MAX_N"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk above 2 GiB
+    assert run(V=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk above 2 GiB
+    for key in ("ndk", "nwk"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert run(N=0, **{key: None}) == STATUS["LDA_ERR_NULL"], key  # tables are cleared
+    for key in ("d", "w", "z"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert run(**{key: A + 2}) == STATUS["LDA_ERR_ALIGN"], key
+    for key in ("ndk", "nwk"):
+        assert run(**{key: A + 1}) == STATUS["LDA_ERR_ALIGN"], key
+
+
+def test_probe_argument_errors():
+    """The probes reject bad arguments before any HIP call."""
+    from paper_1505_03851_amd import probe
+    from paper_1505_03851_amd._lib import STATUS
+    lib = probe.load()
+
+    def floor(N=1000, M=3, V=5, K=64, window=16, wpg=2, wpc=0, **ptr):
+        p = dict(theta=A, phi=A, d=A, w=A, u=A, z=A)
+        p.update(ptr)
+        return lib.lda_probe_draw_floor(p["theta"], p["phi"], p["d"], p["w"], p["u"], p["z"],
+                                        N, M, V, K, window, wpg, wpc, None)
+    for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0)):
+        assert floor(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    for kw in (dict(K=30), dict(K=2052), dict(N=63), dict(window=4), dict(wpg=3),
+               dict(wpc=-1), dict(wpc=33), dict(M=1 << 20, K=1024)):
+        assert floor(**kw) == STATUS["LDA_ERR_UNSUPPORTED"], kw
+    for key in ("theta", "phi", "d", "w", "u", "z"):
+        assert floor(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert floor(**{key: A + 2}) == STATUS["LDA_ERR_ALIGN"], key
+    assert lib.lda_probe_read(A, 4096, 0, A, None) == STATUS["LDA_ERR_SHAPE"]
+    assert lib.lda_probe_read(A, -16, 1, A, None) == STATUS["LDA_ERR_SHAPE"]
+    assert lib.lda_probe_read(A, 0, 1, None, None) == 0             # no-op
+    assert lib.lda_probe_read(None, 4096, 1, A, None) == STATUS["LDA_ERR_NULL"]
+    assert lib.lda_probe_read(A + 4, 4096, 1, A, None) == STATUS["LDA_ERR_ALIGN"]
+    assert lib.lda_probe_read(A, 4100, 1, A, None) == STATUS["LDA_ERR_ALIGN"]

@@ -39,7 +39,8 @@ def test_graph_capture_and_replay(kernel):
     import torch
     import paper_1505_03851_amd as lda
     from paper_1505_03851_amd.inputs import doc_offsets
-    c = make_random(64 * 300 + 17, 200, 3000, 200, seed=5, doc_order="ragged")
+    K = 1000 if kernel == "routed" else 200   # (the routed draw takes K >= 768)
+    c = make_random(64 * 300 + 17, 200, 3000, K, seed=5, doc_order="ragged")
     dev = to_device(c)
     off = torch.from_numpy(doc_offsets(c.doc_id, c.M)).cuda()
     route = lda.route_build(dev["doc_id"], dev["word_id"], c.M, c.V) if kernel == "routed" else None
