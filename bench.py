@@ -4,17 +4,23 @@
 One step = one launch of the draw over every token of the workload (all inputs
 resident in HBM).  The headline workload is the K=1024 corpus (N=16,777,216
 tokens, M=65,536 documents x 256, V=100,000 Zipf(1.05) words); the K=256
-corpus and the naive kernel are reported beside it.
+corpus is reported beside it, and every one of the five workloads is drawn
+and compared with the oracle on every token.
 
-Prints ONE JSON line.  ``roofline.achieved`` is the algorithmic bytes of one
-launch divided by the launch's average duration (HIP events on the launch
-stream); ``roofline.traffic`` is the HBM traffic per launch taken from the
-committed rocprofv3 counter summary, or null when the kernel source changed
-since the counters were collected.
+Prints ONE JSON line.  ``roofline`` sets the draw against the memory floor of
+its own access pattern: ``achieved`` is the launch's algorithmic bytes over
+its average duration (HIP events on the launch stream), ``peak`` the same
+bytes over the average duration of the memory-only probe that moves them in
+the same token order (lda_probe_draw_floor, best of its launch shapes, timed
+in the same run), so ``frac`` = floor time / draw time.  ``traffic`` is the
+bytes the launch moves past L2 (rocprofv3 request-size counters, no
+calibration factor), from the committed counter record while the headline
+kernel's source is unchanged since it was taken, else null.
 """
 from __future__ import annotations
 
 import argparse
+import csv
 import glob
 import hashlib
 import json
@@ -29,17 +35,29 @@ METRIC = ("z draws/sec and achieved HBM GB/s (% of peak) at K=256 and K=1024, "
           "1 MI355X")
 PEAK_HBM_GBPS = 8000.0            # MI355X HBM3E, published
 HEADLINE = "corpus16M-K1024"
-# the device kernel lda_draw_butterfly launches on the headline workload
-HEADLINE_KERNEL = "leaf_eighths_kernel"
 SECOND = "corpus1M-K256"
-COUNTERS = os.path.join(ROOT, "profiles", "butterfly_corpus16M-K1024_counters.json")
-KERNEL_SOURCES = sorted(glob.glob(os.path.join(ROOT, "paper_1505_03851_amd", "csrc", "*.[hc]*")))
+PARITY_WORKLOADS = ("tiny-K32", "corpus1M-K64", "corpus1M-K256", "corpus16M-K1024",
+                    "poisson300-K2048")
+PROFILES = os.path.join(ROOT, "profiles")
+CSRC = os.path.join(ROOT, "paper_1505_03851_amd", "csrc")
+# the device kernel lda_draw_butterfly launches on each timed workload, and
+# the source files it is compiled from
+DEVICE_KERNEL = {HEADLINE: "leaf_eighths_kernel", SECOND: "leaf_group_kernel"}
+_COMMON_SOURCES = ("butterfly.hpp", "philox.hpp", "sources.hpp", "tile.hpp", "tuning.hpp")
+KERNEL_SOURCES = {"leaf_eighths_kernel": _COMMON_SOURCES + ("leaf_eighths.hpp",),
+                  "leaf_group_kernel": _COMMON_SOURCES + ("leaf_group.hpp",)}
 
 
-def kernel_source_hash() -> str:
+def counters_path(workload: str) -> str:
+    return os.path.join(PROFILES, f"butterfly_{workload}_counters.json")
+
+
+def kernel_source_hash(device_kernel: str = "leaf_eighths_kernel") -> str:
+    """sha1 of the files the device kernel is compiled from (in the order
+    listed): a counter record applies while this is unchanged."""
     h = hashlib.sha1()
-    for p in KERNEL_SOURCES:
-        with open(p, "rb") as f:
+    for name in KERNEL_SOURCES[device_kernel]:
+        with open(os.path.join(CSRC, name), "rb") as f:
             h.update(f.read())
     return h.hexdigest()
 
@@ -77,7 +95,18 @@ def upload(c):
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
            "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "philox",
            "routed",
-           "routed+build", "routed-philox")
+           "routed+build", "routed-philox", "floor", "count", "count-clear")
+
+
+def draw_occupancy(K: int) -> tuple[int, int]:
+    """(wavefronts per workgroup, wavefronts per CU) of the kernel
+    lda_draw_butterfly launches for K divisible by 4 (N >= 64): the leaf-group
+    kernel up to K = 256 (2 per workgroup, 3 per SIMD); the leaf-eighths
+    kernel above (4 per workgroup and 2 per SIMD up to 1280 topics, then 2
+    and 4)."""
+    if K <= 256:
+        return 2, 12
+    return (4, 8) if K <= 1280 else (2, 16)
 PHILOX_SEED = 0x5EED20150513
 
 
@@ -86,6 +115,7 @@ def launcher(kernel: str, dev):
     "routed" draws the tokens routed to the XCDs with the routing built once
     beforehand (as a sampler does once per corpus); "routed+build" builds the
     routing again in every launch (one stream synchronisation inside)."""
+    import torch
     import paper_1505_03851_amd as lda
     th, ph, d, w, u = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
     if kernel == "routed":
@@ -108,6 +138,25 @@ def launcher(kernel: str, dev):
             r = lda.route_build(d, w, th.shape[0], ph.shape[0], workspace=ws, stream=stream)
             lda.draw_routed(th, ph, r, u, out=out, stream=stream)
         return build_and_draw
+    if kernel == "floor":
+        from paper_1505_03851_amd import probe
+        window, wpg, wpc = dev.get("floor_cfg") or (16,) + draw_occupancy(th.shape[1])
+        return lambda out, stream: probe.draw_floor(th, ph, d, w, u, out, window=window,
+                                                    waves_per_group=wpg, waves_per_cu=wpc,
+                                                    stream=stream)
+    if kernel in ("count", "count-clear"):
+        M, V, K = th.shape[0], ph.shape[0], th.shape[1]
+        if "z_draw" not in dev:
+            dev["z_draw"] = lda.draw_butterfly(th, ph, d, w, u)
+            dev["ndk"] = torch.empty((M, K), dtype=torch.int32, device=d.device)
+            dev["nwk"] = torch.empty((V, K), dtype=torch.int32, device=d.device)
+        zd, ndk, nwk = dev["z_draw"], dev["ndk"], dev["nwk"]
+        if kernel == "count-clear":     # the tables cleared, no token counted
+            e = d[:0]
+            return lambda out, stream: lda.count_topics(e, e, e, M, V, K, ndk=ndk, nwk=nwk,
+                                                        stream=stream)
+        return lambda out, stream: lda.count_topics(d, w, zd, M, V, K, ndk=ndk, nwk=nwk,
+                                                    stream=stream)
     if kernel == "philox":
         return lambda out, stream: lda.draw_philox(th, ph, d, w, PHILOX_SEED, 0, out=out,
                                                    stream=stream)
@@ -153,19 +202,24 @@ def time_kernel(kernel: str, dev, steps: int, warmup: int, flush=None):
     return wall, [s.elapsed_time(e) for s, e in ev], z
 
 
+def count_bytes(c) -> int:
+    """Bytes the topic counts must move: each token's doc id, word id and z
+    read (12), both tables written whole (4 (M + V) K)."""
+    return 12 * c.N + 4 * (c.M + c.V) * c.K
+
+
 def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None) -> dict:
     wall, per_ms, z = time_kernel(kernel, dev, steps, warmup, flush)
     avg_ms = sum(per_ms) / len(per_ms)
     srt = sorted(per_ms)
     med_ms = srt[len(srt) // 2]
-    b_alg = algorithmic_bytes(c)
+    b_alg = count_bytes(c) if kernel.startswith("count") else algorithmic_bytes(c)
     gbps = b_alg / (avg_ms * 1e-3) / 1e9
     tag = " cold" if flush is not None else ""
     print(f"[bench] {name} {kernel}{tag}: {avg_ms:.3f} ms/launch "
           f"(median {med_ms:.3f}, min {srt[0]:.3f}, max {srt[-1]:.3f}), "
-          f"{c.N / (avg_ms * 1e-3) / 1e9:.3f} G draws/s, "
-          f"{gbps:.0f} GB/s algorithmic ({100 * gbps / PEAK_HBM_GBPS:.1f}% of "
-          f"8 TB/s)", file=sys.stderr, flush=True)
+          f"{c.N / (avg_ms * 1e-3) / 1e9:.3f} G tokens/s, "
+          f"{gbps:.0f} GB/s of algorithmic bytes", file=sys.stderr, flush=True)
     return {
         "workload": name, "kernel": kernel + ("-cold" if flush is not None else ""),
         "N": c.N, "K": c.K, "steps": steps, "wall_s": wall,
@@ -173,9 +227,38 @@ def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None)
         "ms_per_launch_min": srt[0], "ms_per_launch_max": srt[-1],
         "draws_per_s": c.N / (avg_ms * 1e-3),
         "alg_bytes_per_launch": b_alg,
-        "alg_GBps": gbps, "frac_of_hbm_peak": gbps / PEAK_HBM_GBPS,
+        "alg_GBps": gbps,
         "z": z,
     }
+
+
+MALL_PROBE_BYTES = 192 << 20   # above the 8 x 4 MiB of L2, inside the 256 MiB MALL
+MALL_PROBE_PASSES = 8
+HBM_PROBE_BYTES = 4 << 30     # 16x the MALL
+
+
+def read_ceiling(nbytes: int, passes: int, steps: int = 10) -> tuple[float, float]:
+    """(ms per launch, GB/s) of the streaming-read probe over ``nbytes``,
+    ``passes`` times per launch (median of ``steps`` HIP-event-timed
+    launches after two warm-up launches)."""
+    import torch
+    from paper_1505_03851_amd import probe
+    buf = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    out = torch.empty(probe.READ_OUT_FLOATS, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+    for _ in range(2):
+        probe.read(buf, passes, out, stream=stream)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
+    for a, b in ev:
+        a.record(stream)
+        probe.read(buf, passes, out, stream=stream)
+        b.record(stream)
+    torch.cuda.synchronize()
+    ms = sorted(a.elapsed_time(b) for a, b in ev)[steps // 2]
+    del buf, out
+    torch.cuda.empty_cache()
+    return ms, nbytes * passes / (ms * 1e-3) / 1e9
 
 
 def device_copy_GBps(steps: int = 10) -> float:
@@ -200,24 +283,24 @@ def device_copy_GBps(steps: int = 10) -> float:
     return 2 * 4 * n / (ms * 1e-3) / 1e9
 
 
-def traffic_from_counters():
-    """HBM bytes per launch from the committed counter summary, if it was
-    taken on the current kernel source."""
+def traffic_from_counters(workload: str):
+    """Bytes per launch that the headline kernel moves past L2 (read +
+    written), from the committed counter record, if it was taken on the
+    kernel's current source; else None."""
     try:
-        with open(COUNTERS) as f:
+        with open(counters_path(workload)) as f:
             rec = json.load(f)
     except (OSError, ValueError):
         return None
-    if rec.get("kernel_source_sha1") != kernel_source_hash():
+    if rec.get("kernel_source_sha1") != kernel_source_hash(rec.get("device_kernel", "")):
         return None
-    return rec.get("hbm_bytes_per_launch")
+    return rec.get("egress_bytes_per_launch")
 
 
 def _counter_means(d: str, kernel_substr: str) -> dict:
     """Mean per-dispatch value of each counter in a rocprofv3 --pmc csv
     directory, over the dispatches whose kernel name contains
     ``kernel_substr`` (per-dispatch values are summed over instances)."""
-    import csv
     per = {}
     for path in glob.glob(os.path.join(d, "*counter_collection.csv")):
         with open(path) as f:
@@ -229,35 +312,58 @@ def _counter_means(d: str, kernel_substr: str) -> dict:
     out = {}
     for (name, _), v in per.items():
         out.setdefault(name, []).append(v)
+    if not out:
+        raise SystemExit(f"no dispatch of {kernel_substr!r} in {d}")
     return {k: sum(v) / len(v) for k, v in out.items()}
 
 
-def counters_summary(args) -> int:
-    """Turn rocprofv3 counter runs of the draw's kernel (dispatches whose name
-    contains ``--kernel-name``) and of the 1 GiB copy into the record
-    ``traffic_from_counters`` reads."""
-    kname = args.kernel_name
-    copy = "copyBuffer"
-    fetch = _counter_means(args.fetch, kname)["FETCH_SIZE"]
-    write = _counter_means(args.write, kname)["WRITE_SIZE"]
-    copy_fetch = _counter_means(args.copy_fetch, copy)["FETCH_SIZE"]
-    copy_write = _counter_means(args.copy_write, copy)["WRITE_SIZE"]
-    copy_kib = (1 << 30) / 1024
-    f_scale, w_scale = copy_kib / copy_fetch, copy_kib / copy_write
+# rocprofv3 counter passes of one kernel (at most 4 TCC counters per pass)
+PASS_READS = ("TCC_EA0_RDREQ_32B_sum", "TCC_EA0_RDREQ_64B_sum", "TCC_EA0_RDREQ_128B_sum",
+              "TCC_EA0_RDREQ_sum")
+PASS_DRAM = ("TCC_EA0_RDREQ_DRAM_32B_sum", "TCC_EA0_WRREQ_WRITE_DRAM_32B_sum",
+             "TCC_EA0_WRREQ_sum", "TCC_EA0_WRREQ_64B_sum")
+PASS_HIT = ("TCC_HIT_sum", "TCC_MISS_sum", "TCP_TCC_READ_REQ_sum", "SQ_INSTS_VMEM_RD")
+
+
+def egress_record(reads: str, dram: str, kname: str, hit: str | None = None) -> dict:
+    """Bytes that dispatches of ``kname`` move past L2, from the request-size
+    counters: read = 32 n32 + 64 n64 + 128 n128 (the three sizes must add up
+    to all read requests); written = 32 (all - n64) + 64 n64.  Cross-check:
+    the DRAM-side counters count the same reads and writes in 32-byte units."""
+    r = _counter_means(reads, kname)
+    d = _counter_means(dram, kname)
+    n32, n64, n128 = (r["TCC_EA0_RDREQ_32B_sum"], r["TCC_EA0_RDREQ_64B_sum"],
+                      r["TCC_EA0_RDREQ_128B_sum"])
     rec = {
-        "kernel": "butterfly", "device_kernel": kname, "workload": args.workload,
-        "kernel_source_sha1": kernel_source_hash(),
-        "fetch_kib_per_dispatch": fetch, "write_kib_per_dispatch": write,
-        "copy_1GiB_fetch_kib": copy_fetch, "copy_1GiB_write_kib": copy_write,
-        "fetch_scale": f_scale, "write_scale": w_scale,
-        "hbm_bytes_per_launch": 1024 * (fetch * f_scale + write * w_scale),
+        "read_requests": {"32B": n32, "64B": n64, "128B": n128,
+                          "all": r["TCC_EA0_RDREQ_sum"]},
+        "read_sizes_cover_all_requests": (n32 + n64 + n128) / max(r["TCC_EA0_RDREQ_sum"], 1),
+        "bytes_read": 32 * n32 + 64 * n64 + 128 * n128,
+        "bytes_read_dram_side": 32 * d["TCC_EA0_RDREQ_DRAM_32B_sum"],
+        "bytes_written": 32 * (d["TCC_EA0_WRREQ_sum"] - d["TCC_EA0_WRREQ_64B_sum"]) +
+                         64 * d["TCC_EA0_WRREQ_64B_sum"],
+        "bytes_written_dram_side": 32 * d["TCC_EA0_WRREQ_WRITE_DRAM_32B_sum"],
     }
-    if args.hitmiss:
-        hm = _counter_means(args.hitmiss, kname)
-        rec["tcc_hit_per_dispatch"] = hm["TCC_HIT_sum"]
-        rec["tcc_miss_per_dispatch"] = hm["TCC_MISS_sum"]
-        rec["tcc_hit_rate"] = hm["TCC_HIT_sum"] / (hm["TCC_HIT_sum"] + hm["TCC_MISS_sum"])
-    with open(args.out, "w") as f:
+    rec["egress_bytes_per_launch"] = rec["bytes_read"] + rec["bytes_written"]
+    if hit:
+        h = _counter_means(hit, kname)
+        rec["tcc_hit_rate"] = h["TCC_HIT_sum"] / (h["TCC_HIT_sum"] + h["TCC_MISS_sum"])
+        rec["l1_to_l2_read_requests"] = h["TCP_TCC_READ_REQ_sum"]
+        rec["vector_load_instructions"] = h["SQ_INSTS_VMEM_RD"]
+        rec["l2_requests_per_load"] = h["TCP_TCC_READ_REQ_sum"] / max(h["SQ_INSTS_VMEM_RD"], 1)
+    return rec
+
+
+def counters_summary(args) -> int:
+    """The counter record of the draw on one workload (--workload), from the
+    csv directories of its three counter passes (--reads, --dram, --hitmiss);
+    ``traffic_from_counters`` reads it back."""
+    kname = DEVICE_KERNEL[args.workload]
+    rec = {"kernel": "butterfly", "device_kernel": kname, "workload": args.workload,
+           "kernel_source_sha1": kernel_source_hash(kname)}
+    rec.update(egress_record(args.reads, args.dram, kname, args.hitmiss))
+    out = args.out or counters_path(args.workload)
+    with open(out, "w") as f:
         json.dump(rec, f, indent=1)
         f.write("\n")
     print(json.dumps(rec, indent=1))
@@ -299,6 +405,7 @@ def cpu_baseline(c, z_gpu, sample: int) -> dict:
     z_chk, band = oracle.draw(c.theta, c.phi, d, w, u, with_band=True)
     mism = zg != z_chk
     return {
+        "_ref": (z_chk, band),
         "value": n / dt, "unit": "draws/s", "cores": threads,
         "kind": "oracle",
         "sample": f"first {n} tokens of {c.name} (K={c.K}), fp64 oracle, "
@@ -351,6 +458,9 @@ def route_sweep(args) -> int:
                "phi_MiB": 4 * c.V * K / 2 ** 20}
         z_bf = None
         for kernel in ("butterfly", "routed", "routed+build"):
+            if kernel != "butterfly" and not routable(K):
+                rec[kernel + "_ms"] = None      # refused below K = 768
+                continue
             r = measure(c.name, c, dev, kernel, args.steps, args.warmup)
             z = r.pop("z")
             if z_bf is None:
@@ -358,8 +468,9 @@ def route_sweep(args) -> int:
             else:
                 rec[kernel + "_differs_from_butterfly"] = int((z != z_bf).sum())
             rec[kernel + "_ms"] = r["ms_per_launch"]
-        rec["routed_speedup"] = rec["butterfly_ms"] / rec["routed_ms"]
-        rec["routed_build_speedup"] = rec["butterfly_ms"] / rec["routed+build_ms"]
+        if routable(K):
+            rec["routed_speedup"] = rec["butterfly_ms"] / rec["routed_ms"]
+            rec["routed_build_speedup"] = rec["butterfly_ms"] / rec["routed+build_ms"]
         print(json.dumps(rec), flush=True)
         del dev, c
         torch.cuda.empty_cache()
@@ -480,6 +591,276 @@ def graph_timing(args) -> int:
     return 0
 
 
+# ---------------------------------------------------------------------------
+# Profiling: the rocprofv3 runs behind profiles/, and the reductions of their
+# csv files into the committed summaries.
+
+# label -> (substring of the device kernel's name, bench.py arguments)
+PROFILE_TARGETS = {
+    "copy": ("copyBuffer", ["--copy"]),
+    "hbm_read": ("read_kernel", ["--ceiling", "hbm", "--steps", "3"]),
+    "mall_read": ("read_kernel", ["--ceiling", "mall", "--steps", "3"]),
+    "draw_K1024": ("leaf_eighths_kernel", ["--only", "butterfly", "--workload", HEADLINE,
+                                           "--steps", "3", "--warmup", "1"]),
+    "floor_K1024": ("floor_kernel", ["--only", "floor", "--floor-config", "8,4,8",
+                                     "--workload", HEADLINE, "--steps", "3", "--warmup", "1"]),
+    "naive_K1024": ("naive_kernel", ["--only", "naive", "--workload", HEADLINE,
+                                     "--steps", "2", "--warmup", "0"]),
+    "count_K1024": ("count_kernel", ["--only", "count", "--workload", HEADLINE,
+                                     "--steps", "3", "--warmup", "1"]),
+    "draw_K256": ("leaf_group_kernel", ["--only", "butterfly", "--workload", SECOND,
+                                        "--steps", "3", "--warmup", "1"]),
+    "floor_K256": ("floor_kernel", ["--only", "floor", "--floor-config", "16,2,0",
+                                    "--workload", SECOND, "--steps", "3", "--warmup", "1"]),
+    "naive_K256": ("naive_kernel", ["--only", "naive", "--workload", SECOND,
+                                    "--steps", "3", "--warmup", "1"]),
+    "draw_K2048": ("leaf_eighths_kernel", ["--only", "butterfly", "--workload",
+                                           "poisson300-K2048", "--steps", "3", "--warmup", "1"]),
+    "routed_K1024": ("routed_eighths_kernel", ["--only", "routed", "--workload", HEADLINE,
+                                               "--steps", "3", "--warmup", "1"]),
+}
+PROFILE_PASSES = {"reads": PASS_READS, "dram": PASS_DRAM, "hit": PASS_HIT}
+
+
+def profile_commands(d: str) -> list[str]:
+    """The shell commands (repo root on the GPU machine) that take every counter
+    pass of every target into ``d``, and the kernel trace of the default
+    bench run; each rocprofv3 run under its own time limit."""
+    cmds = ["cd /tmp && export TMPDIR=/tmp && cd \"$GRAFT_REPO_ROOT\" && "
+            "export LDA_INPUT_CACHE=/tmp/lda_inputs"]
+    for label, (_, bargs) in PROFILE_TARGETS.items():
+        for pn, ctr in PROFILE_PASSES.items():
+            out = f"{d}/{label}_{pn}"
+            cmds.append(f"timeout -s KILL 300 rocprofv3 --pmc {' '.join(ctr)} -f csv -d {out} "
+                        f"-o c -- python -u bench.py {' '.join(bargs)} > {out}.log 2>&1")
+    cmds.append(f"timeout -k 10 600 rocprofv3 --kernel-trace --stats -f csv -d {d}/trace -o t "
+                f"-- python -u bench.py > {d}/trace.log 2>&1")
+    return cmds
+
+
+def _bench_lines(path: str) -> list[dict]:
+    with open(path) as f:
+        return [json.loads(ln) for ln in f if ln.startswith("{")]
+
+
+def _fmt_bytes(b):
+    return "-" if b is None else f"{b / 1e9:10.3f}"
+
+
+def report_counters(d: str, out_txt: str) -> int:
+    """profiles/counters_all_kernels.txt, and the counter records of the draw
+    on the two timed workloads, from the counter passes in ``d``."""
+    rows = []
+    for label, (kname, bargs) in PROFILE_TARGETS.items():
+        if not os.path.isdir(f"{d}/{label}_reads"):
+            continue
+        rec = egress_record(f"{d}/{label}_reads", f"{d}/{label}_dram", kname,
+                            f"{d}/{label}_hit" if os.path.isdir(f"{d}/{label}_hit") else None)
+        lines = _bench_lines(f"{d}/{label}_reads.log")
+        ms = None
+        if lines:
+            ms = lines[-1].get("ms_per_launch") or lines[-1].get("ms_per_launch_median")
+        if label.startswith("draw_K") and kname in DEVICE_KERNEL.values():
+            wl = bargs[bargs.index("--workload") + 1]
+            if DEVICE_KERNEL.get(wl) == kname:
+                full = {"kernel": "butterfly", "device_kernel": kname, "workload": wl,
+                        "kernel_source_sha1": kernel_source_hash(kname)}
+                full.update(rec)
+                with open(counters_path(wl), "w") as f:
+                    json.dump(full, f, indent=1)
+                    f.write("\n")
+        rows.append((label, kname, ms, rec))
+    L = ["rocprofv3 counters per dispatch: bytes moved past L2, by request size (no calibration factor)",
+         "",
+         "commands (repo root on the GPU box), one run per target and pass:",
+         *("  " + c for c in profile_commands(d)[:1]),
+         "  timeout -s KILL 300 rocprofv3 --pmc <pass counters> -f csv -d <dir>/<target>_<pass> -o c "
+         "-- python -u bench.py <target args>",
+         "passes:",
+         *(f"  {pn:5s} {' '.join(c)}" for pn, c in PROFILE_PASSES.items()),
+         "targets:",
+         *(f"  {lb:12s} {k:22s} bench.py {' '.join(a)}" for lb, (k, a) in PROFILE_TARGETS.items()),
+         f"reduced by: python bench.py --report-counters {d} --out {os.path.relpath(out_txt, ROOT)}",
+         "",
+         "read bytes  = 32 n(32 B) + 64 n(64 B) + 128 n(128 B) requests (TCC_EA0_RDREQ_{32B,64B,128B});",
+         "  'sizes/all' = their count over all read requests (TCC_EA0_RDREQ): 1 means no request is",
+         "  left out; 'DRAM-side' = 32 x TCC_EA0_RDREQ_DRAM_32B, the same reads counted by the",
+         "  memory side in 32-byte units (the MALL is on that side: its hits are included);",
+         "written bytes = 32 (all - n64) + 64 n64 (TCC_EA0_WRREQ, TCC_EA0_WRREQ_64B; atomics travel",
+         "  over the same interface and count here);",
+         "GB/s = (read + written) / the launch time of the same run (HIP events; under the profiler)",
+         "",
+         f"{'target':12s} {'kernel':22s} {'read GB':>10s} {'sizes/all':>9s} {'DRAM-side':>10s} "
+         f"{'written GB':>10s} {'ms':>8s} {'GB/s':>7s} {'L2 hit':>6s} {'L2 req/load':>11s}"]
+    for label, kname, ms, r in rows:
+        gbps = (r["egress_bytes_per_launch"] / (ms * 1e-3) / 1e9) if ms else None
+        L.append(f"{label:12s} {kname:22s} {_fmt_bytes(r['bytes_read'])} "
+                 f"{r['read_sizes_cover_all_requests']:9.4f} {_fmt_bytes(r['bytes_read_dram_side'])} "
+                 f"{_fmt_bytes(r['bytes_written'])} {ms if ms else float('nan'):8.3f} "
+                 f"{gbps if gbps else float('nan'):7.0f} "
+                 f"{r.get('tcc_hit_rate', float('nan')):6.3f} "
+                 f"{r.get('l2_requests_per_load', float('nan')):11.2f}")
+    with open(out_txt, "w") as f:
+        f.write("\n".join(L) + "\n")
+    print("\n".join(L))
+    return 0
+
+
+def report_trace(d: str, bench_log: str, out_txt: str) -> int:
+    """profiles/kernel_trace_bench.txt: rocprofv3's kernel statistics of the
+    default bench run, beside the HIP-event averages bench.py measured for
+    the same launches."""
+    stats = glob.glob(os.path.join(d, "*kernel_stats.csv"))
+    if not stats:
+        raise SystemExit(f"no kernel_stats.csv in {d}")
+    with open(stats[0]) as f:
+        rows = list(csv.DictReader(f))
+    head = _bench_lines(bench_log)[-1]
+    L = ["rocprofv3 kernel trace of the default benchmark run (every workload, every kernel)",
+         "",
+         "command (repo root on the GPU box):",
+         f"  {profile_commands(d)[-1]}",
+         f"reduced by: python bench.py --report-trace {d} --bench-log {bench_log} "
+         f"--out {os.path.relpath(out_txt, ROOT)}",
+         "",
+         f"{'kernel':70s} {'calls':>6s} {'avg ms':>9s} {'min ms':>9s} {'max ms':>9s}"]
+    for r in sorted(rows, key=lambda r: -float(r["TotalDurationNs"])):
+        name = r["Name"].replace("(anonymous namespace)::", "")
+        short = (name[5:] if name.startswith("void ") else name).split("(")[0]
+        L.append(f"{short[:70]:70s} {int(r['Calls']):6d} {float(r['AverageNs']) / 1e6:9.4f} "
+                 f"{float(r['MinNs']) / 1e6:9.4f} {float(r['MaxNs']) / 1e6:9.4f}")
+    L += ["", "bench.py's HIP-event averages in the same run (ms per launch):"]
+    for r in head["results"]:
+        L.append(f"  {r['workload']:20s} {r['kernel']:16s} {r['ms_per_launch']:9.4f}")
+    for w, f_ in head["floor"].items():
+        L.append(f"  {w:20s} {'floor (best)':16s} {f_['ms']:9.4f}  ({f_['shape']})")
+    with open(out_txt, "w") as f:
+        f.write("\n".join(L) + "\n")
+    print("\n".join(L))
+    return 0
+
+
+def report_bench(log: str, out_txt: str) -> int:
+    """profiles/bench_roofline_parity.txt: the default run's JSON line --
+    roofline, floors, ceilings, parity on every workload, CPU baseline."""
+    r = _bench_lines(log)[-1]
+    ro = r["roofline"]
+    L = ["The default benchmark run: roofline against the draw's memory floor, ceilings, parity",
+         "",
+         "command (repo root on the GPU box):",
+         f"  python -u bench.py > {log}",
+         f"reduced by: python bench.py --report-bench {log} --out {os.path.relpath(out_txt, ROOT)}",
+         "",
+         f"headline {r['config']['workload']} (N={r['config']['N']:,}, K={r['config']['K']}): "
+         f"{r['value'] / 1e9:.3f} G draws/s, {r['ms_per_step']:.3f} ms per step",
+         f"  roofline: achieved {ro['achieved']:,.0f} GB/s (algorithmic bytes / draw time), "
+         f"peak {ro['peak']:,.0f} GB/s (the same bytes / floor time), frac {ro['frac']:.3f}",
+         f"  bytes past L2 per launch (counters): "
+         + (f"{ro['traffic'] / 1e9:.2f} GB = {ro['traffic_GBps']:,.0f} GB/s"
+            if ro.get("traffic") else "null (no counter record for the current source)"),
+         f"  effective {r['effective_GBps']:,.0f} GB/s = {r['effective_frac_of_hbm_peak']:.2f} x "
+         f"the {r['hbm_peak_GBps']:,.0f} GB/s HBM peak (L2 and the MALL serve re-read rows)",
+         "",
+         "floors (memory-only probe of the same access pattern, fastest launch shape):"]
+    for w, f in r["floor"].items():
+        L.append(f"  {w:18s} floor {f['ms']:8.4f} ms ({f['shape']})  draw {f['draw_ms']:8.4f} ms  "
+                 f"floor/draw {f['frac_of_floor']:.3f}")
+    shapes = r.get("floors", {})
+    for w, f in shapes.items():
+        L.append(f"  {w:18s} shapes: " + ", ".join(f"{k} {v:.4f}" for k, v in f["shapes_ms"].items()))
+    c = r["ceilings"]
+    L += ["", "ceilings measured in the same run:",
+          f"  streaming read from HBM   {c['hbm_read_GBps']:8,.0f} GB/s  ({c['hbm_read']})",
+          f"  streaming read, MALL      {c['mall_read_GBps']:8,.0f} GB/s  ({c['mall_read']})",
+          f"  device copy (read+write)  {c['device_copy_GBps']:8,.0f} GB/s",
+          "", f"topic counts (lda_count_topics) ms per call: " +
+          ", ".join(f"{k} {v:.4f}" for k, v in r["count_topics_ms"].items()),
+          "", "parity on every token against the oracle (band |u S - S_k| <= 1e-5 S):",
+          f"  {'workload':28s} {'tokens':>10s} {'mismatches':>10s} {'rate':>9s} "
+          f"{'outside band':>12s} {'in-band rate':>12s}"]
+    for w, p in r["parity"].items():
+        L.append(f"  {w:28s} {p['tokens']:10d} {p['mismatches']:10d} {p['mismatch_rate']:9.2e} "
+                 f"{p['mismatches_outside_band']:12d} {p['in_band_rate']:12.2e}")
+    b = r["cpu_baseline"]
+    L += ["", f"CPU baseline (the oracle, {b['cores']} threads, {b.get('cpu', '')}): "
+              f"{b['value'] / 1e6:.1f} M draws/s on {b['sample']}; one thread "
+              f"{b['single_thread']['value'] / 1e6:.2f} M draws/s ({b['single_thread']['sample']})"]
+    with open(out_txt, "w") as f:
+        f.write("\n".join(L) + "\n")
+    print("\n".join(L))
+    return 0
+
+
+def report_jsonl(log: str, out_txt: str, title: str, command: str) -> int:
+    """A table of the JSON lines a bench.py mode printed (one row per line,
+    one column per numeric field)."""
+    lines = _bench_lines(log)
+    if not lines:
+        raise SystemExit(f"no JSON lines in {log}")
+    keys = []
+    for r in lines:
+        for k, v in r.items():
+            if k not in keys and (isinstance(v, (int, float)) or k == "workload"):
+                keys.append(k)
+    L = [title, "", "command (repo root on the GPU box):", f"  {command} > {log}",
+         f"reduced by: python bench.py --report-jsonl {log} --out {os.path.relpath(out_txt, ROOT)} "
+         "--title ... --command ...", ""]
+    for r in lines:
+        L.append(r.get("workload", "") + ":")
+        for k in keys:
+            if k == "workload" or k not in r:
+                continue
+            v = r[k]
+            L.append(f"  {k:40s} {v:.6g}" if isinstance(v, float) else f"  {k:40s} {v}")
+    with open(out_txt, "w") as f:
+        f.write("\n".join(L) + "\n")
+    print("\n".join(L))
+    return 0
+
+
+def floor_configs(K: int):
+    """Launch shapes of the floor probe tried for K: window 8 or 16, 2 or 4
+    wavefronts per workgroup, no occupancy cap or the draw's."""
+    wpg, wpc = draw_occupancy(K)
+    return [(w, g, c) for w in (8, 16) for g in (2, 4) for c in (0, wpc)]
+
+
+def measure_floor(name: str, c, dev, steps: int, warmup: int) -> dict:
+    """The memory-only floor of the draw on this workload: every launch shape
+    of ``floor_configs`` timed, the fastest kept."""
+    shapes = {}
+    for cfg in floor_configs(c.K):
+        dev["floor_cfg"] = cfg
+        r = measure(name, c, dev, "floor", steps, warmup)
+        r.pop("z")
+        shapes["w{}-g{}-c{}".format(*cfg)] = r["ms_per_launch"]
+    best = min(shapes, key=shapes.get)
+    dev.pop("floor_cfg")
+    return {"ms_per_launch": shapes[best], "shape": best, "shapes_ms": shapes,
+            "alg_GBps": algorithmic_bytes(c) / (shapes[best] * 1e-3) / 1e9}
+
+
+def parity_report(c, z_gpu, ref=None) -> dict:
+    """Every token of the GPU's z against the oracle: mismatches, and those
+    outside the rounding band |u S - S_k| <= 1e-5 S (which must be 0)."""
+    import oracle
+    zg = z_gpu.cpu().numpy() if hasattr(z_gpu, "cpu") else z_gpu
+    if ref is None:
+        ref = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u, with_band=True)
+    z_ref, band = ref
+    mism = zg != z_ref
+    return {"tokens": int(c.N), "mismatches": int(mism.sum()),
+            "mismatch_rate": float(mism.mean()) if c.N else 0.0,
+            "mismatches_outside_band": int((mism & ~band).sum()),
+            "in_band_rate": float(band.mean()) if c.N else 0.0}
+
+
+def _brief(r: dict) -> dict:
+    r = dict(r)
+    r.pop("z", None)
+    return r
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -490,9 +871,16 @@ def main() -> int:
     ap.add_argument("--only", choices=KERNELS, default=None,
                     help="time one kernel on one workload (for profiling)")
     ap.add_argument("--workload", default=HEADLINE)
-    ap.add_argument("--copy-calibration", action="store_true",
-                    help="run plain 1 GiB device-to-device copies (the "
-                         "reference for scaling HBM counters)")
+    ap.add_argument("--ceiling", choices=("mall", "hbm"), default=None,
+                    help="time the streaming-read probe over 192 MiB x 8 passes "
+                         "(the passes after the first served by the MALL) or 4 GiB "
+                         "(HBM); one JSON line")
+    ap.add_argument("--floor-config", default=None,
+                    help="window,waves_per_group,waves_per_cu of the floor probe "
+                         "(--only floor); default 16 and the draw's occupancy")
+    ap.add_argument("--copy", action="store_true",
+                    help="three plain 1 GiB device-to-device copies (a check of "
+                         "the request-size counters: 2^30 bytes read, 2^30 written)")
     ap.add_argument("--k-sweep", action="store_true",
                     help="naive vs butterfly over K = 16, 48, ..., 240 on the "
                          "corpus shaped like the paper's evaluation corpus; one "
@@ -510,19 +898,39 @@ def main() -> int:
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
     ap.add_argument("--counters-summary", action="store_true",
-                    help="write the HBM-traffic record from rocprofv3 csv "
-                         "directories (--fetch, --write, --copy-fetch, "
-                         "--copy-write, optional --hitmiss) to --out")
-    for opt in ("--fetch", "--write", "--copy-fetch", "--copy-write",
-                "--hitmiss"):
+                    help="write the counter record of the draw on --workload from "
+                         "the csv directories of rocprofv3 counter passes (--reads, "
+                         "--dram, optional --hitmiss) to --out")
+    for opt in ("--reads", "--dram", "--hitmiss", "--out"):
         ap.add_argument(opt, default=None)
-    ap.add_argument("--out", default=COUNTERS)
-    ap.add_argument("--kernel-name", default=HEADLINE_KERNEL,
-                    help="substring of the device kernel's name in the counter "
-                         "csv files (--counters-summary)")
+    ap.add_argument("--profile-commands", default=None, metavar="DIR",
+                    help="print the rocprofv3 commands behind profiles/ (output to DIR)")
+    ap.add_argument("--report-counters", default=None, metavar="DIR",
+                    help="reduce the counter passes in DIR to --out (and the draw's "
+                         "counter records under profiles/)")
+    ap.add_argument("--report-trace", default=None, metavar="DIR",
+                    help="reduce the kernel trace in DIR (with --bench-log) to --out")
+    ap.add_argument("--bench-log", default=None)
+    ap.add_argument("--report-bench", default=None, metavar="LOG",
+                    help="summarise the default run's JSON line in LOG to --out")
+    ap.add_argument("--report-jsonl", default=None, metavar="LOG",
+                    help="tabulate the JSON lines in LOG to --out (--title, --command)")
+    ap.add_argument("--title", default="")
+    ap.add_argument("--command", default="")
     args = ap.parse_args()
     if args.counters_summary:
         return counters_summary(args)
+    if args.profile_commands:
+        print("\n".join(profile_commands(args.profile_commands)))
+        return 0
+    if args.report_counters:
+        return report_counters(args.report_counters, args.out)
+    if args.report_trace:
+        return report_trace(args.report_trace, args.bench_log, args.out)
+    if args.report_bench:
+        return report_bench(args.report_bench, args.out)
+    if args.report_jsonl:
+        return report_jsonl(args.report_jsonl, args.out, args.title, args.command)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the draw has no multi-GPU path in this build.", file=sys.stderr)
@@ -537,7 +945,15 @@ def main() -> int:
         print("bench.py needs a GPU", file=sys.stderr)
         return 1
 
-    if args.copy_calibration:
+    if args.ceiling:
+        nbytes, passes = {"mall": (MALL_PROBE_BYTES, MALL_PROBE_PASSES),
+                          "hbm": (HBM_PROBE_BYTES, 1)}[args.ceiling]
+        ms, gbps = read_ceiling(nbytes, passes, steps=args.steps)
+        print(json.dumps({"ceiling": args.ceiling, "bytes": nbytes, "passes": passes,
+                          "ms_per_launch_median": ms, "GBps": gbps}), flush=True)
+        return 0
+
+    if args.copy:
         n = 1 << 28                      # 1 GiB of float32
         src = torch.ones(n, dtype=torch.float32, device="cuda")
         dst = torch.empty_like(src)
@@ -562,57 +978,105 @@ def main() -> int:
     if args.only:
         c = make_corpus(args.workload)
         dev = upload(c)
+        if args.floor_config:
+            dev["floor_cfg"] = tuple(int(x) for x in args.floor_config.split(","))
         r = measure(args.workload, c, dev, args.only, args.steps, args.warmup)
         r.pop("z")
         print(json.dumps(r), flush=True)
         return 0
 
-    results = []
+    steps, warmup = args.steps, args.warmup
+    # ceilings of the memory system on this GPU
+    hbm_ms, hbm_GBps = read_ceiling(HBM_PROBE_BYTES, 1)
+    mall_ms, mall_GBps = read_ceiling(MALL_PROBE_BYTES, MALL_PROBE_PASSES)
+    copy_GBps = device_copy_GBps()
+    results, parity, floors, counts = [], {}, {}, {}
+
+    # the small workloads: the draw, and its parity on every token
+    for name in ("tiny-K32", "corpus1M-K64"):
+        c = make_corpus(name)
+        dev = upload(c)
+        r = measure(name, c, dev, "butterfly", steps, warmup)
+        parity[name] = parity_report(c, r["z"])
+        results.append(_brief(r))
+        del dev
+    torch.cuda.empty_cache()
+
+    # K = 256: the draw against the naive and transposed kernels, its floor
+    # and the topic counts of its draws
     c2 = make_corpus(SECOND)
     dev2 = upload(c2)
-    for k in ("butterfly", "transposed", "naive"):
-        r = measure(SECOND, c2, dev2, k, max(args.steps, 20), args.warmup)
-        r.pop("z")
-        results.append(r)
+    second = measure(SECOND, c2, dev2, "butterfly", max(steps, 20), warmup)
+    parity[SECOND] = parity_report(c2, second["z"])
+    results.append(_brief(second))
+    for k in ("transposed", "naive"):
+        results.append(_brief(measure(SECOND, c2, dev2, k, max(steps, 20), warmup)))
+    floors[SECOND] = measure_floor(SECOND, c2, dev2, max(steps, 20), warmup)
+    counts[SECOND] = measure(SECOND, c2, dev2, "count", max(steps, 20), warmup)["ms_per_launch"]
     del dev2, c2
     torch.cuda.empty_cache()
 
+    # K = 2048, Poisson document lengths: the draw (token order and routed)
+    c5 = make_corpus("poisson300-K2048")
+    dev5 = upload(c5)
+    r = measure(c5.name, c5, dev5, "butterfly", steps, warmup)
+    import oracle
+    ref5 = oracle.draw(c5.theta, c5.phi, c5.doc_id, c5.word_id, c5.u, with_band=True)
+    parity[c5.name] = parity_report(c5, r["z"], ref5)
+    results.append(_brief(r))
+    r = measure(c5.name, c5, dev5, "routed", steps, warmup)
+    parity[c5.name + " routed"] = parity_report(c5, r["z"], ref5)
+    results.append(_brief(r))
+    del dev5, c5, ref5
+    torch.cuda.empty_cache()
+
+    # the headline workload, K = 1024
     c = make_corpus(HEADLINE)
     dev = upload(c)
-    naive = measure(HEADLINE, c, dev, "naive", max(3, args.steps // 4), 1)
-    naive.pop("z")
-    results.append(naive)
-    tr = measure(HEADLINE, c, dev, "transposed", args.steps, args.warmup)
-    tr.pop("z")
-    results.append(tr)
-    head = measure(HEADLINE, c, dev, "butterfly", args.steps, args.warmup)
+    results.append(_brief(measure(HEADLINE, c, dev, "naive", max(3, steps // 4), 1)))
+    results.append(_brief(measure(HEADLINE, c, dev, "transposed", steps, warmup)))
+    head = measure(HEADLINE, c, dev, "butterfly", steps, warmup)
     z_head = head.pop("z")
     results.append(head)
     # the same draw over tokens routed to the XCDs by word: routing built once
     # (as per corpus in a sampler), and built again in every step
+    routed = {}
     for k in ("routed", "routed+build"):
-        r = measure(HEADLINE, c, dev, k, args.steps, args.warmup)
-        r["differs_from_butterfly"] = int((r.pop("z") != z_head).sum())
+        r = measure(HEADLINE, c, dev, k, steps, warmup)
+        routed[k] = r.pop("z")
+        r["differs_from_butterfly"] = int((routed[k] != z_head).sum())
         results.append(r)
     # the same launches with L2 and the MALL flushed before each (1 GiB fill)
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
-    cold = measure(HEADLINE, c, dev, "butterfly", args.steps, 1, flush=flush)
-    cold.pop("z")
-    results.append(cold)
+    results.append(_brief(measure(HEADLINE, c, dev, "butterfly", steps, 1, flush=flush)))
     del flush
+    floors[HEADLINE] = measure_floor(HEADLINE, c, dev, steps, warmup)
+    counts[HEADLINE] = measure(HEADLINE, c, dev, "count", steps, warmup)["ms_per_launch"]
+
+    base = cpu_baseline(c, z_head, args.cpu_sample)
+    if base["parity"]["tokens"] == c.N:       # the baseline drew every token
+        parity[HEADLINE] = base["parity"]
+        ref4 = base.pop("_ref")
+    else:
+        base.pop("_ref")
+        ref4 = oracle.draw(c.theta, c.phi, c.doc_id, c.word_id, c.u, with_band=True)
+        parity[HEADLINE] = parity_report(c, z_head, ref4)
+    parity[HEADLINE + " routed"] = parity_report(c, routed["routed"], ref4)
+    del ref4
 
     wall = head["wall_s"]
-    value = c.N * args.steps / wall
-    traffic = traffic_from_counters()
-    copy_GBps = device_copy_GBps()
+    value = c.N * steps / wall
+    fl = floors[HEADLINE]
+    traffic = traffic_from_counters(HEADLINE)
+    egress_GBps = traffic / (head["ms_per_launch"] * 1e-3) / 1e9 if traffic else None
     out = {
         "metric": METRIC,
         "value": value,
         "unit": "draws/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
-        "ms_per_step": 1e3 * wall / args.steps,
+        "steps": steps,
+        "warmup": warmup,
+        "ms_per_step": 1e3 * wall / steps,
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
@@ -621,27 +1085,43 @@ def main() -> int:
         "config": {"workload": HEADLINE, "N": c.N, "M": c.M, "V": c.V,
                    "K": c.K, "kernel": "butterfly"},
         "roofline": {
-            "bound": "hbm",
+            "bound": "memory",
             "achieved": head["alg_GBps"],
-            "peak": PEAK_HBM_GBPS,
+            "peak": fl["alg_GBps"],
             "unit": "GB/s",
-            "frac": head["alg_GBps"] / PEAK_HBM_GBPS,
+            "frac": fl["ms_per_launch"] / head["ms_per_launch"],
             "traffic": traffic,
+            "peak_kind": "measured in this run: the launch's algorithmic bytes over the "
+                         "time of the memory-only probe that moves them in the same token "
+                         "order (lda_probe_draw_floor, fastest of its launch shapes)",
+            "traffic_GBps": egress_GBps,
         },
-        # the counted bytes that leave L2 (FETCH_SIZE + WRITE_SIZE, scaled by
-        # a plain copy) per launch, over the measured launch time
-        "hbm_traffic_GBps": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9
-                             if traffic else None),
-        "hbm_traffic_frac": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9 /
-                             PEAK_HBM_GBPS if traffic else None),
-        # a plain 1 GiB device copy on the same GPU (bytes read + written per
-        # second), and the counted L2 traffic of the draw against it
-        "device_copy_GBps": copy_GBps,
-        "hbm_traffic_frac_of_copy": (traffic / (head["ms_per_launch"] * 1e-3) / 1e9 /
-                                     copy_GBps if traffic else None),
-        "cpu_baseline": cpu_baseline(c, z_head, args.cpu_sample),
+        # algorithmic bytes over time: above the HBM peak, because L2 and the
+        # MALL serve the re-read rows of Zipf-frequent words
+        "effective_GBps": head["alg_GBps"],
+        "effective_frac_of_hbm_peak": head["alg_GBps"] / PEAK_HBM_GBPS,
+        "hbm_peak_GBps": PEAK_HBM_GBPS,
+        "l2_egress_GBps": egress_GBps,
+        "ceilings": {"hbm_read_GBps": hbm_GBps, "mall_read_GBps": mall_GBps,
+                     "device_copy_GBps": copy_GBps,
+                     "hbm_read": f"{HBM_PROBE_BYTES >> 20} MiB read once (lda_probe_read)",
+                     "mall_read": f"{MALL_PROBE_BYTES >> 20} MiB read {MALL_PROBE_PASSES} "
+                                  "times per launch (lda_probe_read)"},
+        "floor": {w: {"ms": f["ms_per_launch"], "shape": f["shape"],
+                      "draw_ms": d["ms_per_launch"],
+                      "frac_of_floor": f["ms_per_launch"] / d["ms_per_launch"]}
+                  for w, f, d in ((HEADLINE, floors[HEADLINE], head),
+                                  (SECOND, floors[SECOND], second))},
+        "second": {"workload": SECOND, "draws_per_s": second["draws_per_s"],
+                   "ms_per_launch": second["ms_per_launch"],
+                   "effective_GBps": second["alg_GBps"],
+                   "frac_of_floor": floors[SECOND]["ms_per_launch"] / second["ms_per_launch"]},
+        "count_topics_ms": counts,
+        "parity": parity,
+        "cpu_baseline": base,
         "results": results,
-        "kernel_source_sha1": kernel_source_hash(),
+        "floors": floors,
+        "kernel_source_sha1": {k: kernel_source_hash(k) for k in KERNEL_SOURCES},
     }
     print(json.dumps(out), flush=True)
     return 0
