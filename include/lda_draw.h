@@ -336,6 +336,29 @@ int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_
                      int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk, int32_t *nwk,
                      void *stream);
 
+/*
+ * For callers that cannot allocate device memory (code under graph capture
+ * aside: this call waits on the stream; tight serving loops; harnesses that
+ * forbid hipMalloc): lda_route_build followed by lda_draw_routed, with the
+ * routing kept in a scratch array the library holds instead of a caller's
+ * workspace.  Arguments, layout, errors and z as lda_draw_routed (K divisible
+ * by 4 with LDA_ROUTE_MIN_K <= K <= 2048), taking doc_id and word_id in
+ * place of a route.  The array is a static device array of
+ * LDA_ROUTED_SCRATCH_BYTES: each GPU the library runs on holds its own copy
+ * until the process ends; N whose routing needs more
+ * (lda_route_workspace_bytes(N) > LDA_ROUTED_SCRATCH_BYTES, about 5.4M
+ * tokens) is refused with LDA_ERR_UNSUPPORTED before any HIP call.  Nothing
+ * is allocated (no hipMalloc, no hipFree).  Like lda_route_build it
+ * synchronises `stream` once.  Every call on one GPU uses that GPU's array
+ * and overwrites the previous call's routing; calls that overlap on one GPU
+ * (other streams, other host threads) race and must be ordered by the
+ * caller.
+ */
+#define LDA_ROUTED_SCRATCH_BYTES 67108864
+int lda_draw_routed_scratch(const float *theta, const float *phi, const int32_t *doc_id,
+                            const int32_t *word_id, const float *u, int32_t *z, int64_t N,
+                            int32_t M, int32_t V, int32_t K, void *stream);
+
 /* The W (butterfly width) the library uses for K, or LDA_ERR_UNSUPPORTED /
  * LDA_ERR_SHAPE for a K it rejects. */
 int lda_butterfly_width(int32_t K);

@@ -13,6 +13,7 @@ _BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "dra
             "draw_variant", "VARIANTS",
             "butterfly_table", "count_topics",
             "route_build", "draw_routed", "draw_routed_philox", "route_workspace_bytes", "Route",
+            "draw_routed_scratch", "ROUTED_SCRATCH_BYTES",
             "butterfly_width", "status_string", "version", "LdaError",
             "load", "MAX_K", "MAX_TABLE_BYTES", "STATUS")
 

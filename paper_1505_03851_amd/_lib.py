@@ -43,6 +43,7 @@ MAX_N = _CONSTS["LDA_MAX_N"]
 MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
 DOC_LANES_MAX_CACHE_BYTES = _CONSTS["LDA_DOC_LANES_MAX_CACHE_BYTES"]
 # table variants of lda_draw_butterfly_variant, by name
+ROUTED_SCRATCH_BYTES = _CONSTS["LDA_ROUTED_SCRATCH_BYTES"]
 VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
             "lds": _CONSTS["LDA_VARIANT_LDS_TABLE"],
             "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"],
@@ -102,6 +103,8 @@ def load() -> ctypes.CDLL:
                                            P, I64, I32, I32, I32, ctypes.c_uint64,
                                            ctypes.c_uint32, P]
     lib.lda_draw_routed_philox.restype = ctypes.c_int
+    lib.lda_draw_routed_scratch.argtypes = draw_args
+    lib.lda_draw_routed_scratch.restype = ctypes.c_int
     lib.lda_count_topics.argtypes = [P, P, P, I64, I32, I32, I32, P, P, P]
     lib.lda_count_topics.restype = ctypes.c_int
     _lib = lib
@@ -493,6 +496,15 @@ def _routed_args(theta, phi, route: "Route", N: int, device, out):
         if out.shape[0] != N or out.device != device:
             raise ValueError("out must be int32[N] on the tensors' device")
     return M, V, K, out
+
+
+def draw_routed_scratch(theta, phi, doc_id, word_id, u, out=None, stream=None,
+                        validate: bool = False) -> torch.Tensor:
+    """The routed draw with the routing built in the library's own scratch
+    array (lda_draw_routed_scratch): no workspace, nothing allocated by the
+    library; waits on the stream once; N up to about 5.4M tokens."""
+    return _draw("lda_draw_routed_scratch", theta, phi, doc_id, word_id, u, out, stream,
+                 validate)
 
 
 def draw_routed(theta, phi, route: Route, u, out=None, stream=None) -> torch.Tensor:

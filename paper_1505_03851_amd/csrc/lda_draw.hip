@@ -28,6 +28,8 @@
 
 #include <stdint.h>
 
+#include <mutex>
+
 #include "lda_draw.h"
 #include "tuning.hpp"
 #include "sources.hpp"
@@ -378,8 +380,6 @@ RoutePlan route_plan(void *ws, const RouteLayout &L) {
                    reinterpret_cast<int32_t *>(b + L.chunk_hist)};
 }
 
-// K the routed draw takes: the leaf kernel's (K divisible by 4 from
-// LDA_EIGHTHS_MIN_K to LDA_EIGHTHS_MAX_BLOCKS blocks of 256).
 // K the routed draw takes: the eighths kernel's K from LDA_ROUTE_MIN_K up.
 // Routing pays only where phi is far larger than the caches: measured on
 // MI355X over 16.8M Zipf tokens with V = 100,000 words, the routed draw is
@@ -561,22 +561,15 @@ extern "C" size_t lda_route_workspace_bytes(int64_t N) {
   return route_layout(N).bytes;
 }
 
-extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, int64_t N,
-                               int32_t M, int32_t V, void *workspace, size_t workspace_bytes,
-                               lda_route *route, void *stream) {
-  if (!route) return LDA_ERR_NULL;
-  if (N < 0 || M <= 0 || V <= 0) return LDA_ERR_SHAPE;
-  if (N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
-  *route = lda_route{};
-  if (N == 0) return LDA_OK;
-  if (!doc_id || !word_id || !workspace) return LDA_ERR_NULL;
-  if ((reinterpret_cast<uintptr_t>(doc_id) | reinterpret_cast<uintptr_t>(word_id)) & 3u ||
-      reinterpret_cast<uintptr_t>(workspace) & 7u)
-    return LDA_ERR_ALIGN;
+namespace lda {
+namespace {
+
+// The routing's kernels and its one read-back, into a workspace already
+// checked to hold route_layout(N).bytes (N > 0, arguments checked).
+int route_build_into(const int32_t *doc_id, const int32_t *word_id, int64_t N, void *workspace,
+                     lda_route *route, hipStream_t s) {
   const RouteLayout L = route_layout(N);
-  if (workspace_bytes < L.bytes) return LDA_ERR_WORKSPACE;
   const RoutePlan P = route_plan(workspace, L);
-  const hipStream_t s = static_cast<hipStream_t>(stream);
   route_fill<<<1, kRouteClasses, 0, s>>>(P.counts, kRouteClasses, 0);
   route_hist<<<(unsigned)(L.nchunks < 256 ? L.nchunks : 256), kRouteThreads, 0, s>>>(
       word_id, N, L.nchunks, P.chunk_hist, P.counts);
@@ -609,6 +602,25 @@ extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, in
     route->length[x] = lists[2 * kRouteXcds + x];
   }
   return LDA_OK;
+}
+
+}  // namespace
+}  // namespace lda
+
+extern "C" int lda_route_build(const int32_t *doc_id, const int32_t *word_id, int64_t N,
+                               int32_t M, int32_t V, void *workspace, size_t workspace_bytes,
+                               lda_route *route, void *stream) {
+  if (!route) return LDA_ERR_NULL;
+  if (N < 0 || M <= 0 || V <= 0) return LDA_ERR_SHAPE;
+  if (N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
+  *route = lda_route{};
+  if (N == 0) return LDA_OK;
+  if (!doc_id || !word_id || !workspace) return LDA_ERR_NULL;
+  if ((reinterpret_cast<uintptr_t>(doc_id) | reinterpret_cast<uintptr_t>(word_id)) & 3u ||
+      reinterpret_cast<uintptr_t>(workspace) & 7u)
+    return LDA_ERR_ALIGN;
+  if (workspace_bytes < route_layout(N).bytes) return LDA_ERR_WORKSPACE;
+  return route_build_into(doc_id, word_id, N, workspace, route, static_cast<hipStream_t>(stream));
 }
 
 namespace lda {
@@ -670,6 +682,68 @@ extern "C" int lda_draw_routed_philox(const float *theta, const float *phi,
   const lda::UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
   return lda::draw_routed(theta, phi, workspace, workspace_bytes, route, z, us, z, N, M, V, K,
                           stream);
+}
+
+// ---------------------------------------------------------------------------
+// The routed draw for callers that cannot allocate: the routing lives in this
+// file-scope array instead of a caller's workspace.  Each GPU the library
+// runs on holds its own copy (LDA_ROUTED_SCRATCH_BYTES) until the process
+// ends; its device address is looked up once per device (hipGetSymbolAddress,
+// with the device current) and only that address is handed to kernels.
+namespace lda {
+namespace {
+
+__device__ __align__(256) unsigned char scratch[LDA_ROUTED_SCRATCH_BYTES];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's address of `scratch` (looked up on the first call on
+// that device), or nullptr with the HIP error recorded.
+void *scratch_address() {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e == hipSuccess && (dev < 0 || dev >= kMaxDevices)) e = hipErrorInvalidDevice;
+  if (e != hipSuccess) {
+    g_last_hip = e;
+    return nullptr;
+  }
+  std::lock_guard<std::mutex> lock(g_scratch_mutex);
+  if (!g_scratch_ptr[dev]) {
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) {
+      g_last_hip = e != hipSuccess ? e : hipErrorInvalidSymbol;
+      return nullptr;
+    }
+    g_scratch_ptr[dev] = ptr;
+  }
+  return g_scratch_ptr[dev];
+}
+
+}  // namespace
+}  // namespace lda
+
+extern "C" int lda_draw_routed_scratch(const float *theta, const float *phi,
+                                       const int32_t *doc_id, const int32_t *word_id,
+                                       const float *u, int32_t *z, int64_t N, int32_t M,
+                                       int32_t V, int32_t K, void *stream) {
+  // every check before any HIP call
+  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
+  if (st != LDA_OK) return st;
+  if (!routed_for(K) || N > LDA_ROUTE_MAX_N) return LDA_ERR_UNSUPPORTED;
+  if (N == 0) return LDA_OK;
+  const size_t bytes = route_layout(N).bytes;
+  if (bytes > LDA_ROUTED_SCRATCH_BYTES) return LDA_ERR_UNSUPPORTED;
+  void *ws = scratch_address();
+  if (!ws) return LDA_ERR_HIP;
+  lda_route route{};
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const int b = route_build_into(doc_id, word_id, N, ws, &route, s);
+  if (b != LDA_OK) return b;
+  const UniformSource us{u, 0, 0, 0};
+  return draw_routed(theta, phi, ws, bytes, &route, u, us, z, N, M, V, K, stream);
 }
 
 extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_t *z,

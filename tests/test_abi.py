@@ -342,3 +342,28 @@ def test_probe_argument_errors():
     assert lib.lda_probe_read(None, 4096, 1, A, None) == STATUS["LDA_ERR_NULL"]
     assert lib.lda_probe_read(A + 4, 4096, 1, A, None) == STATUS["LDA_ERR_ALIGN"]
     assert lib.lda_probe_read(A, 4100, 1, A, None) == STATUS["LDA_ERR_ALIGN"]
+
+
+def test_routed_scratch_argument_errors(lib):
+    """lda_draw_routed_scratch rejects bad arguments, K outside the routed
+    range and N whose routing does not fit its scratch array before any HIP
+    call."""
+    from paper_1505_03851_amd import _lib
+    from paper_1505_03851_amd._lib import STATUS
+
+    def run(N=1000, M=3, V=5, K=1024, **ptr):
+        p = dict(theta=A, phi=A, d=A, w=A, u=A, z=A)
+        p.update(ptr)
+        return lib.lda_draw_routed_scratch(p["theta"], p["phi"], p["d"], p["w"], p["u"],
+                                           p["z"], N, M, V, K, None)
+    for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    for K in (64, 256, 764, 1023, 2052):
+        assert run(K=K) == STATUS["LDA_ERR_UNSUPPORTED"], K
+    n = 5_000_000
+    while lib.lda_route_workspace_bytes(n) <= _lib.ROUTED_SCRATCH_BYTES:
+        n += 4096
+    assert run(N=n) == STATUS["LDA_ERR_UNSUPPORTED"]
+    for key in ("theta", "phi", "d", "w", "u", "z"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+    assert run(N=0) == 0
