@@ -62,8 +62,9 @@ int lda_probe_draw_floor(const float *theta, const float *phi, const int32_t *do
 
 /*
  * Streaming read: `passes` times over, every 16 bytes of buf[0 .. bytes)
- * are read once (grid-stride, 16-byte loads, LDA_PROBE_READ_GROUPS
- * workgroups of 256 lanes) and summed; each lane writes its sum to out
+ * are read once and summed (LDA_PROBE_READ_GROUPS workgroups of 256 lanes,
+ * all resident at once, each reading a contiguous span with 16 loads of 16
+ * bytes in flight per lane); each lane writes its sum to out
  * (float [LDA_PROBE_READ_OUT_FLOATS]).  buf 16-byte aligned and bytes a
  * multiple of 16 (LDA_ERR_ALIGN), passes >= 1 and bytes >= 0
  * (LDA_ERR_SHAPE); bytes = 0 is a no-op.

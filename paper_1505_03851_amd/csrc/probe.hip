@@ -96,22 +96,31 @@ __global__ __launch_bounds__(4 * kWave) void floor_kernel(
   if (store) z[n] = __builtin_bit_cast(int32_t, acc);
 }
 
-// Streaming read: every 16 bytes of buf, `passes` times, grid-stride; four
-// loads in flight per lane.
+// Streaming read: every 16 bytes of buf, `passes` times.  Workgroup b reads
+// its own contiguous span of the buffer (the last span takes the remainder),
+// 16 loads of 16 bytes in flight per lane; all LDA_PROBE_READ_GROUPS
+// workgroups are resident at once (8 per CU), so between two passes over a
+// span every XCD streams its whole share of the buffer.
+constexpr int kReadInFlight = 16;
 __global__ __launch_bounds__(256) void read_kernel(const f4 *__restrict__ buf, int64_t n4,
                                                    int passes, float *__restrict__ out) {
-  const int64_t tid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  const int64_t per = n4 / gridDim.x;
+  const int64_t lo = (int64_t)blockIdx.x * per;
+  const int64_t hi = blockIdx.x + 1 == gridDim.x ? n4 : lo + per;
+  constexpr int64_t step = (int64_t)kReadInFlight * 256;
   float acc = 0.0f;
   for (int p = 0; p < passes; ++p) {
-    int64_t i = tid;
-    for (; i + 3 * stride < n4; i += 4 * stride) {
-      const f4 a = buf[i], b = buf[i + stride], c = buf[i + 2 * stride], d = buf[i + 3 * stride];
-      acc += (sum4(a) + sum4(b)) + (sum4(c) + sum4(d));
+    int64_t i = lo + threadIdx.x;
+    for (; i + (kReadInFlight - 1) * 256 < hi; i += step) {
+      f4 v[kReadInFlight];
+#pragma unroll
+      for (int j = 0; j < kReadInFlight; ++j) v[j] = buf[i + j * 256];
+#pragma unroll
+      for (int j = 0; j < kReadInFlight; ++j) acc += sum4(v[j]);
     }
-    for (; i < n4; i += stride) acc += sum4(buf[i]);
+    for (; i < hi; i += 256) acc += sum4(buf[i]);
   }
-  out[tid] = acc;
+  out[(int64_t)blockIdx.x * blockDim.x + threadIdx.x] = acc;
 }
 
 template <int G, int C>
