@@ -76,10 +76,11 @@ extern "C" {
  * are 64-bit throughout.  Larger N is rejected with LDA_ERR_UNSUPPORTED. */
 #define LDA_MAX_N 4294901760LL
 
-/* Largest size in bytes of theta (4*M*K) or phi (4*V*K): the butterfly
- * kernel addresses both through buffer resources with 31-bit byte offsets.
- * Larger tables are rejected with LDA_ERR_UNSUPPORTED. */
-#define LDA_MAX_TABLE_BYTES 2147483647
+/* Largest size in bytes of theta (4*M*K) or phi (4*V*K) (and of the count
+ * tables): the kernels address both through buffer resources, whose record
+ * count and byte offsets are unsigned 32-bit.  Larger tables are rejected with
+ * LDA_ERR_UNSUPPORTED. */
+#define LDA_MAX_TABLE_BYTES 4294967295LL
 
 /*
  * Baseline draw: Algorithm 1 with the binary search of Algorithm 3.  One lane

@@ -54,7 +54,7 @@ int check_args(const void *theta, const void *phi, const void *doc_id,
                int32_t M, int32_t V, int32_t K) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_MAX_N) return LDA_ERR_UNSUPPORTED;
-  // theta and phi are addressed with 31-bit byte offsets
+  // theta and phi are addressed with unsigned 32-bit byte offsets
   if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES ||
       (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;

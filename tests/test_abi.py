@@ -305,8 +305,8 @@ def test_count_topics_argument_errors(lib):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
     assert run(K=_CONSTS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
     assert run(N=_CONSTS["LDA_COUNT_MAX_N"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk above 2 GiB
-    assert run(V=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk above 2 GiB
+    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 4 GiB
+    assert run(V=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 4 GiB
     for key in ("ndk", "nwk"):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
         assert run(N=0, **{key: None}) == STATUS["LDA_ERR_NULL"], key  # tables are cleared

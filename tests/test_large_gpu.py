@@ -1,8 +1,11 @@
-"""Token counts past 2**31: every kernel indexes tokens with 64-bit integers.
+"""Sizes past 2**31: token counts (every kernel indexes tokens with 64-bit
+integers) and tables (byte offsets into theta, phi and the count tables are
+unsigned 32-bit, so tables up to 4 GiB are addressed).
 
-The inputs are made on the GPU (about 35 GB of token arrays); a sample of the
-tokens -- random ones, the first and last, and those around token 2**31 --
-is checked against the oracle under the rounding-band rule.
+The large-N inputs are made on the GPU (about 35 GB of token arrays); a
+sample of the tokens -- random ones, the first and last, and those around
+token 2**31 -- is checked against the oracle under the rounding-band rule.
+The large tables are checked on every token.
 """
 import numpy as np
 import pytest
@@ -78,3 +81,75 @@ def test_tokens_past_2_31(big, kernel, K):
           f"hard={hard} in_band={int(band.sum())}", flush=True)
     assert hard == 0, big["idx"][np.nonzero(mis & ~band)[0][:5]]
     assert mis.mean() < MAX_MISMATCH_RATE
+
+
+# ---------------------------------------------------------------------------
+# Tables past 2 GiB: phi of about 2.3 GiB, so that rows beyond the 2^31-byte
+# offset are read (byte offsets are unsigned 32-bit); most tokens take words
+# from those rows.  Every token is checked against the oracle.
+
+def _big_phi_case(K, seed):
+    V = int(2.3 * 2 ** 30) // (4 * K) + 1
+    w_min = (1 << 31) // (4 * K) + 1           # first row past the 2 GiB offset
+    assert w_min < V
+    rng = np.random.default_rng(seed)
+    phi = rng.random((V, K), dtype=np.float32)
+    phi *= rng.random((V, K), dtype=np.float32) > 0.37   # exact zeros, as Dirichlet(0.01) gives
+    M = 300
+    theta = rng.random((M, K), dtype=np.float32) ** 8
+    N = 64 * 3000 + 17
+    word = np.where(rng.random(N) < 1 / 3, rng.integers(0, V, N),
+                    rng.integers(w_min, V, N)).astype(np.int32)
+    doc = (np.arange(N, dtype=np.int64) * M // N).astype(np.int32)
+    u = (rng.integers(0, 1 << 24, N) * 2.0 ** -24).astype(np.float32)
+    from paper_1505_03851_amd.inputs import Corpus
+    return Corpus(theta, phi, doc, word, u, name=f"phi-past-2GiB-K{K}")
+
+
+@pytest.mark.parametrize("K", [1024, 256, 96, 130])
+def test_phi_past_2_gib(K):
+    import torch
+    from parity import compare, run_kernel, to_device
+    c = _big_phi_case(K, seed=K)
+    print(f"[case] {c.name} V={c.V} phi={4 * c.V * K / 2 ** 30:.2f} GiB N={c.N}", flush=True)
+    torch.cuda.empty_cache()
+    dev = to_device(c)
+    kernels = ["butterfly", "naive", "transposed", "variant-register", "docs"] + \
+              (["routed"] if K >= 768 and K % 4 == 0 else [])
+    for kernel in kernels:
+        z = run_kernel(kernel, dev)
+        assert z.min() >= 0 and z.max() < K, kernel
+        rep = compare(c, z)
+        print(f"[parity] {c.name} {kernel}: {rep}", flush=True)
+        assert rep.hard == 0, (kernel, rep.first_hard)
+        assert rep.mismatch_rate < MAX_MISMATCH_RATE, (kernel, str(rep))
+    del dev
+    torch.cuda.empty_cache()
+
+
+def test_word_counts_past_2_gib():
+    """nwk of about 2.3 GiB (V x K int32): cells past the 2^31-byte offset are
+    counted exactly."""
+    import torch
+    import oracle
+    import paper_1505_03851_amd as lda
+    K = 1024
+    V = int(2.3 * 2 ** 30) // (4 * K) + 1
+    w_min = (1 << 31) // (4 * K) + 1
+    rng = np.random.default_rng(5)
+    N, M = 500_000, 700
+    word = np.where(rng.random(N) < 0.5, rng.integers(0, V, N), rng.integers(w_min, V, N))
+    d = torch.from_numpy((np.arange(N) * M // N).astype(np.int32)).cuda()
+    w = torch.from_numpy(word.astype(np.int32)).cuda()
+    z = torch.from_numpy(rng.integers(0, K, N).astype(np.int32)).cuda()
+    print(f"[case] counts nwk {4 * V * K / 2 ** 30:.2f} GiB", flush=True)
+    torch.cuda.empty_cache()
+    ndk, nwk = lda.count_topics(d, w, z, M, V, K)
+    torch.cuda.synchronize()
+    want_d, want_w = oracle.counts(d.cpu().numpy(), w.cpu().numpy(), z.cpu().numpy(), M, V, K)
+    assert np.array_equal(ndk.cpu().numpy(), want_d)
+    got_w = nwk.cpu().numpy()
+    assert np.array_equal(got_w, want_w), np.argwhere(got_w != want_w)[:5]
+    assert got_w[w_min:].sum() == (word >= w_min).sum()
+    del ndk, nwk
+    torch.cuda.empty_cache()
