@@ -95,7 +95,7 @@ def upload(c):
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
            "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "philox",
            "routed",
-           "routed+build", "routed-philox", "floor", "count", "count-clear")
+           "routed+build", "routed-philox", "floor", "count", "count-clear", "count-docs")
 
 
 def draw_occupancy(K: int) -> tuple[int, int]:
@@ -144,7 +144,7 @@ def launcher(kernel: str, dev):
         return lambda out, stream: probe.draw_floor(th, ph, d, w, u, out, window=window,
                                                     waves_per_group=wpg, waves_per_cu=wpc,
                                                     stream=stream)
-    if kernel in ("count", "count-clear"):
+    if kernel in ("count", "count-clear", "count-docs"):
         M, V, K = th.shape[0], ph.shape[0], th.shape[1]
         if "z_draw" not in dev:
             dev["z_draw"] = lda.draw_butterfly(th, ph, d, w, u)
@@ -155,6 +155,10 @@ def launcher(kernel: str, dev):
             e = d[:0]
             return lambda out, stream: lda.count_topics(e, e, e, M, V, K, ndk=ndk, nwk=nwk,
                                                         stream=stream)
+        if kernel == "count-docs":      # documents as offsets: rows of ndk written whole
+            off = dev["doc_offsets"]
+            return lambda out, stream: lda.count_topics_docs(off, w, zd, V, K, ndk=ndk, nwk=nwk,
+                                                             stream=stream)
         return lambda out, stream: lda.count_topics(d, w, zd, M, V, K, ndk=ndk, nwk=nwk,
                                                     stream=stream)
     if kernel == "philox":
@@ -608,6 +612,10 @@ PROFILE_TARGETS = {
                                      "--steps", "2", "--warmup", "0"]),
     "count_K1024": ("count_kernel", ["--only", "count", "--workload", HEADLINE,
                                      "--steps", "3", "--warmup", "1"]),
+    "cdocs_K1024": ("count_docs_kernel", ["--only", "count-docs", "--workload", HEADLINE,
+                                          "--steps", "3", "--warmup", "1"]),
+    "cwords_K1024": ("count_words_kernel", ["--only", "count-docs", "--workload", HEADLINE,
+                                            "--steps", "3", "--warmup", "1"]),
     "draw_K256": ("leaf_group_kernel", ["--only", "butterfly", "--workload", SECOND,
                                         "--steps", "3", "--warmup", "1"]),
     "floor_K256": ("floor_kernel", ["--only", "floor", "--floor-config", "16,2,0",
@@ -1012,7 +1020,9 @@ def main() -> int:
     for k in ("transposed", "naive"):
         results.append(_brief(measure(SECOND, c2, dev2, k, max(steps, 20), warmup)))
     floors[SECOND] = measure_floor(SECOND, c2, dev2, max(steps, 20), warmup)
-    counts[SECOND] = measure(SECOND, c2, dev2, "count", max(steps, 20), warmup)["ms_per_launch"]
+    for k in ("count", "count-docs"):
+        counts[f"{SECOND} {k}"] = measure(SECOND, c2, dev2, k, max(steps, 20),
+                                          warmup)["ms_per_launch"]
     del dev2, c2
     torch.cuda.empty_cache()
 
@@ -1051,7 +1061,8 @@ def main() -> int:
     results.append(_brief(measure(HEADLINE, c, dev, "butterfly", steps, 1, flush=flush)))
     del flush
     floors[HEADLINE] = measure_floor(HEADLINE, c, dev, steps, warmup)
-    counts[HEADLINE] = measure(HEADLINE, c, dev, "count", steps, warmup)["ms_per_launch"]
+    for k in ("count", "count-docs"):
+        counts[f"{HEADLINE} {k}"] = measure(HEADLINE, c, dev, k, steps, warmup)["ms_per_launch"]
 
     base = cpu_baseline(c, z_head, args.cpu_sample)
     if base["parity"]["tokens"] == c.N:       # the baseline drew every token

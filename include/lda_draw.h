@@ -338,6 +338,24 @@ int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_
                      void *stream);
 
 /*
+ * lda_count_topics with the documents in the paper's ragged form (Section 2:
+ * document m holds N[m] tokens), as lda_draw_docs takes them: doc_offsets is
+ * an int64 device array [M + 1], non-decreasing, doc_offsets[0] = 0 and
+ * doc_offsets[M] = N, 8-byte aligned (LDA_ERR_ALIGN); document m's tokens are
+ * positions doc_offsets[m] .. doc_offsets[m+1] - 1 of word_id and z.  The
+ * result equals lda_count_topics with doc_id[n] = the document whose range
+ * holds n.  The documents being contiguous, each row of ndk is counted by
+ * one wavefront and written whole: ndk needs no clearing and no atomics in
+ * memory (K <= LDA_MAX_K bins of LDS per wavefront).  Offsets outside [0, N]
+ * are clamped, never dereferenced; their contents are not otherwise checked.
+ * Other arguments and errors as lda_count_topics; doc_offsets may not be
+ * NULL (also when N = 0).
+ */
+int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *word_id, const int32_t *z,
+                          int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk,
+                          int32_t *nwk, void *stream);
+
+/*
  * For callers that cannot allocate device memory (code under graph capture
  * aside: this call waits on the stream; tight serving loops; harnesses that
  * forbid hipMalloc): lda_route_build followed by lda_draw_routed, with the

@@ -11,7 +11,7 @@ on first use, so ``paper_1505_03851_amd.inputs`` can be used without it.
 _BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "draw_doc_lanes",
             "draw_philox", "philox_uniforms",
             "draw_variant", "VARIANTS",
-            "butterfly_table", "count_topics",
+            "butterfly_table", "count_topics", "count_topics_docs",
             "route_build", "draw_routed", "draw_routed_philox", "route_workspace_bytes", "Route",
             "draw_routed_scratch", "ROUTED_SCRATCH_BYTES",
             "butterfly_width", "status_string", "version", "LdaError",

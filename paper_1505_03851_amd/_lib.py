@@ -107,6 +107,8 @@ def load() -> ctypes.CDLL:
     lib.lda_draw_routed_scratch.restype = ctypes.c_int
     lib.lda_count_topics.argtypes = [P, P, P, I64, I32, I32, I32, P, P, P]
     lib.lda_count_topics.restype = ctypes.c_int
+    lib.lda_count_topics_docs.argtypes = [P, P, P, I64, I32, I32, I32, P, P, P]
+    lib.lda_count_topics_docs.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -375,6 +377,45 @@ def count_topics(doc_id, word_id, z, M: int, V: int, K: int, ndk=None, nwk=None,
         st = load().lda_count_topics(doc_id.data_ptr(), word_id.data_ptr(), z.data_ptr(), N,
                                      int(M), int(V), int(K), outs[0].data_ptr(),
                                      outs[1].data_ptr(), _stream_handle(stream))
+    _check(st)
+    return outs[0], outs[1]
+
+
+def count_topics_docs(doc_offsets, word_id, z, V: int, K: int, ndk=None, nwk=None,
+                      stream=None, validate: bool = False) -> tuple[torch.Tensor, torch.Tensor]:
+    """count_topics with the documents as offsets (int64 [M + 1]; document m =
+    tokens doc_offsets[m] .. doc_offsets[m+1] - 1), as draw_docs takes them
+    (lda_count_topics_docs)."""
+    _require(doc_offsets, "doc_offsets", torch.int64, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    _require(z, "z", torch.int32, 1)
+    N = word_id.shape[0]
+    M = doc_offsets.shape[0] - 1
+    if M < 1:
+        raise ValueError("doc_offsets must hold M + 1 >= 2 entries")
+    if z.shape[0] != N:
+        raise ValueError("word_id and z lengths differ")
+    dev = word_id.device
+    if z.device != dev or doc_offsets.device != dev:
+        raise ValueError("all tensors must be on one device")
+    if validate:
+        off = doc_offsets.cpu()
+        if int(off[0]) != 0 or int(off[-1]) != N or bool((off[1:] < off[:-1]).any()):
+            raise ValueError("doc_offsets must be non-decreasing from 0 to N")
+    outs = []
+    for t, name, rows in ((ndk, "ndk", M), (nwk, "nwk", V)):
+        if t is None:
+            t = torch.empty((rows, K), dtype=torch.int32, device=dev)
+        else:
+            _require(t, name, torch.int32, 2)
+            if tuple(t.shape) != (rows, K) or t.device != dev:
+                raise ValueError(f"{name} must be int32[{rows}][{K}] on the tokens' device")
+        outs.append(t)
+    with torch.cuda.device(dev):
+        st = load().lda_count_topics_docs(doc_offsets.data_ptr(), word_id.data_ptr(),
+                                          z.data_ptr(), N, int(M), int(V), int(K),
+                                          outs[0].data_ptr(), outs[1].data_ptr(),
+                                          _stream_handle(stream))
     _check(st)
     return outs[0], outs[1]
 

@@ -17,6 +17,9 @@
 // by the flat cell index, then adds each distinct cell's count with one
 // device-wide atomic: a cell receives at most one atomic per chunk.  The
 // document table is aggregated first, then the word table, in the same LDS.
+// With documents given as offsets (contiguous), each document's row is
+// counted by one wavefront in LDS and written whole instead (count_docs_kernel):
+// no clearing and no atomics for that table.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -115,6 +118,71 @@ __global__ __launch_bounds__(kCountThreads) void count_kernel(
     if (wk[i] != kCountEmpty) count_insert(keys, cnt, wk[i]);
   __syncthreads();
   count_flush(keys, cnt, nwk);
+}
+
+// The word table alone (count_kernel's second half), for the offsets form.
+__global__ __launch_bounds__(kCountThreads) void count_words_kernel(
+    const int32_t *__restrict__ word_id, const int32_t *__restrict__ z, int64_t N, int32_t V,
+    int32_t K, int32_t *__restrict__ nwk) {
+  __shared__ uint32_t keys[kCountSlots];
+  __shared__ uint32_t cnt[kCountSlots];
+  for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
+    keys[s] = kCountEmpty;
+    cnt[s] = 0;
+  }
+  const int64_t c0 = (int64_t)blockIdx.x * kCountChunk + threadIdx.x;
+  uint32_t wk[kCountPer];
+#pragma unroll
+  for (int i = 0; i < kCountPer; ++i) {
+    const int64_t n = c0 + (int64_t)i * kCountThreads;
+    int32_t w = -1, k = -1;
+    if (n < N) {
+      w = word_id[n];
+      k = z[n];
+    }
+    const bool ok = (uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K;
+    wk[i] = ok ? (uint32_t)w * (uint32_t)K + (uint32_t)k : kCountEmpty;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int i = 0; i < kCountPer; ++i)
+    if (wk[i] != kCountEmpty) count_insert(keys, cnt, wk[i]);
+  __syncthreads();
+  count_flush(keys, cnt, nwk);
+}
+
+// The document table from documents given as offsets (document m = tokens
+// doc_offsets[m] .. doc_offsets[m+1] - 1, contiguous): one wavefront per
+// document counts its tokens' topics in an LDS row of K bins and writes the
+// whole row, so that the table needs neither clearing nor atomics in memory.
+// A token is counted when its word and topic are in range (as in
+// count_kernel).  Offsets outside [0, N] are clamped, never dereferenced.
+constexpr int kDocWaves = 4;  // documents (wavefronts) per workgroup
+__global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
+    const int64_t *__restrict__ doc_offsets, const int32_t *__restrict__ word_id,
+    const int32_t *__restrict__ z, int64_t N, int32_t M, int32_t V, int32_t K,
+    int32_t *__restrict__ ndk) {
+  extern __shared__ uint32_t rows[];  // kDocWaves rows of K bins
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
+  const int64_t m = (int64_t)blockIdx.x * kDocWaves + wave;
+  uint32_t *bins = rows + (size_t)wave * (size_t)K;
+  for (int k = lane; k < K; k += 64) bins[k] = 0;
+  __syncthreads();
+  if (m < M) {
+    int64_t lo = doc_offsets[m], hi = doc_offsets[m + 1];
+    lo = lo < 0 ? 0 : (lo > N ? N : lo);
+    hi = hi < lo ? lo : (hi > N ? N : hi);
+    for (int64_t n = lo + lane; n < hi; n += 64) {
+      const int32_t w = word_id[n], k = z[n];
+      if ((uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K) atomicAdd(&bins[k], 1u);
+    }
+  }
+  __syncthreads();
+  if (m < M) {
+    int32_t *row = ndk + m * (int64_t)K;
+    for (int k = lane; k < K; k += 64) row[k] = (int32_t)bins[k];
+  }
 }
 
 }  // namespace

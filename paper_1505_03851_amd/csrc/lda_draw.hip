@@ -774,6 +774,34 @@ extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, c
   return finish_launch();
 }
 
+extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *word_id,
+                                     const int32_t *z, int64_t N, int32_t M, int32_t V,
+                                     int32_t K, int32_t *ndk, int32_t *nwk, void *stream) {
+  if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
+  if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
+  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
+    return LDA_ERR_UNSUPPORTED;
+  if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
+  if (N > 0 && (!word_id || !z)) return LDA_ERR_NULL;
+  const void *ptrs[] = {ndk, nwk, word_id, z};
+  for (const void *p : ptrs)
+    if (reinterpret_cast<uintptr_t>(p) & 3u) return LDA_ERR_ALIGN;
+  if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t cells = (int64_t)V * K;
+  const int64_t blocks = (cells / 4 + 255) / 256;
+  count_clear<<<(unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), 256, 0, s>>>(
+      nwk, cells);
+  const size_t lds = (size_t)kDocWaves * (size_t)K * sizeof(uint32_t);
+  count_docs_kernel<<<(unsigned)((M + kDocWaves - 1) / kDocWaves), kDocWaves * 64, lds, s>>>(
+      doc_offsets, word_id, z, N, M, V, K, ndk);
+  if (N > 0) {
+    const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
+    count_words_kernel<<<(unsigned)chunks, kCountThreads, 0, s>>>(word_id, z, N, V, K, nwk);
+  }
+  return finish_launch();
+}
+
 extern "C" int lda_butterfly_width(int32_t K) {
   if (K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;

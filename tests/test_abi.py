@@ -367,3 +367,20 @@ def test_routed_scratch_argument_errors(lib):
     for key in ("theta", "phi", "d", "w", "u", "z"):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
     assert run(N=0) == 0
+
+
+def test_count_topics_docs_argument_errors(lib):
+    from paper_1505_03851_amd._lib import STATUS
+
+    def run(off=A, w=A, z=A, N=100, M=3, V=5, K=7, ndk=A, nwk=A):
+        return lib.lda_count_topics_docs(off, w, z, N, M, V, K, ndk, nwk, None)
+    for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
+        assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]
+    for key in ("off", "ndk", "nwk"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+        assert run(N=0, **{key: None}) == STATUS["LDA_ERR_NULL"], key
+    for key in ("w", "z"):
+        assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+    assert run(off=A + 4) == STATUS["LDA_ERR_ALIGN"]
+    assert run(w=A + 2) == STATUS["LDA_ERR_ALIGN"]

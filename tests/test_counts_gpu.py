@@ -170,3 +170,83 @@ def test_counts_captured_in_a_graph():
         _same(nwk.cpu().numpy(), want[1], f"nwk replay {rep}")
         ndk.fill_(3)                 # eager work between the replays
         nwk.fill_(-1)
+
+
+# ---------------------------------------------------------------------------
+# Documents as offsets (lda_count_topics_docs): each document's row written
+# whole by one wavefront.
+
+def _offsets(doc_id, M):
+    from paper_1505_03851_amd.inputs import doc_offsets
+    return doc_offsets(doc_id, M)
+
+
+def _gpu_counts_docs(off, w, z, V, K, ndk=None, nwk=None):
+    import torch
+    import paper_1505_03851_amd as lda
+    o = torch.from_numpy(np.ascontiguousarray(off, np.int64)).cuda()
+    wd = torch.from_numpy(np.ascontiguousarray(w, np.int32)).cuda()
+    zd = torch.from_numpy(np.ascontiguousarray(z, np.int32)).cuda()
+    a, b = lda.count_topics_docs(o, wd, zd, V, K, ndk=ndk, nwk=nwk, validate=True)
+    torch.cuda.synchronize()
+    return a.cpu().numpy(), b.cpu().numpy()
+
+
+@pytest.mark.parametrize("name", ["tiny-K32", "corpus1M-K64", "corpus1M-K256",
+                                  "corpus16M-K1024", "poisson300-K2048"])
+def test_counts_docs_of_the_draw_every_config(name):
+    import torch
+    import paper_1505_03851_amd as lda
+    c = named_corpus(name)
+    dev = to_device(c)
+    print(f"[case] counts (offsets) {name}", flush=True)
+    z = lda.draw_butterfly(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    torch.cuda.synchronize()
+    z = z.cpu().numpy()
+    got = _gpu_counts_docs(_offsets(c.doc_id, c.M), c.word_id, z, c.V, c.K)
+    want = oracle.counts(c.doc_id, c.word_id, z, c.M, c.V, c.K)
+    _same(got[0], want[0], "ndk")
+    _same(got[1], want[1], "nwk")
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (7, 30, 5, 3), (2049, 20, 300, 64),
+                                   (64 * 1000 + 13, 5000, 4000, 1000),
+                                   (100_000, 3, 7, 4096), (70_001, 1, 500, 200)],
+                         ids=lambda s: "N{}-M{}-V{}-K{}".format(*s))
+def test_counts_docs_ragged(shape):
+    """Ragged documents, many of them empty (and M above N), random topics;
+    a few words and topics out of range."""
+    N, M, V, K = shape
+    c = make_random(N, M, V, 1, seed=N + M, doc_order="ragged")
+    rng = np.random.default_rng(K)
+    z = rng.integers(0, K, N).astype(np.int32)
+    w = c.word_id.copy()
+    if N > 100:
+        z[::53] = K
+        w[7::61] = -1
+    print(f"[case] counts (offsets) ragged {shape}", flush=True)
+    got = _gpu_counts_docs(_offsets(c.doc_id, M), w, z, V, K)
+    want = oracle.counts(c.doc_id, w, z, M, V, K)
+    _same(got[0], want[0], "ndk")
+    _same(got[1], want[1], "nwk")
+
+
+def test_counts_docs_overwrite_and_equal_to_doc_id_form():
+    """Outputs holding garbage are overwritten; the offsets form equals the
+    doc-id form cell for cell; N = 0 writes zero rows."""
+    import torch
+    import paper_1505_03851_amd as lda
+    N, M, V, K = 90_000, 301, 777, 45
+    c = make_random(N, M, V, 1, seed=3, doc_order="ragged")
+    z = np.random.default_rng(1).integers(0, K, N).astype(np.int32)
+    ndk = torch.full((M, K), 9, dtype=torch.int32, device="cuda")
+    nwk = torch.full((V, K), -9, dtype=torch.int32, device="cuda")
+    got = _gpu_counts_docs(_offsets(c.doc_id, M), c.word_id, z, V, K, ndk=ndk, nwk=nwk)
+    ref = _gpu_counts(c.doc_id, c.word_id, z, M, V, K)
+    _same(got[0], ref[0], "ndk")
+    _same(got[1], ref[1], "nwk")
+    off0 = torch.zeros(M + 1, dtype=torch.int64, device="cuda")
+    e = torch.empty(0, dtype=torch.int32, device="cuda")
+    lda.count_topics_docs(off0, e, e, V, K, ndk=ndk, nwk=nwk)
+    torch.cuda.synchronize()
+    assert int(ndk.abs().sum()) == 0 and int(nwk.abs().sum()) == 0
