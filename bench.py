@@ -622,6 +622,10 @@ PROFILE_TARGETS = {
                                     "--workload", SECOND, "--steps", "3", "--warmup", "1"]),
     "naive_K256": ("naive_kernel", ["--only", "naive", "--workload", SECOND,
                                     "--steps", "3", "--warmup", "1"]),
+    "draw_K64": ("leaf_group_kernel", ["--only", "butterfly", "--workload", "corpus1M-K64",
+                                       "--steps", "3", "--warmup", "1"]),
+    "floor_K64": ("floor_kernel", ["--only", "floor", "--floor-config", "8,2,0",
+                                   "--workload", "corpus1M-K64", "--steps", "3", "--warmup", "1"]),
     "draw_K2048": ("leaf_eighths_kernel", ["--only", "butterfly", "--workload",
                                            "poisson300-K2048", "--steps", "3", "--warmup", "1"]),
     "routed_K1024": ("routed_eighths_kernel", ["--only", "routed", "--workload", HEADLINE,
@@ -1010,6 +1014,16 @@ def main() -> int:
         del dev
     torch.cuda.empty_cache()
 
+    # K = 64: the draw's floor
+    c1 = make_corpus("corpus1M-K64")
+    dev1 = upload(c1)
+    d64 = measure(c1.name, c1, dev1, "butterfly", max(steps, 20), warmup)
+    d64.pop("z")
+    floors[c1.name] = measure_floor(c1.name, c1, dev1, max(steps, 20), warmup)
+    floors[c1.name]["draw_ms"] = d64["ms_per_launch"]
+    del dev1, c1
+    torch.cuda.empty_cache()
+
     # K = 256: the draw against the naive and transposed kernels, its floor
     # and the topic counts of its draws
     c2 = make_corpus(SECOND)
@@ -1020,6 +1034,7 @@ def main() -> int:
     for k in ("transposed", "naive"):
         results.append(_brief(measure(SECOND, c2, dev2, k, max(steps, 20), warmup)))
     floors[SECOND] = measure_floor(SECOND, c2, dev2, max(steps, 20), warmup)
+    floors[SECOND]["draw_ms"] = second["ms_per_launch"]
     for k in ("count", "count-docs"):
         counts[f"{SECOND} {k}"] = measure(SECOND, c2, dev2, k, max(steps, 20),
                                           warmup)["ms_per_launch"]
@@ -1034,6 +1049,8 @@ def main() -> int:
     ref5 = oracle.draw(c5.theta, c5.phi, c5.doc_id, c5.word_id, c5.u, with_band=True)
     parity[c5.name] = parity_report(c5, r["z"], ref5)
     results.append(_brief(r))
+    floors[c5.name] = measure_floor(c5.name, c5, dev5, steps, warmup)
+    floors[c5.name]["draw_ms"] = r["ms_per_launch"]
     r = measure(c5.name, c5, dev5, "routed", steps, warmup)
     parity[c5.name + " routed"] = parity_report(c5, r["z"], ref5)
     results.append(_brief(r))
@@ -1061,6 +1078,7 @@ def main() -> int:
     results.append(_brief(measure(HEADLINE, c, dev, "butterfly", steps, 1, flush=flush)))
     del flush
     floors[HEADLINE] = measure_floor(HEADLINE, c, dev, steps, warmup)
+    floors[HEADLINE]["draw_ms"] = head["ms_per_launch"]
     for k in ("count", "count-docs"):
         counts[f"{HEADLINE} {k}"] = measure(HEADLINE, c, dev, k, steps, warmup)["ms_per_launch"]
 
@@ -1119,10 +1137,9 @@ def main() -> int:
                      "mall_read": f"{MALL_PROBE_BYTES >> 20} MiB read {MALL_PROBE_PASSES} "
                                   "times per launch (lda_probe_read)"},
         "floor": {w: {"ms": f["ms_per_launch"], "shape": f["shape"],
-                      "draw_ms": d["ms_per_launch"],
-                      "frac_of_floor": f["ms_per_launch"] / d["ms_per_launch"]}
-                  for w, f, d in ((HEADLINE, floors[HEADLINE], head),
-                                  (SECOND, floors[SECOND], second))},
+                      "draw_ms": f["draw_ms"],
+                      "frac_of_floor": f["ms_per_launch"] / f["draw_ms"]}
+                  for w, f in floors.items()},
         "second": {"workload": SECOND, "draws_per_s": second["draws_per_s"],
                    "ms_per_launch": second["ms_per_launch"],
                    "effective_GBps": second["alg_GBps"],
