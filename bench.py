@@ -100,13 +100,17 @@ KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_c
 
 def draw_occupancy(K: int) -> tuple[int, int]:
     """(wavefronts per workgroup, wavefronts per CU) of the kernel
-    lda_draw_butterfly launches for K divisible by 4 (N >= 64): the leaf-group
-    kernel up to K = 256 (2 per workgroup, 3 per SIMD); the leaf-eighths
-    kernel above (4 per workgroup and 2 per SIMD up to 1280 topics, then 2
-    and 4)."""
+    lda_draw_butterfly launches for K divisible by 4 (N >= 64), as the
+    compiler's register report for gfx950 gives them: the leaf-group kernel up
+    to K = 256, 2 per workgroup and, per SIMD, 6 for groups of 8 lanes (K <=
+    32), 5 for 16, 4 for 32 and 3 for 64; the leaf-eighths kernel above (4 per
+    workgroup and 2 per SIMD up to 1280 topics, then 2 and 4)."""
     if K <= 256:
-        return 2, 12
+        per_simd = 6 if K <= 32 else 5 if K <= 64 else 4 if K <= 128 else 3
+        return 2, 4 * per_simd
     return (4, 8) if K <= 1280 else (2, 16)
+
+
 PHILOX_SEED = 0x5EED20150513
 
 

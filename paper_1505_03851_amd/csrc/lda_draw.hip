@@ -157,10 +157,11 @@ void launch_groups(const float *theta, const float *phi, DocSource d, const int3
                    hipStream_t s) {
   constexpr int CW = G == kWave ? LDA_GROUP64_WINDOW : LDA_GROUP_WINDOW;
   constexpr int C = CW < G ? CW : G;
-  constexpr int WPEU = G == kWave ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
+  // (8-topic leaves hold twice the registers: the 64-lane groups' setting)
+  constexpr int WPEU = G == kWave || H > 1 ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  const size_t lds = (size_t)kWavesPerBlock * group_lds_bytes<G, H>();  // (0 below 64 lanes)
+  const size_t lds = (size_t)kWavesPerBlock * group_lds_bytes<G, H>();
   if (K == kLeaf * H * G)
     leaf_group_kernel<G, H, C, WPEU, false><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);

@@ -26,20 +26,24 @@ namespace {
 // leaf of its run: for groups of 64 lanes, up to 4 runs, from LDS where the
 // leaves are staged, read a few tokens ahead; below, up to 2 runs, by a
 // select in registers), or any mix (a leaf per token, loaded with its phi
-// leaf).
+// leaf).  In the first two cases every run's leaves are also staged in LDS,
+// and the final reload takes its theta leaf from there (one LDS read in the
+// place of a gather from memory).
 enum GroupTheta : int { kGroupOne = 0, kGroupRuns = 1, kGroupAny = 2 };
 template <int G>
 constexpr int kMaxGroupRuns = G == kWave ? 4 : 2;
 constexpr int kRunAhead = 4;  // tokens whose staged theta leaves are read ahead
-// Runs staged in LDS (measured: 5-15% faster for 64-lane groups than four
-// selects per token; for 32-lane groups, up to 12% slower than one select)
+// Runs read from LDS in the tile (measured: 5-15% faster for 64-lane groups
+// than four selects per token; for 32-lane groups, up to 12% slower than one
+// select)
 template <int G>
 constexpr bool kStageRuns = G == kWave;
 
-// LDS bytes per wavefront of the leaf-group kernel: the staged theta leaves.
+// LDS bytes per wavefront of the leaf-group kernel: the staged theta leaves
+// of up to kMaxGroupRuns<G> runs.
 template <int G, int H>
 constexpr int group_lds_bytes() {
-  return kStageRuns<G> ? kMaxGroupRuns<G> * H * kWave * (int)sizeof(f4) : 0;
+  return kMaxGroupRuns<G> * H * kWave * (int)sizeof(f4);
 }
 
 // A leaf of L = 4 H consecutive topics: H 16-byte quads.
@@ -112,15 +116,15 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
       m &= m - 1;
       th[j] = mask(leaf_of(th_rs, th_lane, p));
     }
-    if constexpr (kStageRuns<G>) {
-      // stage the runs' leaves: quad h of run j at stage[(j H + h) 64 + lane]
-      const int lane = lane_id();
+  }
+  if constexpr (MODE != kGroupAny) {
+    // stage the runs' leaves: quad h of run j at stage[(j H + h) 64 + lane]
+    const int lane = lane_id();
 #pragma unroll
-      for (int j = 0; j < R; ++j)
+    for (int j = 0; j < R; ++j)
 #pragma unroll
-        for (int h = 0; h < H; ++h) stage[(j * H + h) * kWave + lane] = th[j].q[h];
-      lds_order();
-    }
+      for (int h = 0; h < H; ++h) stage[(j * H + h) * kWave + lane] = th[j].q[h];
+    lds_order();
   }
   const auto run_of = [&](int k) {
     // runs opened at the group's tokens 1 .. k
@@ -258,6 +262,11 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   // Padding topics (front of leaf qmin when L does not divide K) have zero
   // weight and a running sum of exactly 0 <= stop, so they are never chosen;
   // with S = 0 every comparison fails and the result is K - 1.
+  // The theta leaf: staged in LDS by lane gbase + q for the run of the
+  // lane's own token (padding quads already zero there), unless the group's
+  // documents were too many runs.
+  const bool staged = most < kMaxGroupRuns<G>;
+  const int run = __builtin_popcountll(gstarts & ((2ull << r) - 1ull));
   const int tq = c0 + L * q;
   float sum = low;
   int i = L - 1;
@@ -265,9 +274,14 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   for (int h = 0; h < H; ++h) {
     const int topic = tq + kLeaf * h;
     const uint32_t qoff = (uint32_t)(topic > 0 ? topic : 0) * 4u;
-    f4 tl = load_f32x4(th_rs, qoff + th_lane, 0);
+    f4 tl;
+    if (staged) {
+      tl = stage[(run * H + h) * kWave + gbase + q];
+    } else {
+      tl = load_f32x4(th_rs, qoff + th_lane, 0);
+      if (PAD && topic < 0) tl = f4{0.0f, 0.0f, 0.0f, 0.0f};
+    }
     const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
-    if (PAD && topic < 0) tl = f4{0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
     for (int e = 0; e < kLeaf; ++e) {
       const int idx = kLeaf * h + e;

@@ -40,7 +40,10 @@
 //   LDA_GROUP_MAX_K           largest K drawn by the leaf-group kernel (K
 //                             divisible by 4, at most 256; 0: never), and its
 //                             tokens in flight per wavefront and wavefronts
-//                             per SIMD.
+//                             per SIMD for groups of 8 to 32 lanes: 8 at 4
+//                             (93-118 VGPRs, no spills) was 4-11% faster than
+//                             8 at 3 at K = 48 ... 112 and within 2% of the
+//                             best of 4 or 8 at 3 ... 5 at K = 16 ... 112.
 #ifndef LDA_GROUP_MAX_K
 #define LDA_GROUP_MAX_K 256
 #endif
@@ -48,7 +51,7 @@
 #define LDA_GROUP_WINDOW 8
 #endif
 #ifndef LDA_GROUP_WAVES_PER_EU
-#define LDA_GROUP_WAVES_PER_EU 3
+#define LDA_GROUP_WAVES_PER_EU 4
 #endif
 //   LDA_GROUP64_WINDOW, LDA_GROUP64_WAVES_PER_EU  the same for groups of 64
 //                             lanes (K from 132 to 256): 8 at 3 was 0-15%
