@@ -116,6 +116,12 @@ int eighths_blocks(int32_t K) { return (K + kBlock4 - 1) / kBlock4; }
 bool eighths_wide_groups(int32_t K) {
   return 3LL * 4 * 8 * eighths_blocks(K) * kWave * (int64_t)sizeof(float) <= 160 * 1024;
 }
+// Whether one-document wavefronts stage their theta row in LDS for the
+// rebuild: while three 4-wavefront workgroups still fit with it.
+bool eighths_stage_theta(int32_t K) {
+  return 3LL * 4 * eighths_lds_floats(eighths_blocks(K), true) * (int64_t)sizeof(float) <=
+         160 * 1024;
+}
 
 template <int C, int WPEU, bool PAD>
 void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
@@ -123,12 +129,17 @@ void launch_eighths(const float *theta, const float *phi, DocSource d, const int
                     hipStream_t s) {
   const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
   const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  const size_t rows = (size_t)8 * eighths_blocks(K) * kWave * sizeof(float);
-  if (eighths_wide_groups(K))
-    leaf_eighths_kernel<C, 4, WPEU, PAD><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
+  const int NB = eighths_blocks(K);
+  const size_t rows = (size_t)eighths_lds_floats(NB, false) * sizeof(float);
+  const size_t staged = (size_t)eighths_lds_floats(NB, true) * sizeof(float);
+  if (eighths_stage_theta(K))
+    leaf_eighths_kernel<C, 4, WPEU, PAD, true><<<wave_grid(N, 4), 4 * kWave, 4 * staged, s>>>(
+        theta, phi, d, wd, u, z, N, K, tb, pb);
+  else if (eighths_wide_groups(K))
+    leaf_eighths_kernel<C, 4, WPEU, PAD, false><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
   else
-    leaf_eighths_kernel<C, 2, WPEU, PAD><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
+    leaf_eighths_kernel<C, 2, WPEU, PAD, false><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 

@@ -25,7 +25,8 @@ namespace {
 // machinery of the half-block tail (two tokens per load instruction).  Against
 // the one-topic sweep this reads the same bytes with four times fewer load
 // instructions (a 64-lane dword load costs the memory pipeline about as many
-// cycles as a 16-byte one), and the rebuild reads 128 B of phi per token.
+// cycles as a 16-byte one), and the rebuild reads 128 B of phi per token
+// (its theta from LDS where one document's row was staged during the sweep).
 //
 // Register slot s of the sweep holds token eighth_slot_token(s): with the
 // stage order above, lane l ends with slot (l5 l4 l3 l0 l1 l2) (bits listed
@@ -89,7 +90,8 @@ __device__ __forceinline__ f4 theta_leaf(rsrc_t rs, int c0, int blk, int r, uint
 // from LDS instead of from memory.
 constexpr int kFewMax = 4;
 struct FewDocs {
-  f4 *lds;                 // this wavefront's kFewMax x 64 leaves
+  f4 *lds;                 // this wavefront's kFewMax x 64 leaves (one-document
+                           // sweeps that stage the theta row: that row)
   int D;                   // runs of documents in the wavefront, uniform
   uint32_t row[kFewMax];   // their theta row offsets, uniform
   int slot;                // this lane's run
@@ -129,7 +131,9 @@ __device__ __forceinline__ f4 few_leaf(const FewDocs &fd, int t, int lane) {
 // rows[q * 64] receives the running prefix at the end of eighth q; returns the
 // prefix at the block's end.  c0 is the first topic of block 0 (PAD: K is not
 // a multiple of 256 and block 0 begins with 256 - K mod 256 empty topics).
-template <int MODE, bool PREFETCH, int C, int CT, bool PAD>
+// With TS (one document) the block's theta leaves also go to LDS, leaf l at
+// fd.lds[blk * 64 + l]: the whole row, in topic order from c0, for the rebuild.
+template <int MODE, bool PREFETCH, int C, int CT, bool PAD, bool TS = false>
 __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const FewDocs &fd,
                                               f4 (&win)[C], f4 (&twin)[CT], f4 (&th)[2],
                                               f4 (&thn)[2], int c0, int blk, int next,
@@ -146,6 +150,7 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
   // before the block's end)
   f4 st[kFewMax];
   if constexpr (MODE == kFewDocs && PREFETCH) few_load<PAD>(fd, w.th_rs, c0, next, w.r, st);
+  if constexpr (TS && MODE == kOneDoc) fd.lds[blk * kWave + lane] = th[0];
   float s[kWave / 2];
   float lo = 0.0f;
 #pragma unroll
@@ -224,7 +229,7 @@ struct NoHook {
   __device__ __forceinline__ void operator()() const {}
 };
 
-template <int MODE, int C, bool PAD, int CF = C, class Hook = NoHook>
+template <int MODE, int C, bool PAD, int CF = C, class Hook = NoHook, bool TS = false>
 __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDocs &fd, int NB,
                                         int c0, float *rows, Hook hook = Hook{}) {
   static_assert(CF <= C && kWave % CF == 0, "the theta window divides 64 and is at most C");
@@ -253,17 +258,42 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
   // flight during the other blocks)
   float prefix = 0.0f;
   for (int b = 0; b < NB - 1; ++b) {
-    prefix = sweep8_block<MODE, true, C, CT, PAD>(w, fd, win, twin, th, thn, c0, b, b + 1,
-                                                  rows + 8 * b * kWave, prefix);
+    prefix = sweep8_block<MODE, true, C, CT, PAD, TS>(w, fd, win, twin, th, thn, c0, b, b + 1,
+                                                      rows + 8 * b * kWave, prefix);
     if (b == 0) hook();
   }
-  prefix = sweep8_block<MODE, false, C, CT, PAD>(w, fd, win, twin, th, thn, c0, NB - 1, 0,
-                                                 rows + 8 * (NB - 1) * kWave, prefix);
+  prefix = sweep8_block<MODE, false, C, CT, PAD, TS>(w, fd, win, twin, th, thn, c0, NB - 1, 0,
+                                                     rows + 8 * (NB - 1) * kWave, prefix);
   if (NB == 1) hook();
   return prefix;
 }
 
-template <int C, int WPB, int WPEU, bool PAD>
+// The rebuild's tile of a one-document wavefront whose theta row is staged in
+// LDS (trow: the row's floats from topic c0, zero in the padding): as
+// load_tile_blocks for W = 32, with theta read from LDS.
+template <bool PADDED>
+__device__ __forceinline__ void load_chunk_staged(const Wave<kWave / 2, false> &w,
+                                                  float (&a)[kWave / 2], int blk, int first,
+                                                  const float *trow) {
+#pragma unroll
+  for (int k = 0; k < kWave / 2; ++k) {
+    const int bk = group_value<kWave / 2>(blk, k);
+    const int i = bk * (kWave / 2) + w.r;  // topic first + i
+    const int t = first + i;
+    const uint32_t voff = (uint32_t)(PADDED && t < 0 ? 0 : t) * 4u;
+    const uint32_t poff = (uint32_t)group_value<kWave / 2>((int)w.ph_lane, k);
+    a[k] = trow[i] * load_row<kWave / 2>(w.ph_rs, voff, poff);
+  }
+}
+
+// LDS floats per wavefront: the 8 NB prefix rows, and with TS the theta row.
+__host__ __device__ constexpr int eighths_lds_floats(int NB, bool TS) {
+  return 8 * NB * kWave + (TS ? NB * kBlock4 : 0);
+}
+
+// TS: one-document wavefronts stage their theta row in LDS during the sweep
+// and the rebuild reads theta from there.
+template <int C, int WPB, int WPEU, bool PAD, bool TS>
 __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                          DocSource docs, const int32_t *__restrict__ word_id,
@@ -289,12 +319,13 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   Wave<kWave, false> w;
   init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, kWave - 1, K,
                           lane, doc, word);
-  float *region = lds + wave * 8 * NB * kWave;
-
+  float *region = lds + wave * eighths_lds_floats(NB, TS);
+  FewDocs stage{};
+  if constexpr (TS) stage.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
   const FewDocs none{};
   float sum;
   if (w.mode == kOneDoc)
-    sum = sweep8<kOneDoc, C, PAD>(w, none, NB, c0, region + lane);
+    sum = sweep8<kOneDoc, C, PAD, C, NoHook, TS>(w, stage, NB, c0, region + lane);
   else if (w.mode == kTwoDocs)
     sum = sweep8<kTwoDocs, C, PAD>(w, none, NB, c0, region + lane);
   else
@@ -320,7 +351,12 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   // S = 0 every comparison fails and the result is K - 1.
   const Wave<kWave / 2, false> wh = half_wave(w, lane);
   float h[kWave / 2];
-  load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+  if (TS && w.mode == kOneDoc) {
+    lds_order();
+    load_chunk_staged<PAD>(wh, h, chunk, c0, reinterpret_cast<const float *>(stage.lds));
+  } else {
+    load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+  }
   butterfly_block<kWave / 2>(h, wh.r, NoStore{});
   const int j = c0 + chunk * (kWave / 2) +
                 inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
