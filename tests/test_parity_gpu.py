@@ -104,6 +104,11 @@ SHAPES = [
     (64 * 9 + 3, 30, 300, 1604, "sequential"),
     (64 * 5 + 30, 3, 100, 772, "sequential"),
     (64 * 5 + 3, 20, 200, 4096, "sequential"),
+    # one-document wavefronts up to K = 1024 stage their theta row in LDS for
+    # the rebuild: with and without empty leading topics
+    (64 * 8 + 50, 2, 200, 260, "single"),
+    (64 * 6 + 20, 3, 200, 768, "single"),
+    (64 * 7 + 11, 2, 200, 1020, "single"),
     # K divisible by 4 up to 128: the leaf-group kernel (groups of 8, 16 or
     # 32 lanes, empty leaves in front when K is below 32, 64 or 128), with
     # every group inside one document (long documents) or not
