@@ -77,10 +77,18 @@ extern "C" {
 #define LDA_MAX_N 4294901760LL
 
 /* Largest size in bytes of theta (4*M*K) or phi (4*V*K) (and of the count
- * tables): the kernels address both through buffer resources, whose record
- * count and byte offsets are unsigned 32-bit.  Larger tables are rejected with
- * LDA_ERR_UNSUPPORTED. */
+ * tables) for most entry points: their kernels address both through buffer
+ * resources, whose record count and byte offsets are unsigned 32-bit.  Larger
+ * tables are rejected with LDA_ERR_UNSUPPORTED. */
 #define LDA_MAX_TABLE_BYTES 4294967295LL
+
+/* Largest size in bytes of theta or phi for lda_draw_butterfly, lda_draw_docs
+ * and lda_draw_butterfly_philox: 2^32 - 1 floats (16 GiB).  When either table
+ * is larger than LDA_MAX_TABLE_BYTES these draw with a second build of the
+ * same kernels that addresses the tables by 32-bit float offsets and 64-bit
+ * loads (ids beyond the table's rows are clamped to its last row there, so
+ * no read leaves the table); the draws are the same. */
+#define LDA_MAX_WIDE_TABLE_BYTES 17179869180LL
 
 /*
  * Baseline draw: Algorithm 1 with the binary search of Algorithm 3.  One lane
@@ -114,7 +122,9 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
  *    rebuilt block (or half-block) with Algorithm 10.
  * Where K is not a multiple of the block (or of the group's 4 W topics), the
  * first K mod block topics (the remnant) form a leading block padded with
- * empty topics, which are never drawn.
+ * empty topics, which are never drawn.  theta and phi may each hold up to
+ * LDA_MAX_WIDE_TABLE_BYTES (past LDA_MAX_TABLE_BYTES the same kernels run
+ * with 64-bit table addressing).
  */
 int lda_draw_butterfly(const float *theta, const float *phi,
                        const int32_t *doc_id, const int32_t *word_id,
@@ -132,7 +142,8 @@ int lda_draw_butterfly(const float *theta, const float *phi,
  * Tokens are still drawn one per lane, 64 consecutive tokens per wavefront:
  * each lane finds its document by binary search over doc_offsets.
  * doc_offsets must be 8-byte aligned (LDA_ERR_ALIGN otherwise); its contents
- * are not checked.
+ * are not checked.  Tables up to LDA_MAX_WIDE_TABLE_BYTES, as
+ * lda_draw_butterfly.
  */
 int lda_draw_docs(const float *theta, const float *phi,
                   const int64_t *doc_offsets, const int32_t *word_id,

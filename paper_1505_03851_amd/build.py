@@ -8,7 +8,9 @@ import subprocess
 
 PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
-SRC = os.path.join(PKG, "csrc", "lda_draw.hip")
+# the draw library: its C ABI with the default build of the kernels, and the
+# build for tables past 4 GiB (lda_draw_wide.hip)
+SRC = [os.path.join(PKG, "csrc", "lda_draw.hip"), os.path.join(PKG, "csrc", "lda_draw_wide.hip")]
 LIB = os.path.join(PKG, "liblda_draw.so")
 PROBE_SRC = os.path.join(PKG, "csrc", "probe.hip")
 PROBE_LIB = os.path.join(PKG, "liblda_probe.so")
@@ -31,8 +33,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str, lib: str, verbose: bool, extra: list[str] | None) -> str:
-    cmd = [HIPCC, *FLAGS, *(extra or []), src, "-o", lib + ".tmp"]
+def _compile(src: str | list[str], lib: str, verbose: bool, extra: list[str] | None) -> str:
+    srcs = [src] if isinstance(src, str) else list(src)
+    cmd = [HIPCC, *FLAGS, *(extra or []), *srcs, "-o", lib + ".tmp"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)

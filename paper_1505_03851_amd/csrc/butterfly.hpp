@@ -10,7 +10,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace lda {
+#include "config.hpp"
+
+namespace LDA_NS {
 
 constexpr int kWave = 64;
 
@@ -217,6 +219,77 @@ __device__ __forceinline__ f4 load_f32x4(rsrc_t r, uint32_t voff, uint32_t soff)
   return __builtin_bit_cast(f4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
 }
 
+// ---------------------------------------------------------------------------
+// A table (theta [M][K] or phi [V][K]) as the draw kernels address it: a row
+// offset (32-bit, `row(id)`, a multiple of the row step) plus a lane offset in
+// bytes (the topics within the row).
+//  * LDA_WIDE_TABLES 0, tables below 4 GiB: a buffer resource over the table;
+//    offsets count bytes, and the resource's range check returns 0 for a read
+//    past the table, so an id out of range reads zeros and cannot fault.
+//  * LDA_WIDE_TABLES 1, tables below 16 GiB: the table's base pointer; row
+//    offsets count floats and each load forms a 64-bit address.  row() clamps
+//    the id to the table's last row, so that here too every read stays
+//    inside the table.
+// `extent` is the table's size in the offsets' unit (bytes, or floats).
+// ld / ld4 take a row offset that is uniform across the wavefront (a scalar
+// operand), ldv / ld4v one that differs between lanes.
+__host__ __device__ constexpr uint32_t table_unit() { return LDA_WIDE_TABLES ? 1u : 4u; }
+__host__ __device__ constexpr uint32_t table_extent(int64_t rows, int32_t K) {
+  return (uint32_t)(rows * (int64_t)K * table_unit());
+}
+
+#if LDA_WIDE_TABLES
+// 16-byte loads at 4-byte alignment (a table's base need only be 4-byte aligned)
+using f4u = float __attribute__((ext_vector_type(4), aligned(4)));
+
+struct Table {
+  const float *base;
+  uint32_t step;   // floats per row (K)
+  uint32_t last;   // offset of the last row
+  __device__ __forceinline__ uint32_t row(uint32_t id) const {
+    const uint64_t off = (uint64_t)id * step;
+    return off < last ? (uint32_t)off : last;
+  }
+  __device__ __forceinline__ const char *at(uint32_t voff, uint32_t row) const {
+    return reinterpret_cast<const char *>(base + row) + voff;
+  }
+  __device__ __forceinline__ float ld(uint32_t voff, uint32_t row) const {
+    return *reinterpret_cast<const float *>(at(voff, row));
+  }
+  __device__ __forceinline__ float ldv(uint32_t voff, uint32_t row) const { return ld(voff, row); }
+  __device__ __forceinline__ f4 ld4(uint32_t voff, uint32_t row) const {
+    return *reinterpret_cast<const f4u *>(at(voff, row));
+  }
+  __device__ __forceinline__ f4 ld4v(uint32_t voff, uint32_t row) const { return ld4(voff, row); }
+};
+
+__device__ __forceinline__ Table make_table(const float *base, uint32_t extent, int K) {
+  return Table{base, (uint32_t)K, extent - (uint32_t)K};
+}
+#else
+struct Table {
+  rsrc_t rs;
+  uint32_t step;   // bytes per row (4 K)
+  __device__ __forceinline__ uint32_t row(uint32_t id) const { return id * step; }
+  __device__ __forceinline__ float ld(uint32_t voff, uint32_t row) const {
+    return load_f32(rs, voff, row);
+  }
+  __device__ __forceinline__ float ldv(uint32_t voff, uint32_t row) const {
+    return load_f32(rs, voff + row, 0);
+  }
+  __device__ __forceinline__ f4 ld4(uint32_t voff, uint32_t row) const {
+    return load_f32x4(rs, voff, row);
+  }
+  __device__ __forceinline__ f4 ld4v(uint32_t voff, uint32_t row) const {
+    return load_f32x4(rs, voff + row, 0);
+  }
+};
+
+__device__ __forceinline__ Table make_table(const float *base, uint32_t extent, int K) {
+  return Table{make_rsrc(base, extent), (uint32_t)K * 4u};
+}
+#endif
+
 // Sum of the four theta-phi products of a leaf of four topics, in topic order
 // (the products of topics 1..3 are fused multiply-adds onto the running sum).
 __device__ __forceinline__ float dot4(f4 t, f4 x) {
@@ -250,4 +323,4 @@ __device__ __forceinline__ float prefix_step(float sum, float th, float ph) {
 }
 
 
-}  // namespace lda
+}  // namespace LDA_NS

@@ -25,7 +25,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace lda {
+#include "config.hpp"
+
+namespace LDA_NS {
 namespace {
 
 constexpr int kCountThreads = 256;                     // threads per workgroup
@@ -186,4 +188,4 @@ __global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

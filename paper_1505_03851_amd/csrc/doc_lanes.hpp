@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Document-per-lane driver (Algorithm 7 with the theta cache of Algorithm 5):
@@ -29,7 +29,7 @@ __device__ __forceinline__ float theta_factor(const Wave<W, false> &w, const flo
   if constexpr (THETA_LDS)
     return cache[(blk * W + k) * kWave + lane_id()];
   else
-    return topic_of(w, blk) >= 0 ? load_row<W>(w.th_rs, voff, theta_row(w, k)) : 0.0f;
+    return topic_of(w, blk) >= 0 ? load_row<W>(w.th, voff, theta_row(w, k)) : 0.0f;
 }
 
 template <int W, bool THETA_LDS>
@@ -37,7 +37,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(L
 void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                       const int64_t *__restrict__ offsets, const int32_t *__restrict__ word_id,
                       UniformSource u, int32_t *__restrict__ z, int64_t N, int M,
-                      int K, int S, uint32_t theta_bytes, uint32_t phi_bytes) {
+                      int K, int S, uint32_t theta_extent, uint32_t phi_extent) {
   extern __shared__ float lds[];
   constexpr int LOG2W = (W == 64) ? 6 : 5;
   const int lane = lane_id();
@@ -55,11 +55,10 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
 
   const int NB = (K + W - 1) >> LOG2W;
   Wave<W, false> w;
-  w.th_rs = make_rsrc(theta, theta_bytes);
-  w.ph_rs = make_rsrc(phi, phi_bytes);
+  w.th = make_table(theta, theta_extent, K);
+  w.ph = make_table(phi, phi_extent, K);
   w.wp = nullptr;
   w.last = kWave - 1;
-  w.row_bytes = (uint32_t)K * 4u;
   w.R = K & (W - 1);
   w.c0 = w.R ? w.R - W : 0;
   w.r = lane & (W - 1);
@@ -68,7 +67,7 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
   w.mode = kAnyDocs;
   w.kb = 0;
   w.th_off0 = w.th_off1 = 0;
-  w.th_lane = (uint32_t)doc * w.row_bytes;
+  w.th_lane = w.th.row((uint32_t)doc);
 
   const int cache_rows = THETA_LDS ? NB * W : 0;
   float *cache = lds + wave * (cache_rows + NB) * kWave;
@@ -79,7 +78,7 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
       const bool real = topic_of(w, b) >= 0;
 #pragma unroll 8
       for (int k = 0; k < W; ++k) {
-        const float th = load_row<W>(w.th_rs, voff, theta_row(w, k));
+        const float th = load_row<W>(w.th, voff, theta_row(w, k));
         cache[(b * W + k) * kWave + lane] = real ? th : 0.0f;
       }
     }
@@ -88,7 +87,7 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
   for (int64_t i = stride0; __builtin_amdgcn_ballot_w64(i < len) != 0; i += S) {
     const int64_t n = len > 0 ? start + (i < len ? i : len - 1) : 0;
     const bool store = i < len;
-    w.ph_lane = (uint32_t)word_id[n] * w.row_bytes;
+    w.ph_lane = w.ph.row((uint32_t)word_id[n]);
     const float un = u(n);
 
     float a[W];
@@ -99,7 +98,7 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
       const uint32_t voff = col_bytes(w, b);
 #pragma unroll
       for (int k = 0; k < W; ++k) {
-        const float ph = load_row<W>(w.ph_rs, voff, (uint32_t)group_value<W>((int)w.ph_lane, k));
+        const float ph = load_row<W>(w.ph, voff, (uint32_t)group_value<W>((int)w.ph_lane, k));
         a[k] = theta_factor<W, THETA_LDS>(w, cache, b, k, voff) * ph;
       }
       reduce_stage<W, W / 2>(a);
@@ -126,12 +125,12 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
       const int bk = group_value<W>(blk, k);
       const int t = w.c0 + bk * W + w.r;
       const uint32_t voff = (uint32_t)(t < 0 ? 0 : t) * 4u;
-      const float ph = load_row<W>(w.ph_rs, voff, (uint32_t)group_value<W>((int)w.ph_lane, k));
+      const float ph = load_row<W>(w.ph, voff, (uint32_t)group_value<W>((int)w.ph_lane, k));
       float th;
       if constexpr (THETA_LDS)
         th = cache[(bk * W + k) * kWave + lane];
       else
-        th = t < 0 ? 0.0f : load_row<W>(w.th_rs, voff, theta_row(w, k));
+        th = t < 0 ? 0.0f : load_row<W>(w.th, voff, theta_row(w, k));
       a[k] = th * ph;
     }
     butterfly_block<W>(a, w.r, NoStore{});
@@ -143,4 +142,4 @@ void doc_lanes_kernel(const float *__restrict__ theta, const float *__restrict__
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

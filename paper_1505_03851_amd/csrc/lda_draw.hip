@@ -37,6 +37,8 @@
 #include "tile.hpp"
 #include "one_topic.hpp"
 #include "leaf_eighths.hpp"
+#include "draw_dispatch.hpp"
+#include "wide.hpp"
 #include "routed_draw.hpp"
 #include "leaf_group.hpp"
 #include "transposed.hpp"
@@ -49,15 +51,21 @@ namespace {
 
 thread_local hipError_t g_last_hip = hipSuccess;
 
+// theta or phi larger than LDA_MAX_TABLE_BYTES: drawn by the wide build
+bool wide_tables(int32_t M, int32_t V, int32_t K) {
+  return (int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES;
+}
+
+// WIDE_OK: the entry point draws tables up to LDA_MAX_WIDE_TABLE_BYTES (with
+// the wide build past LDA_MAX_TABLE_BYTES); otherwise up to
+// LDA_MAX_TABLE_BYTES (unsigned 32-bit byte offsets).
 int check_args(const void *theta, const void *phi, const void *doc_id,
                const void *word_id, const void *u, const void *z, int64_t N,
-               int32_t M, int32_t V, int32_t K) {
+               int32_t M, int32_t V, int32_t K, bool wide_ok = false) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_MAX_N) return LDA_ERR_UNSUPPORTED;
-  // theta and phi are addressed with unsigned 32-bit byte offsets
-  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
-    return LDA_ERR_UNSUPPORTED;
+  const int64_t limit = wide_ok ? LDA_MAX_WIDE_TABLE_BYTES : LDA_MAX_TABLE_BYTES;
+  if ((int64_t)M * K * 4 > limit || (int64_t)V * K * 4 > limit) return LDA_ERR_UNSUPPORTED;
   if (N == 0) return LDA_OK;
   const void *ptrs[] = {theta, phi, doc_id, word_id, u, z};
   for (const void *p : ptrs) {
@@ -76,109 +84,11 @@ int finish_launch() {
   return LDA_OK;
 }
 
-int width_for(int32_t K) { return K >= 64 ? 64 : 32; }
-
-// The rebuilt block's table goes to LDS only for block counts up to
-// LDA_LDS_TABLE_MAX_BLOCKS.  Measured on MI355X, the register table searched
-// with the search-assist shuffle loop is faster at every K (the LDS table
-// costs 16 KiB per wavefront and with it occupancy), so the default is 0 and
-// the LDS variant is kept for comparison builds.
-bool lds_table_for(int32_t K) {
-  const int nb = (K + width_for(K) - 1) / width_for(K);
-  return nb <= LDA_LDS_TABLE_MAX_BLOCKS;
-}
-
-// The half-block tail (W = 64) for block counts up to LDA_HALF_MAX_BLOCKS:
-// it doubles the LDS rows of the block prefixes.
-bool half_tail_for(int32_t K) {
-  const int nb = (K + 63) / 64;
-  return nb >= 2 && nb <= LDA_HALF_MAX_BLOCKS;
-}
-
-dim3 wave_grid(int64_t N, int wpb = kWavesPerBlock) {
-  const int64_t waves = (N + kWave - 1) / kWave;
-  return dim3((unsigned)((waves + wpb - 1) / wpb));
-}
-
 template <int KMAX>
 void launch_naive(const float *theta, const float *phi, DocSource d, const int32_t *w,
                   UniformSource u, int32_t *z, int64_t N, int32_t K, hipStream_t s) {
   const dim3 grid((unsigned)((N + 255) / 256));
   naive_kernel<KMAX><<<grid, 256, 0, s>>>(theta, phi, d, w, u, z, N, K);
-}
-
-// 256-topic blocks of the eighths kernel (the remnant of K mod 256 included).
-int eighths_blocks(int32_t K) { return (K + kBlock4 - 1) / kBlock4; }
-
-// Wavefronts per workgroup of the eighths kernel: 4 while three such
-// workgroups fit in a CU's LDS (8 rows of 64 floats per block and wavefront),
-// else 2.
-bool eighths_wide_groups(int32_t K) {
-  return 3LL * 4 * 8 * eighths_blocks(K) * kWave * (int64_t)sizeof(float) <= 160 * 1024;
-}
-// Whether one-document wavefronts stage their theta row in LDS for the
-// rebuild: while three 4-wavefront workgroups still fit with it.
-bool eighths_stage_theta(int32_t K) {
-  return 3LL * 4 * eighths_lds_floats(eighths_blocks(K), true) * (int64_t)sizeof(float) <=
-         160 * 1024;
-}
-
-template <int C, int WPEU, bool PAD>
-void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
-                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
-                    hipStream_t s) {
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  const int NB = eighths_blocks(K);
-  const size_t rows = (size_t)eighths_lds_floats(NB, false) * sizeof(float);
-  const size_t staged = (size_t)eighths_lds_floats(NB, true) * sizeof(float);
-  if (eighths_stage_theta(K))
-    leaf_eighths_kernel<C, 4, WPEU, PAD, true><<<wave_grid(N, 4), 4 * kWave, 4 * staged, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-  else if (eighths_wide_groups(K))
-    leaf_eighths_kernel<C, 4, WPEU, PAD, false><<<wave_grid(N, 4), 4 * kWave, 4 * rows, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-  else
-    leaf_eighths_kernel<C, 2, WPEU, PAD, false><<<wave_grid(N, 2), 2 * kWave, 2 * rows, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-}
-
-template <int C, int WPEU>
-void launch_eighths(const float *theta, const float *phi, DocSource d, const int32_t *wd,
-                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
-                    hipStream_t s) {
-  if (K % kBlock4 == 0)
-    launch_eighths<C, WPEU, false>(theta, phi, d, wd, u, z, N, M, V, K, s);
-  else
-    launch_eighths<C, WPEU, true>(theta, phi, d, wd, u, z, N, M, V, K, s);
-}
-
-// The leaf-group kernel: K divisible by 4, up to LDA_GROUP_MAX_K (at most
-// 256) topics, N >= 64; groups of 8, 16, 32 or 64 lanes for K up to 32, 64,
-// 128, 256.  Measured on MI355X against the kernels it replaces there: 2.0x to
-// 2.6x faster than the one-topic kernel for K = 16 ... 128, 5-8% faster than
-// the eighths kernel for K = 144 ... 256.
-bool groups_for(int64_t N, int32_t K) {
-  return N >= kWave && K % kLeaf == 0 && K <= LDA_GROUP_MAX_K && K <= kLeaf * kWave;
-}
-
-template <int G, int H>
-void launch_groups(const float *theta, const float *phi, DocSource d, const int32_t *wd,
-                   UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
-                   hipStream_t s) {
-  constexpr int CW = G == kWave ? LDA_GROUP64_WINDOW : LDA_GROUP_WINDOW;
-  constexpr int C = CW < G ? CW : G;
-  // (8-topic leaves hold twice the registers: the 64-lane groups' setting)
-  constexpr int WPEU = G == kWave || H > 1 ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  const size_t lds = (size_t)kWavesPerBlock * group_lds_bytes<G, H>();
-  if (K == kLeaf * H * G)
-    leaf_group_kernel<G, H, C, WPEU, false><<<wave_grid(N), kBlockThreads, lds, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-  else
-    leaf_group_kernel<G, H, C, WPEU, true><<<wave_grid(N), kBlockThreads, lds, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
 }
 
 // Launch of the routed kernel over lists of at most max_len positions: 16
@@ -189,8 +99,8 @@ template <bool PAD>
 void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt, UniformSource u,
                    int32_t *z, int64_t max_len, int32_t M, int32_t V, int32_t K, hipStream_t s) {
   constexpr int C = LDA_EIGHTHS_WINDOW, WPEU = LDA_EIGHTHS_WAVES_PER_EU;
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const uint32_t tb = table_extent(M, K);
+  const uint32_t pb = table_extent(V, K);
   const size_t per_wave = (size_t)routed_lds_floats(eighths_blocks(K)) * sizeof(float);
   if (3 * 4 * per_wave <= 160 * 1024) {
     const int64_t tiles = (max_len + 4 * kWave - 1) / (4 * kWave);
@@ -203,25 +113,13 @@ void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt,
   }
 }
 
-// The eighths kernel takes K divisible by 4 (16-byte leaves) from
-// LDA_EIGHTHS_MIN_K topics to LDA_EIGHTHS_MAX_BLOCKS 256-topic blocks, for
-// N >= 64.  Measured on MI355X against the one-topic kernel: 15-30% faster
-// from K = 144 (K = 144 ... 240 on the paper-shaped corpus), 7% at K = 256,
-// 4% at K = 1024, 5% at K = 2048; 3-4% slower at K = 80 and 112, whose
-// padding fills most of the block.  (The dispatch gives K up to 256 to the
-// leaf-group kernel first.)
-bool eighths_for(int64_t N, int32_t K) {
-  return N >= kWave && K % kLeaf == 0 && K >= LDA_EIGHTHS_MIN_K &&
-         eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
-}
-
 void launch_transposed(const float *theta, const float *phi, DocSource d,
                        const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
   const int nb = (K + kWave - 1) / kWave;
   const size_t lds = (size_t)kWavesPerBlock * (kTileFloats + nb * kWave) * sizeof(float);
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const uint32_t tb = table_extent(M, K);
+  const uint32_t pb = table_extent(V, K);
   if (N < kWave)
     transposed_kernel<true><<<wave_grid(N), kBlockThreads, lds, s>>>(theta, phi, d, wd, u, z, N,
                                                                       K, tb, pb);
@@ -229,23 +127,6 @@ void launch_transposed(const float *theta, const float *phi, DocSource d,
     transposed_kernel<false><<<wave_grid(N), kBlockThreads, lds, s>>>(theta, phi, d, wd, u, z,
                                                                        N, K, tb, pb);
 }
-
-template <int W, bool LDS_TABLE, bool ALT = false, bool HALF = false, int WPB = kWavesPerBlock>
-void launch_butterfly(const float *theta, const float *phi, DocSource d,
-                      const int32_t *wd, UniformSource u, int32_t *z, int64_t N,
-                      int32_t M, int32_t V, int32_t K, hipStream_t s) {
-  const int nb = (K + W - 1) / W;  // blocks, the remnant included
-  const size_t lds = (size_t)WPB * region_rows(nb, W, LDS_TABLE, HALF) * kWave * sizeof(float);
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
-  if (N < kWave)
-    butterfly_kernel<W, LDS_TABLE, true, ALT, HALF, WPB><<<wave_grid(N, WPB), WPB * kWave, lds, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-  else
-    butterfly_kernel<W, LDS_TABLE, false, ALT, HALF, WPB><<<wave_grid(N, WPB), WPB * kWave, lds, s>>>(
-        theta, phi, d, wd, u, z, N, K, tb, pb);
-}
-
 
 // The W = 32 / 64 butterfly kernel with a chosen table: in registers with the
 // paper's search-assist loop, in LDS with direct reads, or the alternative
@@ -289,69 +170,13 @@ template <int W, bool THETA_LDS>
 void launch_doc_lanes(const float *theta, const float *phi, const int64_t *off,
                       const int32_t *wd, UniformSource u, int32_t *z, int64_t N, int32_t M,
                       int32_t V, int32_t K, hipStream_t s) {
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const uint32_t tb = table_extent(M, K);
+  const uint32_t pb = table_extent(V, K);
   const int S = doc_lanes_split(N, M);
   const int64_t groups = (M + kWave - 1) / kWave;
   doc_lanes_kernel<W, THETA_LDS>
       <<<wave_grid(groups * S * kWave), kBlockThreads, doc_lanes_lds(K, THETA_LDS), s>>>(
           theta, phi, off, wd, u, z, N, M, K, S, tb, pb);
-}
-
-// The leaf-group kernel with groups just wide enough for K: K up to 32, 64,
-// 128, 256 topics take 8, 16, 32, 64 lanes with 4-topic leaves (H = 1), half
-// as many with 8-topic leaves (H = 2).
-template <int H>
-void dispatch_groups(const float *theta, const float *phi, DocSource d, const int32_t *word_id,
-                     UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
-                     hipStream_t s) {
-  if (K <= kLeaf * 8)
-    launch_groups<8 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-  else if (K <= kLeaf * 16)
-    launch_groups<16 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-  else if (K <= kLeaf * 32)
-    launch_groups<32 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-  else
-    launch_groups<64 / H, H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-}
-
-// The butterfly draw for either document source (kernel choice by K); with
-// H = 2 the leaf groups take 8-topic leaves.
-template <int H = LDA_GROUP_LEAF / kLeaf>
-void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
-                        const int32_t *word_id, UniformSource u, int32_t *z, int64_t N,
-                        int32_t M, int32_t V, int32_t K, hipStream_t s) {
-  if (groups_for(N, K)) {
-    dispatch_groups<H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    return;
-  }
-  if (eighths_for(N, K)) {
-    // launch shapes measured on MI355X: up to five blocks, 16 tokens in
-    // flight per wavefront at 2 wavefronts per SIMD (1-2% faster than 8 at 3
-    // or 4 at 4); six to eight, 4 at 4 (3-5% faster than 16 at 2 or 8 at 3;
-    // 2 in flight: 30% slower)
-    if (eighths_blocks(K) <= LDA_EIGHTHS_SPLIT)
-      launch_eighths<LDA_EIGHTHS_WINDOW, LDA_EIGHTHS_WAVES_PER_EU>(theta, phi, d, word_id, u, z,
-                                                                   N, M, V, K, s);
-    else
-      launch_eighths<LDA_EIGHTHS_WINDOW_LARGE, LDA_EIGHTHS_WAVES_PER_EU_LARGE>(
-          theta, phi, d, word_id, u, z, N, M, V, K, s);
-    return;
-  }
-  const bool lt = lds_table_for(K);
-  if (width_for(K) == 64) {
-    if (lt)
-      launch_butterfly<64, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else if (half_tail_for(K))
-      launch_butterfly<64, false, false, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else
-      launch_butterfly<64, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-  } else {
-    if (lt)
-      launch_butterfly<32, true>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-    else
-      launch_butterfly<32, false>(theta, phi, d, word_id, u, z, N, M, V, K, s);
-  }
 }
 
 // Workspace of the routing: the routed arrays and the builder's tables, each
@@ -434,11 +259,14 @@ extern "C" int lda_draw_butterfly(const float *theta, const float *phi,
                                   const float *u, int32_t *z, int64_t N,
                                   int32_t M, int32_t V, int32_t K,
                                   void *stream) {
-  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
+  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K, true);
   if (st != LDA_OK || N == 0) return st;
-  const UniformSource us{u, 0, 0, 0};
-  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id, us, z, N, M, V, K,
-                     static_cast<hipStream_t>(stream));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (wide_tables(M, V, K))
+    lda_wide::draw(theta, phi, doc_id, nullptr, word_id, u, 0, 0, 0, z, N, M, V, K, s);
+  else
+    dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id,
+                       UniformSource{u, 0, 0, 0}, z, N, M, V, K, s);
   return finish_launch();
 }
 
@@ -513,13 +341,32 @@ extern "C" int lda_draw_butterfly_philox(const float *theta, const float *phi,
                                          int32_t K, uint64_t seed, uint32_t sweep,
                                          void *stream) {
   // (z stands in for the absent u in the pointer checks)
-  const int st = check_args(theta, phi, doc_id, word_id, z, z, N, M, V, K);
+  const int st = check_args(theta, phi, doc_id, word_id, z, z, N, M, V, K, true);
   if (st != LDA_OK || N == 0) return st;
-  const UniformSource us{nullptr, (uint32_t)seed, (uint32_t)(seed >> 32), sweep};
-  dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id, us, z, N, M, V, K,
-                     static_cast<hipStream_t>(stream));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  const uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
+  if (wide_tables(M, V, K))
+    lda_wide::draw(theta, phi, doc_id, nullptr, word_id, nullptr, k0, k1, sweep, z, N, M, V, K,
+                   s);
+  else
+    dispatch_butterfly(theta, phi, DocSource{doc_id, nullptr, M, N}, word_id,
+                       UniformSource{nullptr, k0, k1, sweep}, z, N, M, V, K, s);
   return finish_launch();
 }
+
+namespace lda {
+namespace {
+
+// The in-kernel uniforms written out: u[i] = uniform of token first + i.
+__global__ __launch_bounds__(256) void uniforms_kernel(float *__restrict__ u, int64_t count,
+                                                       int64_t first, UniformSource us) {
+  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
+  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
+    u[i] = us(first + i);
+}
+
+}  // namespace
+}  // namespace lda
 
 extern "C" int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
                                    uint32_t sweep, void *stream) {
@@ -538,12 +385,15 @@ extern "C" int lda_draw_docs(const float *theta, const float *phi,
                              const int64_t *doc_offsets, const int32_t *word_id,
                              const float *u, int32_t *z, int64_t N, int32_t M,
                              int32_t V, int32_t K, void *stream) {
-  int st = check_args(theta, phi, doc_offsets, word_id, u, z, N, M, V, K);
+  int st = check_args(theta, phi, doc_offsets, word_id, u, z, N, M, V, K, true);
   if (st != LDA_OK || N == 0) return st;
   if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
-  const UniformSource us{u, 0, 0, 0};
-  dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M, N}, word_id, us, z, N, M, V,
-                     K, static_cast<hipStream_t>(stream));
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  if (wide_tables(M, V, K))
+    lda_wide::draw(theta, phi, nullptr, doc_offsets, word_id, u, 0, 0, 0, z, N, M, V, K, s);
+  else
+    dispatch_butterfly(theta, phi, DocSource{nullptr, doc_offsets, M, N}, word_id,
+                       UniformSource{u, 0, 0, 0}, z, N, M, V, K, s);
   return finish_launch();
 }
 
@@ -557,8 +407,8 @@ extern "C" int lda_butterfly_table(const float *theta, const float *phi,
                             K);
   if (st != LDA_OK || N == 0) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const uint32_t tb = (uint32_t)((int64_t)M * K * 4);
-  const uint32_t pb = (uint32_t)((int64_t)V * K * 4);
+  const uint32_t tb = table_extent(M, K);
+  const uint32_t pb = table_extent(V, K);
   if (width_for(K) == 64)
     table_kernel<64, true><<<wave_grid(N), kBlockThreads, 0, s>>>(
         theta, phi, doc_id, word_id, table, N, K, tb, pb);

@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Leaf kernel with 32-topic prefix rows (K divisible by 4, from
@@ -75,8 +75,8 @@ __device__ __forceinline__ uint32_t leaf_bytes(int c0, int blk, int r) {
 
 // Theta leaf of block `blk` at row offset `row`; zero for a padding leaf.
 template <bool PAD>
-__device__ __forceinline__ f4 theta_leaf(rsrc_t rs, int c0, int blk, int r, uint32_t row) {
-  const f4 t = load_f32x4(rs, leaf_bytes(c0, blk, r), row);
+__device__ __forceinline__ f4 theta_leaf(const Table &tt, int c0, int blk, int r, uint32_t row) {
+  const f4 t = tt.ld4(leaf_bytes(c0, blk, r), row);
   if constexpr (PAD) {
     const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
     return leaf_topic(c0, blk, r) >= 0 ? t : zero;
@@ -99,11 +99,11 @@ struct FewDocs {
 
 // Loads of block `blk`'s leaves of the wavefront's runs (to be staged later).
 template <bool PAD>
-__device__ __forceinline__ void few_load(const FewDocs &fd, rsrc_t th_rs, int c0, int blk, int r,
+__device__ __forceinline__ void few_load(const FewDocs &fd, const Table &tt, int c0, int blk, int r,
                                          f4 (&st)[kFewMax]) {
 #pragma unroll
   for (int d = 0; d < kFewMax; ++d)
-    if (d < fd.D) st[d] = theta_leaf<PAD>(th_rs, c0, blk, r, fd.row[d]);
+    if (d < fd.D) st[d] = theta_leaf<PAD>(tt, c0, blk, r, fd.row[d]);
 }
 
 // Stage the loaded leaves in LDS.  The wavefront's earlier LDS reads are
@@ -149,7 +149,7 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
   // this block's last reads of the staged leaves have been issued (CT slots
   // before the block's end)
   f4 st[kFewMax];
-  if constexpr (MODE == kFewDocs && PREFETCH) few_load<PAD>(fd, w.th_rs, c0, next, w.r, st);
+  if constexpr (MODE == kFewDocs && PREFETCH) few_load<PAD>(fd, w.th, c0, next, w.r, st);
   if constexpr (TS && MODE == kOneDoc) fd.lds[blk * kWave + lane] = th[0];
   float s[kWave / 2];
   float lo = 0.0f;
@@ -180,12 +180,12 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
       const int tn = eighth_slot_token(pair_token(refill ? i + C : i + C - kWave));
       const uint32_t voff = refill ? vcur : vnext;
       if (!refill && (MODE == kOneDoc || MODE == kTwoDocs) && i + C == kWave) {
-        thn[0] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off0);
-        if constexpr (MODE == kTwoDocs) thn[1] = theta_leaf<PAD>(w.th_rs, c0, next, w.r, w.th_off1);
+        thn[0] = theta_leaf<PAD>(w.th, c0, next, w.r, w.th_off0);
+        if constexpr (MODE == kTwoDocs) thn[1] = theta_leaf<PAD>(w.th, c0, next, w.r, w.th_off1);
       }
-      win[i % C] = load_f32x4(w.ph_rs, voff, __builtin_amdgcn_readlane(w.ph_lane, tn));
+      win[i % C] = w.ph.ld4(voff, __builtin_amdgcn_readlane(w.ph_lane, tn));
       if constexpr (MODE == kAnyDocs)
-        twin[i % C] = load_f32x4(w.th_rs, voff, __builtin_amdgcn_readlane(w.th_lane, tn));
+        twin[i % C] = w.th.ld4(voff, __builtin_amdgcn_readlane(w.th_lane, tn));
     }
     if constexpr (MODE == kFewDocs) {
       const bool trefill = i + CT < kWave;
@@ -237,20 +237,20 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
   f4 win[C], twin[CT], th[2], thn[2];
   const uint32_t v0 = leaf_bytes(c0, 0, w.r);
   if constexpr (MODE == kOneDoc || MODE == kTwoDocs) {
-    th[0] = theta_leaf<PAD>(w.th_rs, c0, 0, w.r, w.th_off0);
-    th[1] = MODE == kTwoDocs ? theta_leaf<PAD>(w.th_rs, c0, 0, w.r, w.th_off1) : th[0];
+    th[0] = theta_leaf<PAD>(w.th, c0, 0, w.r, w.th_off0);
+    th[1] = MODE == kTwoDocs ? theta_leaf<PAD>(w.th, c0, 0, w.r, w.th_off1) : th[0];
   }
   if constexpr (MODE == kFewDocs) {
     f4 st[kFewMax];
-    few_load<PAD>(fd, w.th_rs, c0, 0, w.r, st);
+    few_load<PAD>(fd, w.th, c0, 0, w.r, st);
     few_stage(fd, st, lane_id());
   }
 #pragma unroll
   for (int i = 0; i < C; ++i) {
     const int t = eighth_slot_token(pair_token(i));
-    win[i] = load_f32x4(w.ph_rs, v0, __builtin_amdgcn_readlane(w.ph_lane, t));
+    win[i] = w.ph.ld4(v0, __builtin_amdgcn_readlane(w.ph_lane, t));
     if constexpr (MODE == kAnyDocs)
-      twin[i] = load_f32x4(w.th_rs, v0, __builtin_amdgcn_readlane(w.th_lane, t));
+      twin[i] = w.th.ld4(v0, __builtin_amdgcn_readlane(w.th_lane, t));
     if constexpr (MODE == kFewDocs)
       if (i < CT) twin[i % CT] = few_leaf(fd, t, lane_id());
   }
@@ -282,7 +282,7 @@ __device__ __forceinline__ void load_chunk_staged(const Wave<kWave / 2, false> &
     const int t = first + i;
     const uint32_t voff = (uint32_t)(PADDED && t < 0 ? 0 : t) * 4u;
     const uint32_t poff = (uint32_t)group_value<kWave / 2>((int)w.ph_lane, k);
-    a[k] = trow[i] * load_row<kWave / 2>(w.ph_rs, voff, poff);
+    a[k] = trow[i] * load_row<kWave / 2>(w.ph, voff, poff);
   }
 }
 
@@ -298,7 +298,7 @@ __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPE
 void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                          DocSource docs, const int32_t *__restrict__ word_id,
                          UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
-                         uint32_t theta_bytes, uint32_t phi_bytes) {
+                         uint32_t theta_extent, uint32_t phi_extent) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -317,7 +317,7 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
   const int NB = (K + kBlock4 - 1) / kBlock4;
   const int c0 = K - NB * kBlock4;
   Wave<kWave, false> w;
-  init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, kWave - 1, K,
+  init_wave<kWave, false>(w, theta, phi, theta_extent, phi_extent, word_id, t0, kWave - 1, K,
                           lane, doc, word);
   float *region = lds + wave * eighths_lds_floats(NB, TS);
   FewDocs stage{};
@@ -364,4 +364,4 @@ void leaf_eighths_kernel(const float *__restrict__ theta, const float *__restric
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Leaf groups for K up to 256 (K divisible by 4, at most 4 G topics for a
@@ -71,7 +71,7 @@ __device__ __forceinline__ float leaf_dot(const Leaf<H> &t, const Leaf<H> &p) {
 // voff[h]: byte offset of quad h of this lane's leaf in a row; real[h]: the
 // quad holds topics (false: front padding, its theta is zero).
 template <int G, int H, int C, int MODE>
-__device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t ph_rs,
+__device__ __forceinline__ void group_tile(float (&a)[G], const Table &th_t, const Table &ph_t,
                                            const uint32_t (&voff)[H], const bool (&real)[H],
                                            uint32_t ph_lane, uint32_t th_lane, int gbase,
                                            uint64_t gstarts, f4 *stage) {
@@ -81,16 +81,16 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   // leaf of token k of the group at row offset `row` of that token (held by
   // the lane that owns the token): with G = 64 the row is uniform and goes in
   // the scalar offset, else it is fetched per lane
-  const auto leaf_of = [&](rsrc_t rs, uint32_t row, int k) {
+  const auto leaf_of = [&](const Table &t, uint32_t row, int k) {
     Leaf<H> l;
     if constexpr (G == kWave) {
       const uint32_t srow = (uint32_t)__builtin_amdgcn_readlane((int)row, k);
 #pragma unroll
-      for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(rs, voff[h], srow);
+      for (int h = 0; h < H; ++h) l.q[h] = t.ld4(voff[h], srow);
     } else {
       const uint32_t vrow = (uint32_t)__builtin_amdgcn_ds_bpermute((gbase + k) << 2, (int)row);
 #pragma unroll
-      for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(rs, voff[h] + vrow, 0);
+      for (int h = 0; h < H; ++h) l.q[h] = t.ld4v(voff[h], vrow);
     }
     return l;
   };
@@ -105,16 +105,16 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   if constexpr (MODE == kGroupOne) {
     Leaf<H> l;
 #pragma unroll
-    for (int h = 0; h < H; ++h) l.q[h] = load_f32x4(th_rs, voff[h] + th_lane, 0);
+    for (int h = 0; h < H; ++h) l.q[h] = th_t.ld4v(voff[h], th_lane);
     th[0] = mask(l);
   } else if constexpr (MODE == kGroupRuns) {
     uint64_t m = gstarts;
-    th[0] = mask(leaf_of(th_rs, th_lane, 0));
+    th[0] = mask(leaf_of(th_t, th_lane, 0));
 #pragma unroll
     for (int j = 1; j < R; ++j) {
       const int p = m ? (int)__builtin_ctzll(m) : 0;
       m &= m - 1;
-      th[j] = mask(leaf_of(th_rs, th_lane, p));
+      th[j] = mask(leaf_of(th_t, th_lane, p));
     }
   }
   if constexpr (MODE != kGroupAny) {
@@ -143,8 +143,8 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
   Leaf<H> win[C], twin[CT];
 #pragma unroll
   for (int k = 0; k < C; ++k) {
-    win[k] = leaf_of(ph_rs, ph_lane, k);
-    if constexpr (MODE == kGroupAny) twin[k] = leaf_of(th_rs, th_lane, k);
+    win[k] = leaf_of(ph_t, ph_lane, k);
+    if constexpr (MODE == kGroupAny) twin[k] = leaf_of(th_t, th_lane, k);
   }
   if constexpr (STAGED) {
 #pragma unroll
@@ -169,8 +169,8 @@ __device__ __forceinline__ void group_tile(float (&a)[G], rsrc_t th_rs, rsrc_t p
     }
     a[k] = leaf_dot(tv, win[k % C]);
     if (k + C < G) {
-      win[k % C] = leaf_of(ph_rs, ph_lane, k + C);
-      if constexpr (MODE == kGroupAny) twin[k % C] = leaf_of(th_rs, th_lane, k + C);
+      win[k % C] = leaf_of(ph_t, ph_lane, k + C);
+      if constexpr (MODE == kGroupAny) twin[k % C] = leaf_of(th_t, th_lane, k + C);
     }
     if constexpr (STAGED)
       if (k + CT < G) twin[k % CT] = staged(k + CT);
@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(W
 void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                        DocSource docs, const int32_t *__restrict__ word_id,
                        UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
-                       uint32_t theta_bytes, uint32_t phi_bytes) {
+                       uint32_t theta_extent, uint32_t phi_extent) {
   constexpr int L = kLeaf * H;
   extern __shared__ float lds[];
   const int lane = lane_id();
@@ -200,11 +200,10 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   const int word = word_id[n];
   const float un = u(n);
 
-  const rsrc_t th_rs = make_rsrc(theta, theta_bytes);
-  const rsrc_t ph_rs = make_rsrc(phi, phi_bytes);
-  const uint32_t row_bytes = (uint32_t)K * 4u;
-  const uint32_t ph_lane = (uint32_t)word * row_bytes;
-  const uint32_t th_lane = (uint32_t)doc * row_bytes;
+  const Table th_t = make_table(theta, theta_extent, K);
+  const Table ph_t = make_table(phi, phi_extent, K);
+  const uint32_t ph_lane = ph_t.row((uint32_t)word);
+  const uint32_t th_lane = th_t.row((uint32_t)doc);
   const int r = lane & (G - 1), gbase = lane & ~(G - 1);
   const int c0 = K - L * G;  // first topic of leaf 0 (< 0: front padding)
   uint32_t voff[H];
@@ -231,13 +230,13 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
 
   float a[G];
   if (most == 0)
-    group_tile<G, H, C, kGroupOne>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0,
+    group_tile<G, H, C, kGroupOne>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase, 0,
                                    stage);
   else if (most < kMaxGroupRuns<G>)
-    group_tile<G, H, C, kGroupRuns>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase,
+    group_tile<G, H, C, kGroupRuns>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase,
                                     gstarts, stage);
   else
-    group_tile<G, H, C, kGroupAny>(a, th_rs, ph_rs, voff, real, ph_lane, th_lane, gbase, 0,
+    group_tile<G, H, C, kGroupAny>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase, 0,
                                    stage);
   butterfly_block<G>(a, r, NoStore{});
   const float total = a[G - 1];
@@ -278,10 +277,10 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
     if (staged) {
       tl = stage[(run * H + h) * kWave + gbase + q];
     } else {
-      tl = load_f32x4(th_rs, qoff + th_lane, 0);
+      tl = th_t.ld4v(qoff, th_lane);
       if (PAD && topic < 0) tl = f4{0.0f, 0.0f, 0.0f, 0.0f};
     }
-    const f4 pl = load_f32x4(ph_rs, qoff + ph_lane, 0);
+    const f4 pl = ph_t.ld4v(qoff, ph_lane);
 #pragma unroll
     for (int e = 0; e < kLeaf; ++e) {
       const int idx = kLeaf * h + e;
@@ -294,4 +293,4 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

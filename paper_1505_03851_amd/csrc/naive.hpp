@@ -3,7 +3,7 @@
 
 #include "sources.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Naive kernel (Algorithm 1 with Algorithm 3).  Lane n walks the K topics of
@@ -37,4 +37,4 @@ __global__ __launch_bounds__(256) void naive_kernel(
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Butterfly kernel.  Wavefront g takes tokens [64 g, 64 g + 64); lanes past N
@@ -34,7 +34,7 @@ __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(LDA
 void butterfly_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi, DocSource docs,
     const int32_t *__restrict__ word_id, UniformSource u,
-    int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_bytes, uint32_t phi_bytes) {
+    int32_t *__restrict__ z, int64_t N, int K, uint32_t theta_extent, uint32_t phi_extent) {
   static_assert(!ALT || LDS_TABLE, "the alternative table is searched in LDS");
   static_assert(!HALF || (W == kWave && !LDS_TABLE), "half-block tail: W = 64, register table");
   extern __shared__ float lds[];
@@ -60,7 +60,7 @@ void butterfly_kernel(
   // at its front with empty topics
   const int NB = (K + W - 1) >> LOG2W;
   Wave<W, SMALL> w;
-  init_wave<W, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
+  init_wave<W, SMALL>(w, theta, phi, theta_extent, phi_extent, word_id, t0, last, K,
                       lane, doc, word);
   float *region = lds + wave * region_rows(NB, W, LDS_TABLE, HALF) * kWave;
 
@@ -160,4 +160,4 @@ void butterfly_kernel(
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -12,7 +12,9 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
-namespace lda {
+#include "config.hpp"
+
+namespace LDA_NS {
 
 __device__ __forceinline__ uint32_t philox4x32_10_word0(uint32_t x0, uint32_t x1,
                                                         uint32_t x2, uint32_t x3,
@@ -46,4 +48,4 @@ __device__ __forceinline__ float philox_uniform(uint64_t n, uint32_t sweep, uint
   return (float)(y >> 8) * 0x1p-24f;
 }
 
-}  // namespace lda
+}  // namespace LDA_NS

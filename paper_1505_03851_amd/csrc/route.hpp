@@ -21,9 +21,11 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "config.hpp"
+
 #include <algorithm>
 
-namespace lda {
+namespace LDA_NS {
 
 constexpr int kRouteXcds = 8;           // lists (XCDs of the MI355X)
 constexpr int kRouteClasses = 256;      // word classes
@@ -262,4 +264,4 @@ __global__ void route_pad(const int64_t *__restrict__ lists, int32_t *perm, int3
   }
 }
 
-}  // namespace lda
+}  // namespace LDA_NS

@@ -4,7 +4,7 @@
 #include "leaf_eighths.hpp"
 #include "route.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // The leaf kernel on routed tokens.  Workgroups are dispatched to the GPU's
@@ -35,8 +35,8 @@ __host__ __device__ constexpr int routed_lds_floats(int NB) {
 // (kFewDocs).  region: the wavefront's routed_lds_floats(NB) floats of LDS.
 template <int C, bool PAD>
 __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
-                                            const float *__restrict__ phi, uint32_t theta_bytes,
-                                            uint32_t phi_bytes, int K, const int32_t *wp,
+                                            const float *__restrict__ phi, uint32_t theta_extent,
+                                            uint32_t phi_extent, int K, const int32_t *wp,
                                             int64_t first, int lane, float *region, int64_t n,
                                             bool store, int doc, int word, const UniformSource &u,
                                             int32_t *__restrict__ z) {
@@ -45,7 +45,7 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
   FewDocs fd;
   fd.lds = reinterpret_cast<f4 *>(region + 8 * NB * kWave);
   Wave<kWave, false> w;
-  init_wave<kWave, false>(w, theta, phi, theta_bytes, phi_bytes, wp, first, kWave - 1, K, lane,
+  init_wave<kWave, false>(w, theta, phi, theta_extent, phi_extent, wp, first, kWave - 1, K, lane,
                           doc, word);
   // runs of documents among the wavefront's tokens
   const int prev = __builtin_amdgcn_ds_bpermute(((lane + kWave - 1) & (kWave - 1)) << 2, doc);
@@ -59,7 +59,7 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
     if (m) {
       const int ln = __builtin_ctzll(m);
       m &= m - 1;
-      fd.row[d] = (uint32_t)__builtin_amdgcn_readlane(doc, ln) * w.row_bytes;
+      fd.row[d] = w.th.row((uint32_t)__builtin_amdgcn_readlane(doc, ln));
     }
   }
   // The uniform's load depends on the token index's; issued before the
@@ -105,7 +105,7 @@ template <int C, int WPB, int WPEU, bool PAD>
 __global__ __launch_bounds__(WPB * kWave) __attribute__((amdgpu_waves_per_eu(WPEU)))
 void routed_eighths_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                            RoutedTokens rt, UniformSource u, int32_t *__restrict__ z, int K,
-                           uint32_t theta_bytes, uint32_t phi_bytes) {
+                           uint32_t theta_extent, uint32_t phi_extent) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -119,10 +119,10 @@ void routed_eighths_kernel(const float *__restrict__ theta, const float *__restr
   if (first >= len) return;
   const int64_t i = base + first + lane;
   const int n = rt.perm[i];
-  draw_listed<C, PAD>(theta, phi, theta_bytes, phi_bytes, K, rt.rword + base, first, lane,
+  draw_listed<C, PAD>(theta, phi, theta_extent, phi_extent, K, rt.rword + base, first, lane,
                       lds + wave * routed_lds_floats(NB), n >= 0 ? n : 0, n >= 0, rt.rdoc[i],
                       rt.rword[i], u, z);
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -8,7 +8,7 @@
 #include "philox.hpp"
 #include "tuning.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 constexpr int kWavesPerBlock = LDA_WAVES_PER_BLOCK;
@@ -102,13 +102,5 @@ struct UniformSource {
   }
 };
 
-// The in-kernel uniforms written out: u[i] = uniform of token first + i.
-__global__ __launch_bounds__(256) void uniforms_kernel(float *__restrict__ u, int64_t count,
-                                                       int64_t first, UniformSource us) {
-  const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-  for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < count; i += stride)
-    u[i] = us(first + i);
-}
-
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

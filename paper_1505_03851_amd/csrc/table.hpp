@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Table dump: the per-lane table p[K] of Algorithm 7 for every token, built
@@ -12,8 +12,8 @@ template <int W, bool SMALL>
 __global__ __launch_bounds__(kBlockThreads) void table_kernel(
     const float *__restrict__ theta, const float *__restrict__ phi,
     const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
-    float *__restrict__ table, int64_t N, int K, uint32_t theta_bytes,
-    uint32_t phi_bytes) {
+    float *__restrict__ table, int64_t N, int K, uint32_t theta_extent,
+    uint32_t phi_extent) {
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
@@ -26,7 +26,7 @@ __global__ __launch_bounds__(kBlockThreads) void table_kernel(
   const bool store = lane <= last;
   const int doc = doc_id[n];
   Wave<W, true> w;
-  init_wave<W, true>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
+  init_wave<W, true>(w, theta, phi, theta_extent, phi_extent, word_id, t0, last, K,
                      lane, doc, word_id[n]);
   const int R = w.R;
   const int NB = K / W;
@@ -49,4 +49,4 @@ __global__ __launch_bounds__(kBlockThreads) void table_kernel(
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -3,7 +3,7 @@
 
 #include "sources.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Order one wavefront's earlier LDS writes before its later LDS reads.
@@ -19,10 +19,9 @@ __device__ __forceinline__ void lds_order() {
 // loaded (SMALL: the window is padded by repeating token N - 1).
 template <int W, bool SMALL>
 struct Wave {
-  rsrc_t th_rs, ph_rs;  // theta, phi
+  Table th, ph;         // theta, phi
   const int32_t *wp;    // word_id + t0
   int last;             // SMALL: index in the window of token N - 1
-  uint32_t row_bytes;   // 4 * K
   int R;                // remnant topics (K mod W)
   int c0;               // first topic of block 0: R - W if R > 0 (the remnant is
                         // block 0, padded at its front with W - R empty
@@ -60,34 +59,34 @@ __device__ __forceinline__ int window_at(const int32_t *p, int last, int k) {
   return SMALL ? p[k < last ? k : last] : p[k];
 }
 
-// Byte offset of the phi row of token k of this lane's group: uniform for
+// Row offset of the phi row of token k of this lane's group: uniform for
 // W = 64, one value per half-wave for W = 32.
 template <int W, bool SMALL>
 __device__ __forceinline__ uint32_t phi_row(const Wave<W, SMALL> &w, const int32_t *wp, int k) {
   if constexpr (W == kWave) {
-    return (uint32_t)window_at<SMALL>(wp, w.last, k) * w.row_bytes;
+    return w.ph.row((uint32_t)window_at<SMALL>(wp, w.last, k));
   } else {
-    const uint32_t lo = (uint32_t)window_at<SMALL>(wp, w.last, k) * w.row_bytes;
-    const uint32_t hi = (uint32_t)window_at<SMALL>(wp, w.last, 32 + k) * w.row_bytes;
+    const uint32_t lo = w.ph.row((uint32_t)window_at<SMALL>(wp, w.last, k));
+    const uint32_t hi = w.ph.row((uint32_t)window_at<SMALL>(wp, w.last, 32 + k));
     return w.gbase ? hi : lo;
   }
 }
 
-// Byte offset of the theta row of token k's document, from the lane that
+// Row offset of the theta row of token k's document, from the lane that
 // holds token k (uniform for W = 64, per half-wave for W = 32).
 template <int W, bool SMALL>
 __device__ __forceinline__ uint32_t theta_row(const Wave<W, SMALL> &w, int k) {
   return (uint32_t)group_value<W>((int)w.th_lane, k);
 }
 
-// buffer load at a per-lane offset plus a row offset that is uniform for
-// W = 64 (scalar operand) and per half-wave for W = 32 (added per lane).
+// Load at a per-lane offset plus a row offset that is uniform for W = 64
+// (scalar operand) and per half-wave for W = 32 (per lane).
 template <int W>
-__device__ __forceinline__ float load_row(rsrc_t rs, uint32_t voff, uint32_t row) {
+__device__ __forceinline__ float load_row(const Table &t, uint32_t voff, uint32_t row) {
   if constexpr (W == kWave)
-    return load_f32(rs, voff, row);
+    return t.ld(voff, row);
   else
-    return load_f32(rs, voff + row, 0);
+    return t.ldv(voff, row);
 }
 
 // This lane's topic in block `blk` (negative in the padding of block 0), and
@@ -111,7 +110,7 @@ __device__ __forceinline__ void issue_phi(const Wave<W, SMALL> &w, const int32_t
   const uint32_t voff = col_bytes(w, blk);
 #pragma unroll
   for (int k = LO; k < HI; ++k)
-    a[k] = load_row<W>(w.ph_rs, voff, phi_row(w, wp, reg_token<W, HALF>(k)));
+    a[k] = load_row<W>(w.ph, voff, phi_row(w, wp, reg_token<W, HALF>(k)));
 }
 
 // Theta of block `blk` at this lane's topic, for the first and last document
@@ -120,9 +119,9 @@ template <int W, bool SMALL, int MODE = -1>
 __device__ __forceinline__ void issue_theta(const Wave<W, SMALL> &w, int blk, float &th0,
                                             float &th1) {
   const uint32_t voff = col_bytes(w, blk);
-  th0 = load_f32(w.th_rs, voff, w.th_off0);
+  th0 = w.th.ld(voff, w.th_off0);
   if (MODE == kTwoDocs || (MODE < 0 && w.mode == kTwoDocs))
-    th1 = load_f32(w.th_rs, voff, w.th_off1);
+    th1 = w.th.ld(voff, w.th_off1);
 }
 
 // The stages of the block-total reduce-scatter from BIT down to 1.  With
@@ -232,8 +231,8 @@ __device__ __forceinline__ float sweep_block_any(const Wave<W, SMALL> &w, const 
 #pragma unroll
   for (int k = 0; k < W; ++k) {
     const int t = reg_token<W, HALF>(k);
-    a[k] = (real ? load_row<W>(w.th_rs, voff, theta_row(w, t)) : 0.0f) *
-           load_row<W>(w.ph_rs, voff, phi_row(w, wp, t));
+    a[k] = (real ? load_row<W>(w.th, voff, theta_row(w, t)) : 0.0f) *
+           load_row<W>(w.ph, voff, phi_row(w, wp, t));
   }
   reduce_stage<W, W / 2, HALF>(a);
   reduce_rest<W, SMALL, W / 4, false, HALF>(w, wp, a, 0, lower);
@@ -256,21 +255,20 @@ __device__ __forceinline__ void load_tile_blocks(const Wave<W, SMALL> &w, float 
     const uint32_t voff = (uint32_t)(PADDED && t < 0 ? 0 : t) * 4u;
     const uint32_t toff = (uint32_t)group_value<W>((int)w.th_lane, k);
     const uint32_t poff = (uint32_t)group_value<W>((int)w.ph_lane, k);
-    const float th = load_row<W>(w.th_rs, voff, toff);
-    a[k] = (PADDED && t < 0 ? 0.0f : th) * load_row<W>(w.ph_rs, voff, poff);
+    const float th = load_row<W>(w.th, voff, toff);
+    a[k] = (PADDED && t < 0 ? 0.0f : th) * load_row<W>(w.ph, voff, poff);
   }
 }
 
 template <int W, bool SMALL>
 __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
-                                          const float *phi, uint32_t theta_bytes,
-                                          uint32_t phi_bytes, const int32_t *word_id, int64_t t0, int last,
+                                          const float *phi, uint32_t theta_extent,
+                                          uint32_t phi_extent, const int32_t *word_id, int64_t t0, int last,
                                           int K, int lane, int doc, int word) {
-  w.th_rs = make_rsrc(theta, theta_bytes);
-  w.ph_rs = make_rsrc(phi, phi_bytes);
+  w.th = make_table(theta, theta_extent, K);
+  w.ph = make_table(phi, phi_extent, K);
   w.wp = word_id + t0;
   w.last = last;
-  w.row_bytes = (uint32_t)K * 4u;
   w.R = K & (W - 1);
   w.c0 = w.R ? w.R - W : 0;
   w.r = lane & (W - 1);
@@ -290,10 +288,10 @@ __device__ __forceinline__ void init_wave(Wave<W, SMALL> &w, const float *theta,
     w.mode = kAnyDocs;
     w.kb = 0;
   }
-  w.th_off0 = (uint32_t)d0 * w.row_bytes;
-  w.th_off1 = (uint32_t)d1 * w.row_bytes;
-  w.ph_lane = (uint32_t)word * w.row_bytes;
-  w.th_lane = (uint32_t)doc * w.row_bytes;
+  w.th_off0 = w.th.row((uint32_t)d0);
+  w.th_off1 = w.th.row((uint32_t)d1);
+  w.ph_lane = w.ph.row((uint32_t)word);
+  w.th_lane = w.th.row((uint32_t)doc);
 }
 
 
@@ -303,11 +301,10 @@ template <bool SMALL>
 __device__ __forceinline__ Wave<kWave / 2, SMALL> half_wave(const Wave<kWave, SMALL> &w,
                                                            int lane) {
   Wave<kWave / 2, SMALL> h;
-  h.th_rs = w.th_rs;
-  h.ph_rs = w.ph_rs;
+  h.th = w.th;
+  h.ph = w.ph;
   h.wp = w.wp;
   h.last = w.last;
-  h.row_bytes = w.row_bytes;
   h.R = w.R;
   h.c0 = w.c0;
   h.r = lane & (kWave / 2 - 1);
@@ -400,4 +397,4 @@ __host__ __device__ constexpr int region_rows(int NB, int W, bool lds_table, boo
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

@@ -3,7 +3,7 @@
 
 #include "tile.hpp"
 
-namespace lda {
+namespace LDA_NS {
 namespace {
 
 // Transposed-access kernel (Algorithms 4, 5 and 6 with the binary search of
@@ -35,7 +35,7 @@ __global__ __launch_bounds__(kBlockThreads) __attribute__((amdgpu_waves_per_eu(L
 void transposed_kernel(const float *__restrict__ theta, const float *__restrict__ phi,
                        DocSource docs, const int32_t *__restrict__ word_id,
                        UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
-                       uint32_t theta_bytes, uint32_t phi_bytes) {
+                       uint32_t theta_extent, uint32_t phi_extent) {
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
@@ -51,7 +51,7 @@ void transposed_kernel(const float *__restrict__ theta, const float *__restrict_
   const float un = u(n);
   const int NB = (K + kWave - 1) / kWave;  // the remnant is block 0, padded
   Wave<kWave, SMALL> w;
-  init_wave<kWave, SMALL>(w, theta, phi, theta_bytes, phi_bytes, word_id, t0, last, K,
+  init_wave<kWave, SMALL>(w, theta, phi, theta_extent, phi_extent, word_id, t0, last, K,
                           lane, doc, word);
   float *tile = lds + wave * (kTileFloats + NB * kWave);
   float *region = tile + kTileFloats;
@@ -123,4 +123,4 @@ void transposed_kernel(const float *__restrict__ theta, const float *__restrict_
 }
 
 }  // namespace
-}  // namespace lda
+}  // namespace LDA_NS

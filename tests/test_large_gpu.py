@@ -1,6 +1,8 @@
 """Sizes past 2**31: token counts (every kernel indexes tokens with 64-bit
 integers) and tables (byte offsets into theta, phi and the count tables are
-unsigned 32-bit, so tables up to 4 GiB are addressed).
+unsigned 32-bit, so tables up to 4 GiB are addressed; past 4 GiB
+lda_draw_butterfly, lda_draw_docs and lda_draw_butterfly_philox draw with the
+wide build, float offsets and 64-bit loads, up to 16 GiB).
 
 The large-N inputs are made on the GPU (about 35 GB of token arrays); a
 sample of the tokens -- random ones, the first and last, and those around
@@ -152,4 +154,101 @@ def test_word_counts_past_2_gib():
     assert np.array_equal(got_w, want_w), np.argwhere(got_w != want_w)[:5]
     assert got_w[w_min:].sum() == (word >= w_min).sum()
     del ndk, nwk
+    torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# Tables past 4 GiB: the wide build of the draw kernels.  phi (or theta) of
+# about 4.3 GiB; most tokens take rows past the 2^32-byte offset, the rest
+# rows anywhere; a few carry ids past the table (clamped to its last row by
+# the wide build: such draws are not compared).  Every in-range token is
+# checked against the oracle, for the doc-id form, the offsets form and the
+# in-kernel uniforms.
+
+WIDE_BYTES = int(4.3 * 2 ** 30)
+
+
+def _wide_case(K, seed, big):
+    """`big` = "phi" or "theta": the table past 4 GiB."""
+    rng = np.random.default_rng(seed)
+    rows = WIDE_BYTES // (4 * K) + 1
+    r_min = (1 << 32) // (4 * K) + 1           # first row past the 4 GiB offset
+    assert r_min < rows and 4 * rows * K > (1 << 32)
+    N = 64 * 3000 + 17
+    far = np.where(rng.random(N) < 1 / 3, rng.integers(0, rows, N),
+                   rng.integers(r_min, rows, N)).astype(np.int32)
+    if big == "phi":
+        V, M = rows, 300
+        word = far
+        doc = (np.arange(N, dtype=np.int64) * M // N).astype(np.int32)
+    else:
+        V, M = 5000, rows
+        word = rng.integers(0, V, N).astype(np.int32)
+        doc = np.sort(far)                     # contiguous documents, most past 4 GiB
+    phi = rng.random((V, K), dtype=np.float32)
+    phi *= rng.random((V, K), dtype=np.float32) > 0.37   # exact zeros, as Dirichlet(0.01) gives
+    theta = rng.random((M, K), dtype=np.float32) ** 8
+    u = (rng.integers(0, 1 << 24, N) * 2.0 ** -24).astype(np.float32)
+    from paper_1505_03851_amd.inputs import Corpus
+    return Corpus(theta, phi, doc, word, u, name=f"{big}-past-4GiB-K{K}")
+
+
+@pytest.mark.parametrize("big,K", [("phi", 1024), ("phi", 256), ("phi", 96), ("phi", 130),
+                                   ("theta", 1024), ("theta", 20)])
+def test_tables_past_4_gib(big, K):
+    import torch
+    import paper_1505_03851_amd as lda
+    from oracle import philox as px
+    from parity import compare, run_kernel, to_device
+    c = _wide_case(K, seed=K + (7 if big == "theta" else 0), big=big)
+    size = 4 * (c.V if big == "phi" else c.M) * K
+    print(f"[case] {c.name} M={c.M} V={c.V} {big}={size / 2 ** 30:.2f} GiB N={c.N}", flush=True)
+    assert size > lda.MAX_TABLE_BYTES
+    torch.cuda.empty_cache()
+    dev = to_device(c)
+    for kernel in ("butterfly", "docs"):
+        z = run_kernel(kernel, dev)
+        assert z.min() >= 0 and z.max() < K, kernel
+        rep = compare(c, z)
+        print(f"[parity] {c.name} {kernel}: {rep}", flush=True)
+        assert rep.hard == 0, (kernel, rep.first_hard)
+        assert rep.mismatch_rate < MAX_MISMATCH_RATE, (kernel, str(rep))
+    seed, sweep = 20150513, 3
+    z = lda.draw_philox(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], seed, sweep)
+    torch.cuda.synchronize()
+    c.u = px.token_uniforms(seed, sweep, 0, c.N)
+    rep = compare(c, z.cpu().numpy())
+    print(f"[parity] {c.name} philox: {rep}", flush=True)
+    assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
+    # the narrow entry points refuse such tables
+    with pytest.raises(lda.LdaError):
+        lda.draw_naive(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    del dev
+    torch.cuda.empty_cache()
+
+
+def test_wide_ids_past_the_table_stay_inside():
+    """With tables past 4 GiB no buffer range check guards the reads: ids
+    past the last row are clamped to it, so every read stays inside the
+    table (the draws of such tokens are those of the last row)."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from parity import compare, to_device
+    K = 256
+    c = _wide_case(K, seed=11, big="phi")
+    bad = np.arange(0, c.N, 97)
+    word = c.word_id.copy()
+    word[bad] = np.where(bad % 2 == 0, c.V + 5, -3)
+    print(f"[case] wide ids past the table K={K} bad={bad.size}", flush=True)
+    dev = to_device(c)
+    dev["word_id"] = torch.from_numpy(word).cuda()
+    z = lda.draw_butterfly(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    torch.cuda.synchronize()
+    z = z.cpu().numpy()
+    assert z.min() >= 0 and z.max() < K
+    c.word_id = np.where(np.isin(np.arange(c.N), bad), c.V - 1, c.word_id).astype(np.int32)
+    rep = compare(c, z)
+    print(f"[parity] wide clamped ids: {rep}", flush=True)
+    assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
+    del dev
     torch.cuda.empty_cache()
