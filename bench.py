@@ -93,7 +93,8 @@ def upload(c):
 
 # kernels bench.py can time: name -> entry point of the binding
 KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_cache",
-           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "philox",
+           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "variant-wide",
+           "philox",
            "routed",
            "routed+build", "routed-philox", "floor", "count", "count-clear", "count-docs")
 
@@ -487,9 +488,10 @@ def route_sweep(args) -> int:
 
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
-    registers or LDS, the alternative rule in LDS), 8-topic leaves, the offsets form of the
-    documents, the document-per-lane driver, the draw with in-kernel
-    uniforms and the default dispatch, on the two corpora and the corpus
+    registers or LDS, the alternative rule in LDS), 8-topic leaves, the build
+    for tables past 4 GiB, the offsets form of the documents, the
+    document-per-lane driver, the draw with in-kernel uniforms and the default
+    dispatch, on the two corpora and the corpus
     shaped like the paper's at K = 80 and 240; one JSON line per workload.
     z of every variant is compared with the default kernel's (identical
     unless a token lies in the fp32 rounding band)."""
@@ -502,8 +504,12 @@ def ablation(args) -> int:
         rec = {"workload": name, "N": c.N, "K": c.K}
         z_ref = None
         kernels = ["butterfly", "variant-register", "variant-lds", "variant-lds_alt",
-                   "variant-leaf8", "docs", "doc_lanes"] + \
+                   "variant-leaf8", "variant-wide", "docs", "doc_lanes"] + \
                   (["doc_lanes_cache"] if c.K <= 256 else []) + ["philox"]
+        # one untimed pass first: the first kernel timed after the upload
+        # otherwise runs a few percent slow (measured: docs and philox, the
+        # same kernel, 1.5-4.5% faster than the butterfly timed before them)
+        measure(name, c, dev, "butterfly", args.steps, args.warmup)
         for kernel in kernels:
             r = measure(name, c, dev, kernel, args.steps, args.warmup)
             z = r.pop("z")
@@ -514,6 +520,36 @@ def ablation(args) -> int:
                 rec[kernel + "_differs"] = int((z != z_ref).sum())
         print(json.dumps(rec), flush=True)
         del dev
+        torch.cuda.empty_cache()
+    return 0
+
+
+def wide_builds(args) -> int:
+    """The default build of the draw kernels against the build for tables past
+    4 GiB (float offsets, 64-bit loads; lda_draw_butterfly_variant with
+    LDA_VARIANT_WIDE_TABLES) on the same workloads: three alternating rounds
+    of each after an untimed pass, the median launch of each round, the
+    fastest round kept; z of the two compared.  One JSON line per workload."""
+    import torch
+    from paper_1505_03851_amd.inputs import CONFIGS, make_corpus, wiki_shaped
+    names = [n for n in CONFIGS if not n.startswith("wiki-shaped")] + \
+            [wiki_shaped(k).name for k in (16, 48, 80, 112, 144, 176, 208, 240)]
+    for name in names:
+        c = make_corpus(name)
+        dev = upload(c)
+        time_kernel("butterfly", dev, args.steps, args.warmup)
+        best = {"butterfly": float("inf"), "variant-wide": float("inf")}
+        zs = {}
+        for _ in range(3):
+            for kernel in best:
+                _, per_ms, zs[kernel] = time_kernel(kernel, dev, args.steps, args.warmup)
+                best[kernel] = min(best[kernel], sorted(per_ms)[len(per_ms) // 2])
+        rec = {"workload": name, "N": c.N, "K": c.K, "default_ms": best["butterfly"],
+               "wide_ms": best["variant-wide"],
+               "wide_over_default": best["variant-wide"] / best["butterfly"],
+               "z_identical": bool(torch.equal(zs["butterfly"], zs["variant-wide"]))}
+        print(json.dumps(rec), flush=True)
+        del dev, zs
         torch.cuda.empty_cache()
     return 0
 
@@ -913,6 +949,9 @@ def main() -> int:
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
+    ap.add_argument("--wide-builds", action="store_true",
+                    help="the default build of the draw kernels against the build "
+                         "for tables past 4 GiB, on every workload; one JSON line each")
     ap.add_argument("--counters-summary", action="store_true",
                     help="write the counter record of the draw on --workload from "
                          "the csv directories of rocprofv3 counter passes (--reads, "
@@ -984,6 +1023,8 @@ def main() -> int:
         return k_sweep(args)
     if args.ablation:
         return ablation(args)
+    if args.wide_builds:
+        return wide_builds(args)
     if args.route_sweep:
         return route_sweep(args)
     if args.all_configs:

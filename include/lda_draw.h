@@ -216,7 +216,12 @@ int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
  *   LDA_VARIANT_LEAF8           where lda_draw_butterfly uses its leaf groups
  *                               (K divisible by 4 up to 256, N >= 64), leaves
  *                               of 8 topics per lane in groups half as wide;
- *                               elsewhere the kernels of lda_draw_butterfly.
+ *                               elsewhere the kernels of lda_draw_butterfly;
+ *   LDA_VARIANT_WIDE_TABLES     the kernels of lda_draw_butterfly as built for
+ *                               tables past 4 GiB (float offsets, 64-bit
+ *                               loads), at any table size up to
+ *                               LDA_MAX_WIDE_TABLE_BYTES: the same draws as
+ *                               lda_draw_butterfly, to compare the two builds.
  * The three table variants use the one-topic-per-lane kernel for all K
  * (W = 64 for K >= 64, else 32).  Any other `variant` returns
  * LDA_ERR_UNSUPPORTED.
@@ -225,6 +230,7 @@ int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
 #define LDA_VARIANT_LDS_TABLE 1
 #define LDA_VARIANT_LDS_TABLE_ALT 2
 #define LDA_VARIANT_LEAF8 3
+#define LDA_VARIANT_WIDE_TABLES 4
 int lda_draw_butterfly_variant(const float *theta, const float *phi,
                                const int32_t *doc_id, const int32_t *word_id,
                                const float *u, int32_t *z, int64_t N, int32_t M,

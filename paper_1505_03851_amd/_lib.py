@@ -48,7 +48,8 @@ ROUTED_SCRATCH_BYTES = _CONSTS["LDA_ROUTED_SCRATCH_BYTES"]
 VARIANTS = {"register": _CONSTS["LDA_VARIANT_REGISTER_TABLE"],
             "lds": _CONSTS["LDA_VARIANT_LDS_TABLE"],
             "lds_alt": _CONSTS["LDA_VARIANT_LDS_TABLE_ALT"],
-            "leaf8": _CONSTS["LDA_VARIANT_LEAF8"]}
+            "leaf8": _CONSTS["LDA_VARIANT_LEAF8"],
+            "wide": _CONSTS["LDA_VARIANT_WIDE_TABLES"]}
 
 
 class RouteInfo(ctypes.Structure):
@@ -221,8 +222,9 @@ def draw_variant(theta, phi, doc_id, word_id, u, variant: str = "register",
     """z[N] (int32) by a variant of the butterfly draw: the one-topic-per-lane
     kernel with a chosen block table, "register" (the paper's rule,
     search-assist loop), "lds" (the same table in LDS) or "lds_alt" (the
-    alternative rule [a b; c d] -> [a c; a+b c+d], Section 4); or "leaf8",
-    the default kernels with 8-topic leaves in the leaf groups."""
+    alternative rule [a b; c d] -> [a c; a+b c+d], Section 4); "leaf8",
+    the default kernels with 8-topic leaves in the leaf groups; or "wide",
+    the default kernels as built for tables past 4 GiB (the same draws)."""
     if variant not in VARIANTS:
         raise ValueError(f"variant must be one of {sorted(VARIANTS)}")
     return _draw("lda_draw_butterfly_variant", theta, phi, doc_id, word_id, u,

@@ -6,8 +6,9 @@
 // lda_draw_docs       the same, documents given as offsets.
 // lda_draw_doc_lanes  Algorithm 7's document-per-lane driver.
 // lda_draw_transposed Algorithms 4-6, for comparison.
-// lda_draw_butterfly_variant  the block-table variants of Section 4, and
-//                     8-topic leaves.
+// lda_draw_butterfly_variant  the block-table variants of Section 4,
+//                     8-topic leaves, and the build for tables past 4 GiB
+//                     (lda_draw_wide.hip) at any size.
 // lda_draw_butterfly_philox   the butterfly draw with in-kernel uniforms.
 // lda_philox_uniforms         those uniforms, written out.
 // lda_butterfly_table the butterfly-patterned tables (Fig. 1, right).
@@ -288,14 +289,18 @@ extern "C" int lda_draw_butterfly_variant(const float *theta, const float *phi,
                                           int32_t V, int32_t K, int32_t variant,
                                           void *stream) {
   if (variant != LDA_VARIANT_REGISTER_TABLE && variant != LDA_VARIANT_LDS_TABLE &&
-      variant != LDA_VARIANT_LDS_TABLE_ALT && variant != LDA_VARIANT_LEAF8)
+      variant != LDA_VARIANT_LDS_TABLE_ALT && variant != LDA_VARIANT_LEAF8 &&
+      variant != LDA_VARIANT_WIDE_TABLES)
     return LDA_ERR_UNSUPPORTED;
-  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K);
+  const bool wide = variant == LDA_VARIANT_WIDE_TABLES;
+  const int st = check_args(theta, phi, doc_id, word_id, u, z, N, M, V, K, wide);
   if (st != LDA_OK || N == 0) return st;
   const UniformSource us{u, 0, 0, 0};
   const DocSource d{doc_id, nullptr, M, N};
   hipStream_t s = static_cast<hipStream_t>(stream);
-  if (variant == LDA_VARIANT_LEAF8)
+  if (wide)
+    lda_wide::draw(theta, phi, doc_id, nullptr, word_id, u, 0, 0, 0, z, N, M, V, K, s);
+  else if (variant == LDA_VARIANT_LEAF8)
     dispatch_butterfly<2>(theta, phi, d, word_id, us, z, N, M, V, K, s);
   else if (variant == LDA_VARIANT_REGISTER_TABLE)
     launch_table_variant<false, false>(theta, phi, d, word_id, us, z, N, M, V, K, s);

@@ -147,12 +147,19 @@ def test_empty_is_noop(lib, fn):
 
 def test_variant_codes(lib):
     from paper_1505_03851_amd._lib import STATUS, VARIANTS
-    assert sorted(VARIANTS.values()) == [0, 1, 2, 3]
-    for bad in (-1, 4, 99):
+    assert sorted(VARIANTS.values()) == [0, 1, 2, 3, 4]
+    for bad in (-1, 5, 99):
         assert call(lib, "lda_draw_butterfly_variant", variant=bad) == \
             STATUS["LDA_ERR_UNSUPPORTED"]
     # a known variant still goes through the argument checks
     assert call(lib, "lda_draw_butterfly_variant", variant=0, K=0) == STATUS["LDA_ERR_SHAPE"]
+    # the wide build takes tables past 4 GiB; the others do not (N = 0: no launch)
+    from paper_1505_03851_amd._lib import MAX_TABLE_BYTES
+    past = MAX_TABLE_BYTES // (4 * 1024) + 1
+    for name, code in VARIANTS.items():
+        want = 0 if name == "wide" else STATUS["LDA_ERR_UNSUPPORTED"]
+        assert call(lib, "lda_draw_butterfly_variant", variant=code, K=1024, V=past, N=0) == \
+            want, name
 
 
 def test_doc_lanes_theta_cache_limits(lib):

@@ -17,7 +17,7 @@ from parity import (MAX_MISMATCH_RATE, compare, named_corpus, reference, run_ker
 pytestmark = pytest.mark.gpu
 
 KERNELS = ["naive", "butterfly", "transposed",
-           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8"]
+           "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "variant-wide"]
 
 
 def _check(c, kernel, idx=None, rate=True, ref=None):
