@@ -76,14 +76,15 @@ extern "C" {
  * are 64-bit throughout.  Larger N is rejected with LDA_ERR_UNSUPPORTED. */
 #define LDA_MAX_N 4294901760LL
 
-/* Largest size in bytes of theta (4*M*K) or phi (4*V*K) (and of the count
- * tables) for most entry points: their kernels address both through buffer
+/* Largest size in bytes of theta (4*M*K) or phi (4*V*K) for most entry
+ * points: their kernels address both through buffer
  * resources, whose record count and byte offsets are unsigned 32-bit.  Larger
  * tables are rejected with LDA_ERR_UNSUPPORTED. */
 #define LDA_MAX_TABLE_BYTES 4294967295LL
 
 /* Largest size in bytes of theta or phi for lda_draw_butterfly, lda_draw_docs
- * and lda_draw_butterfly_philox: 2^32 - 1 floats (16 GiB).  When either table
+ * and lda_draw_butterfly_philox, and of the count tables of lda_count_topics
+ * and lda_count_topics_docs: 2^32 - 1 elements (16 GiB).  When either table
  * is larger than LDA_MAX_TABLE_BYTES these draw with a second build of the
  * same kernels that addresses the tables by 32-bit float offsets and 64-bit
  * loads (ids beyond the table's rows are clamped to its last row there, so
@@ -346,7 +347,8 @@ int lda_draw_routed_philox(const float *theta, const float *phi, const void *wor
  * order of the tokens.  Every pointer 4-byte aligned (LDA_ERR_ALIGN); ndk and
  * nwk may not be NULL (LDA_ERR_NULL), nor the token arrays when N > 0;
  * N above LDA_COUNT_MAX_N (counts are int32), K above LDA_MAX_K, or either
- * table above LDA_MAX_TABLE_BYTES give LDA_ERR_UNSUPPORTED.  Enqueues two
+ * table above LDA_MAX_WIDE_TABLE_BYTES (2^32 - 1 cells: cells are addressed by
+ * unsigned 32-bit indices) give LDA_ERR_UNSUPPORTED.  Enqueues two
  * kernels that clear the tables, then one that counts; nothing is allocated.
  */
 #define LDA_COUNT_MAX_N 2147483647LL

@@ -78,8 +78,8 @@ __device__ __forceinline__ void count_flush(uint32_t *keys, uint32_t *cnt, int32
 }
 
 // One workgroup per chunk of kCountChunk consecutive tokens.  Cells are
-// addressed by d K + k and w K + k, below 2^30 (each table is below 4 GiB),
-// never equal to kCountEmpty.
+// addressed by d K + k and w K + k, below 2^32 - 1 (each table holds at most
+// 2^32 - 1 cells), so never equal to kCountEmpty.
 __global__ __launch_bounds__(kCountThreads) void count_kernel(
     const int32_t *__restrict__ doc_id, const int32_t *__restrict__ word_id,
     const int32_t *__restrict__ z, int64_t N, int32_t M, int32_t V, int32_t K,

@@ -618,7 +618,9 @@ extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, c
                                 int32_t *nwk, void *stream) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
-  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
+  // cells are addressed by unsigned 32-bit indices (d K + k, w K + k)
+  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;
   if (!ndk || !nwk) return LDA_ERR_NULL;
   if (N > 0 && (!doc_id || !word_id || !z)) return LDA_ERR_NULL;
@@ -646,7 +648,9 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
                                      int32_t K, int32_t *ndk, int32_t *nwk, void *stream) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
-  if ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES)
+  // cells are addressed by unsigned 32-bit indices (d K + k, w K + k)
+  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;
   if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
   if (N > 0 && (!word_id || !z)) return LDA_ERR_NULL;
@@ -681,8 +685,8 @@ extern "C" const char *lda_status_string(int status) {
     case LDA_ERR_NULL: return "a required pointer is NULL";
     case LDA_ERR_SHAPE: return "invalid shape (N < 0, M <= 0, V <= 0 or K <= 0)";
     case LDA_ERR_UNSUPPORTED:
-      return "unsupported size (K > LDA_MAX_K, N > LDA_MAX_N, theta or phi larger than "
-             "LDA_MAX_TABLE_BYTES, or a K or N the entry point does not take)";
+      return "unsupported size (K > LDA_MAX_K, N > LDA_MAX_N, a table larger than the entry "
+             "point takes, or a K or N the entry point does not take)";
     case LDA_ERR_HIP: return "HIP runtime error";
     case LDA_ERR_ALIGN: return "a pointer is not aligned (4 bytes; 8 for offsets and workspaces)";
     case LDA_ERR_WORKSPACE:

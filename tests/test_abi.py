@@ -328,8 +328,8 @@ def test_count_topics_argument_errors(lib):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
     assert run(K=_CONSTS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
     assert run(N=_CONSTS["LDA_COUNT_MAX_N"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 4 GiB
-    assert run(V=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 4 GiB
+    assert run(M=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 16 GiB
+    assert run(V=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 16 GiB
     for key in ("ndk", "nwk"):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
         assert run(N=0, **{key: None}) == STATUS["LDA_ERR_NULL"], key  # tables are cleared
@@ -399,7 +399,8 @@ def test_count_topics_docs_argument_errors(lib):
         return lib.lda_count_topics_docs(off, w, z, N, M, V, K, ndk, nwk, None)
     for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
-    assert run(M=1 << 20, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert run(M=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 16 GiB
+    assert run(V=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 16 GiB
     for key in ("off", "ndk", "nwk"):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
         assert run(N=0, **{key: None}) == STATUS["LDA_ERR_NULL"], key

@@ -252,3 +252,39 @@ def test_wide_ids_past_the_table_stay_inside():
     assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
     del dev
     torch.cuda.empty_cache()
+
+
+def test_word_counts_past_4_gib():
+    """nwk of about 4.3 GiB (V x K int32, more cells than a byte offset can
+    reach): cells past the 2^32-byte offset are counted exactly, by both
+    count entry points."""
+    import torch
+    import oracle
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd.inputs import doc_offsets
+    K = 1024
+    V = WIDE_BYTES // (4 * K) + 1
+    w_min = (1 << 32) // (4 * K) + 1
+    rng = np.random.default_rng(6)
+    N, M = 500_000, 700
+    word = np.where(rng.random(N) < 0.5, rng.integers(0, V, N), rng.integers(w_min, V, N))
+    doc = (np.arange(N) * M // N).astype(np.int32)
+    d = torch.from_numpy(doc).cuda()
+    w = torch.from_numpy(word.astype(np.int32)).cuda()
+    z = torch.from_numpy(rng.integers(0, K, N).astype(np.int32)).cuda()
+    print(f"[case] counts nwk {4 * V * K / 2 ** 30:.2f} GiB", flush=True)
+    torch.cuda.empty_cache()
+    want_d, want_w = oracle.counts(doc, word.astype(np.int32), z.cpu().numpy(), M, V, K)
+    ndk, nwk = lda.count_topics(d, w, z, M, V, K)
+    torch.cuda.synchronize()
+    assert np.array_equal(ndk.cpu().numpy(), want_d)
+    got_w = nwk.cpu().numpy()
+    assert np.array_equal(got_w, want_w), np.argwhere(got_w != want_w)[:5]
+    assert got_w[w_min:].sum() == (word >= w_min).sum()
+    off = torch.from_numpy(doc_offsets(doc, M)).cuda()
+    ndk2, nwk2 = lda.count_topics_docs(off, w, z, V, K, ndk=ndk, nwk=nwk)
+    torch.cuda.synchronize()
+    assert np.array_equal(ndk2.cpu().numpy(), want_d)
+    assert np.array_equal(nwk2.cpu().numpy(), want_w)
+    del ndk, nwk, ndk2, nwk2, got_w
+    torch.cuda.empty_cache()
