@@ -96,7 +96,8 @@ KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_c
            "variant-register", "variant-lds", "variant-lds_alt", "variant-leaf8", "variant-wide",
            "philox",
            "routed",
-           "routed+build", "routed-philox", "floor", "count", "count-clear", "count-docs")
+           "routed+build", "routed-philox", "floor", "count", "count-clear", "count-docs",
+           "count-indexed", "word-index")
 
 
 def draw_occupancy(K: int) -> tuple[int, int]:
@@ -149,7 +150,11 @@ def launcher(kernel: str, dev):
         return lambda out, stream: probe.draw_floor(th, ph, d, w, u, out, window=window,
                                                     waves_per_group=wpg, waves_per_cu=wpc,
                                                     stream=stream)
-    if kernel in ("count", "count-clear", "count-docs"):
+    if kernel == "word-index":          # the index build (once per corpus in a sampler)
+        V = ph.shape[0]
+        ws = torch.empty(lda.word_index_bytes(w.shape[0], V), dtype=torch.uint8, device=w.device)
+        return lambda out, stream: lda.word_index_build(w, V, workspace=ws, stream=stream)
+    if kernel in ("count", "count-clear", "count-docs", "count-indexed"):
         M, V, K = th.shape[0], ph.shape[0], th.shape[1]
         if "z_draw" not in dev:
             dev["z_draw"] = lda.draw_butterfly(th, ph, d, w, u)
@@ -164,6 +169,13 @@ def launcher(kernel: str, dev):
             off = dev["doc_offsets"]
             return lambda out, stream: lda.count_topics_docs(off, w, zd, V, K, ndk=ndk, nwk=nwk,
                                                              stream=stream)
+        if kernel == "count-indexed":   # and nwk from the word index (built once per corpus)
+            off = dev["doc_offsets"]
+            if "word_index" not in dev:
+                dev["word_index"] = lda.word_index_build(w, V)
+            idx = dev["word_index"]
+            return lambda out, stream: lda.count_topics_indexed(off, w, zd, idx, K, ndk=ndk,
+                                                                nwk=nwk, stream=stream)
         return lambda out, stream: lda.count_topics(d, w, zd, M, V, K, ndk=ndk, nwk=nwk,
                                                     stream=stream)
     if kernel == "philox":
@@ -222,7 +234,12 @@ def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None)
     avg_ms = sum(per_ms) / len(per_ms)
     srt = sorted(per_ms)
     med_ms = srt[len(srt) // 2]
-    b_alg = count_bytes(c) if kernel.startswith("count") else algorithmic_bytes(c)
+    if kernel.startswith("count"):
+        b_alg = count_bytes(c)
+    elif kernel == "word-index":     # word ids read twice, perm and wsorted written
+        b_alg = 16 * c.N
+    else:
+        b_alg = algorithmic_bytes(c)
     gbps = b_alg / (avg_ms * 1e-3) / 1e9
     tag = " cold" if flush is not None else ""
     print(f"[bench] {name} {kernel}{tag}: {avg_ms:.3f} ms/launch "
@@ -656,6 +673,8 @@ PROFILE_TARGETS = {
                                           "--steps", "3", "--warmup", "1"]),
     "cwords_K1024": ("count_words_kernel", ["--only", "count-docs", "--workload", HEADLINE,
                                             "--steps", "3", "--warmup", "1"]),
+    "cindexed_K1024": ("count_words_indexed", ["--only", "count-indexed", "--workload", HEADLINE,
+                                               "--steps", "3", "--warmup", "1"]),
     "draw_K256": ("leaf_group_kernel", ["--only", "butterfly", "--workload", SECOND,
                                         "--steps", "3", "--warmup", "1"]),
     "floor_K256": ("floor_kernel", ["--only", "floor", "--floor-config", "16,2,0",
@@ -825,7 +844,8 @@ def report_bench(log: str, out_txt: str) -> int:
           f"  streaming read from HBM   {c['hbm_read_GBps']:8,.0f} GB/s  ({c['hbm_read']})",
           f"  streaming read, MALL      {c['mall_read_GBps']:8,.0f} GB/s  ({c['mall_read']})",
           f"  device copy (read+write)  {c['device_copy_GBps']:8,.0f} GB/s",
-          "", f"topic counts (lda_count_topics) ms per call: " +
+          "", f"topic counts (lda_count_topics, _docs, _indexed; word-index: the index build) "
+          f"ms per call: " +
           ", ".join(f"{k} {v:.4f}" for k, v in r["count_topics_ms"].items()),
           "", "parity on every token against the oracle (band |u S - S_k| <= 1e-5 S):",
           f"  {'workload':28s} {'tokens':>10s} {'mismatches':>10s} {'rate':>9s} "
@@ -1080,7 +1100,7 @@ def main() -> int:
         results.append(_brief(measure(SECOND, c2, dev2, k, max(steps, 20), warmup)))
     floors[SECOND] = measure_floor(SECOND, c2, dev2, max(steps, 20), warmup)
     floors[SECOND]["draw_ms"] = second["ms_per_launch"]
-    for k in ("count", "count-docs"):
+    for k in ("count", "count-docs", "count-indexed", "word-index"):
         counts[f"{SECOND} {k}"] = measure(SECOND, c2, dev2, k, max(steps, 20),
                                           warmup)["ms_per_launch"]
     del dev2, c2
@@ -1124,7 +1144,7 @@ def main() -> int:
     del flush
     floors[HEADLINE] = measure_floor(HEADLINE, c, dev, steps, warmup)
     floors[HEADLINE]["draw_ms"] = head["ms_per_launch"]
-    for k in ("count", "count-docs"):
+    for k in ("count", "count-docs", "count-indexed", "word-index"):
         counts[f"{HEADLINE} {k}"] = measure(HEADLINE, c, dev, k, steps, warmup)["ms_per_launch"]
 
     base = cpu_baseline(c, z_head, args.cpu_sample)

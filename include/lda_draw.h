@@ -375,6 +375,49 @@ int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *word_id, co
                           int32_t *nwk, void *stream);
 
 /*
+ * A word index of the tokens, for the topic counts of many sweeps over one
+ * corpus (the word ids do not change between sweeps; the counts do): the
+ * positions of each word's tokens, built once by a counting sort on the GPU.
+ * The caller provides `index`, device memory of at least
+ * lda_word_index_bytes(N, V) bytes, 8-byte aligned (LDA_ERR_ALIGN), which
+ * the index occupies until the caller frees it; the library keeps no state.
+ * Layout inside it, each section on a 256-byte boundary: off int32 [V + 1]
+ * (the positions of word w are off[w] .. off[w+1] - 1; off[V] = the tokens
+ * indexed), a histogram / cursor int32 [V], the scan's workgroup sums, perm
+ * int32 [N] (the token at each position) and wsorted int32 [N] (its word).
+ * Tokens whose word id lies outside [0, V) are not indexed.  The order of a
+ * word's tokens is not fixed; the counts do not depend on it.
+ * lda_word_index_bytes returns 0 for N < 0, V <= 0, N > LDA_COUNT_MAX_N or
+ * V > LDA_WORD_INDEX_MAX_V.  The build enqueues seven kernels on `stream`
+ * (no memset, no wait: it may be captured into a graph); word_id int32 [N]
+ * device, 4-byte aligned, NULL only when N = 0; errors LDA_ERR_SHAPE (N < 0,
+ * V <= 0), LDA_ERR_UNSUPPORTED (N > LDA_COUNT_MAX_N, V >
+ * LDA_WORD_INDEX_MAX_V), LDA_ERR_NULL, LDA_ERR_ALIGN, LDA_ERR_WORKSPACE
+ * (index_bytes too small).
+ */
+#define LDA_WORD_INDEX_MAX_V 16777215
+size_t lda_word_index_bytes(int64_t N, int32_t V);
+int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V, void *index,
+                         size_t index_bytes, void *stream);
+
+/*
+ * lda_count_topics_docs with the word table counted from a word index
+ * (lda_word_index_build over the same word_id, N and V): the tokens are taken
+ * word by word in segments of 2,048 positions; within a segment each cell's
+ * tokens are summed in LDS, and the cells of a word whose tokens all lie in
+ * the segment are written with plain stores, the others (words that straddle
+ * segments) added with device atomics.  Same results as lda_count_topics_docs
+ * (exact); same arguments and errors, plus those of the index
+ * (LDA_ERR_WORKSPACE when index_bytes < lda_word_index_bytes(N, V)).  An index
+ * built from other tokens gives wrong counts but no access outside ndk, nwk,
+ * the index and the token arrays.
+ */
+int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_t *word_id,
+                             const int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
+                             const void *index, size_t index_bytes, int32_t *ndk, int32_t *nwk,
+                             void *stream);
+
+/*
  * For callers that cannot allocate device memory (code under graph capture
  * aside: this call waits on the stream; tight serving loops; harnesses that
  * forbid hipMalloc): lda_route_build followed by lda_draw_routed, with the

@@ -111,6 +111,13 @@ def load() -> ctypes.CDLL:
     lib.lda_count_topics.restype = ctypes.c_int
     lib.lda_count_topics_docs.argtypes = [P, P, P, I64, I32, I32, I32, P, P, P]
     lib.lda_count_topics_docs.restype = ctypes.c_int
+    lib.lda_word_index_bytes.argtypes = [I64, I32]
+    lib.lda_word_index_bytes.restype = ctypes.c_size_t
+    lib.lda_word_index_build.argtypes = [P, I64, I32, P, ctypes.c_size_t, P]
+    lib.lda_word_index_build.restype = ctypes.c_int
+    lib.lda_count_topics_indexed.argtypes = [P, P, P, I64, I32, I32, I32, P, ctypes.c_size_t,
+                                             P, P, P]
+    lib.lda_count_topics_indexed.restype = ctypes.c_int
     _lib = lib
     return lib
 
@@ -419,6 +426,98 @@ def count_topics_docs(doc_offsets, word_id, z, V: int, K: int, ndk=None, nwk=Non
                                           z.data_ptr(), N, int(M), int(V), int(K),
                                           outs[0].data_ptr(), outs[1].data_ptr(),
                                           _stream_handle(stream))
+    _check(st)
+    return outs[0], outs[1]
+
+
+class WordIndex:
+    """The tokens grouped by word (lda_word_index_build): a uint8 device
+    workspace holding off [V + 1], perm [N] and wsorted [N], for N tokens and
+    V words."""
+
+    def __init__(self, workspace: torch.Tensor, N: int, V: int):
+        self.workspace, self.N, self.V = workspace, N, V
+
+    def arrays(self) -> dict[str, torch.Tensor]:
+        """Views of off (int32 [V + 1]), perm and wsorted (int32 [N])."""
+        lay = word_index_layout(self.N, self.V)
+        return {"off": self.workspace[lay["off"]:lay["off"] + 4 * (self.V + 1)].view(torch.int32),
+                "perm": self.workspace[lay["perm"]:lay["perm"] + 4 * self.N].view(torch.int32),
+                "wsorted": self.workspace[lay["wsorted"]:lay["wsorted"] + 4 * self.N]
+                .view(torch.int32)}
+
+
+def word_index_bytes(N: int, V: int) -> int:
+    """Bytes of device workspace ``word_index_build`` needs (0: unsupported)."""
+    return int(load().lda_word_index_bytes(int(N), int(V)))
+
+
+def word_index_layout(N: int, V: int) -> dict[str, int]:
+    """Byte offsets of the index's sections (the layout the header states)."""
+    def up(b):
+        return (b + 255) & ~255
+    lay, at = {}, 0
+    for name, b in (("off", 4 * (V + 1)), ("cursor", 4 * V), ("sums", 4 * 4096),
+                    ("perm", 4 * max(N, 1)), ("wsorted", 4 * max(N, 1))):
+        lay[name] = at
+        at += up(b)
+    lay["bytes"] = at
+    return lay
+
+
+def word_index_build(word_id, V: int, workspace=None, stream=None) -> WordIndex:
+    """Group the tokens (word_id: int32 [N] on the GPU) by word, once per
+    corpus (lda_word_index_build).  ``workspace``: a uint8 tensor of at least
+    ``word_index_bytes(N, V)`` bytes on the same GPU, or None to allocate one."""
+    _require(word_id, "word_id", torch.int32, 1)
+    N = word_id.shape[0]
+    need = word_index_bytes(N, V)
+    if need == 0:
+        raise LdaError(STATUS["LDA_ERR_UNSUPPORTED"], status_string(STATUS["LDA_ERR_UNSUPPORTED"]))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=word_id.device)
+    else:
+        _require(workspace, "workspace", torch.uint8, 1)
+        if workspace.device != word_id.device:
+            raise ValueError("workspace must be on word_id's device")
+    with torch.cuda.device(word_id.device):
+        st = load().lda_word_index_build(word_id.data_ptr(), N, int(V), workspace.data_ptr(),
+                                         workspace.numel(), _stream_handle(stream))
+    _check(st)
+    return WordIndex(workspace, N, int(V))
+
+
+def count_topics_indexed(doc_offsets, word_id, z, index: WordIndex, K: int, ndk=None, nwk=None,
+                         stream=None) -> tuple[torch.Tensor, torch.Tensor]:
+    """count_topics_docs with the word table counted from ``index``
+    (word_index_build over the same word_id): lda_count_topics_indexed."""
+    _require(doc_offsets, "doc_offsets", torch.int64, 1)
+    _require(word_id, "word_id", torch.int32, 1)
+    _require(z, "z", torch.int32, 1)
+    N, V = word_id.shape[0], index.V
+    M = doc_offsets.shape[0] - 1
+    if M < 1:
+        raise ValueError("doc_offsets must hold M + 1 >= 2 entries")
+    if z.shape[0] != N or index.N != N:
+        raise ValueError("word_id, z and the index must cover the same N tokens")
+    dev = word_id.device
+    if z.device != dev or doc_offsets.device != dev or index.workspace.device != dev:
+        raise ValueError("all tensors must be on one device")
+    outs = []
+    for t, name, rows in ((ndk, "ndk", M), (nwk, "nwk", V)):
+        if t is None:
+            t = torch.empty((rows, K), dtype=torch.int32, device=dev)
+        else:
+            _require(t, name, torch.int32, 2)
+            if tuple(t.shape) != (rows, K) or t.device != dev:
+                raise ValueError(f"{name} must be int32[{rows}][{K}] on the tokens' device")
+        outs.append(t)
+    with torch.cuda.device(dev):
+        st = load().lda_count_topics_indexed(doc_offsets.data_ptr(), word_id.data_ptr(),
+                                             z.data_ptr(), N, int(M), int(V), int(K),
+                                             index.workspace.data_ptr(), index.workspace.numel(),
+                                             outs[0].data_ptr(), outs[1].data_ptr(),
+                                             _stream_handle(stream))
     _check(st)
     return outs[0], outs[1]
 

@@ -16,7 +16,9 @@
 //                     the leaf kernel drawing them (lda_draw_routed_philox:
 //                     with in-kernel uniforms).
 // lda_count_topics    the per-document and per-word topic counts of a set of
-//                     draws (counts.hpp).
+//                     draws (counts.hpp); lda_word_index_build and
+//                     lda_count_topics_indexed: the same counts with the tokens
+//                     grouped by word once per corpus (word_index.hpp).
 //
 // Device code: butterfly.hpp (lane exchanges, the butterfly, buffer loads),
 // philox.hpp, sources.hpp (document and uniform sources), tile.hpp (the
@@ -46,6 +48,7 @@
 #include "table.hpp"
 #include "doc_lanes.hpp"
 #include "counts.hpp"
+#include "word_index.hpp"
 
 namespace lda {
 namespace {
@@ -669,6 +672,121 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
   if (N > 0) {
     const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
     count_words_kernel<<<(unsigned)chunks, kCountThreads, 0, s>>>(word_id, z, N, V, K, nwk);
+  }
+  return finish_launch();
+}
+
+// ---------------------------------------------------------------------------
+// The word index: off [V + 1], a cursor / histogram [V], the scan's workgroup
+// sums, perm [N] and wsorted [N], each section on a 256-byte boundary.
+namespace lda {
+namespace {
+
+struct WordIndexLayout {
+  size_t off, cursor, sums, perm, wsorted, bytes;
+};
+
+WordIndexLayout word_index_layout(int64_t N, int32_t V) {
+  WordIndexLayout L;
+  size_t at = 0;
+  auto take = [&](size_t b) {
+    const size_t o = at;
+    at += (b + 255) & ~(size_t)255;
+    return o;
+  };
+  L.off = take(4 * ((size_t)V + 1));
+  L.cursor = take(4 * (size_t)V);
+  L.sums = take(4 * (size_t)kScanMaxBlocks);
+  L.perm = take(4 * (size_t)(N > 0 ? N : 1));
+  L.wsorted = take(4 * (size_t)(N > 0 ? N : 1));
+  L.bytes = at;
+  return L;
+}
+
+int check_word_index(int64_t N, int32_t V, const void *index, size_t index_bytes) {
+  if (N < 0 || V <= 0) return LDA_ERR_SHAPE;
+  if (N > LDA_COUNT_MAX_N || V > LDA_WORD_INDEX_MAX_V) return LDA_ERR_UNSUPPORTED;
+  if (!index) return LDA_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(index) & 7u) return LDA_ERR_ALIGN;
+  if (index_bytes < word_index_layout(N, V).bytes) return LDA_ERR_WORKSPACE;
+  return LDA_OK;
+}
+
+unsigned fill_grid(int64_t n) {
+  const int64_t b = (n + 255) / 256;
+  return (unsigned)(b < 4096 ? (b > 0 ? b : 1) : 4096);
+}
+
+}  // namespace
+}  // namespace lda
+
+extern "C" size_t lda_word_index_bytes(int64_t N, int32_t V) {
+  if (N < 0 || V <= 0 || N > LDA_COUNT_MAX_N || V > LDA_WORD_INDEX_MAX_V) return 0;
+  return word_index_layout(N, V).bytes;
+}
+
+extern "C" int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V, void *index,
+                                    size_t index_bytes, void *stream) {
+  const int st = check_word_index(N, V, index, index_bytes);
+  if (st != LDA_OK) return st;
+  if (N > 0 && !word_id) return LDA_ERR_NULL;
+  if (reinterpret_cast<uintptr_t>(word_id) & 3u) return LDA_ERR_ALIGN;
+  const WordIndexLayout L = word_index_layout(N, V);
+  char *b = static_cast<char *>(index);
+  int32_t *off = reinterpret_cast<int32_t *>(b + L.off);
+  int32_t *cursor = reinterpret_cast<int32_t *>(b + L.cursor);
+  int32_t *sums = reinterpret_cast<int32_t *>(b + L.sums);
+  int32_t *perm = reinterpret_cast<int32_t *>(b + L.perm);
+  int32_t *wsorted = reinterpret_cast<int32_t *>(b + L.wsorted);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const unsigned chunks = (unsigned)((N + kCountChunk - 1) / kCountChunk);
+  // histogram of the words into cursor, then its exclusive scan into off
+  index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
+  if (N > 0) index_hist<<<chunks, kCountThreads, 0, s>>>(word_id, N, V, cursor);
+  const int64_t items = (int64_t)V + 1;
+  const unsigned nb = (unsigned)((items + kScanItems - 1) / kScanItems);
+  index_scan_local<<<nb, kScanThreads, 0, s>>>(cursor, V, items, off, sums);
+  index_scan_sums<<<1, kScanThreads, 0, s>>>(sums, (int32_t)nb);
+  index_scan_add<<<nb, kScanThreads, 0, s>>>(off, items, sums);
+  // the tokens placed word by word
+  index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
+  if (N > 0)
+    index_scatter<<<chunks, kCountThreads, 0, s>>>(word_id, N, V, off, cursor, perm, wsorted, N);
+  return finish_launch();
+}
+
+extern "C" int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_t *word_id,
+                                        const int32_t *z, int64_t N, int32_t M, int32_t V,
+                                        int32_t K, const void *index, size_t index_bytes,
+                                        int32_t *ndk, int32_t *nwk, void *stream) {
+  if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
+  if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
+  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
+    return LDA_ERR_UNSUPPORTED;
+  const int st = check_word_index(N, V, index, index_bytes);
+  if (st != LDA_OK) return st;
+  if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
+  if (N > 0 && (!word_id || !z)) return LDA_ERR_NULL;
+  const void *ptrs[] = {ndk, nwk, word_id, z};
+  for (const void *p : ptrs)
+    if (reinterpret_cast<uintptr_t>(p) & 3u) return LDA_ERR_ALIGN;
+  if (reinterpret_cast<uintptr_t>(doc_offsets) & 7u) return LDA_ERR_ALIGN;
+  const WordIndexLayout L = word_index_layout(N, V);
+  const char *b = static_cast<const char *>(index);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t cells = (int64_t)V * K;
+  const int64_t blocks = (cells / 4 + 255) / 256;
+  count_clear<<<(unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), 256, 0, s>>>(
+      nwk, cells);
+  const size_t lds = (size_t)kDocWaves * (size_t)K * sizeof(uint32_t);
+  count_docs_kernel<<<(unsigned)((M + kDocWaves - 1) / kDocWaves), kDocWaves * 64, lds, s>>>(
+      doc_offsets, word_id, z, N, M, V, K, ndk);
+  if (N > 0) {
+    const unsigned chunks = (unsigned)((N + kCountChunk - 1) / kCountChunk);
+    count_words_indexed<<<chunks, kCountThreads, 0, s>>>(
+        reinterpret_cast<const int32_t *>(b + L.perm), reinterpret_cast<const int32_t *>(b + L.wsorted),
+        reinterpret_cast<const int32_t *>(b + L.off), z, N, V, K, nwk);
   }
   return finish_launch();
 }

@@ -408,3 +408,48 @@ def test_count_topics_docs_argument_errors(lib):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
     assert run(off=A + 4) == STATUS["LDA_ERR_ALIGN"]
     assert run(w=A + 2) == STATUS["LDA_ERR_ALIGN"]
+
+
+def test_word_index_sizes_and_layout(lib):
+    """lda_word_index_bytes agrees with the layout the header states (and the
+    binding's views use); 0 for sizes the index does not take."""
+    from paper_1505_03851_amd._lib import _CONSTS, word_index_layout
+    for N, V in ((0, 1), (1, 1), (1000, 7), (2048, 300), (16_777_216, 100_000),
+                 (2 ** 31 - 1, _CONSTS["LDA_WORD_INDEX_MAX_V"])):
+        assert lib.lda_word_index_bytes(N, V) == word_index_layout(N, V)["bytes"], (N, V)
+    for N, V in ((-1, 5), (10, 0), (2 ** 31, 5), (10, _CONSTS["LDA_WORD_INDEX_MAX_V"] + 1)):
+        assert lib.lda_word_index_bytes(N, V) == 0, (N, V)
+
+
+def test_word_index_argument_errors(lib):
+    """The build and the indexed counts reject bad arguments before any HIP
+    call (calls that pass every check launch kernels, so none is made)."""
+    from paper_1505_03851_amd._lib import STATUS, _CONSTS
+    ws = lib.lda_word_index_bytes(100, 5)
+
+    def build(w=A, N=100, V=5, index=A, nbytes=ws):
+        return lib.lda_word_index_build(w, N, V, index, nbytes, None)
+    assert build(N=-1) == STATUS["LDA_ERR_SHAPE"]
+    assert build(V=0) == STATUS["LDA_ERR_SHAPE"]
+    assert build(N=2 ** 31) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert build(V=_CONSTS["LDA_WORD_INDEX_MAX_V"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert build(index=None) == STATUS["LDA_ERR_NULL"]
+    assert build(w=None) == STATUS["LDA_ERR_NULL"]
+    assert build(index=A + 4) == STATUS["LDA_ERR_ALIGN"]
+    assert build(w=A + 2) == STATUS["LDA_ERR_ALIGN"]
+    assert build(nbytes=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
+
+    def count(off=A, w=A, z=A, N=100, M=3, V=5, K=7, index=A, nbytes=ws, ndk=A, nwk=A):
+        return lib.lda_count_topics_indexed(off, w, z, N, M, V, K, index, nbytes, ndk, nwk, None)
+    for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
+        assert count(**kw) == STATUS["LDA_ERR_SHAPE"], kw
+    assert count(K=_CONSTS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
+    assert count(M=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 16 GiB
+    assert count(nbytes=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
+    assert count(N=1000) == STATUS["LDA_ERR_WORKSPACE"]                # an index of 100 tokens
+    for key in ("off", "ndk", "nwk", "index", "w", "z"):
+        assert count(**{key: None}) == STATUS["LDA_ERR_NULL"], key
+    for key in ("w", "z", "ndk", "nwk"):
+        assert count(**{key: A + 2}) == STATUS["LDA_ERR_ALIGN"], key
+    assert count(off=A + 4) == STATUS["LDA_ERR_ALIGN"]
+    assert count(index=A + 4) == STATUS["LDA_ERR_ALIGN"]

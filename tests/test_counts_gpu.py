@@ -250,3 +250,154 @@ def test_counts_docs_overwrite_and_equal_to_doc_id_form():
     lda.count_topics_docs(off0, e, e, V, K, ndk=ndk, nwk=nwk)
     torch.cuda.synchronize()
     assert int(ndk.abs().sum()) == 0 and int(nwk.abs().sum()) == 0
+
+
+# ---------------------------------------------------------------------------
+# The word index (lda_word_index_build) and the counts taken from it
+# (lda_count_topics_indexed).  The index is checked against its definition:
+# off = the exclusive prefix sum of the in-range words' token counts, and
+# positions off[w] .. off[w+1] - 1 hold exactly the tokens of word w (in any
+# order); the counts against the oracle, cell for cell.
+
+def _check_index(idx, w, V):
+    import torch
+    torch.cuda.synchronize()
+    a = {k: v.cpu().numpy() for k, v in idx.arrays().items()}
+    valid = (w >= 0) & (w < V)
+    hist = np.bincount(w[valid], minlength=V)
+    want_off = np.concatenate([[0], np.cumsum(hist)]).astype(np.int64)
+    assert np.array_equal(a["off"].astype(np.int64), want_off)
+    n = int(want_off[-1])
+    perm, ws = a["perm"][:n], a["wsorted"][:n]
+    assert np.array_equal(np.sort(perm), np.nonzero(valid)[0])   # each in-range token once
+    assert np.array_equal(w[perm], ws)                            # its own word
+    assert np.all(np.diff(ws) >= 0)                               # grouped by word
+    return a
+
+
+def _gpu_counts_indexed(off, w, z, V, K, idx=None, ndk=None, nwk=None):
+    import torch
+    import paper_1505_03851_amd as lda
+    o = torch.from_numpy(np.ascontiguousarray(off, np.int64)).cuda()
+    wd = torch.from_numpy(np.ascontiguousarray(w, np.int32)).cuda()
+    zd = torch.from_numpy(np.ascontiguousarray(z, np.int32)).cuda()
+    if idx is None:
+        idx = lda.word_index_build(wd, V)
+    a, b = lda.count_topics_indexed(o, wd, zd, idx, K, ndk=ndk, nwk=nwk)
+    torch.cuda.synchronize()
+    return a.cpu().numpy(), b.cpu().numpy(), idx
+
+
+@pytest.mark.parametrize("name", ["tiny-K32", "corpus1M-K64", "corpus1M-K256",
+                                  "corpus16M-K1024", "poisson300-K2048"])
+def test_counts_indexed_of_the_draw_every_config(name):
+    """Index once, draw, count from the index: every cell equals the oracle's,
+    and the index is the counting sort of the words."""
+    import torch
+    import paper_1505_03851_amd as lda
+    c = named_corpus(name)
+    dev = to_device(c)
+    print(f"[case] counts indexed {name} N={c.N} M={c.M} V={c.V} K={c.K}", flush=True)
+    idx = lda.word_index_build(dev["word_id"], c.V)
+    _check_index(idx, c.word_id, c.V)
+    off = torch.from_numpy(_offsets(c.doc_id, c.M)).cuda()
+    z = lda.draw_butterfly(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    ndk, nwk = lda.count_topics_indexed(off, dev["word_id"], z, idx, c.K)
+    torch.cuda.synchronize()
+    want = oracle.counts(c.doc_id, c.word_id, z.cpu().numpy(), c.M, c.V, c.K)
+    _same(ndk.cpu().numpy(), want[0], "ndk")
+    _same(nwk.cpu().numpy(), want[1], "nwk")
+    print(f"[counts] indexed {name}: ndk and nwk equal the oracle's", flush=True)
+
+
+@pytest.mark.parametrize("shape", [(1, 1, 1, 1), (7, 30, 5, 3), (2047, 20, 300, 33),
+                                   (2048, 20, 300, 64), (2049, 20, 300, 64),
+                                   (64013, 5000, 4000, 1000), (100_000, 3, 7, 4096),
+                                   (300_001, 3000, 20_000, 200), (70_001, 1, 500, 200)],
+                         ids=lambda s: "N{}-M{}-V{}-K{}".format(*s))
+def test_counts_indexed_random(shape):
+    """Random topics over Zipf words (a few words span many segments, many
+    words a single one), ragged documents; also the index of V = 7 words for
+    100,000 tokens (every word spans many segments)."""
+    N, M, V, K = shape
+    c = make_random(N, M, V, 1, seed=N + 3 * K, doc_order="ragged")
+    z = np.random.default_rng(K + 1).integers(0, K, N).astype(np.int32)
+    print(f"[case] counts indexed random {shape}", flush=True)
+    off = _offsets(c.doc_id, M)
+    got_d, got_w, idx = _gpu_counts_indexed(off, c.word_id, z, V, K)
+    _check_index(idx, c.word_id, V)
+    want = oracle.counts(c.doc_id, c.word_id, z, M, V, K)
+    _same(got_d, want[0], "ndk")
+    _same(got_w, want[1], "nwk")
+
+
+def test_counts_indexed_out_of_range_and_reuse():
+    """Words and topics out of range are neither indexed nor counted; one
+    index serves several sweeps (new topics each time, outputs with garbage
+    overwritten); empty words have zero rows."""
+    import torch
+    N, M, V, K = 50_000, 40, 3000, 70
+    rng = np.random.default_rng(8)
+    w = np.minimum(rng.zipf(1.3, N) - 1, V + 50).astype(np.int32)   # some past V
+    w[3::101] = -7
+    doc = np.sort(rng.integers(0, M, N)).astype(np.int32)
+    off = _offsets(doc, M)
+    idx = None
+    ndk = torch.full((M, K), 9, dtype=torch.int32, device="cuda")
+    nwk = torch.full((V, K), -4, dtype=torch.int32, device="cuda")
+    for sweep in range(3):
+        z = rng.integers(0, K, N).astype(np.int32)
+        z[sweep::53] = K + sweep
+        got_d, got_w, idx = _gpu_counts_indexed(off, w, z, V, K, idx=idx, ndk=ndk, nwk=nwk)
+        want = oracle.counts(doc, w, z, M, V, K)
+        _same(got_d, want[0], f"ndk sweep {sweep}")
+        _same(got_w, want[1], f"nwk sweep {sweep}")
+        ndk.fill_(9)
+        nwk.fill_(-4)
+    a = _check_index(idx, w, V)
+    assert int(a["off"][-1]) < N                   # out-of-range words left out
+    assert (np.bincount(w[(w >= 0) & (w < V)], minlength=V) == 0).any()
+
+
+def test_word_index_captured_in_a_graph():
+    """Build the index, draw and count from it, all captured in one HIP graph
+    and replayed (eager work between the replays, the index workspace
+    scribbled over): every replay's index and counts are right."""
+    import torch
+    import paper_1505_03851_amd as lda
+    c = make_random(64 * 400 + 9, 300, 5000, 96, seed=12, doc_order="ragged")
+    dev = to_device(c)
+    off = torch.from_numpy(_offsets(c.doc_id, c.M)).cuda()
+    z = torch.empty(c.N, dtype=torch.int32, device="cuda")
+    ndk = torch.empty((c.M, c.K), dtype=torch.int32, device="cuda")
+    nwk = torch.empty((c.V, c.K), dtype=torch.int32, device="cuda")
+    ws = torch.empty(lda.word_index_bytes(c.N, c.V), dtype=torch.uint8, device="cuda")
+    holder = {}
+
+    def step():
+        holder["idx"] = lda.word_index_build(dev["word_id"], c.V, workspace=ws)
+        lda.draw_butterfly(dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"],
+                           out=z)
+        lda.count_topics_indexed(off, dev["word_id"], z, holder["idx"], c.K, ndk=ndk, nwk=nwk)
+
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        step()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        step()
+    rng = np.random.default_rng(13)
+    for rep in range(3):
+        new_u = (rng.integers(0, 1 << 24, c.N) * 2.0 ** -24).astype(np.float32)
+        dev["u"].copy_(torch.from_numpy(new_u))
+        g.replay()
+        torch.cuda.synchronize()
+        _check_index(holder["idx"], c.word_id, c.V)
+        want = oracle.counts(c.doc_id, c.word_id, z.cpu().numpy(), c.M, c.V, c.K)
+        _same(ndk.cpu().numpy(), want[0], f"ndk replay {rep}")
+        _same(nwk.cpu().numpy(), want[1], f"nwk replay {rep}")
+        ws.fill_(255)                # eager work between the replays
+        ndk.fill_(3)
