@@ -403,10 +403,11 @@ int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V, void *ind
 /*
  * lda_count_topics_docs with the word table counted from a word index
  * (lda_word_index_build over the same word_id, N and V): the tokens are taken
- * word by word in segments of 2,048 positions; within a segment each cell's
- * tokens are summed in LDS, and the cells of a word whose tokens all lie in
- * the segment are written with plain stores, the others (words that straddle
- * segments) added with device atomics.  Same results as lda_count_topics_docs
+ * word by word, each workgroup a run of 2,048-position chunks; each cell's
+ * tokens are summed in an LDS table, and when the table is written out the
+ * cells of a word whose tokens all lie in the positions summed since the last
+ * write are stored, the others (words that straddle writes or workgroups)
+ * added with device atomics.  Same results as lda_count_topics_docs
  * (exact); same arguments and errors, plus those of the index
  * (LDA_ERR_WORKSPACE when index_bytes < lda_word_index_bytes(N, V)).  An index
  * built from other tokens gives wrong counts but no access outside ndk, nwk,

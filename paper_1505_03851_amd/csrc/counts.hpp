@@ -65,6 +65,20 @@ __device__ __forceinline__ void count_insert(uint32_t *keys, uint32_t *cnt, uint
   }
 }
 
+// The same, returning whether the insert took a free slot (a key new to the
+// table).
+__device__ __forceinline__ bool count_insert_new(uint32_t *keys, uint32_t *cnt, uint32_t key) {
+  uint32_t s = (key * 2654435761u) >> (32 - __builtin_ctz(kCountSlots));
+  while (true) {
+    const uint32_t prev = atomicCAS(&keys[s], kCountEmpty, key);
+    if (prev == kCountEmpty || prev == key) {
+      atomicAdd(&cnt[s], 1u);
+      return prev == kCountEmpty;
+    }
+    s = (s + 1) & (kCountSlots - 1);
+  }
+}
+
 // The same, returning the slot and, in `rank`, the key's count before this
 // insert (the insert's rank among the chunk's inserts of the key).
 __device__ __forceinline__ uint32_t count_insert_ranked(uint32_t *keys, uint32_t *cnt,

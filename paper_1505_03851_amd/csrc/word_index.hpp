@@ -15,11 +15,12 @@
 // chunk of tokens reserves a run of positions per distinct word with one
 // atomic and places its tokens; the order of a word's tokens is not fixed).
 // Tokens whose word id lies outside [0, V) are left out.  The counts then
-// take the positions in segments of kCountChunk: within a segment a cell's
-// tokens are aggregated in LDS as in count_kernel, and a cell of a word whose
-// tokens all lie in the segment is written with a plain store (no other
-// segment touches it); only words that straddle segments (the frequent ones,
-// and at most two per segment at its ends) add with atomics.
+// take the positions in runs of chunks: a cell's tokens are aggregated in LDS
+// as in count_kernel, and at each flush of the table a cell of a word whose
+// tokens all lie in the positions taken since the last flush is written with
+// a plain store (no other workgroup touches it); only words that straddle
+// flushes (the frequent ones, and at most two per flush at its ends) add
+// with atomics.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -42,30 +43,51 @@ __global__ __launch_bounds__(256) void index_fill(int32_t *p, int64_t n, int32_t
   for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = v;
 }
 
-// Tokens per word (word ids in [0, V)), aggregated per chunk in LDS, added to
-// counts[V] (zero beforehand) with one atomic per distinct word and chunk.
+// Each workgroup of the build and of the indexed counts takes a run of
+// kIndexRun chunks and keeps one LDS table across them, flushing it (to
+// memory, with one atomic or store per distinct key) only when it holds more
+// than kFlushAt keys (so that after the next chunk it is at most 3/4 full)
+// and at the end of the run: a frequent word's counter or cell then takes
+// one atomic per flush rather than per chunk, and atomics on one address are
+// executed one after another on the memory side.
+constexpr int kIndexRun = 8;
+constexpr uint32_t kFlushAt = kCountSlots / 2 - kCountChunk / 2;
+
+// Tokens per word (word ids in [0, V)), aggregated per run in LDS, added to
+// counts[V] (zero beforehand) with one atomic per distinct word and flush.
 __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__restrict__ word_id,
                                                              int64_t N, int32_t V,
                                                              int32_t *__restrict__ counts) {
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
+  __shared__ uint32_t used;  // keys in the table
   for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
     keys[s] = kCountEmpty;
     cnt[s] = 0;
   }
-  const int64_t c0 = (int64_t)blockIdx.x * kCountChunk + threadIdx.x;
-  int32_t w[kCountPer];
+  if (threadIdx.x == 0) used = 0;
+  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
+  for (int c = 0; c < kIndexRun; ++c) {
+    const int64_t c0 = run0 + (int64_t)c * kCountChunk;
+    if (c0 >= N) break;
+    int32_t w[kCountPer];
 #pragma unroll
-  for (int i = 0; i < kCountPer; ++i) {
-    const int64_t n = c0 + (int64_t)i * kCountThreads;
-    w[i] = n < N ? word_id[n] : -1;
+    for (int i = 0; i < kCountPer; ++i) {
+      const int64_t n = c0 + threadIdx.x + (int64_t)i * kCountThreads;
+      w[i] = n < N ? word_id[n] : -1;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < kCountPer; ++i)
+      if ((uint32_t)w[i] < (uint32_t)V && count_insert_new(keys, cnt, (uint32_t)w[i]))
+        atomicAdd(&used, 1u);
+    __syncthreads();
+    if (used > kFlushAt || c == kIndexRun - 1 || c0 + kCountChunk >= N) {
+      count_flush(keys, cnt, counts);
+      __syncthreads();
+      if (threadIdx.x == 0) used = 0;
+    }
   }
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kCountPer; ++i)
-    if ((uint32_t)w[i] < (uint32_t)V) count_insert(keys, cnt, (uint32_t)w[i]);
-  __syncthreads();
-  count_flush(keys, cnt, counts);
 }
 
 // Exclusive scan of the kScanThreads values v of a workgroup (one per
@@ -144,13 +166,13 @@ __global__ __launch_bounds__(kScanThreads) void index_scan_add(int32_t *__restri
     if (i0 + j < n) out[i0 + j] += add;
 }
 
-// Place the tokens: each chunk counts its tokens per word in LDS (each token
-// learns its rank among its word's tokens in the chunk), reserves a run of
-// positions per distinct word with one atomic on cursor[w] (zero
-// beforehand), and writes perm and wsorted at off[w] + run start + rank.
-// The token set is index_hist's (n < N, word id in [0, V)), so every word's
-// positions end at off[w + 1]; a position past `limit` (an index whose
-// offsets do not belong to these tokens) is not written.
+// Place the tokens, run by run: the tokens since the last flush are counted
+// per word in LDS; at a flush each distinct word reserves a run of positions
+// with one atomic on cursor[w] (zero beforehand), then those tokens are read
+// again and each writes perm and wsorted at off[w] + run start + its rank
+// among the word's tokens there.  The token set is index_hist's (n < N, word
+// id in [0, V)), so every word's positions end at off[w + 1]; a position past
+// `limit` (offsets that do not belong to these tokens) is not written.
 __global__ __launch_bounds__(kCountThreads) void index_scatter(
     const int32_t *__restrict__ word_id, int64_t N, int32_t V, const int32_t *__restrict__ off,
     int32_t *__restrict__ cursor, int32_t *__restrict__ perm, int32_t *__restrict__ wsorted,
@@ -158,87 +180,126 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
   __shared__ int32_t start[kCountSlots];
+  __shared__ uint32_t used;
   for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
     keys[s] = kCountEmpty;
     cnt[s] = 0;
   }
-  const int64_t c0 = (int64_t)blockIdx.x * kCountChunk + threadIdx.x;
-  int32_t w[kCountPer];
+  if (threadIdx.x == 0) used = 0;
+  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
+  int64_t from = run0;  // first token since the last flush
+  for (int c = 0; c < kIndexRun; ++c) {
+    const int64_t c0 = run0 + (int64_t)c * kCountChunk;
+    if (c0 >= N) break;
+    int32_t w[kCountPer];
 #pragma unroll
-  for (int i = 0; i < kCountPer; ++i) {
-    const int64_t n = c0 + (int64_t)i * kCountThreads;
-    w[i] = n < N ? word_id[n] : -1;
-  }
-  __syncthreads();
-  uint32_t slot[kCountPer], rank[kCountPer];
+    for (int i = 0; i < kCountPer; ++i) {
+      const int64_t n = c0 + threadIdx.x + (int64_t)i * kCountThreads;
+      w[i] = n < N ? word_id[n] : -1;
+    }
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kCountPer; ++i)
-    if ((uint32_t)w[i] < (uint32_t)V) slot[i] = count_insert_ranked(keys, cnt, (uint32_t)w[i], rank[i]);
-  __syncthreads();
-  for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads)
-    if (keys[s] != kCountEmpty) start[s] = atomicAdd(&cursor[keys[s]], (int32_t)cnt[s]);
-  __syncthreads();
-#pragma unroll
-  for (int i = 0; i < kCountPer; ++i) {
-    if ((uint32_t)w[i] < (uint32_t)V) {
-      const int64_t p = (int64_t)off[w[i]] + start[slot[i]] + rank[i];
-      if (p >= 0 && p < limit) {
-        perm[p] = (int32_t)(c0 + (int64_t)i * kCountThreads);
-        wsorted[p] = w[i];
+    for (int i = 0; i < kCountPer; ++i)
+      if ((uint32_t)w[i] < (uint32_t)V && count_insert_new(keys, cnt, (uint32_t)w[i]))
+        atomicAdd(&used, 1u);
+    __syncthreads();
+    const int64_t to = c0 + kCountChunk < N ? c0 + kCountChunk : N;
+    if (used > kFlushAt || c == kIndexRun - 1 || to >= N) {
+      for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
+        if (keys[s] != kCountEmpty) start[s] = atomicAdd(&cursor[keys[s]], (int32_t)cnt[s]);
+        cnt[s] = 0;
       }
+      __syncthreads();
+      for (int64_t p0 = from; p0 < to; p0 += kCountChunk) {
+#pragma unroll
+        for (int i = 0; i < kCountPer; ++i) {
+          const int64_t n = p0 + threadIdx.x + (int64_t)i * kCountThreads;
+          const int32_t wn = n < to ? word_id[n] : -1;
+          if ((uint32_t)wn < (uint32_t)V) {
+            uint32_t rank;
+            const uint32_t slot = count_insert_ranked(keys, cnt, (uint32_t)wn, rank);
+            const int64_t p = (int64_t)off[wn] + start[slot] + rank;
+            if (p >= 0 && p < limit) {
+              perm[p] = (int32_t)n;
+              wsorted[p] = wn;
+            }
+          }
+        }
+      }
+      __syncthreads();
+      for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
+        keys[s] = kCountEmpty;
+        cnt[s] = 0;
+      }
+      if (threadIdx.x == 0) used = 0;
+      from = to;
     }
   }
 }
 
-// The word table from the index: one workgroup per segment of kCountChunk
-// positions (positions past off[V] hold no token).  A token counts when its
-// topic is in [0, K); its cell w K + k.  A cell of a word whose positions
-// all lie in the segment is stored, the others added atomically, into nwk
-// (zero beforehand).  Positions past N, perm entries outside [0, N) and
-// words outside [0, V) (an index that does not belong to these tokens) are
-// skipped.
+// The word table from the index: one workgroup per run of kIndexRun
+// segments of kCountChunk positions (positions past off[V] hold no token).
+// A token counts when its topic is in [0, K); its cell w K + k.  At a flush,
+// a cell of a word whose positions all lie in the positions since the last
+// flush is stored, the others added atomically, into nwk (zero beforehand).
+// Positions past N, perm entries outside [0, N) and words outside [0, V) (an
+// index that does not belong to these tokens) are skipped.
 __global__ __launch_bounds__(kCountThreads) void count_words_indexed(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ wsorted,
     const int32_t *__restrict__ off, const int32_t *__restrict__ z, int64_t N, int32_t V,
     int32_t K, int32_t *__restrict__ nwk) {
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
-  const int64_t lo = (int64_t)blockIdx.x * kCountChunk;
+  __shared__ uint32_t used;
+  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
   // (at most N positions, whatever an index of other tokens says)
   const int64_t total = off[V] < N ? off[V] : N;
-  if (lo >= total) return;  // (uniform: the whole workgroup leaves)
-  const int64_t hi = lo + kCountChunk < total ? lo + kCountChunk : total;
+  if (run0 >= total) return;  // (uniform: the whole workgroup leaves)
   for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
     keys[s] = kCountEmpty;
     cnt[s] = 0;
   }
-  uint32_t key[kCountPer];
+  if (threadIdx.x == 0) used = 0;
+  int64_t from = run0;  // first position since the last flush
+  for (int c = 0; c < kIndexRun; ++c) {
+    const int64_t lo = run0 + (int64_t)c * kCountChunk;
+    if (lo >= total) break;
+    const int64_t hi = lo + kCountChunk < total ? lo + kCountChunk : total;
+    uint32_t key[kCountPer];
 #pragma unroll
-  for (int i = 0; i < kCountPer; ++i) {
-    const int64_t p = lo + threadIdx.x + (int64_t)i * kCountThreads;
-    int32_t n = -1, w = -1, k = -1;
-    if (p < hi) {
-      n = perm[p];
-      w = wsorted[p];
+    for (int i = 0; i < kCountPer; ++i) {
+      const int64_t p = lo + threadIdx.x + (int64_t)i * kCountThreads;
+      int32_t n = -1, w = -1, k = -1;
+      if (p < hi) {
+        n = perm[p];
+        w = wsorted[p];
+      }
+      if ((uint64_t)(int64_t)n < (uint64_t)N) k = z[n];
+      const bool ok = (uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K;
+      key[i] = ok ? (uint32_t)w * (uint32_t)K + (uint32_t)k : kCountEmpty;
     }
-    if ((uint64_t)(int64_t)n < (uint64_t)N) k = z[n];
-    const bool ok = (uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K;
-    key[i] = ok ? (uint32_t)w * (uint32_t)K + (uint32_t)k : kCountEmpty;
-  }
-  __syncthreads();
+    __syncthreads();
 #pragma unroll
-  for (int i = 0; i < kCountPer; ++i)
-    if (key[i] != kCountEmpty) count_insert(keys, cnt, key[i]);
-  __syncthreads();
-  for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
-    const uint32_t kk = keys[s];
-    if (kk != kCountEmpty) {
-      const uint32_t w = kk / (uint32_t)K;
-      const bool whole = off[w] >= lo && off[w + 1] <= hi;
-      if (whole)
-        nwk[kk] = (int32_t)cnt[s];
-      else
-        atomicAdd(&nwk[kk], (int32_t)cnt[s]);
+    for (int i = 0; i < kCountPer; ++i)
+      if (key[i] != kCountEmpty && count_insert_new(keys, cnt, key[i])) atomicAdd(&used, 1u);
+    __syncthreads();
+    if (used > kFlushAt || c == kIndexRun - 1 || hi >= total) {
+      for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
+        const uint32_t kk = keys[s];
+        if (kk != kCountEmpty) {
+          const uint32_t w = kk / (uint32_t)K;
+          const bool whole = off[w] >= from && off[w + 1] <= hi;
+          if (whole)
+            nwk[kk] = (int32_t)cnt[s];
+          else
+            atomicAdd(&nwk[kk], (int32_t)cnt[s]);
+          keys[s] = kCountEmpty;
+          cnt[s] = 0;
+        }
+      }
+      __syncthreads();
+      if (threadIdx.x == 0) used = 0;
+      from = hi;
     }
   }
 }
