@@ -739,11 +739,12 @@ extern "C" int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V
   int32_t *perm = reinterpret_cast<int32_t *>(b + L.perm);
   int32_t *wsorted = reinterpret_cast<int32_t *>(b + L.wsorted);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int64_t run = (int64_t)kIndexRun * kCountChunk;
-  const unsigned runs = (unsigned)((N + run - 1) / run);
+  const int run = index_run(N);
+  const int64_t per = (int64_t)run * kCountChunk;
+  const unsigned runs = (unsigned)((N + per - 1) / per);
   // histogram of the words into cursor, then its exclusive scan into off
   index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
-  if (N > 0) index_hist<<<runs, kCountThreads, 0, s>>>(word_id, N, V, cursor);
+  if (N > 0) index_hist<<<runs, kCountThreads, 0, s>>>(word_id, N, V, run, cursor);
   const int64_t items = (int64_t)V + 1;
   const unsigned nb = (unsigned)((items + kScanItems - 1) / kScanItems);
   index_scan_local<<<nb, kScanThreads, 0, s>>>(cursor, V, items, off, sums);
@@ -752,7 +753,8 @@ extern "C" int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V
   // the tokens placed word by word
   index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
   if (N > 0)
-    index_scatter<<<runs, kCountThreads, 0, s>>>(word_id, N, V, off, cursor, perm, wsorted, N);
+    index_scatter<<<runs, kCountThreads, 0, s>>>(word_id, N, V, run, off, cursor, perm, wsorted,
+                                                 N);
   return finish_launch();
 }
 
@@ -784,10 +786,11 @@ extern "C" int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_
   count_docs_kernel<<<(unsigned)((M + kDocWaves - 1) / kDocWaves), kDocWaves * 64, lds, s>>>(
       doc_offsets, word_id, z, N, M, V, K, ndk);
   if (N > 0) {
-    const int64_t run = (int64_t)kIndexRun * kCountChunk;
-    count_words_indexed<<<(unsigned)((N + run - 1) / run), kCountThreads, 0, s>>>(
+    const int run = index_run(N);
+    const int64_t per = (int64_t)run * kCountChunk;
+    count_words_indexed<<<(unsigned)((N + per - 1) / per), kCountThreads, 0, s>>>(
         reinterpret_cast<const int32_t *>(b + L.perm), reinterpret_cast<const int32_t *>(b + L.wsorted),
-        reinterpret_cast<const int32_t *>(b + L.off), z, N, V, K, nwk);
+        reinterpret_cast<const int32_t *>(b + L.off), z, N, V, K, run, nwk);
   }
   return finish_launch();
 }

@@ -44,19 +44,28 @@ __global__ __launch_bounds__(256) void index_fill(int32_t *p, int64_t n, int32_t
 }
 
 // Each workgroup of the build and of the indexed counts takes a run of
-// kIndexRun chunks and keeps one LDS table across them, flushing it (to
-// memory, with one atomic or store per distinct key) only when it holds more
-// than kFlushAt keys (so that after the next chunk it is at most 3/4 full)
-// and at the end of the run: a frequent word's counter or cell then takes
-// one atomic per flush rather than per chunk, and atomics on one address are
-// executed one after another on the memory side.
+// `run` chunks (index_run: up to kIndexRun, while the grid keeps
+// kIndexGroups workgroups) and keeps one LDS table across them, flushing it
+// (to memory, with one atomic or store per distinct key) only when it holds
+// more than kFlushAt keys (so that after the next chunk it is at most 3/4
+// full) and at the end of the run: a frequent word's counter or cell then
+// takes one atomic per flush rather than per chunk, and atomics on one
+// address are executed one after another on the memory side.
 constexpr int kIndexRun = 8;
+constexpr int64_t kIndexGroups = 2048;
 constexpr uint32_t kFlushAt = kCountSlots / 2 - kCountChunk / 2;
+
+// Chunks per workgroup for N tokens.
+__host__ __device__ inline int index_run(int64_t N) {
+  const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
+  const int64_t r = chunks / kIndexGroups;
+  return r < 1 ? 1 : (r > kIndexRun ? kIndexRun : (int)r);
+}
 
 // Tokens per word (word ids in [0, V)), aggregated per run in LDS, added to
 // counts[V] (zero beforehand) with one atomic per distinct word and flush.
 __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__restrict__ word_id,
-                                                             int64_t N, int32_t V,
+                                                             int64_t N, int32_t V, int run,
                                                              int32_t *__restrict__ counts) {
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
@@ -66,8 +75,8 @@ __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__res
     cnt[s] = 0;
   }
   if (threadIdx.x == 0) used = 0;
-  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
-  for (int c = 0; c < kIndexRun; ++c) {
+  const int64_t run0 = (int64_t)blockIdx.x * run * kCountChunk;
+  for (int c = 0; c < run; ++c) {
     const int64_t c0 = run0 + (int64_t)c * kCountChunk;
     if (c0 >= N) break;
     int32_t w[kCountPer];
@@ -82,7 +91,7 @@ __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__res
       if ((uint32_t)w[i] < (uint32_t)V && count_insert_new(keys, cnt, (uint32_t)w[i]))
         atomicAdd(&used, 1u);
     __syncthreads();
-    if (used > kFlushAt || c == kIndexRun - 1 || c0 + kCountChunk >= N) {
+    if (used > kFlushAt || c == run - 1 || c0 + kCountChunk >= N) {
       count_flush(keys, cnt, counts);
       __syncthreads();
       if (threadIdx.x == 0) used = 0;
@@ -174,9 +183,9 @@ __global__ __launch_bounds__(kScanThreads) void index_scan_add(int32_t *__restri
 // id in [0, V)), so every word's positions end at off[w + 1]; a position past
 // `limit` (offsets that do not belong to these tokens) is not written.
 __global__ __launch_bounds__(kCountThreads) void index_scatter(
-    const int32_t *__restrict__ word_id, int64_t N, int32_t V, const int32_t *__restrict__ off,
-    int32_t *__restrict__ cursor, int32_t *__restrict__ perm, int32_t *__restrict__ wsorted,
-    int64_t limit) {
+    const int32_t *__restrict__ word_id, int64_t N, int32_t V, int run,
+    const int32_t *__restrict__ off, int32_t *__restrict__ cursor, int32_t *__restrict__ perm,
+    int32_t *__restrict__ wsorted, int64_t limit) {
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
   __shared__ int32_t start[kCountSlots];
@@ -186,9 +195,9 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
     cnt[s] = 0;
   }
   if (threadIdx.x == 0) used = 0;
-  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
+  const int64_t run0 = (int64_t)blockIdx.x * run * kCountChunk;
   int64_t from = run0;  // first token since the last flush
-  for (int c = 0; c < kIndexRun; ++c) {
+  for (int c = 0; c < run; ++c) {
     const int64_t c0 = run0 + (int64_t)c * kCountChunk;
     if (c0 >= N) break;
     int32_t w[kCountPer];
@@ -204,7 +213,7 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
         atomicAdd(&used, 1u);
     __syncthreads();
     const int64_t to = c0 + kCountChunk < N ? c0 + kCountChunk : N;
-    if (used > kFlushAt || c == kIndexRun - 1 || to >= N) {
+    if (used > kFlushAt || c == run - 1 || to >= N) {
       for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
         if (keys[s] != kCountEmpty) start[s] = atomicAdd(&cursor[keys[s]], (int32_t)cnt[s]);
         cnt[s] = 0;
@@ -237,8 +246,8 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
   }
 }
 
-// The word table from the index: one workgroup per run of kIndexRun
-// segments of kCountChunk positions (positions past off[V] hold no token).
+// The word table from the index: one workgroup per run of `run` chunks of
+// kCountChunk positions (positions past off[V] hold no token).
 // A token counts when its topic is in [0, K); its cell w K + k.  At a flush,
 // a cell of a word whose positions all lie in the positions since the last
 // flush is stored, the others added atomically, into nwk (zero beforehand).
@@ -247,11 +256,11 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
 __global__ __launch_bounds__(kCountThreads) void count_words_indexed(
     const int32_t *__restrict__ perm, const int32_t *__restrict__ wsorted,
     const int32_t *__restrict__ off, const int32_t *__restrict__ z, int64_t N, int32_t V,
-    int32_t K, int32_t *__restrict__ nwk) {
+    int32_t K, int run, int32_t *__restrict__ nwk) {
   __shared__ uint32_t keys[kCountSlots];
   __shared__ uint32_t cnt[kCountSlots];
   __shared__ uint32_t used;
-  const int64_t run0 = (int64_t)blockIdx.x * kIndexRun * kCountChunk;
+  const int64_t run0 = (int64_t)blockIdx.x * run * kCountChunk;
   // (at most N positions, whatever an index of other tokens says)
   const int64_t total = off[V] < N ? off[V] : N;
   if (run0 >= total) return;  // (uniform: the whole workgroup leaves)
@@ -261,7 +270,7 @@ __global__ __launch_bounds__(kCountThreads) void count_words_indexed(
   }
   if (threadIdx.x == 0) used = 0;
   int64_t from = run0;  // first position since the last flush
-  for (int c = 0; c < kIndexRun; ++c) {
+  for (int c = 0; c < run; ++c) {
     const int64_t lo = run0 + (int64_t)c * kCountChunk;
     if (lo >= total) break;
     const int64_t hi = lo + kCountChunk < total ? lo + kCountChunk : total;
@@ -283,7 +292,7 @@ __global__ __launch_bounds__(kCountThreads) void count_words_indexed(
     for (int i = 0; i < kCountPer; ++i)
       if (key[i] != kCountEmpty && count_insert_new(keys, cnt, key[i])) atomicAdd(&used, 1u);
     __syncthreads();
-    if (used > kFlushAt || c == kIndexRun - 1 || hi >= total) {
+    if (used > kFlushAt || c == run - 1 || hi >= total) {
       for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
         const uint32_t kk = keys[s];
         if (kk != kCountEmpty) {
