@@ -11,9 +11,10 @@
 //   perm[p]                  the token at position p              int32 [N]
 //   wsorted[p]               its word                             int32 [N]
 //
-// (a counting sort: a histogram of the words, an exclusive scan, then each
-// chunk of tokens reserves a run of positions per distinct word with one
-// atomic and places its tokens; the order of a word's tokens is not fixed).
+// (a counting sort: a histogram of the words, an exclusive scan, then the
+// tokens summed in a workgroup's LDS table reserve a run of positions per
+// distinct word with one atomic and are placed there; the order of a word's
+// tokens is not fixed).
 // Tokens whose word id lies outside [0, V) are left out.  The counts then
 // take the positions in runs of chunks: a cell's tokens are aggregated in LDS
 // as in count_kernel, and at each flush of the table a cell of a word whose
