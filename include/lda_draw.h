@@ -36,7 +36,9 @@
  * owned by the caller, 4-byte aligned.  The library keeps no state between
  * calls and allocates no device memory; kernels use on-chip LDS only (and,
  * in the naive kernel, the per-lane private segment the HIP runtime manages).
- * The routed draw keeps its routing in a workspace the caller provides.
+ * The routed draw keeps its routing, and the indexed counts their word
+ * index, in a workspace the caller provides (lda_draw_routed_scratch: in a
+ * static array the library holds).
  *
  * Streams: `stream` is a hipStream_t (NULL = the default stream).  Calls only
  * enqueue work and return; the caller synchronises (lda_route_build alone
@@ -45,9 +47,13 @@
  *
  * Errors: every entry point returns LDA_OK (0) or a negative status.  Argument
  * checks happen before any HIP call, so a rejected call has no effect and
- * touches no device.  N == 0 is a no-op returning LDA_OK.  Preconditions that
- * are not checked (ids in range, finite non-negative weights, u in [0, 1))
- * are the caller's: an out-of-range id reads outside theta or phi.
+ * touches no device.  N == 0 is a no-op returning LDA_OK (the counts: tables
+ * cleared).  Preconditions that are not checked (ids in range, finite
+ * non-negative weights, u in [0, 1)) are the caller's: an out-of-range id
+ * gives a meaningless draw, and in lda_draw_naive and lda_butterfly_table,
+ * which address theta and phi directly, reads outside them (the other draws
+ * read through range-checked buffer resources, or past 4 GiB clamp the id to
+ * the last row).
  */
 #ifndef LDA_DRAW_H
 #define LDA_DRAW_H
