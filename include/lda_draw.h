@@ -389,7 +389,8 @@ int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *word_id, co
  * the index occupies until the caller frees it; the library keeps no state.
  * Layout inside it, each section on a 256-byte boundary: off int32 [V + 1]
  * (the positions of word w are off[w] .. off[w+1] - 1; off[V] = the tokens
- * indexed), a histogram / cursor int32 [V], the scan's workgroup sums, perm
+ * indexed), the build's per-word counters int32 [16 V] (one to a 64-byte
+ * line), the scan's workgroup sums, perm
  * int32 [N] (the token at each position) and wsorted int32 [N] (its word).
  * Tokens whose word id lies outside [0, V) are not indexed.  The order of a
  * word's tokens is not fixed; the counts do not depend on it.

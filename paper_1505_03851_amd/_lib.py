@@ -457,7 +457,7 @@ def word_index_layout(N: int, V: int) -> dict[str, int]:
     def up(b):
         return (b + 255) & ~255
     lay, at = {}, 0
-    for name, b in (("off", 4 * (V + 1)), ("cursor", 4 * V), ("sums", 4 * 4096),
+    for name, b in (("off", 4 * (V + 1)), ("cursor", 4 * V * 16), ("sums", 4 * 4096),
                     ("perm", 4 * max(N, 1)), ("wsorted", 4 * max(N, 1))):
         lay[name] = at
         at += up(b)

@@ -677,8 +677,9 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
 }
 
 // ---------------------------------------------------------------------------
-// The word index: off [V + 1], a cursor / histogram [V], the scan's workgroup
-// sums, perm [N] and wsorted [N], each section on a 256-byte boundary.
+// The word index: off [V + 1], the histogram / cursors [V kCounterStride],
+// the scan's workgroup sums, perm [N] and wsorted [N], each section on a
+// 256-byte boundary.
 namespace lda {
 namespace {
 
@@ -695,7 +696,7 @@ WordIndexLayout word_index_layout(int64_t N, int32_t V) {
     return o;
   };
   L.off = take(4 * ((size_t)V + 1));
-  L.cursor = take(4 * (size_t)V);
+  L.cursor = take(4 * (size_t)V * kCounterStride);
   L.sums = take(4 * (size_t)kScanMaxBlocks);
   L.perm = take(4 * (size_t)(N > 0 ? N : 1));
   L.wsorted = take(4 * (size_t)(N > 0 ? N : 1));
@@ -743,15 +744,16 @@ extern "C" int lda_word_index_build(const int32_t *word_id, int64_t N, int32_t V
   const int64_t per = (int64_t)run * kCountChunk;
   const unsigned runs = (unsigned)((N + per - 1) / per);
   // histogram of the words into cursor, then its exclusive scan into off
-  index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
+  const int64_t counters = (int64_t)V * kCounterStride;
+  index_fill<<<fill_grid(counters), 256, 0, s>>>(cursor, counters, 0);
   if (N > 0) index_hist<<<runs, kCountThreads, 0, s>>>(word_id, N, V, run, cursor);
   const int64_t items = (int64_t)V + 1;
   const unsigned nb = (unsigned)((items + kScanItems - 1) / kScanItems);
-  index_scan_local<<<nb, kScanThreads, 0, s>>>(cursor, V, items, off, sums);
+  index_scan_local<<<nb, kScanThreads, 0, s>>>(cursor, V, kCounterStride, items, off, sums);
   index_scan_sums<<<1, kScanThreads, 0, s>>>(sums, (int32_t)nb);
   index_scan_add<<<nb, kScanThreads, 0, s>>>(off, items, sums);
   // the tokens placed word by word
-  index_fill<<<fill_grid(V), 256, 0, s>>>(cursor, V, 0);
+  index_fill<<<fill_grid(counters), 256, 0, s>>>(cursor, counters, 0);
   if (N > 0)
     index_scatter<<<runs, kCountThreads, 0, s>>>(word_id, N, V, run, off, cursor, perm, wsorted,
                                                  N);

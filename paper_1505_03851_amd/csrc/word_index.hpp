@@ -56,6 +56,17 @@ constexpr int kIndexRun = 8;
 constexpr int64_t kIndexGroups = 2048;
 constexpr uint32_t kFlushAt = kCountSlots / 2 - kCountChunk / 2;
 
+// The build's per-word counters (the histogram, then the cursors of the
+// scatter) lie kCounterStride ints apart, one to a 64-byte line: atomics on
+// one line are executed one after another on the memory side, and the
+// frequent words' counters, adjacent when the vocabulary is sorted by
+// frequency, would otherwise share lines (measured on MI355X: the build of
+// the 16.8M-token corpus takes 0.88 ms with them apart, 3.15 ms packed).
+#ifndef LDA_COUNTER_STRIDE
+#define LDA_COUNTER_STRIDE 16
+#endif
+constexpr int kCounterStride = LDA_COUNTER_STRIDE;
+
 // Chunks per workgroup for N tokens.
 __host__ __device__ inline int index_run(int64_t N) {
   const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
@@ -64,7 +75,8 @@ __host__ __device__ inline int index_run(int64_t N) {
 }
 
 // Tokens per word (word ids in [0, V)), aggregated per run in LDS, added to
-// counts[V] (zero beforehand) with one atomic per distinct word and flush.
+// counts[w kCounterStride] (zero beforehand) with one atomic per distinct
+// word and flush.
 __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__restrict__ word_id,
                                                              int64_t N, int32_t V, int run,
                                                              int32_t *__restrict__ counts) {
@@ -93,7 +105,14 @@ __global__ __launch_bounds__(kCountThreads) void index_hist(const int32_t *__res
         atomicAdd(&used, 1u);
     __syncthreads();
     if (used > kFlushAt || c == run - 1 || c0 + kCountChunk >= N) {
-      count_flush(keys, cnt, counts);
+      for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
+        const uint32_t key = keys[s];
+        if (key != kCountEmpty) {
+          atomicAdd(&counts[(size_t)key * kCounterStride], (int32_t)cnt[s]);
+          keys[s] = kCountEmpty;
+          cnt[s] = 0;
+        }
+      }
       __syncthreads();
       if (threadIdx.x == 0) used = 0;
     }
@@ -119,12 +138,14 @@ __device__ __forceinline__ int32_t block_exclusive_scan(int32_t v, int32_t &tota
   return incl - v;
 }
 
-// Exclusive scan of in[0 .. n) into out[0 .. n), per workgroup of
-// kScanItems items (each thread kScanPer consecutive ones); the workgroup's
-// total goes to sums[blockIdx.x].  Items at or past n_in count as 0 (so that
-// scanning n = V + 1 items of V counts leaves the grand total in out[V]).
+// Exclusive scan of in[0], in[stride], ... (n_in items) into out[0 .. n),
+// per workgroup of kScanItems items (each thread kScanPer consecutive ones);
+// the workgroup's total goes to sums[blockIdx.x].  Items at or past n_in
+// count as 0 (so that scanning n = V + 1 items of V counts leaves the grand
+// total in out[V]).
 __global__ __launch_bounds__(kScanThreads) void index_scan_local(const int32_t *__restrict__ in,
-                                                                  int64_t n_in, int64_t n,
+                                                                  int64_t n_in, int stride,
+                                                                  int64_t n,
                                                                   int32_t *__restrict__ out,
                                                                   int32_t *__restrict__ sums) {
   const int64_t i0 = ((int64_t)blockIdx.x * kScanThreads + threadIdx.x) * kScanPer;
@@ -132,7 +153,7 @@ __global__ __launch_bounds__(kScanThreads) void index_scan_local(const int32_t *
   int32_t run = 0;
 #pragma unroll
   for (int j = 0; j < kScanPer; ++j) {
-    v[j] = i0 + j < n_in ? in[i0 + j] : 0;
+    v[j] = i0 + j < n_in ? in[(i0 + j) * stride] : 0;
     run += v[j];
   }
   int32_t total;
@@ -178,7 +199,8 @@ __global__ __launch_bounds__(kScanThreads) void index_scan_add(int32_t *__restri
 
 // Place the tokens, run by run: the tokens since the last flush are counted
 // per word in LDS; at a flush each distinct word reserves a run of positions
-// with one atomic on cursor[w] (zero beforehand), then those tokens are read
+// with one atomic on cursor[w kCounterStride] (zero beforehand), then those
+// tokens are read
 // again and each writes perm and wsorted at off[w] + run start + its rank
 // among the word's tokens there.  The token set is index_hist's (n < N, word
 // id in [0, V)), so every word's positions end at off[w + 1]; a position past
@@ -216,7 +238,8 @@ __global__ __launch_bounds__(kCountThreads) void index_scatter(
     const int64_t to = c0 + kCountChunk < N ? c0 + kCountChunk : N;
     if (used > kFlushAt || c == run - 1 || to >= N) {
       for (int s = threadIdx.x; s < kCountSlots; s += kCountThreads) {
-        if (keys[s] != kCountEmpty) start[s] = atomicAdd(&cursor[keys[s]], (int32_t)cnt[s]);
+        if (keys[s] != kCountEmpty)
+          start[s] = atomicAdd(&cursor[(size_t)keys[s] * kCounterStride], (int32_t)cnt[s]);
         cnt[s] = 0;
       }
       __syncthreads();
