@@ -256,8 +256,8 @@ def test_wide_ids_past_the_table_stay_inside():
 
 def test_word_counts_past_4_gib():
     """nwk of about 4.3 GiB (V x K int32, more cells than a byte offset can
-    reach): cells past the 2^32-byte offset are counted exactly, by both
-    count entry points."""
+    reach): cells past the 2^32-byte offset are counted exactly, by every
+    count entry point (document ids, offsets, the word index)."""
     import torch
     import oracle
     import paper_1505_03851_amd as lda
@@ -286,5 +286,12 @@ def test_word_counts_past_4_gib():
     torch.cuda.synchronize()
     assert np.array_equal(ndk2.cpu().numpy(), want_d)
     assert np.array_equal(nwk2.cpu().numpy(), want_w)
-    del ndk, nwk, ndk2, nwk2, got_w
+    nwk2.fill_(-1)
+    index = lda.word_index_build(w, V)
+    ndk3, nwk3 = lda.count_topics_indexed(off, w, z, index, K, ndk=ndk2, nwk=nwk2)
+    torch.cuda.synchronize()
+    assert np.array_equal(ndk3.cpu().numpy(), want_d)
+    got_w = nwk3.cpu().numpy()
+    assert np.array_equal(got_w, want_w), np.argwhere(got_w != want_w)[:5]
+    del ndk, nwk, ndk2, nwk2, ndk3, nwk3, got_w, index
     torch.cuda.empty_cache()
