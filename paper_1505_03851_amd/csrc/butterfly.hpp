@@ -213,6 +213,7 @@ __device__ __forceinline__ float load_f32(rsrc_t r, uint32_t voff, uint32_t soff
 // Four consecutive floats per lane (one 16-byte buffer load): a leaf of
 // kLeaf topics.
 using f4 = float __attribute__((ext_vector_type(4)));
+using f2 = float __attribute__((ext_vector_type(2)));
 constexpr int kLeaf = 4;
 
 __device__ __forceinline__ f4 load_f32x4(rsrc_t r, uint32_t voff, uint32_t soff) {

@@ -38,11 +38,20 @@ constexpr int kRunAhead = 4;  // tokens whose staged theta leaves are read ahead
 // select)
 template <int G>
 constexpr bool kStageRuns = G == kWave;
+// Groups of at most LDA_GROUP_KEEP_MAX_G lanes with 4-topic leaves keep, in
+// LDS, each leaf's running sums after its first three topics for every token
+// of the group (the dot4's intermediate values), so that the final scan
+// reads them there instead of reloading the chosen leaf from memory:
+// 12 (G + 1) bytes per token (rows padded by one leaf against LDS bank
+// conflicts).
+template <int G, int H>
+constexpr bool kKeepLeaves = H == 1 && G <= LDA_GROUP_KEEP_MAX_G;
 
 // LDS bytes per wavefront of the leaf-group kernel: the staged theta leaves
-// of up to kMaxGroupRuns<G> runs.
+// of up to kMaxGroupRuns<G> runs, or the kept leaf sums.
 template <int G, int H>
 constexpr int group_lds_bytes() {
+  if constexpr (kKeepLeaves<G, H>) return kWave * (G + 1) * 3 * (int)sizeof(float);
   return kMaxGroupRuns<G> * H * kWave * (int)sizeof(f4);
 }
 
@@ -69,12 +78,17 @@ __device__ __forceinline__ float leaf_dot(const Leaf<H> &t, const Leaf<H> &p) {
 
 // The tile of a group: a[k] = this lane's leaf sum of token k of its group.
 // voff[h]: byte offset of quad h of this lane's leaf in a row; real[h]: the
-// quad holds topics (false: front padding, its theta is zero).
+// quad holds topics (false: front padding, its theta is zero).  With
+// kKeepLeaves, the running sums after the leaf's first one, two and three
+// topics go to keep2[t (G + 1) + r] (the first two) and keep1[t (G + 1) + r]
+// for the wavefront's token t = gbase + k and this lane's leaf r.
 template <int G, int H, int C, int MODE>
 __device__ __forceinline__ void group_tile(float (&a)[G], const Table &th_t, const Table &ph_t,
                                            const uint32_t (&voff)[H], const bool (&real)[H],
                                            uint32_t ph_lane, uint32_t th_lane, int gbase,
-                                           uint64_t gstarts, f4 *stage) {
+                                           uint64_t gstarts, f4 *stage, f2 *keep2,
+                                           float *keep1) {
+  constexpr bool KEEP = kKeepLeaves<G, H>;
   static_assert(G % C == 0, "the window size must divide G");
   constexpr int R = MODE == kGroupRuns ? kMaxGroupRuns<G> : 1;
   const f4 zero = {0.0f, 0.0f, 0.0f, 0.0f};
@@ -117,7 +131,7 @@ __device__ __forceinline__ void group_tile(float (&a)[G], const Table &th_t, con
       th[j] = mask(leaf_of(th_t, th_lane, p));
     }
   }
-  if constexpr (MODE != kGroupAny) {
+  if constexpr (MODE != kGroupAny && !KEEP) {
     // stage the runs' leaves: quad h of run j at stage[(j H + h) 64 + lane]
     const int lane = lane_id();
 #pragma unroll
@@ -167,7 +181,19 @@ __device__ __forceinline__ void group_tile(float (&a)[G], const Table &th_t, con
     } else {
       tv = th[0];
     }
-    a[k] = leaf_dot(tv, win[k % C]);
+    if constexpr (KEEP) {
+      // dot4's steps, the first three sums kept
+      const f4 t = tv.q[0], p = win[k % C].q[0];
+      const float s0 = t.x * p.x;
+      const float s1 = __builtin_fmaf(t.y, p.y, s0);
+      const float s2 = __builtin_fmaf(t.z, p.z, s1);
+      a[k] = __builtin_fmaf(t.w, p.w, s2);
+      const int at = (gbase + k) * (G + 1) + (lane_id() & (G - 1));
+      keep2[at] = f2{s0, s1};
+      keep1[at] = s2;
+    } else {
+      a[k] = leaf_dot(tv, win[k % C]);
+    }
     if (k + C < G) {
       win[k % C] = leaf_of(ph_t, ph_lane, k + C);
       if constexpr (MODE == kGroupAny) twin[k % C] = leaf_of(th_t, th_lane, k + C);
@@ -176,6 +202,7 @@ __device__ __forceinline__ void group_tile(float (&a)[G], const Table &th_t, con
       if (k + CT < G) twin[k % CT] = staged(k + CT);
     __builtin_amdgcn_sched_barrier(0);
   }
+  if constexpr (KEEP) lds_order();
 }
 
 // L = 4 H topics per lane: groups of G lanes cover 4 H G topics.
@@ -186,10 +213,14 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
                        UniformSource u, int32_t *__restrict__ z, int64_t N, int K,
                        uint32_t theta_extent, uint32_t phi_extent) {
   constexpr int L = kLeaf * H;
+  constexpr bool KEEP = kKeepLeaves<G, H>;
   extern __shared__ float lds[];
   const int lane = lane_id();
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kWave);
-  f4 *stage = reinterpret_cast<f4 *>(lds) + wave * (group_lds_bytes<G, H>() / (int)sizeof(f4));
+  float *region = lds + wave * (group_lds_bytes<G, H>() / (int)sizeof(float));
+  f4 *stage = reinterpret_cast<f4 *>(region);
+  f2 *keep2 = reinterpret_cast<f2 *>(region);
+  float *keep1 = region + 2 * kWave * (G + 1);
   const int64_t first = ((int64_t)blockIdx.x * kWavesPerBlock + wave) * kWave;
   if (first >= N) return;  // whole wavefront past the end
   // Window of 64 tokens as in butterfly_kernel (N >= 64 here).
@@ -231,13 +262,13 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   float a[G];
   if (most == 0)
     group_tile<G, H, C, kGroupOne>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase, 0,
-                                   stage);
+                                   stage, keep2, keep1);
   else if (most < kMaxGroupRuns<G>)
     group_tile<G, H, C, kGroupRuns>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase,
-                                    gstarts, stage);
+                                    gstarts, stage, keep2, keep1);
   else
     group_tile<G, H, C, kGroupAny>(a, th_t, ph_t, voff, real, ph_lane, th_lane, gbase, 0,
-                                   stage);
+                                   stage, keep2, keep1);
   butterfly_block<G>(a, r, NoStore{});
   const float total = a[G - 1];
   const float stop = total * un;
@@ -264,9 +295,19 @@ void leaf_group_kernel(const float *__restrict__ theta, const float *__restrict_
   // The theta leaf: staged in LDS by lane gbase + q for the run of the
   // lane's own token (padding quads already zero there), unless the group's
   // documents were too many runs.
+  const int tq = c0 + L * q;
+  if constexpr (KEEP) {
+    // the kept sums of leaf q of this lane's token (nondecreasing: the
+    // products are not negative), added to the prefix before the leaf
+    const int at = lane * (G + 1) + q;
+    const f2 s01 = keep2[at];
+    const float s2 = keep1[at];
+    const int i = stop < low + s01.x ? 0 : stop < low + s01.y ? 1 : stop < low + s2 ? 2 : 3;
+    if (store) z[n] = tq + i;
+    return;
+  }
   const bool staged = most < kMaxGroupRuns<G>;
   const int run = __builtin_popcountll(gstarts & ((2ull << r) - 1ull));
-  const int tq = c0 + L * q;
   float sum = low;
   int i = L - 1;
 #pragma unroll
