@@ -97,7 +97,7 @@ KERNELS = ("butterfly", "naive", "transposed", "docs", "doc_lanes", "doc_lanes_c
            "philox",
            "routed",
            "routed+build", "routed-philox", "floor", "count", "count-clear", "count-docs",
-           "count-indexed", "word-index")
+           "count-indexed", "word-index", "sweep")
 
 
 def draw_occupancy(K: int) -> tuple[int, int]:
@@ -154,6 +154,19 @@ def launcher(kernel: str, dev):
         V = ph.shape[0]
         ws = torch.empty(lda.word_index_bytes(w.shape[0], V), dtype=torch.uint8, device=w.device)
         return lambda out, stream: lda.word_index_build(w, V, workspace=ws, stream=stream)
+    if kernel == "sweep":               # one sampler sweep: the draw, then its topic counts
+        M, V, K = th.shape[0], ph.shape[0], th.shape[1]
+        off = dev["doc_offsets"]
+        if "word_index" not in dev:
+            dev["word_index"] = lda.word_index_build(w, V)
+        idx = dev["word_index"]
+        ndk = torch.empty((M, K), dtype=torch.int32, device=d.device)
+        nwk = torch.empty((V, K), dtype=torch.int32, device=d.device)
+
+        def draw_and_count(out, stream):
+            lda.draw_butterfly(th, ph, d, w, u, out=out, stream=stream)
+            lda.count_topics_indexed(off, w, out, idx, K, ndk=ndk, nwk=nwk, stream=stream)
+        return draw_and_count
     if kernel in ("count", "count-clear", "count-docs", "count-indexed"):
         M, V, K = th.shape[0], ph.shape[0], th.shape[1]
         if "z_draw" not in dev:
@@ -238,6 +251,8 @@ def measure(name: str, c, dev, kernel: str, steps: int, warmup: int, flush=None)
         b_alg = count_bytes(c)
     elif kernel == "word-index":     # word ids read twice, perm and wsorted written
         b_alg = 16 * c.N
+    elif kernel == "sweep":
+        b_alg = algorithmic_bytes(c) + count_bytes(c)
     else:
         b_alg = algorithmic_bytes(c)
     gbps = b_alg / (avg_ms * 1e-3) / 1e9
@@ -844,8 +859,8 @@ def report_bench(log: str, out_txt: str) -> int:
           f"  streaming read from HBM   {c['hbm_read_GBps']:8,.0f} GB/s  ({c['hbm_read']})",
           f"  streaming read, MALL      {c['mall_read_GBps']:8,.0f} GB/s  ({c['mall_read']})",
           f"  device copy (read+write)  {c['device_copy_GBps']:8,.0f} GB/s",
-          "", f"topic counts (lda_count_topics, _docs, _indexed; word-index: the index build) "
-          f"ms per call: " +
+          "", f"topic counts (lda_count_topics, _docs, _indexed; word-index: the index build; "
+          f"sweep: lda_draw_butterfly then lda_count_topics_indexed on one stream) ms per call: " +
           ", ".join(f"{k} {v:.4f}" for k, v in r["count_topics_ms"].items()),
           "", "parity on every token against the oracle (band |u S - S_k| <= 1e-5 S):",
           f"  {'workload':28s} {'tokens':>10s} {'mismatches':>10s} {'rate':>9s} "
@@ -1100,7 +1115,7 @@ def main() -> int:
         results.append(_brief(measure(SECOND, c2, dev2, k, max(steps, 20), warmup)))
     floors[SECOND] = measure_floor(SECOND, c2, dev2, max(steps, 20), warmup)
     floors[SECOND]["draw_ms"] = second["ms_per_launch"]
-    for k in ("count", "count-docs", "count-indexed", "word-index"):
+    for k in ("count", "count-docs", "count-indexed", "word-index", "sweep"):
         counts[f"{SECOND} {k}"] = measure(SECOND, c2, dev2, k, max(steps, 20),
                                           warmup)["ms_per_launch"]
     del dev2, c2
@@ -1144,7 +1159,7 @@ def main() -> int:
     del flush
     floors[HEADLINE] = measure_floor(HEADLINE, c, dev, steps, warmup)
     floors[HEADLINE]["draw_ms"] = head["ms_per_launch"]
-    for k in ("count", "count-docs", "count-indexed", "word-index"):
+    for k in ("count", "count-docs", "count-indexed", "word-index", "sweep"):
         counts[f"{HEADLINE} {k}"] = measure(HEADLINE, c, dev, k, steps, warmup)["ms_per_launch"]
 
     base = cpu_baseline(c, z_head, args.cpu_sample)
