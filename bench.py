@@ -304,7 +304,7 @@ def read_ceiling(nbytes: int, passes: int, steps: int = 10) -> tuple[float, floa
 
 def device_copy_GBps(steps: int = 10) -> float:
     """Bytes read plus bytes written per second by a plain 1 GiB device copy
-    (torch's copy kernel, HIP events): the practical HBM ceiling on the box."""
+    (torch's copy kernel, HIP events): the practical HBM ceiling on this machine."""
     import torch
     n = 1 << 28
     src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -709,7 +709,7 @@ PROFILE_PASSES = {"reads": PASS_READS, "dram": PASS_DRAM, "hit": PASS_HIT}
 
 
 def profile_commands(d: str) -> list[str]:
-    """The shell commands (repo root on the GPU machine) that take every counter
+    """The shell commands (repository root, on the MI355X machine) that take every counter
     pass of every target into ``d``, and the kernel trace of the default
     bench run; each rocprofv3 run under its own time limit."""
     cmds = ["cd /tmp && export TMPDIR=/tmp && cd \"$GRAFT_REPO_ROOT\" && "
@@ -758,7 +758,7 @@ def report_counters(d: str, out_txt: str) -> int:
         rows.append((label, kname, ms, rec))
     L = ["rocprofv3 counters per dispatch: bytes moved past L2, by request size (no calibration factor)",
          "",
-         "commands (repo root on the GPU box), one run per target and pass:",
+         "commands (repository root, on the MI355X machine), one run per target and pass:",
          *("  " + c for c in profile_commands(d)[:1]),
          "  timeout -s KILL 300 rocprofv3 --pmc <pass counters> -f csv -d <dir>/<target>_<pass> -o c "
          "-- python -u bench.py <target args>",
@@ -804,7 +804,7 @@ def report_trace(d: str, bench_log: str, out_txt: str) -> int:
     head = _bench_lines(bench_log)[-1]
     L = ["rocprofv3 kernel trace of the default benchmark run (every workload, every kernel)",
          "",
-         "command (repo root on the GPU box):",
+         "command (repository root, on the MI355X machine):",
          f"  {profile_commands(d)[-1]}",
          f"reduced by: python bench.py --report-trace {d} --bench-log {bench_log} "
          f"--out {os.path.relpath(out_txt, ROOT)}",
@@ -833,7 +833,7 @@ def report_bench(log: str, out_txt: str) -> int:
     ro = r["roofline"]
     L = ["The default benchmark run: roofline against the draw's memory floor, ceilings, parity",
          "",
-         "command (repo root on the GPU box):",
+         "command (repository root, on the MI355X machine):",
          f"  python -u bench.py > {log}",
          f"reduced by: python bench.py --report-bench {log} --out {os.path.relpath(out_txt, ROOT)}",
          "",
@@ -889,7 +889,7 @@ def report_jsonl(log: str, out_txt: str, title: str, command: str) -> int:
         for k, v in r.items():
             if k not in keys and (isinstance(v, (int, float)) or k == "workload"):
                 keys.append(k)
-    L = [title, "", "command (repo root on the GPU box):", f"  {command} > {log}",
+    L = [title, "", "command (repository root, on the MI355X machine):", f"  {command} > {log}",
          f"reduced by: python bench.py --report-jsonl {log} --out {os.path.relpath(out_txt, ROOT)} "
          "--title ... --command ...", ""]
     for r in lines:
