@@ -1023,7 +1023,8 @@ def main() -> int:
         return report_jsonl(args.report_jsonl, args.out, args.title, args.command)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the draw has no multi-GPU path in this build.", file=sys.stderr)
+              "the draw has no multi-GPU path (each GPU would draw its own "
+              "document-aligned share of the tokens with no exchange).", file=sys.stderr)
         return 2
 
     import torch
