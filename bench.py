@@ -586,6 +586,56 @@ def wide_builds(args) -> int:
     return 0
 
 
+def permuted_ids(args) -> int:
+    """Sensitivity of the draw, the routed draw, the word index build and the
+    indexed counts to the order of the word ids: each workload as generated
+    (ids by falling frequency, so the frequent rows of phi lie together) and
+    with its ids renamed by a fixed random permutation, phi's rows moved with
+    them (every token draws from the same weights).  Three alternating rounds
+    after an untimed pass, the median launch of each round, the fastest round
+    kept; z and the counts of the two orders compared.  One JSON line per
+    workload."""
+    import numpy as np
+    import torch
+    from paper_1505_03851_amd.inputs import Corpus, make_corpus
+    for name in ("corpus1M-K64", SECOND, HEADLINE, "poisson300-K2048"):
+        c = make_corpus(name)
+        perm = np.random.default_rng(150503851).permutation(c.V).astype(np.int32)
+        phi_p = np.empty_like(c.phi)
+        phi_p[perm] = c.phi
+        cp = Corpus(c.theta, phi_p, c.doc_id, perm[c.word_id], c.u, name=name + "-permuted")
+        devs = {"sorted": upload(c), "permuted": upload(cp)}
+        kernels = ["butterfly"] + (["routed"] if routable(c.K) else []) + \
+                  ["word-index", "count-indexed"]
+        for dev in devs.values():
+            time_kernel("butterfly", dev, args.steps, args.warmup)
+        best = {(o, k): float("inf") for o in devs for k in kernels}
+        zs = {}
+        for _ in range(3):
+            for k in kernels:
+                for o, dev in devs.items():
+                    _, per_ms, zs[o, k] = time_kernel(k, dev, args.steps, args.warmup)
+                    best[o, k] = min(best[o, k], sorted(per_ms)[len(per_ms) // 2])
+        rec = {"workload": name, "N": c.N, "V": c.V, "K": c.K}
+        for k in kernels:
+            rec[k + "_sorted_ms"] = best["sorted", k]
+            rec[k + "_permuted_ms"] = best["permuted", k]
+            rec[k + "_permuted_over_sorted"] = best["permuted", k] / best["sorted", k]
+        rec["z_identical"] = bool(torch.equal(zs["sorted", "butterfly"],
+                                              zs["permuted", "butterfly"]))
+        if routable(c.K):
+            rec["routed_z_differs"] = int((zs["sorted", "routed"]
+                                           != zs["permuted", "routed"]).sum())
+        perm_t = torch.from_numpy(perm).long().cuda()
+        s, p = devs["sorted"], devs["permuted"]
+        rec["counts_identical"] = bool(torch.equal(s["ndk"], p["ndk"]) and
+                                       torch.equal(s["nwk"], p["nwk"][perm_t]))
+        print(json.dumps(rec), flush=True)
+        del devs, zs, s, p
+        torch.cuda.empty_cache()
+    return 0
+
+
 def all_configs(args) -> int:
     """Every kernel on every workload of inputs.CONFIGS but the K sweep's, warm
     and (butterfly) with a cold cache; one JSON line per workload."""
@@ -984,6 +1034,9 @@ def main() -> int:
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
+    ap.add_argument("--permuted-ids", action="store_true",
+                    help="each workload with its word ids as generated and renamed by a "
+                         "random permutation (phi's rows moved with them); one JSON line each")
     ap.add_argument("--wide-builds", action="store_true",
                     help="the default build of the draw kernels against the build "
                          "for tables past 4 GiB, on every workload; one JSON line each")
@@ -1061,6 +1114,8 @@ def main() -> int:
         return ablation(args)
     if args.wide_builds:
         return wide_builds(args)
+    if args.permuted_ids:
+        return permuted_ids(args)
     if args.route_sweep:
         return route_sweep(args)
     if args.all_configs:
