@@ -25,6 +25,7 @@ import glob
 import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -53,12 +54,17 @@ def counters_path(workload: str) -> str:
 
 
 def kernel_source_hash(device_kernel: str = "leaf_eighths_kernel") -> str:
-    """sha1 of the files the device kernel is compiled from (in the order
-    listed): a counter record applies while this is unchanged."""
+    """sha1 of the code of the files the device kernel is compiled from (in
+    the order listed), with comments removed and runs of white space made one
+    space: a counter record applies while this is unchanged.  (The files hold
+    no comment markers inside string literals.)"""
     h = hashlib.sha1()
     for name in KERNEL_SOURCES[device_kernel]:
-        with open(os.path.join(CSRC, name), "rb") as f:
-            h.update(f.read())
+        with open(os.path.join(CSRC, name), encoding="utf-8") as f:
+            text = f.read()
+        text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+        text = re.sub(r"//[^\n]*", " ", text)
+        h.update(" ".join(text.split()).encode())
     return h.hexdigest()
 
 
