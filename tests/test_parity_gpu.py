@@ -3,9 +3,9 @@
 Rule: z equals the oracle's bit for bit except at tokens where
 |u*S - S_k| <= 1e-5 * S for some k (fp32 rounding may move such a draw to a
 neighbouring topic); the rate of such exceptions must stay below 1e-4 on the
-full-size workloads.  Full-size workloads run the kernel on every token in the
-benchmark's launch configuration and check a sample of tokens against the
-oracle; smaller ones check every token.
+full-size workloads.  Every workload runs the kernel on every token, the
+full-size ones in the benchmark's launch configuration, and every token is
+checked against the oracle.
 """
 import numpy as np
 import pytest
@@ -192,6 +192,35 @@ def test_tiny_uniforms_with_empty_leading_topics(K, kernel):
     c.u[:] = ((np.arange(N) % 8) * 2.0 ** -24).astype(np.float32)
     rep = _check(c, kernel, rate=False)
     assert rep.hard == 0
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+@pytest.mark.parametrize("K", [4, 8, 20, 32, 48, 64, 100, 256, 1000, 1024, 2048])
+def test_uniforms_just_below_one_with_empty_trailing_topics(K, kernel):
+    """Every u is 1 - j 2**-24 (j = 1 ... 8), and half the words give their
+    last three topics zero weight.  stop = u S then lies within a few ulps of
+    S, inside the rounding band of every token, so the band rule alone would
+    admit any topic; the draw must instead be a topic whose prefix range
+    [S_{z-1}, S_z] comes within the band of stop (in fp64): the last topic of
+    nonzero weight, a trailing empty one (rounding, or S = 0: K - 1), or one
+    whose whole weight is below the band, never an earlier topic."""
+    import oracle
+    N = 64 * 40 + 7
+    c = make_random(N, 30, 400, K, seed=K + 11, doc_order="sequential")
+    c.phi[::2, max(K - 3, 1):] = 0.0
+    c.u[:] = (1.0 - ((np.arange(N) % 8) + 1) * 2.0 ** -24).astype(np.float32)
+    print(f"[case] near-one-K{K} kernel={kernel}", flush=True)
+    z = run_kernel(kernel, to_device(c))
+    assert z.min() >= 0 and z.max() < K
+    S = np.cumsum(c.theta[c.doc_id].astype(np.float64) *
+                  c.phi[c.word_id].astype(np.float64), axis=1)
+    total = S[:, -1]
+    stop = c.u.astype(np.float64) * total
+    tol = oracle.BAND_REL * total
+    rows = np.arange(N)
+    below = np.where(z > 0, S[rows, np.maximum(z - 1, 0)], 0.0)   # S_{z-1}
+    ok = (below <= stop + tol) & ((S[rows, z] >= stop - tol) | (z == K - 1))
+    assert ok.all(), [(int(i), int(z[i])) for i in np.nonzero(~ok)[0][:5]]
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
