@@ -465,6 +465,7 @@ def cpu_baseline(c, z_gpu, sample: int) -> dict:
             "mismatches": int(mism.sum()),
             "mismatch_rate": float(mism.mean()),
             "mismatches_outside_band": int((mism & ~band).sum()),
+            "mismatches_not_admitted": not_admitted(c, d, w, u, zg, z_chk, band),
             "in_band_rate": float(band.mean()),
         },
     }
@@ -918,12 +919,16 @@ def report_bench(log: str, out_txt: str) -> int:
           "", f"topic counts (lda_count_topics, _docs, _indexed; word-index: the index build; "
           f"sweep: lda_draw_butterfly then lda_count_topics_indexed on one stream) ms per call: " +
           ", ".join(f"{k} {v:.4f}" for k, v in r["count_topics_ms"].items()),
-          "", "parity on every token against the oracle (band |u S - S_k| <= 1e-5 S):",
+          "", "parity on every token against the oracle (band |u S - S_k| <= 1e-5 S; 'not "
+          "admitted': in-band mismatches at a topic whose prefix range does not come within "
+          "the band of u S):",
           f"  {'workload':28s} {'tokens':>10s} {'mismatches':>10s} {'rate':>9s} "
-          f"{'outside band':>12s} {'in-band rate':>12s}"]
+          f"{'outside band':>12s} {'not admitted':>12s} {'in-band rate':>12s}"]
     for w, p in r["parity"].items():
+        na = p.get("mismatches_not_admitted")
         L.append(f"  {w:28s} {p['tokens']:10d} {p['mismatches']:10d} {p['mismatch_rate']:9.2e} "
-                 f"{p['mismatches_outside_band']:12d} {p['in_band_rate']:12.2e}")
+                 f"{p['mismatches_outside_band']:12d} {'-' if na is None else na:>12} "
+                 f"{p['in_band_rate']:12.2e}")
     b = r["cpu_baseline"]
     L += ["", f"CPU baseline (the oracle, {b['cores']} threads, {b.get('cpu', '')}): "
               f"{b['value'] / 1e6:.1f} M draws/s on {b['sample']}; one thread "
@@ -983,6 +988,27 @@ def measure_floor(name: str, c, dev, steps: int, warmup: int) -> dict:
             "alg_GBps": algorithmic_bytes(c) / (shapes[best] * 1e-3) / 1e9}
 
 
+def not_admitted(c, d, w, u, zg, z_ref, band) -> int:
+    """In-band mismatches drawn at a topic the band does not admit.  In the
+    band several topics are correct, but only those whose fp64 prefix range
+    [S_{z-1}, S_z] comes within 1e-5 S of stop = u S (z = K - 1 also when stop
+    lies past S_{K-1}; with S = 0 only K - 1)."""
+    import numpy as np
+    import oracle
+    K = c.K
+    bad = 0
+    for i in np.nonzero((zg != z_ref) & band)[0]:
+        S = oracle.prefix_np(c.theta[d[i]], c.phi[w[i]])
+        total, k = S[-1], int(zg[i])
+        if total == 0.0:
+            bad += k != K - 1
+            continue
+        stop, tol = float(u[i]) * total, 1e-5 * total
+        below = S[k - 1] if k > 0 else 0.0
+        bad += not (below <= stop + tol and (S[k] >= stop - tol or k == K - 1))
+    return int(bad)
+
+
 def parity_report(c, z_gpu, ref=None) -> dict:
     """Every token of the GPU's z against the oracle: mismatches, and those
     outside the rounding band |u S - S_k| <= 1e-5 S (which must be 0)."""
@@ -995,6 +1021,8 @@ def parity_report(c, z_gpu, ref=None) -> dict:
     return {"tokens": int(c.N), "mismatches": int(mism.sum()),
             "mismatch_rate": float(mism.mean()) if c.N else 0.0,
             "mismatches_outside_band": int((mism & ~band).sum()),
+            "mismatches_not_admitted": not_admitted(c, c.doc_id, c.word_id, c.u, zg,
+                                                    z_ref, band),
             "in_band_rate": float(band.mean()) if c.N else 0.0}
 
 

@@ -16,7 +16,8 @@ MAX_MISMATCH_RATE = 1e-4  # mismatches (all in-band) per token
 class ParityReport:
     n: int
     mismatches: int
-    hard: int            # mismatches outside the band
+    hard: int            # mismatches outside the band, or inside it at a topic
+                         # the band does not admit (see ``admissible``)
     in_band: int         # tokens inside the band (a property of the data)
     first_hard: list
 
@@ -28,6 +29,28 @@ class ParityReport:
         return (f"n={self.n} mismatches={self.mismatches} "
                 f"({self.mismatch_rate:.2e}) hard={self.hard} "
                 f"in_band={self.in_band} ({self.in_band / max(self.n, 1):.2e})")
+
+
+def admissible(theta, phi, d, w, u, z) -> np.ndarray:
+    """For tokens (documents d, words w, uniforms u) drawn as topics z: whether
+    each z is a topic the rounding band admits.  In the band several topics
+    are correct, but only those whose fp64 prefix range [S_{z-1}, S_z] comes
+    within 1e-5 S of stop = u S (z = K - 1 also when stop lies past S_{K-1});
+    with S = 0 only K - 1 (no prefix exceeds stop)."""
+    K = theta.shape[1]
+    ok = np.empty(len(z), bool)
+    for i in range(len(z)):
+        S = oracle.prefix_np(theta[d[i]], phi[w[i]])
+        total = S[-1]
+        k = int(z[i])
+        if total == 0.0:
+            ok[i] = k == K - 1
+            continue
+        stop = float(u[i]) * total
+        tol = BAND_REL * total
+        below = S[k - 1] if k > 0 else 0.0
+        ok[i] = below <= stop + tol and (S[k] >= stop - tol or k == K - 1)
+    return ok
 
 
 def to_device(c, device="cuda"):
@@ -117,6 +140,9 @@ def compare(c, z_gpu, idx=None, ref=None) -> ParityReport:
         z_ref, band = oracle.draw(c.theta, c.phi, d, w, u, band_rel=BAND_REL)
     mis = zg != z_ref
     hard = mis & ~band
+    soft = np.nonzero(mis & band)[0]          # in the band: check the topic is admitted
+    if soft.size:
+        hard[soft] = ~admissible(c.theta, c.phi, d[soft], w[soft], u[soft], zg[soft])
     where = np.nonzero(hard)[0][:5]
     first = [(int(i if idx is None else idx[i]), int(zg[i]), int(z_ref[i]))
              for i in where]
