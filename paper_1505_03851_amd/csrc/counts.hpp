@@ -193,12 +193,18 @@ __global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
     const int64_t *__restrict__ doc_offsets, const int32_t *__restrict__ word_id,
     const int32_t *__restrict__ z, int64_t N, int32_t M, int32_t V, int32_t K,
     int32_t *__restrict__ ndk) {
-  extern __shared__ uint32_t rows[];  // kDocWaves rows of K bins
+  extern __shared__ __align__(16) uint32_t rows[];  // kDocWaves rows of K bins
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int64_t m = (int64_t)blockIdx.x * kDocWaves + wave;
   uint32_t *bins = rows + (size_t)wave * (size_t)K;
-  for (int k = lane; k < K; k += 64) bins[k] = 0;
+  // (K divisible by 4: the row's bins are 16-byte aligned in LDS)
+  const bool quads = (K & 3) == 0;
+  if (quads)
+    for (int k = 4 * lane; k < K; k += 4 * 64)
+      *reinterpret_cast<uint4 *>(bins + k) = uint4{0u, 0u, 0u, 0u};
+  else
+    for (int k = lane; k < K; k += 64) bins[k] = 0;
   __syncthreads();
   if (m < M) {
     int64_t lo = doc_offsets[m], hi = doc_offsets[m + 1];
@@ -212,7 +218,15 @@ __global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
   __syncthreads();
   if (m < M) {
     int32_t *row = ndk + m * (int64_t)K;
-    for (int k = lane; k < K; k += 64) row[k] = (int32_t)bins[k];
+    if (quads && (reinterpret_cast<uintptr_t>(row) & 15u) == 0) {
+      for (int k = 4 * lane; k < K; k += 4 * 64) {
+        const uint4 v = *reinterpret_cast<const uint4 *>(bins + k);
+        *reinterpret_cast<int4 *>(row + k) =
+            int4{(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
+      }
+    } else {
+      for (int k = lane; k < K; k += 64) row[k] = (int32_t)bins[k];
+    }
   }
 }
 
