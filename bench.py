@@ -966,6 +966,42 @@ def report_jsonl(log: str, out_txt: str, title: str, command: str) -> int:
     return 0
 
 
+_PARITY_LINE = re.compile(r"^\[parity\] (?P<case>.+?): n=(?P<n>\d+) mismatches=(?P<mis>\d+) "
+                          r"\((?P<rate>[^)]+)\) hard=(?P<hard>\d+) in_band=(?P<band>\d+) "
+                          r"\((?P<brate>[^)]+)\)")
+
+
+def report_parity(log: str, out_txt: str, command: str) -> int:
+    """A table of the parity lines the GPU tests print ("[parity] <workload>
+    <kernel>: n=... mismatches=... hard=... in_band=..."), for the named
+    workloads (the five and the corpus shaped like the paper's), every
+    kernel, in the order the tests ran."""
+    from paper_1505_03851_amd.inputs import CONFIGS
+    rows = []
+    with open(log, errors="replace") as f:
+        for ln in f:
+            m = _PARITY_LINE.match(ln.strip())
+            if m and m["case"].split()[0] in CONFIGS:
+                rows.append(m)
+    if not rows:
+        raise SystemExit(f"no parity lines for the named workloads in {log}")
+    L = ["Parity of every kernel on every token of the named workloads, against the oracle: "
+         "mismatches, their rate, 'hard' (outside the band |u S - S_k| <= 1e-5 S, or in it at a "
+         "topic the band does not admit: must be 0) and the tokens in the band",
+         "", "command (repository root, on the MI355X machine):", f"  {command} > {log}",
+         f"reduced by: python bench.py --report-parity {log} --out "
+         f"{os.path.relpath(out_txt, ROOT)} --command ...", "",
+         f"  {'workload and kernel':44s} {'tokens':>10s} {'mismatches':>10s} {'rate':>9s} "
+         f"{'hard':>5s} {'in band':>8s} {'band rate':>9s}"]
+    for m in rows:
+        L.append(f"  {m['case']:44s} {int(m['n']):10d} {int(m['mis']):10d} {m['rate']:>9s} "
+                 f"{int(m['hard']):5d} {int(m['band']):8d} {m['brate']:>9s}")
+    with open(out_txt, "w") as f:
+        f.write("\n".join(L) + "\n")
+    print("\n".join(L))
+    return 0
+
+
 def floor_configs(K: int):
     """Launch shapes of the floor probe tried for K: window 8 or 16, 2 or 4
     wavefronts per workgroup, no occupancy cap or the draw's."""
@@ -1092,6 +1128,8 @@ def main() -> int:
                     help="summarise the default run's JSON line in LOG to --out")
     ap.add_argument("--report-jsonl", default=None, metavar="LOG",
                     help="tabulate the JSON lines in LOG to --out (--title, --command)")
+    ap.add_argument("--report-parity", default=None, metavar="LOG",
+                    help="tabulate the parity lines of a GPU test log (pytest -s) to --out")
     ap.add_argument("--title", default="")
     ap.add_argument("--command", default="")
     args = ap.parse_args()
@@ -1108,6 +1146,8 @@ def main() -> int:
         return report_bench(args.report_bench, args.out)
     if args.report_jsonl:
         return report_jsonl(args.report_jsonl, args.out, args.title, args.command)
+    if args.report_parity:
+        return report_parity(args.report_parity, args.out, args.command)
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the draw has no multi-GPU path (each GPU would draw its own "
