@@ -89,8 +89,9 @@ extern "C" {
 #define LDA_MAX_TABLE_BYTES 4294967295LL
 
 /* Largest size in bytes of theta or phi for lda_draw_butterfly, lda_draw_docs
- * and lda_draw_butterfly_philox, and of the count tables of lda_count_topics
- * and lda_count_topics_docs: 2^32 - 1 elements (16 GiB).  When either table
+ * and lda_draw_butterfly_philox, and of the count tables of lda_count_topics,
+ * lda_count_topics_docs and lda_count_topics_indexed: 2^32 - 1 elements
+ * (16 GiB).  When either table
  * is larger than LDA_MAX_TABLE_BYTES these draw with a second build of the
  * same kernels that addresses the tables by 32-bit float offsets and 64-bit
  * loads (ids beyond the table's rows are clamped to its last row there, so
@@ -119,7 +120,9 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
  *  - K divisible by 4 up to 256 (N >= 64): groups of W = 8, 16, 32 or 64
  *    lanes, each lane one leaf of 4 topics; load k brings token k's whole
  *    row into its group; the butterfly runs over the W leaf sums, Algorithm
- *    10 finds the token's leaf and a scan of its 4 products the topic;
+ *    10 finds the token's leaf and a scan of its 4 products the topic
+ *    (groups of 8 lanes keep each leaf's partial sums in LDS for that scan;
+ *    the others read the leaf again);
  *  - K divisible by 4 from 260 to 2048: 256-topic blocks read as leaves of 4
  *    topics per lane; a first sweep keeps every token's prefix at the end of
  *    each 32-topic part of each block, Algorithm 9 finds the part holding
@@ -281,8 +284,8 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * only the grouping of tokens into wavefronts changes.  Routing pays where
  * phi is far larger than the caches and costs where phi fits the 256 MiB
  * MALL.  Measured on MI355X over 16.8M Zipf tokens with V = 100,000 words:
- * 28% slower than lda_draw_butterfly at K = 256, 3% slower at K = 512, 3%
- * faster at K = 768, 6% at K = 1024, 11% at K = 2048 (25% on 9.8M tokens
+ * 28% slower than lda_draw_butterfly at K = 256, 3% slower at K = 512, 2%
+ * faster at K = 768, 5% at K = 1024, 11% at K = 2048 (24% on 9.8M tokens
  * with V = 50,000 at K = 2048); so lda_draw_routed takes K >= LDA_ROUTE_MIN_K
  * only.
  *
