@@ -69,9 +69,9 @@
 //                             keeps its leaves' partial sums in LDS for the
 //                             final scan instead of reloading the chosen leaf
 //                             (0: none).  Groups of 8 (K <= 32): 9-16% faster
-//                             at 3-4M tokens (6.75 KiB per wavefront, no loss
-//                             of occupancy); groups of 16: 4-12% slower (12.75
-//                             KiB: 12 wavefronts per CU instead of 20).
+//                             at 3-4M tokens (6.75 KiB per wavefront: 22
+//                             wavefronts per CU instead of 24); groups of 16:
+//                             4-12% slower (12.75 KiB: 12 instead of 20).
 #ifndef LDA_GROUP_KEEP_MAX_G
 #define LDA_GROUP_KEEP_MAX_G 8
 #endif
