@@ -757,6 +757,12 @@ PROFILE_TARGETS = {
                                        "--steps", "3", "--warmup", "1"]),
     "floor_K64": ("floor_kernel", ["--only", "floor", "--floor-config", "8,2,0",
                                    "--workload", "corpus1M-K64", "--steps", "3", "--warmup", "1"]),
+    # groups of 8 lanes, which keep their leaves' partial sums in LDS (no reload)
+    "draw_W16": ("leaf_group_kernel", ["--only", "butterfly", "--workload", "wiki-shaped-K16",
+                                       "--steps", "3", "--warmup", "1"]),
+    "floor_W16": ("floor_kernel", ["--only", "floor", "--floor-config", "8,2,0",
+                                   "--workload", "wiki-shaped-K16", "--steps", "3",
+                                   "--warmup", "1"]),
     "draw_K2048": ("leaf_eighths_kernel", ["--only", "butterfly", "--workload",
                                            "poisson300-K2048", "--steps", "3", "--warmup", "1"]),
     "routed_K1024": ("routed_eighths_kernel", ["--only", "routed", "--workload", HEADLINE,
