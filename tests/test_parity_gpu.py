@@ -456,3 +456,44 @@ def test_butterfly_table_matches_closed_form(K):
         err = np.abs(got - exp)
         tol = 2e-5 * np.abs(exp) + 1e-37
         assert (err <= tol).all(), (g0, np.argwhere(err > tol)[:5])
+
+
+# One fixed distribution drawn 10^6 times on the GPU (K = 8, one topic of zero
+# weight): the counts fit the normalised weights, the empty topic is never
+# drawn, and with the uniforms of the oracle's own chi-square pin every draw
+# agrees with the oracle under the band rule.
+CHI_WEIGHTS = np.array([0.05, 0.2, 0.0, 0.1, 0.3, 0.15, 0.12, 0.08], np.float32)
+
+
+def _chi_square_pvalue(z):
+    from scipy import stats
+    counts = np.bincount(z, minlength=CHI_WEIGHTS.size)
+    assert counts[2] == 0, counts
+    nz = CHI_WEIGHTS > 0
+    p = CHI_WEIGHTS[nz].astype(np.float64) / CHI_WEIGHTS.astype(np.float64).sum()
+    return stats.chisquare(counts[nz], z.size * p).pvalue
+
+
+@pytest.mark.parametrize("kernel", KERNELS)
+def test_chi_square_of_gpu_draws(kernel):
+    N = 1_000_000
+    c = _corpus(CHI_WEIGHTS[None, :], np.ones((1, CHI_WEIGHTS.size)), np.zeros(N),
+                np.zeros(N), _grid_u(N, 20150513), "chi-square-K8")
+    rep = _check(c, kernel)
+    z = run_kernel(kernel, to_device(c))
+    assert _chi_square_pvalue(z) >= 1e-3, rep
+
+
+def test_chi_square_of_gpu_draws_with_philox_uniforms():
+    """The same distribution with the uniforms generated in the kernel."""
+    import torch
+    import paper_1505_03851_amd as lda
+    N = 1_000_000
+    th = torch.from_numpy(CHI_WEIGHTS[None, :].copy()).cuda()
+    ph = torch.ones((1, CHI_WEIGHTS.size), dtype=torch.float32, device="cuda")
+    zeros = torch.zeros(N, dtype=torch.int32, device="cuda")
+    print("[case] chi-square-K8 philox", flush=True)
+    for sweep in (0, 1):
+        z = lda.draw_philox(th, ph, zeros, zeros, seed=0x5EED, sweep=sweep)
+        torch.cuda.synchronize()
+        assert _chi_square_pvalue(z.cpu().numpy()) >= 1e-4, sweep
