@@ -300,3 +300,64 @@ def test_word_counts_past_4_gib():
     assert np.array_equal(got_w, want_w), np.argwhere(got_w != want_w)[:5]
     del ndk, nwk, ndk2, nwk2, ndk3, nwk3, got_w, index
     torch.cuda.empty_cache()
+
+
+def test_counts_at_the_largest_n():
+    """N = LDA_COUNT_MAX_N = 2^31 - 1 tokens, where the index's positions and
+    offsets fill int32: the three count entry points agree cell for cell, and
+    every table has the sums the tokens fix, computed by torch on the same
+    arrays (rows of ndk: the document lengths; rows of nwk: the word
+    frequencies; columns: the topic totals); the word index's offsets are the
+    exclusive prefix sums of the word frequencies, its positions hold every
+    token exactly once, and each position's word is that token's word, in
+    non-decreasing order."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd import _lib
+    N = _lib._CONSTS["LDA_COUNT_MAX_N"]
+    M, V, K = 1 << 20, 5000, 16
+    step = 1 << 28
+    print(f"[case] counts at N={N}", flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(11)
+    w = torch.randint(0, V, (N,), dtype=torch.int32, device="cuda", generator=g)
+    z = torch.randint(0, K, (N,), dtype=torch.int32, device="cuda", generator=g)
+    off = torch.arange(M + 1, dtype=torch.int64, device="cuda") * N // M
+    lengths = off[1:] - off[:-1]
+    d = torch.repeat_interleave(torch.arange(M, dtype=torch.int32, device="cuda"), lengths,
+                                output_size=N)
+    ndk1, nwk1 = lda.count_topics(d, w, z, M, V, K)
+    torch.cuda.synchronize()
+    del d
+    ndk2, nwk2 = lda.count_topics_docs(off, w, z, V, K)
+    index = lda.word_index_build(w, V)
+    ndk3, nwk3 = lda.count_topics_indexed(off, w, z, index, K)
+    torch.cuda.synchronize()
+    assert torch.equal(ndk1, ndk2) and torch.equal(ndk1, ndk3)
+    assert torch.equal(nwk1, nwk2) and torch.equal(nwk1, nwk3)
+
+    def counts_of(x, n):
+        c = torch.zeros(n, dtype=torch.int64, device="cuda")
+        for s in range(0, N, step):
+            c += torch.bincount(x[s:s + step].long(), minlength=n)
+        return c
+    freq, ztot = counts_of(w, V), counts_of(z, K)
+    assert torch.equal(ndk1.sum(1, dtype=torch.int64), lengths)
+    assert torch.equal(nwk1.sum(1, dtype=torch.int64), freq)
+    assert torch.equal(ndk1.sum(0, dtype=torch.int64), ztot)
+    assert torch.equal(nwk1.sum(0, dtype=torch.int64), ztot)
+
+    a = index.arrays()
+    assert torch.equal(a["off"][:V].long(), torch.cumsum(freq, 0) - freq)
+    assert int(a["off"][V]) == N
+    seen = torch.zeros(N, dtype=torch.bool, device="cuda")
+    for s in range(0, N, step):
+        p, ws = a["perm"][s:s + step].long(), a["wsorted"][s:s + step]
+        assert torch.equal(w[p], ws)
+        seen[p] = True
+        assert bool((ws[1:] >= ws[:-1]).all())
+        if s:
+            assert int(a["wsorted"][s - 1]) <= int(ws[0])
+    assert bool(seen.all())
+    del w, z, index, seen
+    torch.cuda.empty_cache()
