@@ -361,3 +361,70 @@ def test_counts_at_the_largest_n():
     assert bool(seen.all())
     del w, z, index, seen
     torch.cuda.empty_cache()
+
+
+def test_routed_at_the_largest_n():
+    """N = LDA_ROUTE_MAX_N = 2^31 - 513 tokens, where the routed positions
+    (N plus up to 8 x 64 of padding) fill int32: the routing is a layout of
+    every token exactly once, each list in token order and padded with -1,
+    carrying each token's word and document; the routed draw agrees with the
+    token-order draw except on a handful of tokens, and a sample of 2^20
+    tokens (among them the last 4,096) agrees with the oracle under the band
+    rule."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd import _lib
+    from paper_1505_03851_amd.inputs import Corpus
+    from parity import compare
+    N = _lib._CONSTS["LDA_ROUTE_MAX_N"]
+    M, V, K = 1 << 16, 1000, 768
+    step = 1 << 28
+    print(f"[case] routed at N={N}", flush=True)
+    g = torch.Generator(device="cuda")
+    g.manual_seed(13)
+    theta = torch.rand((M, K), generator=g, device="cuda") ** 8
+    phi = torch.rand((V, K), generator=g, device="cuda")
+    phi *= torch.rand((V, K), generator=g, device="cuda") > 0.37
+    w = torch.randint(0, V, (N,), dtype=torch.int32, device="cuda", generator=g)
+    u = torch.rand(N, generator=g, device="cuda")
+    off = torch.arange(M + 1, dtype=torch.int64, device="cuda") * N // M
+    d = torch.repeat_interleave(torch.arange(M, dtype=torch.int32, device="cuda"),
+                                off[1:] - off[:-1], output_size=N)
+    route = lda.route_build(d, w, M, V)
+    torch.cuda.synchronize()
+    assert route.N == N and sum(route.tokens) == N
+    a = route.arrays()
+    seen = torch.zeros(N, dtype=torch.bool, device="cuda")
+    at = 0
+    for x in range(8):
+        t, s0, ln = route.tokens[x], route.start[x], route.length[x]
+        assert s0 == at and ln == (t + 63) // 64 * 64
+        at += ln
+        assert bool((a["perm"][s0 + t:s0 + ln] == -1).all())
+        for s in range(s0, s0 + t, step):
+            e = min(s + step, s0 + t)
+            p = a["perm"][s:e].long()
+            assert bool((p >= 0).all()) and bool((p[1:] > p[:-1]).all())
+            if s > s0:
+                assert int(a["perm"][s - 1]) < int(p[0])
+            assert torch.equal(a["rword"][s:e], w[p]) and torch.equal(a["rdoc"][s:e], d[p])
+            seen[p] = True
+    assert bool(seen.all())
+    del seen, a
+    z_r = lda.draw_routed(theta, phi, route, u)
+    z_b = lda.draw_butterfly(theta, phi, d, w, u)
+    torch.cuda.synchronize()
+    differ = int((z_r != z_b).sum())
+    print(f"[parity] routed at N={N}: {differ} tokens differ from the token-order draw",
+          flush=True)
+    assert differ <= N // 10000
+    rng = np.random.default_rng(13)
+    idx = np.unique(np.concatenate([rng.integers(0, N, 1 << 20), np.arange(N - 4096, N)]))
+    it = torch.from_numpy(idx).cuda()
+    c = Corpus(theta.cpu().numpy(), phi.cpu().numpy(), d[it].cpu().numpy(),
+               w[it].cpu().numpy(), u[it].cpu().numpy(), name=f"routed-N{N}-sample")
+    rep = compare(c, z_r[it].cpu().numpy())
+    print(f"[parity] {c.name}: {rep}", flush=True)
+    assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
+    del d, w, u, z_r, z_b, route
+    torch.cuda.empty_cache()
