@@ -54,6 +54,30 @@ def test_scratch_routed_draw_two_calls():
         assert rep.hard == 0, rep.first_hard
 
 
+def test_scratch_routed_draw_at_its_largest_n():
+    """The largest N whose routing fits the array (about 5.4M tokens): the
+    whole array in use, the same z as with a caller's workspace."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd import _lib
+    cap = _lib.ROUTED_SCRATCH_BYTES
+    lo, hi = 1, 1 << 24              # route_workspace_bytes(lo) <= cap < ...(hi)
+    while hi - lo > 1:
+        mid = (lo + hi) // 2
+        lo, hi = (mid, hi) if lda.route_workspace_bytes(mid) <= cap else (lo, mid)
+    c = make_random(lo, 4000, 5000, 768, seed=43, doc_order="sequential")
+    print(f"[case] scratch routed draw at its largest N={c.N}", flush=True)
+    dev = to_device(c)
+    out = torch.full((c.N,), -1, dtype=torch.int32, device="cuda")
+    z = _scratch_draw(dev, c, out)
+    z_ws = _workspace_draw(dev, c)
+    diff = np.nonzero(z != z_ws)[0]
+    assert diff.size == 0, (diff.size, diff[:5])
+    rep = compare(c, z)
+    print(f"[parity] {c.name} routed scratch: {rep}", flush=True)
+    assert rep.hard == 0 and rep.mismatch_rate < 1e-4, rep.first_hard
+
+
 def test_scratch_refuses_what_does_not_fit():
     """Rejected on the host (no kernel runs): a routing larger than the
     array, K below the routed draw's range, and bad shapes."""
