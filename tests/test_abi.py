@@ -231,6 +231,7 @@ def test_philox_uniforms_argument_errors(lib):
     assert f(A, -1, 0, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
     assert f(A, 5, -1, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
     assert f(A, 2, 2 ** 63 - 1, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]
+    assert f(A, 301, 2 ** 63 - 301, 1, 0, None) == STATUS["LDA_ERR_SHAPE"]  # first + count = 2^63
     assert f(None, 5, 0, 1, 0, None) == STATUS["LDA_ERR_NULL"]
     assert f(A + 1, 5, 0, 1, 0, None) == STATUS["LDA_ERR_ALIGN"]
 

@@ -20,6 +20,7 @@ SEED = 0x5EED_2015_0513_0001
     ((1 << 20) + 77, 12345, SEED, 0),
     (5000, (1 << 32) - 2500, SEED, 1),          # across the counter's word boundary
     (300, (1 << 40) + 5, 2 ** 64 - 1, 2 ** 32 - 1),
+    (301, (1 << 63) - 302, SEED, 7),            # first + count = INT64_MAX, the limit
 ])
 def test_uniforms_bit_exact(count, first, seed, sweep):
     import torch
