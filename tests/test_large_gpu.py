@@ -18,7 +18,8 @@ from paper_1505_03851_amd.inputs import dirichlet_columns, dirichlet_rows
 pytestmark = pytest.mark.gpu
 
 N_BIG = (1 << 31) + 4099          # past the signed 32-bit range, ragged tail
-M_BIG = 32771                     # documents of about 65,500 tokens
+N_MAX = (1 << 32) - (1 << 16)     # LDA_MAX_N: a dispatch's work-items fill 32 bits
+M_BIG = 32771                     # documents of about 65,500 tokens (131,000 at N_MAX)
 V_BIG = 5000
 
 
@@ -29,13 +30,13 @@ def _sample(N):
     return np.unique(np.concatenate(parts))
 
 
-@pytest.fixture(scope="module")
-def big():
+@pytest.fixture(scope="module", params=[N_BIG, N_MAX], ids=["N2^31+4099", "N_MAX"])
+def big(request):
     import torch
     torch.cuda.empty_cache()
     g = torch.Generator(device="cuda")
     g.manual_seed(2015)
-    N = N_BIG
+    N = request.param
     doc = torch.empty(N, dtype=torch.int32, device="cuda")
     chunk = 1 << 27
     for a in range(0, N, chunk):
@@ -84,7 +85,7 @@ def test_tokens_past_2_31(big, kernel, K):
         bad[soft] = ~admissible(theta, phi, h["doc"][soft], h["word"][soft], h["u"][soft],
                                 z[soft])
     hard = int(bad.sum())
-    print(f"[parity] large-N{N_BIG}-K{K} {kernel}: n={z.size} mismatches={int(mis.sum())} "
+    print(f"[parity] large-N{big['doc'].numel()}-K{K} {kernel}: n={z.size} mismatches={int(mis.sum())} "
           f"hard={hard} in_band={int(band.sum())}", flush=True)
     assert hard == 0, big["idx"][np.nonzero(bad)[0][:5]]
     assert mis.mean() < MAX_MISMATCH_RATE
