@@ -429,3 +429,79 @@ def test_routed_at_the_largest_n():
     assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
     del d, w, u, z_r, z_b, route
     torch.cuda.empty_cache()
+
+
+# ---------------------------------------------------------------------------
+# Tables at the top of the wide build's range: theta or phi of 2^32 - 1 floats
+# or just under (16 GiB), generated on the GPU; most tokens take rows whose
+# float offsets lie at or past 2^31 (the top half of the unsigned 32-bit
+# offsets), the last 64 rows among them.  The oracle is given only the rows
+# the tokens use.
+
+def _top_rows_case(big, K, seed):
+    import torch
+    rows = (2 ** 32 - 1) // K
+    g = torch.Generator(device="cuda")
+    g.manual_seed(seed)
+    table = torch.empty((rows, K), dtype=torch.float32, device="cuda")
+    step = max(1, (1 << 28) // K)
+    for r in range(0, rows, step):
+        e = min(rows, r + step)
+        blk = torch.rand((e - r, K), generator=g, device="cuda")
+        if big == "phi":
+            blk *= torch.rand((e - r, K), generator=g, device="cuda") > 0.37
+        else:
+            blk = blk ** 8
+        table[r:e] = blk
+        del blk
+    rng = np.random.default_rng(seed)
+    N = 64 * 1000 + 17
+    r_min = (1 << 31) // K + 1
+    ids = np.where(rng.random(N) < 0.25, rng.integers(0, rows, N), rng.integers(r_min, rows, N))
+    ids[:64] = rows - 1 - np.arange(64)
+    uniq, remap = np.unique(ids, return_inverse=True)
+    used = table[torch.from_numpy(uniq).cuda()].cpu().numpy()
+    return table, ids.astype(np.int32), used, remap.astype(np.int32), N
+
+
+@pytest.mark.parametrize("big,K", [("phi", 1024), ("phi", 96), ("phi", 130),
+                                   ("theta", 20), ("theta", 1024)])
+def test_tables_at_16_gib(big, K):
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd.inputs import Corpus, doc_offsets
+    from parity import compare
+    print(f"[case] {big} of 16 GiB at K={K}", flush=True)
+    table, ids, used, remap, N = _top_rows_case(big, K, 1000 + K)
+    rng = np.random.default_rng(K)
+    u = (rng.integers(0, 1 << 24, N) * 2.0 ** -24).astype(np.float32)
+    if big == "phi":
+        M = 300
+        other = (rng.random((M, K), dtype=np.float32) ** 8)
+        doc = (np.arange(N, dtype=np.int64) * M // N).astype(np.int32)
+        th, ph, d_dev, w_dev = torch.from_numpy(other).cuda(), table, doc, ids
+        c = Corpus(other, used, doc, remap, u, name=f"phi-16GiB-K{K}")
+    else:
+        V = 5000
+        other = rng.random((V, K), dtype=np.float32) * (rng.random((V, K)) > 0.37)
+        other = other.astype(np.float32)
+        word = rng.integers(0, V, N).astype(np.int32)
+        order = np.argsort(ids, kind="stable")  # contiguous documents
+        ids, remap, word, u = ids[order], remap[order], word[order], u[order]
+        th, ph, d_dev, w_dev = table, torch.from_numpy(other).cuda(), ids, word
+        c = Corpus(used, other, remap, word, u, name=f"theta-16GiB-K{K}")
+    dd, wd = torch.from_numpy(d_dev).cuda(), torch.from_numpy(w_dev).cuda()
+    ud = torch.from_numpy(u).cuda()
+    z = lda.draw_butterfly(th, ph, dd, wd, ud)
+    torch.cuda.synchronize()
+    rep = compare(c, z.cpu().numpy())
+    print(f"[parity] {c.name}: {rep}", flush=True)
+    assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE
+    if big == "theta":
+        off = torch.from_numpy(doc_offsets(d_dev, th.shape[0])).cuda()
+        z2 = lda.draw_docs(th, ph, off, wd, ud)
+        torch.cuda.synchronize()
+        assert torch.equal(z, z2)
+        del off, z2
+    del table, th, ph, z
+    torch.cuda.empty_cache()
