@@ -438,9 +438,10 @@ def test_routed_at_the_largest_n():
 # offsets), the last 64 rows among them.  The oracle is given only the rows
 # the tokens use.
 
-def _top_rows_case(big, K, seed):
+def _top_rows_case(big, K, seed, unit=1):
+    """unit: 1 fills 2^32 - 1 floats (16 GiB), 4 fills 2^32 - 1 bytes (4 GiB)."""
     import torch
-    rows = (2 ** 32 - 1) // K
+    rows = (2 ** 32 - 1) // (K * unit)
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     table = torch.empty((rows, K), dtype=torch.float32, device="cuda")
@@ -456,7 +457,7 @@ def _top_rows_case(big, K, seed):
         del blk
     rng = np.random.default_rng(seed)
     N = 64 * 1000 + 17
-    r_min = (1 << 31) // K + 1
+    r_min = (1 << 31) // (K * unit) + 1
     ids = np.where(rng.random(N) < 0.25, rng.integers(0, rows, N), rng.integers(r_min, rows, N))
     ids[:64] = rows - 1 - np.arange(64)
     uniq, remap = np.unique(ids, return_inverse=True)
@@ -504,4 +505,36 @@ def test_tables_at_16_gib(big, K):
         assert torch.equal(z, z2)
         del off, z2
     del table, th, ph, z
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("K", [1024, 256, 50])
+def test_phi_at_4_gib(K):
+    """phi of 2^32 - 1 bytes or just under, the most the buffer-resource build
+    addresses (byte offsets up to 2^32 - 1), three quarters of the tokens on
+    rows past the 2^31-byte offset and the last 64 rows among them: every
+    kernel that stays on that build, against the oracle."""
+    import torch
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd.inputs import Corpus
+    from parity import compare, run_kernel
+    print(f"[case] phi of 4 GiB at K={K}", flush=True)
+    table, ids, used, remap, N = _top_rows_case("phi", K, 2000 + K, unit=4)
+    assert table.numel() * 4 <= lda.MAX_TABLE_BYTES
+    rng = np.random.default_rng(K)
+    M = 300
+    theta = rng.random((M, K), dtype=np.float32) ** 8
+    doc = (np.arange(N, dtype=np.int64) * M // N).astype(np.int32)
+    u = (rng.integers(0, 1 << 24, N) * 2.0 ** -24).astype(np.float32)
+    c = Corpus(theta, used, doc, remap, u, name=f"phi-4GiB-K{K}")
+    dev = {"theta": torch.from_numpy(theta).cuda(), "phi": table,
+           "doc_id": torch.from_numpy(doc).cuda(), "word_id": torch.from_numpy(ids).cuda(),
+           "u": torch.from_numpy(u).cuda()}
+    kernels = ["butterfly", "docs", "transposed", "naive"] + (["routed"] if K >= 768 else [])
+    for kernel in kernels:
+        z = run_kernel(kernel, dev)
+        rep = compare(c, z)
+        print(f"[parity] {c.name} {kernel}: {rep}", flush=True)
+        assert rep.hard == 0 and rep.mismatch_rate < MAX_MISMATCH_RATE, kernel
+    del table, dev
     torch.cuda.empty_cache()
