@@ -910,13 +910,14 @@ def report_bench(log: str, out_txt: str) -> int:
          f"  effective {r['effective_GBps']:,.0f} GB/s = {r['effective_frac_of_hbm_peak']:.2f} x "
          f"the {r['hbm_peak_GBps']:,.0f} GB/s HBM peak (L2 and the MALL serve re-read rows)",
          "",
-         "floors (memory-only probe of the same access pattern, fastest launch shape):"]
+         "floors (memory-only probe of the same access pattern, fastest launch shape; 'routed': "
+         "the probe over the routed arrays, in the routed draw's workgroup order):"]
     for w, f in r["floor"].items():
-        L.append(f"  {w:18s} floor {f['ms']:8.4f} ms ({f['shape']})  draw {f['draw_ms']:8.4f} ms  "
+        L.append(f"  {w:25s} floor {f['ms']:8.4f} ms ({f['shape']})  draw {f['draw_ms']:8.4f} ms  "
                  f"floor/draw {f['frac_of_floor']:.3f}")
     shapes = r.get("floors", {})
     for w, f in shapes.items():
-        L.append(f"  {w:18s} shapes: " + ", ".join(f"{k} {v:.4f}" for k, v in f["shapes_ms"].items()))
+        L.append(f"  {w:25s} shapes: " + ", ".join(f"{k} {v:.4f}" for k, v in f["shapes_ms"].items()))
     c = r["ceilings"]
     L += ["", "ceilings measured in the same run:",
           f"  streaming read from HBM   {c['hbm_read_GBps']:8,.0f} GB/s  ({c['hbm_read']})",
@@ -1026,6 +1027,48 @@ def measure_floor(name: str, c, dev, steps: int, warmup: int) -> dict:
         shapes["w{}-g{}-c{}".format(*cfg)] = r["ms_per_launch"]
     best = min(shapes, key=shapes.get)
     dev.pop("floor_cfg")
+    return {"ms_per_launch": shapes[best], "shape": best, "shapes_ms": shapes,
+            "alg_GBps": algorithmic_bytes(c) / (shapes[best] * 1e-3) / 1e9}
+
+
+def measure_routed_floor(name: str, c, dev, steps: int, warmup: int) -> dict:
+    """The memory-only floor of the routed draw: the floor probe over the
+    routing's own arrays (each routed position's document, word and uniform),
+    laid out so that probe workgroup b takes tile b div 8 of list b mod 8, as
+    routed workgroup b does, so every list stays on its XCD; 2 or 4
+    wavefronts per workgroup (the routed draw uses one of them) and windows of
+    8 or 16 tokens, the fastest kept.  Workgroups past a list's end read its
+    last position again, where the draw's simply exit."""
+    import torch
+    import paper_1505_03851_amd as lda
+    th, ph, d, w, u = (dev["theta"], dev["phi"], dev["doc_id"], dev["word_id"], dev["u"])
+    if "route" not in dev:
+        dev["route"] = lda.route_build(d, w, th.shape[0], ph.shape[0])
+    route = dev["route"]
+    a = route.arrays()
+    if min(route.length) == 0:
+        raise ValueError("an empty routed list: no routed floor")
+    start = torch.tensor(route.start, dtype=torch.int64, device=d.device)
+    length = torch.tensor(route.length, dtype=torch.int64, device=d.device)
+    shapes = {}
+    for wpb in (2, 4):
+        tile = wpb * 64
+        tiles = -(-max(route.length) // tile)
+        b = torch.arange(8 * tiles, device=d.device)
+        x, t = b % 8, b // 8
+        off = t[:, None] * tile + torch.arange(tile, device=d.device)[None, :]
+        pos = (start[x][:, None] + torch.minimum(off, (length[x] - 1)[:, None])).reshape(-1)
+        probe_dev = {"theta": th, "phi": ph, "doc_id": a["rdoc"][pos], "word_id": a["rword"][pos],
+                     "u": u[a["perm"][pos].long().clamp(min=0)]}
+        for window in (8, 16):
+            probe_dev["floor_cfg"] = (window, wpb, 0)
+            _, per_ms, _ = time_kernel("floor", probe_dev, steps, warmup)
+            ms = sum(per_ms) / len(per_ms)
+            shapes[f"w{window}-g{wpb}-c0"] = ms
+            print(f"[bench] {name} routed floor w{window}-g{wpb}: {ms:.3f} ms/launch",
+                  file=sys.stderr, flush=True)
+        del probe_dev, pos, off
+    best = min(shapes, key=shapes.get)
     return {"ms_per_launch": shapes[best], "shape": best, "shapes_ms": shapes,
             "alg_GBps": algorithmic_bytes(c) / (shapes[best] * 1e-3) / 1e9}
 
@@ -1270,6 +1313,8 @@ def main() -> int:
     r = measure(c5.name, c5, dev5, "routed", steps, warmup)
     parity[c5.name + " routed"] = parity_report(c5, r["z"], ref5)
     results.append(_brief(r))
+    floors[c5.name + " routed"] = measure_routed_floor(c5.name, c5, dev5, steps, warmup)
+    floors[c5.name + " routed"]["draw_ms"] = r["ms_per_launch"]
     del dev5, c5, ref5
     torch.cuda.empty_cache()
 
@@ -1289,6 +1334,9 @@ def main() -> int:
         routed[k] = r.pop("z")
         r["differs_from_butterfly"] = int((routed[k] != z_head).sum())
         results.append(r)
+        if k == "routed":
+            floors[HEADLINE + " routed"] = measure_routed_floor(HEADLINE, c, dev, steps, warmup)
+            floors[HEADLINE + " routed"]["draw_ms"] = r["ms_per_launch"]
     # the same launches with L2 and the MALL flushed before each (1 GiB fill)
     flush = torch.empty(1 << 28, dtype=torch.float32, device="cuda")
     results.append(_brief(measure(HEADLINE, c, dev, "butterfly", steps, 1, flush=flush)))
