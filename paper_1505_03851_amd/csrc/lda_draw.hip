@@ -105,8 +105,13 @@ void launch_routed(const float *theta, const float *phi, const RoutedTokens &rt,
   constexpr int C = LDA_EIGHTHS_WINDOW, WPEU = LDA_EIGHTHS_WAVES_PER_EU;
   const uint32_t tb = table_extent(M, K);
   const uint32_t pb = table_extent(V, K);
-  const size_t per_wave = (size_t)routed_lds_floats(eighths_blocks(K)) * sizeof(float);
-  if (3 * 4 * per_wave <= 160 * 1024) {
+  const int NB = eighths_blocks(K);
+  const size_t per_wave = (size_t)routed_lds_floats(NB) * sizeof(float);
+  // Measured on MI355X (16.8M tokens): 2 wavefronts per workgroup where the
+  // runs' theta rows are staged (K <= 1024: 4 were 1-2% slower), 4 above,
+  // two such workgroups fitting in LDS (0.5-2.6% faster than 2 from K = 1280
+  // to 2048).
+  if (NB > kRowsMaxBlocks && 2 * 4 * per_wave <= 160 * 1024) {
     const int64_t tiles = (max_len + 4 * kWave - 1) / (4 * kWave);
     routed_eighths_kernel<C, 4, WPEU, PAD><<<(unsigned)(kXcds * tiles), 4 * kWave, 4 * per_wave, s>>>(
         theta, phi, rt, u, z, K, tb, pb);

@@ -86,15 +86,19 @@ __device__ __forceinline__ f4 theta_leaf(const Table &tt, int c0, int blk, int r
 
 // Theta leaves of a wavefront whose tokens form D <= kFewMax runs of documents
 // (kFewDocs): per block, each run's leaf at this lane's topics is loaded once
-// and staged in LDS (lds[d * 64 + lane]); each token then reads its run's leaf
-// from LDS instead of from memory.
+// and staged in LDS, leaf `lane` of run d and block b at lds[d rstride +
+// b bstride + lane]; each token then reads its run's leaf from LDS instead of
+// from memory.  With rstride = 64 and bstride = 0 every block's leaves replace
+// the last ones; with rstride = 64 NB and bstride = 64 the runs' whole rows
+// stay, for the rebuild.
 constexpr int kFewMax = 4;
 struct FewDocs {
-  f4 *lds;                 // this wavefront's kFewMax x 64 leaves (one-document
+  f4 *lds;                 // this wavefront's staged leaves (one-document
                            // sweeps that stage the theta row: that row)
   int D;                   // runs of documents in the wavefront, uniform
   uint32_t row[kFewMax];   // their theta row offsets, uniform
   int slot;                // this lane's run
+  int rstride, bstride;    // staging layout, uniform (in leaves)
 };
 
 // Loads of block `blk`'s leaves of the wavefront's runs (to be staged later).
@@ -109,18 +113,19 @@ __device__ __forceinline__ void few_load(const FewDocs &fd, const Table &tt, int
 // Stage the loaded leaves in LDS.  The wavefront's earlier LDS reads are
 // issued before these writes and LDS executes one wavefront's operations in
 // order, so the writes may replace leaves the wavefront has read already.
-__device__ __forceinline__ void few_stage(const FewDocs &fd, const f4 (&st)[kFewMax], int lane) {
+__device__ __forceinline__ void few_stage(const FewDocs &fd, const f4 (&st)[kFewMax], int lane,
+                                          int blk) {
 #pragma unroll
   for (int d = 0; d < kFewMax; ++d)
-    if (d < fd.D) fd.lds[d * kWave + lane] = st[d];
+    if (d < fd.D) fd.lds[d * fd.rstride + blk * fd.bstride + lane] = st[d];
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// The staged leaf of token t's run.
-__device__ __forceinline__ f4 few_leaf(const FewDocs &fd, int t, int lane) {
-  return fd.lds[__builtin_amdgcn_readlane(fd.slot, t) * kWave + lane];
+// The staged leaf of token t's run in block blk.
+__device__ __forceinline__ f4 few_leaf(const FewDocs &fd, int t, int lane, int blk) {
+  return fd.lds[__builtin_amdgcn_readlane(fd.slot, t) * fd.rstride + blk * fd.bstride + lane];
 }
 
 // Sweep step for one 256-topic block: win[] holds (or awaits) the phi leaves
@@ -190,9 +195,9 @@ __device__ __forceinline__ float sweep8_block(const Wave<kWave, false> &w, const
     if constexpr (MODE == kFewDocs) {
       const bool trefill = i + CT < kWave;
       if (trefill || PREFETCH) {
-        if (!trefill && i + CT == kWave) few_stage(fd, st, lane);
+        if (!trefill && i + CT == kWave) few_stage(fd, st, lane, next);
         const int tt = eighth_slot_token(pair_token(trefill ? i + CT : i + CT - kWave));
-        twin[i % CT] = few_leaf(fd, tt, lane);
+        twin[i % CT] = few_leaf(fd, tt, lane, trefill ? blk : next);
       }
     }
     // keep the window rolling: no load is hoisted past this point (hoisting
@@ -243,7 +248,7 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
   if constexpr (MODE == kFewDocs) {
     f4 st[kFewMax];
     few_load<PAD>(fd, w.th, c0, 0, w.r, st);
-    few_stage(fd, st, lane_id());
+    few_stage(fd, st, lane_id(), 0);
   }
 #pragma unroll
   for (int i = 0; i < C; ++i) {
@@ -252,7 +257,7 @@ __device__ __forceinline__ float sweep8(const Wave<kWave, false> &w, const FewDo
     if constexpr (MODE == kAnyDocs)
       twin[i] = w.th.ld4(v0, __builtin_amdgcn_readlane(w.th_lane, t));
     if constexpr (MODE == kFewDocs)
-      if (i < CT) twin[i % CT] = few_leaf(fd, t, lane_id());
+      if (i < CT) twin[i % CT] = few_leaf(fd, t, lane_id(), 0);
   }
   // hook() runs once, after the first block's step (loads it issues are in
   // flight during the other blocks)

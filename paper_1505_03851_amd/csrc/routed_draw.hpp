@@ -23,10 +23,38 @@ struct RoutedTokens {
   int64_t base[kXcds], len[kXcds];  // list starts and lengths
 };
 
+// Up to kRowsMaxBlocks 256-topic blocks, a wavefront whose tokens form at
+// most kRowsMax runs of documents keeps the runs' whole theta rows in LDS
+// (staged leaf by leaf during the sweep), and the rebuild reads its theta
+// values there rather than from memory.
+constexpr int kRowsMax = 3;
+constexpr int kRowsMaxBlocks = 4;
+
 // LDS floats per wavefront of the routed kernel: the prefix rows, then the
-// staged theta leaves of up to kFewMax runs.
+// staged theta leaves of up to kFewMax runs, or the kRowsMax runs' rows.
 __host__ __device__ constexpr int routed_lds_floats(int NB) {
-  return 8 * NB * kWave + kFewMax * kWave * 4;
+  const int leaves = kFewMax * kWave * 4;
+  const int rows = NB <= kRowsMaxBlocks ? kRowsMax * NB * kBlock4 : 0;
+  return 8 * NB * kWave + (rows > leaves ? rows : leaves);
+}
+
+// The rebuild's tile (load_tile_blocks for W = 32) with theta read from the
+// runs' rows staged in LDS: token k's topic first + i of run s_k at
+// trow[s_k * row + i] (zero in the padding).
+template <bool PADDED>
+__device__ __forceinline__ void load_chunk_rows(const Wave<kWave / 2, false> &w,
+                                                float (&a)[kWave / 2], int blk, int first,
+                                                const float *trow, int slot, int row) {
+#pragma unroll
+  for (int k = 0; k < kWave / 2; ++k) {
+    const int bk = group_value<kWave / 2>(blk, k);
+    const int sk = group_value<kWave / 2>(slot, k);
+    const int i = bk * (kWave / 2) + w.r;  // topic first + i
+    const int t = first + i;
+    const uint32_t voff = (uint32_t)(PADDED && t < 0 ? 0 : t) * 4u;
+    const uint32_t poff = (uint32_t)group_value<kWave / 2>((int)w.ph_lane, k);
+    a[k] = trow[sk * row + i] * load_row<kWave / 2>(w.ph, voff, poff);
+  }
 }
 
 // One wavefront of the leaf kernel over 64 listed tokens: lane `lane` draws
@@ -52,6 +80,9 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
   const uint64_t starts = __builtin_amdgcn_ballot_w64(lane == 0 || doc != prev);
   fd.D = __builtin_amdgcn_readfirstlane(__builtin_popcountll(starts));
   fd.slot = __builtin_popcountll(starts & ((2ull << lane) - 1ull)) - 1;
+  const bool rows = NB <= kRowsMaxBlocks && fd.D <= kRowsMax;
+  fd.rstride = rows ? NB * kWave : kWave;
+  fd.bstride = rows ? kWave : 0;
   uint64_t m = starts;
 #pragma unroll
   for (int d = 0; d < kFewMax; ++d) {
@@ -69,7 +100,9 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
   const auto load_u = [&]() { un = u(n); };
   region += lane;
   float sum;
-  if (fd.D == 1)
+  if (fd.D == 1 && rows)
+    sum = sweep8<kOneDoc, C, PAD, C, decltype(load_u), true>(w, fd, NB, c0, region, load_u);
+  else if (fd.D == 1)
     sum = sweep8<kOneDoc, C, PAD>(w, fd, NB, c0, region, load_u);
   else if (fd.D <= kFewMax)
     sum = sweep8<kFewDocs, LDA_ROUTED_FEW_WINDOW, PAD, LDA_ROUTED_FEW_THETA>(w, fd, NB, c0,
@@ -93,7 +126,13 @@ __device__ __forceinline__ void draw_listed(const float *__restrict__ theta,
   // leaf_eighths_kernel.
   const Wave<kWave / 2, false> wh = half_wave(w, lane);
   float h[kWave / 2];
-  load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+  if (rows) {
+    lds_order();
+    load_chunk_rows<PAD>(wh, h, chunk, c0, reinterpret_cast<const float *>(fd.lds), fd.slot,
+                         NB * kBlock4);
+  } else {
+    load_tile_blocks<kWave / 2, false, PAD>(wh, h, chunk, c0);
+  }
   butterfly_block<kWave / 2>(h, wh.r, NoStore{});
   const int j = c0 + chunk * (kWave / 2) +
                 inblock_search<kWave / 2, false>(h, nullptr, wh.r, wh.gbase, stop, low, high);
