@@ -284,8 +284,8 @@ int lda_butterfly_table(const float *theta, const float *phi,
  * only the grouping of tokens into wavefronts changes.  Routing pays where
  * phi is far larger than the caches and costs where phi fits the 256 MiB
  * MALL.  Measured on MI355X over 16.8M Zipf tokens with V = 100,000 words:
- * 28% slower than lda_draw_butterfly at K = 256, 3% slower at K = 512, 2%
- * faster at K = 768, 5% at K = 1024, 11% at K = 2048 (24% on 9.8M tokens
+ * 28% slower than lda_draw_butterfly at K = 256, 3% slower at K = 512, 4%
+ * faster at K = 768, 6% at K = 1024, 13% at K = 2048 (28% on 9.8M tokens
  * with V = 50,000 at K = 2048); so lda_draw_routed takes K >= LDA_ROUTE_MIN_K
  * only.
  *

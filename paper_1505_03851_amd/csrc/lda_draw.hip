@@ -231,8 +231,8 @@ RoutePlan route_plan(void *ws, const RouteLayout &L) {
 // MI355X over 16.8M Zipf tokens with V = 100,000 words, the routed draw is
 // 28% slower than the token-order draw at K = 256 and 3% at K = 512 (phi of
 // 98 and 195 MiB: it fits the 256 MiB MALL, and the few-documents theta path
-// costs more than routing saves), and 2-11% faster from K = 768 (293 MiB) to
-// 2048 (24% on the Poisson corpus at K = 2048).  Smaller K are refused.
+// costs more than routing saves), and 2-13% faster from K = 768 (293 MiB) to
+// 2048 (28% on the Poisson corpus at K = 2048).  Smaller K are refused.
 bool routed_for(int32_t K) {
   return K % kLeaf == 0 && K >= LDA_ROUTE_MIN_K && K >= LDA_EIGHTHS_MIN_K &&
          eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
