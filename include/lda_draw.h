@@ -88,15 +88,17 @@ extern "C" {
  * tables are rejected with LDA_ERR_UNSUPPORTED. */
 #define LDA_MAX_TABLE_BYTES 4294967295LL
 
-/* Largest size in bytes of theta or phi for lda_draw_butterfly, lda_draw_docs
- * and lda_draw_butterfly_philox, and of the count tables of lda_count_topics,
- * lda_count_topics_docs and lda_count_topics_indexed: 2^32 - 1 elements
- * (16 GiB).  When either table
- * is larger than LDA_MAX_TABLE_BYTES these draw with a second build of the
- * same kernels that addresses the tables by 32-bit float offsets and 64-bit
- * loads (ids beyond the table's rows are clamped to its last row there, so
- * no read leaves the table); the draws are the same. */
-#define LDA_MAX_WIDE_TABLE_BYTES 17179869180LL
+/* lda_draw_butterfly, lda_draw_docs and lda_draw_butterfly_philox take theta
+ * and phi of any size (M and V below 2^31): when either table is larger than
+ * LDA_MAX_TABLE_BYTES they draw with a second build of the same kernels that
+ * addresses rows by index and forms 64-bit addresses (ids beyond the table's
+ * rows are clamped to its last row there, so no read leaves the table); the
+ * draws are the same.
+ *
+ * Largest size in bytes of each count table of lda_count_topics,
+ * lda_count_topics_docs and lda_count_topics_indexed: 2^32 - 1 cells
+ * (16 GiB; cells are addressed by unsigned 32-bit indices). */
+#define LDA_MAX_COUNT_TABLE_BYTES 17179869180LL
 
 /*
  * Baseline draw: Algorithm 1 with the binary search of Algorithm 3.  One lane
@@ -132,9 +134,9 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
  *    rebuilt block (or half-block) with Algorithm 10.
  * Where K is not a multiple of the block (or of the group's 4 W topics), the
  * first K mod block topics (the remnant) form a leading block padded with
- * empty topics, which are never drawn.  theta and phi may each hold up to
- * LDA_MAX_WIDE_TABLE_BYTES (past LDA_MAX_TABLE_BYTES the same kernels run
- * with 64-bit table addressing).
+ * empty topics, which are never drawn.  theta and phi may be of any size
+ * (past LDA_MAX_TABLE_BYTES the same kernels run with 64-bit table
+ * addressing).
  */
 int lda_draw_butterfly(const float *theta, const float *phi,
                        const int32_t *doc_id, const int32_t *word_id,
@@ -152,8 +154,7 @@ int lda_draw_butterfly(const float *theta, const float *phi,
  * Tokens are still drawn one per lane, 64 consecutive tokens per wavefront:
  * each lane finds its document by binary search over doc_offsets.
  * doc_offsets must be 8-byte aligned (LDA_ERR_ALIGN otherwise); its contents
- * are not checked.  Tables up to LDA_MAX_WIDE_TABLE_BYTES, as
- * lda_draw_butterfly.
+ * are not checked.  Tables of any size, as lda_draw_butterfly.
  */
 int lda_draw_docs(const float *theta, const float *phi,
                   const int64_t *doc_offsets, const int32_t *word_id,
@@ -228,9 +229,8 @@ int lda_philox_uniforms(float *u, int64_t count, int64_t first, uint64_t seed,
  *                               of 8 topics per lane in groups half as wide;
  *                               elsewhere the kernels of lda_draw_butterfly;
  *   LDA_VARIANT_WIDE_TABLES     the kernels of lda_draw_butterfly as built for
- *                               tables past 4 GiB (float offsets, 64-bit
- *                               loads), at any table size up to
- *                               LDA_MAX_WIDE_TABLE_BYTES: the same draws as
+ *                               tables past 4 GiB (rows by index, 64-bit
+ *                               loads), at any table size: the same draws as
  *                               lda_draw_butterfly, to compare the two builds.
  * The three table variants use the one-topic-per-lane kernel for all K
  * (W = 64 for K >= 64, else 32).  Any other `variant` returns
@@ -356,8 +356,8 @@ int lda_draw_routed_philox(const float *theta, const float *phi, const void *wor
  * order of the tokens.  Every pointer 4-byte aligned (LDA_ERR_ALIGN); ndk and
  * nwk may not be NULL (LDA_ERR_NULL), nor the token arrays when N > 0;
  * N above LDA_COUNT_MAX_N (counts are int32), K above LDA_MAX_K, or either
- * table above LDA_MAX_WIDE_TABLE_BYTES (2^32 - 1 cells: cells are addressed by
- * unsigned 32-bit indices) give LDA_ERR_UNSUPPORTED.  Enqueues two
+ * table above LDA_MAX_COUNT_TABLE_BYTES (2^32 - 1 cells: cells are addressed
+ * by unsigned 32-bit indices) give LDA_ERR_UNSUPPORTED.  Enqueues two
  * kernels that clear the tables, then one that counts; nothing is allocated.
  */
 #define LDA_COUNT_MAX_N 2147483647LL

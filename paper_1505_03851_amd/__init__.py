@@ -17,7 +17,7 @@ _BINDING = ("draw_naive", "draw_butterfly", "draw_transposed", "draw_docs", "dra
             "route_build", "draw_routed", "draw_routed_philox", "route_workspace_bytes", "Route",
             "draw_routed_scratch", "ROUTED_SCRATCH_BYTES",
             "butterfly_width", "status_string", "version", "LdaError",
-            "load", "MAX_K", "MAX_TABLE_BYTES", "MAX_WIDE_TABLE_BYTES", "STATUS")
+            "load", "MAX_K", "MAX_TABLE_BYTES", "MAX_COUNT_TABLE_BYTES", "STATUS")
 
 __all__ = list(_BINDING)
 

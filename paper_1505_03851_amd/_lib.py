@@ -41,7 +41,7 @@ STATUS = {k: v for k, v in _CONSTS.items() if k == "LDA_OK" or k.startswith("LDA
 MAX_K = _CONSTS["LDA_MAX_K"]
 MAX_N = _CONSTS["LDA_MAX_N"]
 MAX_TABLE_BYTES = _CONSTS["LDA_MAX_TABLE_BYTES"]
-MAX_WIDE_TABLE_BYTES = _CONSTS["LDA_MAX_WIDE_TABLE_BYTES"]
+MAX_COUNT_TABLE_BYTES = _CONSTS["LDA_MAX_COUNT_TABLE_BYTES"]
 DOC_LANES_MAX_CACHE_BYTES = _CONSTS["LDA_DOC_LANES_MAX_CACHE_BYTES"]
 # table variants of lda_draw_butterfly_variant, by name
 ROUTED_SCRATCH_BYTES = _CONSTS["LDA_ROUTED_SCRATCH_BYTES"]

@@ -221,22 +221,22 @@ __device__ __forceinline__ f4 load_f32x4(rsrc_t r, uint32_t voff, uint32_t soff)
 }
 
 // ---------------------------------------------------------------------------
-// A table (theta [M][K] or phi [V][K]) as the draw kernels address it: a row
-// offset (32-bit, `row(id)`, a multiple of the row step) plus a lane offset in
-// bytes (the topics within the row).
+// A table (theta [M][K] or phi [V][K]) as the draw kernels address it: a
+// 32-bit row handle (`row(id)`) plus a lane offset in bytes (the topics
+// within the row).  The kernels only pass handles on (also across lanes).
 //  * LDA_WIDE_TABLES 0, tables below 4 GiB: a buffer resource over the table;
-//    offsets count bytes, and the resource's range check returns 0 for a read
-//    past the table, so an id out of range reads zeros and cannot fault.
-//  * LDA_WIDE_TABLES 1, tables below 16 GiB: the table's base pointer; row
-//    offsets count floats and each load forms a 64-bit address.  row() clamps
-//    the id to the table's last row, so that here too every read stays
-//    inside the table.
-// `extent` is the table's size in the offsets' unit (bytes, or floats).
-// ld / ld4 take a row offset that is uniform across the wavefront (a scalar
+//    the handle is the row's byte offset, and the resource's range check
+//    returns 0 for a read past the table, so an id out of range reads zeros
+//    and cannot fault.
+//  * LDA_WIDE_TABLES 1, any size (fewer than 2^31 rows): the table's base
+//    pointer; the handle is the row index, and each load forms the 64-bit
+//    address base + row K + the lane offset.  row() clamps the id to the
+//    table's last row, so that here too every read stays inside the table.
+// `extent` is the table's size in the handles' unit (bytes, or rows).
+// ld / ld4 take a handle that is uniform across the wavefront (a scalar
 // operand), ldv / ld4v one that differs between lanes.
-__host__ __device__ constexpr uint32_t table_unit() { return LDA_WIDE_TABLES ? 1u : 4u; }
 __host__ __device__ constexpr uint32_t table_extent(int64_t rows, int32_t K) {
-  return (uint32_t)(rows * (int64_t)K * table_unit());
+  return LDA_WIDE_TABLES ? (uint32_t)rows : (uint32_t)(rows * (int64_t)K * 4);
 }
 
 #if LDA_WIDE_TABLES
@@ -246,13 +246,10 @@ using f4u = float __attribute__((ext_vector_type(4), aligned(4)));
 struct Table {
   const float *base;
   uint32_t step;   // floats per row (K)
-  uint32_t last;   // offset of the last row
-  __device__ __forceinline__ uint32_t row(uint32_t id) const {
-    const uint64_t off = (uint64_t)id * step;
-    return off < last ? (uint32_t)off : last;
-  }
+  uint32_t last;   // the last row
+  __device__ __forceinline__ uint32_t row(uint32_t id) const { return id < last ? id : last; }
   __device__ __forceinline__ const char *at(uint32_t voff, uint32_t row) const {
-    return reinterpret_cast<const char *>(base + row) + voff;
+    return reinterpret_cast<const char *>(base + (uint64_t)row * step) + voff;
   }
   __device__ __forceinline__ float ld(uint32_t voff, uint32_t row) const {
     return *reinterpret_cast<const float *>(at(voff, row));
@@ -265,7 +262,7 @@ struct Table {
 };
 
 __device__ __forceinline__ Table make_table(const float *base, uint32_t extent, int K) {
-  return Table{base, (uint32_t)K, extent - (uint32_t)K};
+  return Table{base, (uint32_t)K, extent - 1u};
 }
 #else
 struct Table {

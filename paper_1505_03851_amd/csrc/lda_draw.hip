@@ -60,16 +60,17 @@ bool wide_tables(int32_t M, int32_t V, int32_t K) {
   return (int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES || (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES;
 }
 
-// WIDE_OK: the entry point draws tables up to LDA_MAX_WIDE_TABLE_BYTES (with
-// the wide build past LDA_MAX_TABLE_BYTES); otherwise up to
-// LDA_MAX_TABLE_BYTES (unsigned 32-bit byte offsets).
+// WIDE_OK: the entry point draws tables of any size (the wide build past
+// LDA_MAX_TABLE_BYTES, addressing rows by index; M and V are below 2^31);
+// otherwise up to LDA_MAX_TABLE_BYTES (unsigned 32-bit byte offsets).
 int check_args(const void *theta, const void *phi, const void *doc_id,
                const void *word_id, const void *u, const void *z, int64_t N,
                int32_t M, int32_t V, int32_t K, bool wide_ok = false) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_MAX_N) return LDA_ERR_UNSUPPORTED;
-  const int64_t limit = wide_ok ? LDA_MAX_WIDE_TABLE_BYTES : LDA_MAX_TABLE_BYTES;
-  if ((int64_t)M * K * 4 > limit || (int64_t)V * K * 4 > limit) return LDA_ERR_UNSUPPORTED;
+  if (!wide_ok && ((int64_t)M * K * 4 > LDA_MAX_TABLE_BYTES ||
+                   (int64_t)V * K * 4 > LDA_MAX_TABLE_BYTES))
+    return LDA_ERR_UNSUPPORTED;
   if (N == 0) return LDA_OK;
   const void *ptrs[] = {theta, phi, doc_id, word_id, u, z};
   for (const void *p : ptrs) {
@@ -627,8 +628,8 @@ extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, c
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
   // cells are addressed by unsigned 32-bit indices (d K + k, w K + k)
-  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
+  if ((int64_t)M * K * 4 > LDA_MAX_COUNT_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;
   if (!ndk || !nwk) return LDA_ERR_NULL;
   if (N > 0 && (!doc_id || !word_id || !z)) return LDA_ERR_NULL;
@@ -657,8 +658,8 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
   // cells are addressed by unsigned 32-bit indices (d K + k, w K + k)
-  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
+  if ((int64_t)M * K * 4 > LDA_MAX_COUNT_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;
   if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
   if (N > 0 && (!word_id || !z)) return LDA_ERR_NULL;
@@ -771,8 +772,8 @@ extern "C" int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_
                                         int32_t *ndk, int32_t *nwk, void *stream) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
-  if ((int64_t)M * K * 4 > LDA_MAX_WIDE_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_WIDE_TABLE_BYTES)
+  if ((int64_t)M * K * 4 > LDA_MAX_COUNT_TABLE_BYTES ||
+      (int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES)
     return LDA_ERR_UNSUPPORTED;
   const int st = check_word_index(N, V, index, index_bytes);
   if (st != LDA_OK) return st;

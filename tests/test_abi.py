@@ -97,7 +97,8 @@ def call(lib, fn, **kw):
 
 FNS = ["lda_draw_naive", "lda_draw_butterfly", "lda_draw_transposed", "lda_draw_docs",
        "lda_draw_doc_lanes", "lda_draw_butterfly_variant", "lda_butterfly_table"]
-# entry points that take tables up to LDA_MAX_WIDE_TABLE_BYTES
+# entry points that take tables of any size (past LDA_MAX_TABLE_BYTES with the
+# wide build)
 WIDE_FNS = ("lda_draw_butterfly", "lda_draw_docs")
 
 
@@ -114,19 +115,19 @@ def test_shape_errors(lib, fn):
     assert MAX_N >= 2 ** 32 - 2 ** 16
     assert call(lib, fn, N=MAX_N + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
     assert call(lib, fn, N=2 ** 40) == STATUS["LDA_ERR_UNSUPPORTED"]
-    # tables past the byte limit are rejected before any HIP call (N = 0
-    # below: an accepted call then launches nothing, so the fake addresses
-    # are never read)
-    from paper_1505_03851_amd._lib import MAX_WIDE_TABLE_BYTES
-    limit = MAX_WIDE_TABLE_BYTES if fn in WIDE_FNS else MAX_TABLE_BYTES
-    big = limit // (4 * 1024) + 1
-    assert call(lib, fn, K=1024, V=big) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert call(lib, fn, K=1024, M=big) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert call(lib, fn, K=1024, V=big - 1, M=big - 1, N=0) == 0
+    # tables past the buffer resources' byte limit are rejected before any
+    # HIP call, except by the entry points that take any size; every call
+    # that is accepted here has N = 0, so it launches nothing and the fake
+    # addresses are never read
     past_4_gib = MAX_TABLE_BYTES // (4 * 1024) + 1
-    want = 0 if fn in WIDE_FNS else STATUS["LDA_ERR_UNSUPPORTED"]
-    assert call(lib, fn, K=1024, V=past_4_gib, N=0) == want
-    assert call(lib, fn, K=1024, M=past_4_gib, N=0) == want
+    if fn in WIDE_FNS:
+        for kw in (dict(V=past_4_gib), dict(M=past_4_gib), dict(V=2 ** 31 - 1),
+                   dict(M=2 ** 31 - 1, V=2 ** 31 - 1)):
+            assert call(lib, fn, K=1024, N=0, **kw) == 0, kw
+    else:
+        assert call(lib, fn, K=1024, V=past_4_gib) == STATUS["LDA_ERR_UNSUPPORTED"]
+        assert call(lib, fn, K=1024, M=past_4_gib) == STATUS["LDA_ERR_UNSUPPORTED"]
+        assert call(lib, fn, K=1024, V=past_4_gib - 1, M=past_4_gib - 1, N=0) == 0
 
 
 @pytest.mark.parametrize("fn", FNS)
@@ -216,12 +217,9 @@ def test_philox_draw_argument_errors(lib):
     for kw in (dict(N=-1), dict(M=0), dict(V=0), dict(K=0)):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
     assert run(N=0, theta=None, phi=None, doc=None, word=None, z=None) == 0
-    # tables up to LDA_MAX_WIDE_TABLE_BYTES (N = 0: nothing is launched)
-    from paper_1505_03851_amd._lib import MAX_TABLE_BYTES, MAX_WIDE_TABLE_BYTES
-    big = MAX_WIDE_TABLE_BYTES // (4 * 1024) + 1
-    assert run(K=1024, V=big) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert run(K=1024, M=big) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert run(K=1024, V=MAX_TABLE_BYTES // 4096 + 1, M=big - 1, N=0) == 0
+    # tables of any size (N = 0: nothing is launched)
+    from paper_1505_03851_amd._lib import MAX_TABLE_BYTES
+    assert run(K=1024, V=MAX_TABLE_BYTES // 4096 + 1, M=2 ** 31 - 1, N=0) == 0
 
 
 def test_philox_uniforms_argument_errors(lib):

@@ -438,10 +438,12 @@ def test_routed_at_the_largest_n():
 # offsets), the last 64 rows among them.  The oracle is given only the rows
 # the tokens use.
 
-def _top_rows_case(big, K, seed, unit=1):
-    """unit: 1 fills 2^32 - 1 floats (16 GiB), 4 fills 2^32 - 1 bytes (4 GiB)."""
+def _top_rows_case(big, K, seed, unit=1, rows=None, past=1 << 31):
+    """unit: 1 fills 2^32 - 1 floats (16 GiB), 4 fills 2^32 - 1 bytes (4 GiB);
+    or `rows` rows.  Most tokens take rows whose offset in `unit`s is at or
+    past `past`."""
     import torch
-    rows = (2 ** 32 - 1) // (K * unit)
+    rows = rows or (2 ** 32 - 1) // (K * unit)
     g = torch.Generator(device="cuda")
     g.manual_seed(seed)
     table = torch.empty((rows, K), dtype=torch.float32, device="cuda")
@@ -457,7 +459,7 @@ def _top_rows_case(big, K, seed, unit=1):
         del blk
     rng = np.random.default_rng(seed)
     N = 64 * 1000 + 17
-    r_min = (1 << 31) // (K * unit) + 1
+    r_min = past // (K * unit) + 1
     ids = np.where(rng.random(N) < 0.25, rng.integers(0, rows, N), rng.integers(r_min, rows, N))
     ids[:64] = rows - 1 - np.arange(64)
     uniq, remap = np.unique(ids, return_inverse=True)
@@ -465,15 +467,24 @@ def _top_rows_case(big, K, seed, unit=1):
     return table, ids.astype(np.int32), used, remap.astype(np.int32), N
 
 
-@pytest.mark.parametrize("big,K", [("phi", 1024), ("phi", 96), ("phi", 130),
-                                   ("theta", 20), ("theta", 1024)])
-def test_tables_at_16_gib(big, K):
+@pytest.mark.parametrize("big,K,gib", [("phi", 1024, 16), ("phi", 96, 16), ("phi", 130, 16),
+                                       ("theta", 20, 16), ("theta", 1024, 16),
+                                       ("phi", 1024, 20), ("phi", 96, 20), ("theta", 1024, 20),
+                                       ("theta", 20, 20)])
+def test_tables_at_16_gib(big, K, gib):
+    """gib = 16: tables of 2^32 - 1 floats or just under, most tokens on rows
+    whose float offsets lie at or past 2^31; gib = 20: tables of 20 GiB, past
+    the reach of 32-bit float offsets, most tokens on rows past 2^32 floats."""
     import torch
     import paper_1505_03851_amd as lda
     from paper_1505_03851_amd.inputs import Corpus, doc_offsets
     from parity import compare
-    print(f"[case] {big} of 16 GiB at K={K}", flush=True)
-    table, ids, used, remap, N = _top_rows_case(big, K, 1000 + K)
+    print(f"[case] {big} of {gib} GiB at K={K}", flush=True)
+    if gib == 16:
+        table, ids, used, remap, N = _top_rows_case(big, K, 1000 + K)
+    else:
+        table, ids, used, remap, N = _top_rows_case(big, K, 3000 + K,
+                                                    rows=(gib << 30) // (4 * K), past=1 << 32)
     rng = np.random.default_rng(K)
     u = (rng.integers(0, 1 << 24, N) * 2.0 ** -24).astype(np.float32)
     if big == "phi":
@@ -481,7 +492,7 @@ def test_tables_at_16_gib(big, K):
         other = (rng.random((M, K), dtype=np.float32) ** 8)
         doc = (np.arange(N, dtype=np.int64) * M // N).astype(np.int32)
         th, ph, d_dev, w_dev = torch.from_numpy(other).cuda(), table, doc, ids
-        c = Corpus(other, used, doc, remap, u, name=f"phi-16GiB-K{K}")
+        c = Corpus(other, used, doc, remap, u, name=f"phi-{gib}GiB-K{K}")
     else:
         V = 5000
         other = rng.random((V, K), dtype=np.float32) * (rng.random((V, K)) > 0.37)
@@ -490,7 +501,7 @@ def test_tables_at_16_gib(big, K):
         order = np.argsort(ids, kind="stable")  # contiguous documents
         ids, remap, word, u = ids[order], remap[order], word[order], u[order]
         th, ph, d_dev, w_dev = table, torch.from_numpy(other).cuda(), ids, word
-        c = Corpus(used, other, remap, word, u, name=f"theta-16GiB-K{K}")
+        c = Corpus(used, other, remap, word, u, name=f"theta-{gib}GiB-K{K}")
     dd, wd = torch.from_numpy(d_dev).cuda(), torch.from_numpy(w_dev).cuda()
     ud = torch.from_numpy(u).cuda()
     z = lda.draw_butterfly(th, ph, dd, wd, ud)
