@@ -1,9 +1,8 @@
 // The draw kernels built for tables past 4 GiB (gfx950).  The same kernels as
-// lda_draw.hip, with theta and phi addressed by 32-bit float offsets and
-// 64-bit loads (config.hpp), so that each table may hold up to 2^32 - 1
-// floats (16 GiB).  lda_draw_butterfly, lda_draw_docs and
-// lda_draw_butterfly_philox come here when theta or phi is larger than
-// LDA_MAX_TABLE_BYTES.
+// lda_draw.hip, with theta and phi rows addressed by index and 64-bit loads
+// (config.hpp), so that a table may be of any size (fewer than 2^31 rows).
+// lda_draw_butterfly, lda_draw_docs and lda_draw_butterfly_philox come here
+// when theta or phi is larger than LDA_MAX_TABLE_BYTES.
 #define LDA_WIDE_TABLES 1
 
 #include "draw_dispatch.hpp"

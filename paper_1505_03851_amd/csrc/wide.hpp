@@ -1,6 +1,6 @@
 // Entry into the build of the draw kernels for tables past 4 GiB
-// (lda_draw_wide.hip): theta and phi addressed with 32-bit float offsets and
-// 64-bit loads, up to (2^32 - 1) floats per table.
+// (lda_draw_wide.hip): theta and phi rows addressed by index with 64-bit
+// loads, tables of any size (fewer than 2^31 rows).
 #pragma once
 
 #include <hip/hip_runtime.h>
