@@ -95,9 +95,11 @@ extern "C" {
  * rows are clamped to its last row there, so no read leaves the table); the
  * draws are the same.
  *
- * Largest size in bytes of each count table of lda_count_topics,
- * lda_count_topics_docs and lda_count_topics_indexed: 2^32 - 1 cells
- * (16 GiB; cells are addressed by unsigned 32-bit indices). */
+ * Largest size in bytes of both count tables of lda_count_topics, and of
+ * nwk in lda_count_topics_docs and lda_count_topics_indexed: 2^32 - 1 cells
+ * (16 GiB; those cells are keyed by unsigned 32-bit indices).  The latter two
+ * take ndk of any size (M below 2^31): its rows are written whole at 64-bit
+ * addresses. */
 #define LDA_MAX_COUNT_TABLE_BYTES 17179869180LL
 
 /*
@@ -376,8 +378,9 @@ int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_
  * one wavefront and written whole: ndk needs no clearing and no atomics in
  * memory (K <= LDA_MAX_K bins of LDS per wavefront).  Offsets outside [0, N]
  * are clamped, never dereferenced; their contents are not otherwise checked.
- * Other arguments and errors as lda_count_topics; doc_offsets may not be
- * NULL (also when N = 0).
+ * Other arguments and errors as lda_count_topics, except that ndk may be of
+ * any size (only nwk above LDA_MAX_COUNT_TABLE_BYTES gives
+ * LDA_ERR_UNSUPPORTED); doc_offsets may not be NULL (also when N = 0).
  */
 int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *word_id, const int32_t *z,
                           int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk,

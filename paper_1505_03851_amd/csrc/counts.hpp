@@ -185,10 +185,15 @@ __global__ __launch_bounds__(kCountThreads) void count_words_kernel(
 // The document table from documents given as offsets (document m = tokens
 // doc_offsets[m] .. doc_offsets[m+1] - 1, contiguous): one wavefront per
 // document counts its tokens' topics in an LDS row of K bins and writes the
-// whole row, so that the table needs neither clearing nor atomics in memory.
-// A token is counted when its word and topic are in range (as in
-// count_kernel).  Offsets outside [0, N] are clamped, never dereferenced.
-constexpr int kDocWaves = 4;  // documents (wavefronts) per workgroup
+// whole row, at a 64-bit address (ndk may hold any number of cells), so that
+// the table needs neither clearing nor atomics in memory.  A token is counted
+// when its word and topic are in range (as in count_kernel).  Offsets outside
+// [0, N] are clamped, never dereferenced.  Workgroup b takes documents
+// b kDocWaves .. b kDocWaves + kDocWaves - 1, then the same again every
+// gridDim.x kDocWaves documents: the grid is capped at kDocGridMax
+// workgroups, since one dispatch holds fewer than 2^32 work-items.
+constexpr int kDocWaves = 4;             // documents (wavefronts) per workgroup
+constexpr int64_t kDocGridMax = 1 << 20;  // workgroups per launch (2^28 work-items)
 __global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
     const int64_t *__restrict__ doc_offsets, const int32_t *__restrict__ word_id,
     const int32_t *__restrict__ z, int64_t N, int32_t M, int32_t V, int32_t K,
@@ -196,37 +201,42 @@ __global__ __launch_bounds__(kDocWaves * 64) void count_docs_kernel(
   extern __shared__ __align__(16) uint32_t rows[];  // kDocWaves rows of K bins
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
-  const int64_t m = (int64_t)blockIdx.x * kDocWaves + wave;
   uint32_t *bins = rows + (size_t)wave * (size_t)K;
   // (K divisible by 4: the row's bins are 16-byte aligned in LDS)
   const bool quads = (K & 3) == 0;
-  if (quads)
-    for (int k = 4 * lane; k < K; k += 4 * 64)
-      *reinterpret_cast<uint4 *>(bins + k) = uint4{0u, 0u, 0u, 0u};
-  else
-    for (int k = lane; k < K; k += 64) bins[k] = 0;
-  __syncthreads();
-  if (m < M) {
-    int64_t lo = doc_offsets[m], hi = doc_offsets[m + 1];
-    lo = lo < 0 ? 0 : (lo > N ? N : lo);
-    hi = hi < lo ? lo : (hi > N ? N : hi);
-    for (int64_t n = lo + lane; n < hi; n += 64) {
-      const int32_t w = word_id[n], k = z[n];
-      if ((uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K) atomicAdd(&bins[k], 1u);
-    }
-  }
-  __syncthreads();
-  if (m < M) {
-    int32_t *row = ndk + m * (int64_t)K;
-    if (quads && (reinterpret_cast<uintptr_t>(row) & 15u) == 0) {
-      for (int k = 4 * lane; k < K; k += 4 * 64) {
-        const uint4 v = *reinterpret_cast<const uint4 *>(bins + k);
-        *reinterpret_cast<int4 *>(row + k) =
-            int4{(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
+  // (m0 is the same for the whole workgroup: every barrier is reached by all)
+  for (int64_t m0 = (int64_t)blockIdx.x * kDocWaves; m0 < M;
+       m0 += (int64_t)gridDim.x * kDocWaves) {
+    const int64_t m = m0 + wave;
+    if (quads)
+      for (int k = 4 * lane; k < K; k += 4 * 64)
+        *reinterpret_cast<uint4 *>(bins + k) = uint4{0u, 0u, 0u, 0u};
+    else
+      for (int k = lane; k < K; k += 64) bins[k] = 0;
+    __syncthreads();
+    if (m < M) {
+      int64_t lo = doc_offsets[m], hi = doc_offsets[m + 1];
+      lo = lo < 0 ? 0 : (lo > N ? N : lo);
+      hi = hi < lo ? lo : (hi > N ? N : hi);
+      for (int64_t n = lo + lane; n < hi; n += 64) {
+        const int32_t w = word_id[n], k = z[n];
+        if ((uint32_t)w < (uint32_t)V && (uint32_t)k < (uint32_t)K) atomicAdd(&bins[k], 1u);
       }
-    } else {
-      for (int k = lane; k < K; k += 64) row[k] = (int32_t)bins[k];
     }
+    __syncthreads();
+    if (m < M) {
+      int32_t *row = ndk + m * (int64_t)K;
+      if (quads && (reinterpret_cast<uintptr_t>(row) & 15u) == 0) {
+        for (int k = 4 * lane; k < K; k += 4 * 64) {
+          const uint4 v = *reinterpret_cast<const uint4 *>(bins + k);
+          *reinterpret_cast<int4 *>(row + k) =
+              int4{(int32_t)v.x, (int32_t)v.y, (int32_t)v.z, (int32_t)v.w};
+        }
+      } else {
+        for (int k = lane; k < K; k += 64) row[k] = (int32_t)bins[k];
+      }
+    }
+    __syncthreads();  // (the row is read out before the next documents clear it)
   }
 }
 

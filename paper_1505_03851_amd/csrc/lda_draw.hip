@@ -622,6 +622,19 @@ extern "C" int lda_draw_routed_scratch(const float *theta, const float *phi,
   return draw_routed(theta, phi, ws, bytes, &route, u, us, z, N, M, V, K, stream);
 }
 
+namespace lda {
+namespace {
+
+// Workgroups of count_docs_kernel for M documents: one per kDocWaves
+// documents, at most kDocGridMax (the kernel strides over the rest).
+unsigned doc_grid(int32_t M) {
+  const int64_t b = ((int64_t)M + kDocWaves - 1) / kDocWaves;
+  return (unsigned)(b < kDocGridMax ? b : kDocGridMax);
+}
+
+}  // namespace
+}  // namespace lda
+
 extern "C" int lda_count_topics(const int32_t *doc_id, const int32_t *word_id, const int32_t *z,
                                 int64_t N, int32_t M, int32_t V, int32_t K, int32_t *ndk,
                                 int32_t *nwk, void *stream) {
@@ -657,10 +670,9 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
                                      int32_t K, int32_t *ndk, int32_t *nwk, void *stream) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K || N > LDA_COUNT_MAX_N) return LDA_ERR_UNSUPPORTED;
-  // cells are addressed by unsigned 32-bit indices (d K + k, w K + k)
-  if ((int64_t)M * K * 4 > LDA_MAX_COUNT_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES)
-    return LDA_ERR_UNSUPPORTED;
+  // nwk's cells are keyed by unsigned 32-bit indices (w K + k); ndk's rows
+  // are written whole at 64-bit addresses, of any size
+  if ((int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES) return LDA_ERR_UNSUPPORTED;
   if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
   if (N > 0 && (!word_id || !z)) return LDA_ERR_NULL;
   const void *ptrs[] = {ndk, nwk, word_id, z};
@@ -673,8 +685,8 @@ extern "C" int lda_count_topics_docs(const int64_t *doc_offsets, const int32_t *
   count_clear<<<(unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), 256, 0, s>>>(
       nwk, cells);
   const size_t lds = (size_t)kDocWaves * (size_t)K * sizeof(uint32_t);
-  count_docs_kernel<<<(unsigned)((M + kDocWaves - 1) / kDocWaves), kDocWaves * 64, lds, s>>>(
-      doc_offsets, word_id, z, N, M, V, K, ndk);
+  count_docs_kernel<<<doc_grid(M), kDocWaves * 64, lds, s>>>(doc_offsets, word_id, z, N, M, V,
+                                                              K, ndk);
   if (N > 0) {
     const int64_t chunks = (N + kCountChunk - 1) / kCountChunk;
     count_words_kernel<<<(unsigned)chunks, kCountThreads, 0, s>>>(word_id, z, N, V, K, nwk);
@@ -772,9 +784,8 @@ extern "C" int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_
                                         int32_t *ndk, int32_t *nwk, void *stream) {
   if (N < 0 || M <= 0 || V <= 0 || K <= 0) return LDA_ERR_SHAPE;
   if (K > LDA_MAX_K) return LDA_ERR_UNSUPPORTED;
-  if ((int64_t)M * K * 4 > LDA_MAX_COUNT_TABLE_BYTES ||
-      (int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES)
-    return LDA_ERR_UNSUPPORTED;
+  // (as lda_count_topics_docs: only nwk is limited)
+  if ((int64_t)V * K * 4 > LDA_MAX_COUNT_TABLE_BYTES) return LDA_ERR_UNSUPPORTED;
   const int st = check_word_index(N, V, index, index_bytes);
   if (st != LDA_OK) return st;
   if (!ndk || !nwk || !doc_offsets) return LDA_ERR_NULL;
@@ -791,8 +802,8 @@ extern "C" int lda_count_topics_indexed(const int64_t *doc_offsets, const int32_
   count_clear<<<(unsigned)(blocks < 4096 ? (blocks > 0 ? blocks : 1) : 4096), 256, 0, s>>>(
       nwk, cells);
   const size_t lds = (size_t)kDocWaves * (size_t)K * sizeof(uint32_t);
-  count_docs_kernel<<<(unsigned)((M + kDocWaves - 1) / kDocWaves), kDocWaves * 64, lds, s>>>(
-      doc_offsets, word_id, z, N, M, V, K, ndk);
+  count_docs_kernel<<<doc_grid(M), kDocWaves * 64, lds, s>>>(doc_offsets, word_id, z, N, M, V,
+                                                              K, ndk);
   if (N > 0) {
     const int run = index_run(N);
     const int64_t per = (int64_t)run * kCountChunk;

@@ -398,7 +398,8 @@ def test_count_topics_docs_argument_errors(lib):
         return lib.lda_count_topics_docs(off, w, z, N, M, V, K, ndk, nwk, None)
     for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
         assert run(**kw) == STATUS["LDA_ERR_SHAPE"], kw
-    assert run(M=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 16 GiB
+    # (ndk may be of any size: a call with a large M passes every check and
+    # would launch, so none is made here)
     assert run(V=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 16 GiB
     for key in ("off", "ndk", "nwk"):
         assert run(**{key: None}) == STATUS["LDA_ERR_NULL"], key
@@ -443,7 +444,7 @@ def test_word_index_argument_errors(lib):
     for kw in (dict(N=-1), dict(M=0), dict(V=-2), dict(K=0)):
         assert count(**kw) == STATUS["LDA_ERR_SHAPE"], kw
     assert count(K=_CONSTS["LDA_MAX_K"] + 1) == STATUS["LDA_ERR_UNSUPPORTED"]
-    assert count(M=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # ndk of 16 GiB
+    assert count(V=1 << 22, K=1024) == STATUS["LDA_ERR_UNSUPPORTED"]   # nwk of 16 GiB
     assert count(nbytes=ws - 1) == STATUS["LDA_ERR_WORKSPACE"]
     assert count(N=1000) == STATUS["LDA_ERR_WORKSPACE"]                # an index of 100 tokens
     for key in ("off", "ndk", "nwk", "index", "w", "z"):

@@ -1,8 +1,9 @@
 """Sizes past 2**31: token counts (every kernel indexes tokens with 64-bit
-integers) and tables (byte offsets into theta, phi and the count tables are
-unsigned 32-bit, so tables up to 4 GiB are addressed; past 4 GiB
-lda_draw_butterfly, lda_draw_docs and lda_draw_butterfly_philox draw with the
-wide build, float offsets and 64-bit loads, up to 16 GiB).
+integers) and tables (byte offsets into theta and phi are unsigned 32-bit,
+so tables up to 4 GiB are addressed; past 4 GiB the draws take the wide
+build, which addresses rows by index and forms 64-bit addresses, for tables
+of any size; count-table cells are keyed by 32-bit indices, except the rows
+of ndk in the offsets and indexed forms, written at 64-bit addresses).
 
 The large-N inputs are made on the GPU (about 35 GB of token arrays); a
 sample of the tokens -- random ones, the first and last, and those around
@@ -361,6 +362,58 @@ def test_counts_at_the_largest_n():
             assert int(a["wsorted"][s - 1]) <= int(ws[0])
     assert bool(seen.all())
     del w, z, index, seen
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("M,K", [((1 << 22) + 4096, 1024), ((1 << 27) + 5, 16)],
+                         ids=["ndk-16GiB", "M2^27"])
+def test_doc_counts_of_any_size(M, K):
+    """ndk past 16 GiB (more cells than a 32-bit key holds) and M past 2^26
+    documents (more work-items than one dispatch holds, at one wavefront a
+    document): the offsets and indexed forms write every row of ndk (filled
+    with -1 before) -- the rows with tokens equal the oracle's counts of those
+    documents, every cell is non-negative and the cells sum to the tokens
+    counted, so the other rows are zero -- and nwk equals the oracle's."""
+    import torch
+    import oracle
+    import paper_1505_03851_amd as lda
+    from paper_1505_03851_amd.inputs import doc_offsets
+    V, N = 3000, 400_000
+    rng = np.random.default_rng(8)
+    # half the tokens in random documents, half in the last 5,000 (past 2^32
+    # cells at K = 1024; the last workgroups' documents at M = 2^27 + 5)
+    doc = np.sort(np.concatenate([rng.integers(0, M, N // 2),
+                                  rng.integers(M - 5000, M, N - N // 2)])).astype(np.int32)
+    word = rng.integers(0, V, N).astype(np.int32)
+    zh = rng.integers(0, K, N).astype(np.int32)
+    rows = np.unique(doc)
+    want_d, want_w = oracle.counts(np.searchsorted(rows, doc).astype(np.int32), word, zh,
+                                   rows.size, V, K)
+    print(f"[case] doc counts M={M} K={K} ndk {4 * M * K / 2 ** 30:.2f} GiB", flush=True)
+    torch.cuda.empty_cache()
+    off = torch.from_numpy(doc_offsets(doc, M)).cuda()
+    w = torch.from_numpy(word).cuda()
+    z = torch.from_numpy(zh).cuda()
+    at = torch.from_numpy(rows.astype(np.int64)).cuda()
+    ndk = torch.full((M, K), -1, dtype=torch.int32, device="cuda")
+    nwk = torch.full((V, K), -1, dtype=torch.int32, device="cuda")
+
+    def check(form):
+        torch.cuda.synchronize()
+        got = ndk[at].cpu().numpy()
+        assert np.array_equal(got, want_d), (form, np.argwhere(got != want_d)[:5])
+        assert int(ndk.min()) >= 0, form
+        assert int(ndk.sum()) == N, form
+        assert np.array_equal(nwk.cpu().numpy(), want_w), form
+
+    lda.count_topics_docs(off, w, z, V, K, ndk=ndk, nwk=nwk)
+    check("offsets")
+    ndk.fill_(-1)
+    nwk.fill_(-1)
+    index = lda.word_index_build(w, V)
+    lda.count_topics_indexed(off, w, z, index, K, ndk=ndk, nwk=nwk)
+    check("indexed")
+    del ndk, nwk, off, w, z, at, index
     torch.cuda.empty_cache()
 
 
