@@ -565,8 +565,8 @@ def ablation(args) -> int:
 
 def wide_builds(args) -> int:
     """The default build of the draw kernels against the build for tables past
-    4 GiB (float offsets, 64-bit loads; lda_draw_butterfly_variant with
-    LDA_VARIANT_WIDE_TABLES) on the same workloads: three alternating rounds
+    4 GiB (rows addressed by index, 64-bit addresses;
+    lda_draw_butterfly_variant with LDA_VARIANT_WIDE_TABLES) on the same workloads: three alternating rounds
     of each after an untimed pass, the median launch of each round, the
     fastest round kept; z of the two compared.  One JSON line per workload."""
     import torch
