@@ -525,6 +525,39 @@ def route_sweep(args) -> int:
     return 0
 
 
+FLOOR_SWEEP_K = (256, 260, 384, 512, 640, 768, 1024, 1280, 1536, 2048)
+
+
+def floor_sweep(args) -> int:
+    """Each draw against its own floor across K on the 16.8M-token corpus:
+    the token-order draw and the fastest launch shape of the floor probe, and
+    (K >= 768) the routed draw, routing built once, and the routed order's
+    floor; one JSON line per K, with each draw's fraction of its floor."""
+    import torch
+    from paper_1505_03851_amd.inputs import corpus16M_at, make_corpus
+    for K in FLOOR_SWEEP_K:
+        c = make_corpus(corpus16M_at(K))
+        dev = upload(c)
+        rec = {"workload": c.name, "N": c.N, "V": c.V, "K": K}
+        measure(c.name, c, dev, "butterfly", args.steps, args.warmup)  # (untimed pass)
+        r = measure(c.name, c, dev, "butterfly", args.steps, args.warmup)
+        r.pop("z")
+        f = measure_floor(c.name, c, dev, args.steps, args.warmup)
+        rec.update({"butterfly_ms": r["ms_per_launch"], "floor_ms": f["ms_per_launch"],
+                    "floor_shape": f["shape"], "frac": f["ms_per_launch"] / r["ms_per_launch"]})
+        if routable(K):
+            r = measure(c.name, c, dev, "routed", args.steps, args.warmup)
+            r.pop("z")
+            f = measure_routed_floor(c.name, c, dev, args.steps, args.warmup)
+            rec.update({"routed_ms": r["ms_per_launch"], "routed_floor_ms": f["ms_per_launch"],
+                        "routed_floor_shape": f["shape"],
+                        "routed_frac": f["ms_per_launch"] / r["ms_per_launch"]})
+        print(json.dumps(rec), flush=True)
+        del dev, c
+        torch.cuda.empty_cache()
+    return 0
+
+
 def ablation(args) -> int:
     """The table variants of Section 4 (the paper's rule with the table in
     registers or LDS, the alternative rule in LDS), 8-topic leaves, the build
@@ -1150,6 +1183,9 @@ def main() -> int:
     ap.add_argument("--route-sweep", action="store_true",
                     help="plain against routed draw on the 16.8M-token corpus at "
                          "K = 256 ... 2048; one JSON line per K")
+    ap.add_argument("--floor-sweep", action="store_true",
+                    help="each draw against its own floor on the 16.8M-token "
+                         "corpus at K = 256 ... 2048; one JSON line per K")
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
@@ -1241,6 +1277,8 @@ def main() -> int:
         return permuted_ids(args)
     if args.route_sweep:
         return route_sweep(args)
+    if args.floor_sweep:
+        return floor_sweep(args)
     if args.all_configs:
         return all_configs(args)
     if args.graph:

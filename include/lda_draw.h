@@ -126,8 +126,9 @@ int lda_draw_naive(const float *theta, const float *phi, const int32_t *doc_id,
  *    row into its group; the butterfly runs over the W leaf sums, Algorithm
  *    10 finds the token's leaf and a scan of its 4 products the topic
  *    (groups of 8 lanes keep each leaf's partial sums in LDS for that scan;
- *    the others read the leaf again);
- *  - K divisible by 4 from 260 to 2048: 256-topic blocks read as leaves of 4
+ *    the others read the leaf again); from 260 to 508 (multiples of 32 only
+ *    up to 416) the same with 64 lanes and leaves of 8 topics;
+ *  - K divisible by 4 from 260 to 2048 otherwise: 256-topic blocks read as leaves of 4
  *    topics per lane; a first sweep keeps every token's prefix at the end of
  *    each 32-topic part of each block, Algorithm 9 finds the part holding
  *    u*S, whose butterfly table is rebuilt on chip and searched;

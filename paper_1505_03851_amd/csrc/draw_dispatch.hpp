@@ -97,14 +97,13 @@ bool groups_for(int64_t N, int32_t K) {
   return N >= kWave && K % kLeaf == 0 && K <= LDA_GROUP_MAX_K && K <= kLeaf * kWave;
 }
 
-template <int G, int H>
+// (8-topic leaves hold twice the registers: the 64-lane groups' setting)
+template <int G, int H, int CW = (G == kWave ? LDA_GROUP64_WINDOW : LDA_GROUP_WINDOW),
+          int WPEU = ((G == kWave || H > 1) ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU)>
 void launch_groups(const float *theta, const float *phi, DocSource d, const int32_t *wd,
                    UniformSource u, int32_t *z, int64_t N, int32_t M, int32_t V, int32_t K,
                    hipStream_t s) {
-  constexpr int CW = G == kWave ? LDA_GROUP64_WINDOW : LDA_GROUP_WINDOW;
   constexpr int C = CW < G ? CW : G;
-  // (8-topic leaves hold twice the registers: the 64-lane groups' setting)
-  constexpr int WPEU = G == kWave || H > 1 ? LDA_GROUP64_WAVES_PER_EU : LDA_GROUP_WAVES_PER_EU;
   const uint32_t tb = table_extent(M, K);
   const uint32_t pb = table_extent(V, K);
   const size_t lds = (size_t)kWavesPerBlock * group_lds_bytes<G, H>();
@@ -114,6 +113,17 @@ void launch_groups(const float *theta, const float *phi, DocSource d, const int3
   else
     leaf_group_kernel<G, H, C, WPEU, true><<<wave_grid(N), kBlockThreads, lds, s>>>(
         theta, phi, d, wd, u, z, N, K, tb, pb);
+}
+
+// Groups of 64 lanes with 8-topic leaves for K from 260 to LDA_LEAF8_MAX_K
+// (at most 512), multiples of 32 only up to LDA_LEAF8_ALIGNED_MAX_K: the
+// whole row in one tile, as the leaf groups do up to 256.  Measured on MI355X
+// against the eighths kernel, which pads such K to two 256-topic blocks:
+// 17-21% faster at K = 260 ... 320, 7% at 384, 1-4% up to 508; 2-3% slower at
+// K = 448, 480 and 512.
+bool leaf8_for(int64_t N, int32_t K) {
+  return N >= kWave && K % kLeaf == 0 && K > kLeaf * kWave && K <= LDA_LEAF8_MAX_K &&
+         K <= 2 * kLeaf * kWave && (K % 32 != 0 || K <= LDA_LEAF8_ALIGNED_MAX_K);
 }
 
 // The eighths kernel takes K divisible by 4 (16-byte leaves) from
@@ -170,6 +180,13 @@ void dispatch_butterfly(const float *theta, const float *phi, DocSource d,
   if (groups_for(N, K)) {
     dispatch_groups<H>(theta, phi, d, word_id, u, z, N, M, V, K, s);
     return;
+  }
+  if constexpr (LDA_LEAF8_MAX_K > 0) {
+    if (leaf8_for(N, K)) {
+      launch_groups<kWave, 2, LDA_LEAF8_WINDOW, LDA_LEAF8_WAVES_PER_EU>(theta, phi, d, word_id,
+                                                                         u, z, N, M, V, K, s);
+      return;
+    }
   }
   if (eighths_for(N, K)) {
     // launch shapes measured on MI355X: up to five blocks, 16 tokens in

@@ -1,4 +1,5 @@
-// Leaf-group kernel for K up to 256 (gfx950).
+// Leaf-group kernel for K up to 256, and with 8-topic leaves up to 508
+// (gfx950).
 #pragma once
 
 #include "tile.hpp"
@@ -7,7 +8,8 @@ namespace LDA_NS {
 namespace {
 
 // Leaf groups for K up to 256 (K divisible by 4, at most 4 G topics for a
-// group size G of 8, 16, 32 or 64 lanes; N >= 64).  Sections 3 and 4 with a
+// group size G of 8, 16, 32 or 64 lanes; N >= 64), and with leaves of 4 H
+// topics (H quads) up to 4 H G; below, H = 1.  Sections 3 and 4 with a
 // 4-topic leaf in the place of a topic: a wavefront holds 64 / G groups of G
 // tokens, lane r of a group owns token r of the group and, in the tile, leaf
 // r (topics c0 + 4r .. c0 + 4r + 3, c0 = K - 4G <= 0: the first 4G - K

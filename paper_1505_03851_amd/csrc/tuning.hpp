@@ -81,6 +81,34 @@
 #ifndef LDA_GROUP64_WAVES_PER_EU
 #define LDA_GROUP64_WAVES_PER_EU 3
 #endif
+//   LDA_LEAF8_MAX_K, LDA_LEAF8_ALIGNED_MAX_K
+//                             K above 256 drawn by groups of 64 lanes with
+//                             8-topic leaves, the whole row in one tile (K
+//                             divisible by 4): up to LDA_LEAF8_MAX_K (at most
+//                             512; 0: none), except multiples of 32 above
+//                             LDA_LEAF8_ALIGNED_MAX_K; the eighths kernel
+//                             draws the rest.  Measured on the 16.8M-token
+//                             corpus against the eighths kernel: 17-21%
+//                             faster at K = 260 ... 320, 7% at 384, 1-4% at
+//                             392 ... 508 (416 included); 2-3% slower at 448,
+//                             480 and 512 (rows of whole 128-byte lines).
+//   LDA_LEAF8_WINDOW, LDA_LEAF8_WAVES_PER_EU  their tokens in flight per
+//                             wavefront and wavefronts per SIMD: 4 at 3
+//                             (154-160 VGPRs) was 3-6% faster than 8 at 2 at
+//                             K = 260 ... 384 and within 0.5% above; 2 at 4
+//                             spills.
+#ifndef LDA_LEAF8_MAX_K
+#define LDA_LEAF8_MAX_K 508
+#endif
+#ifndef LDA_LEAF8_ALIGNED_MAX_K
+#define LDA_LEAF8_ALIGNED_MAX_K 416
+#endif
+#ifndef LDA_LEAF8_WINDOW
+#define LDA_LEAF8_WINDOW 4
+#endif
+#ifndef LDA_LEAF8_WAVES_PER_EU
+#define LDA_LEAF8_WAVES_PER_EU 3
+#endif
 //   LDA_EIGHTHS_MIN_K         smallest K it takes (K divisible by 4; the first
 //                             block is padded with empty topics up to a
 //                             multiple of 256).

@@ -46,6 +46,15 @@ def test_config_every_token(name, kernel):
     _check(c, kernel, rate=c.N >= 1 << 20, ref=reference(name))
 
 
+@pytest.mark.parametrize("K", [260, 384, 508])
+def test_corpus16M_eight_topic_leaves_every_token(K):
+    """The 16.8M-token corpus (V = 100,000, Zipf 1.05) at K from 260 to 508,
+    where the draw takes 64-lane groups of 8-topic leaves: every token against
+    the oracle, under the band rule and the mismatch-rate bound."""
+    from paper_1505_03851_amd.inputs import corpus16M_at, make_corpus
+    _check(make_corpus(corpus16M_at(K)), "butterfly")
+
+
 @pytest.mark.parametrize("kernel", KERNELS)
 @pytest.mark.parametrize("K", WIKI_K)
 def test_wiki_shaped_every_token(K, kernel):
@@ -128,6 +137,19 @@ SHAPES = [
     (64 * 20 + 7, 64, 300, 128, "sequential"),
     (64 * 30 + 5, 60, 300, 200, "sequential"),
     (64 * 30 + 5, 110, 300, 256, "sequential"),
+    # K divisible by 4 from 260 to 508 (multiples of 32 up to 416): groups of
+    # 64 lanes with 8-topic leaves, empty topics in front below 512 (a whole
+    # empty quad when K mod 8 = 4), every group in one document, in up to
+    # three runs, or more; 448 and N < 64 go to the other kernels
+    (64 * 9 + 5, 40, 300, 264, "sequential"),
+    (64 * 12 + 3, 3, 300, 300, "single"),
+    (64 * 10 + 1, 30, 200, 384, "shuffled"),
+    (64 * 8 + 9, 12, 300, 416, "sequential"),
+    (64 * 30 + 5, 100, 300, 352, "sequential"),
+    (64 * 6 + 7, 4, 200, 508, "ragged"),
+    (64 * 5, 2, 100, 500, "single"),
+    (64 * 7 + 30, 9, 300, 448, "sequential"),
+    (40, 3, 50, 300, "shuffled"),
     # K a multiple of 256 (the leaf kernel with 32-topic prefix rows up to 2048)
     (1, 1, 7, 256, "sequential"),
     (63, 5, 50, 512, "shuffled"),
@@ -178,7 +200,8 @@ def test_equal_power_of_two_weights_exact(K, kernel):
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("K", [20, 50, 100, 130, 144, 208, 240, 1000, 2044, 2047])
+@pytest.mark.parametrize("K", [20, 50, 100, 130, 144, 208, 240, 260, 300, 508, 1000, 2044,
+                               2047])
 def test_tiny_uniforms_with_empty_leading_topics(K, kernel):
     """Every u is 0 or a few multiples of 2**-24, at K whose kernels pad the
     front of the first block (or leaf group) with empty topics: the search
@@ -195,7 +218,7 @@ def test_tiny_uniforms_with_empty_leading_topics(K, kernel):
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("K", [4, 8, 20, 32, 48, 64, 100, 256, 1000, 1024, 2048])
+@pytest.mark.parametrize("K", [4, 8, 20, 32, 48, 64, 100, 256, 300, 1000, 1024, 2048])
 def test_uniforms_just_below_one_with_empty_trailing_topics(K, kernel):
     """Every u is 1 - j 2**-24 (j = 1 ... 8), and half the words give their
     last three topics zero weight.  stop = u S then lies within a few ulps of
@@ -318,6 +341,8 @@ RAGGED = [
     (64 * 33 + 63, 60, 500, 129),
     (64 * 33 + 63, 60, 500, 200),
     (64 * 9 + 33, 40, 100, 256),      # leaf kernel, one block
+    (64 * 11 + 7, 50, 300, 300),      # 64-lane groups of 8-topic leaves
+    (64 * 8 + 40, 9, 200, 436),
     (64 * 7 + 5, 300, 90, 1280),
     (64 * 17 + 9, 60, 500, 2047),
     (64 * 5 + 3, 20, 200, 4096),

@@ -72,7 +72,7 @@ def test_philox_draw_full_size_every_token(name):
 
 
 @pytest.mark.parametrize("N,K", [(1, 5), (63, 64), (64 * 9 + 17, 19), (64 * 21 + 5, 256),
-                                 (64 * 17 + 9, 1000)])
+                                 (64 * 13 + 3, 300), (64 * 17 + 9, 1000)])
 def test_philox_draw_equals_draw_with_written_uniforms(N, K):
     """Same kernel, same uniforms: identical z to the draw given the
     uniforms lda_philox_uniforms writes."""
