@@ -1014,14 +1014,16 @@ _PARITY_LINE = re.compile(r"^\[parity\] (?P<case>.+?): n=(?P<n>\d+) mismatches=(
 def report_parity(log: str, out_txt: str, command: str) -> int:
     """A table of the parity lines the GPU tests print ("[parity] <workload>
     <kernel>: n=... mismatches=... hard=... in_band=..."), for the named
-    workloads (the five and the corpus shaped like the paper's), every
-    kernel, in the order the tests ran."""
+    workloads (the five, the corpus shaped like the paper's, and the
+    16.8M-token corpus at other K), every kernel, in the order the tests
+    ran."""
     from paper_1505_03851_amd.inputs import CONFIGS
     rows = []
     with open(log, errors="replace") as f:
         for ln in f:
             m = _PARITY_LINE.match(ln.strip())
-            if m and m["case"].split()[0] in CONFIGS:
+            name = m["case"].split()[0] if m else ""
+            if m and (name in CONFIGS or name.startswith("corpus16M-sweep-K")):
                 rows.append(m)
     if not rows:
         raise SystemExit(f"no parity lines for the named workloads in {log}")
