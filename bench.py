@@ -529,14 +529,15 @@ FLOOR_SWEEP_K = (256, 260, 384, 512, 640, 768, 1024, 1280, 1536, 2048)
 
 
 def floor_sweep(args) -> int:
-    """Each draw against its own floor across K on the 16.8M-token corpus:
-    the token-order draw and the fastest launch shape of the floor probe, and
+    """Each draw against its own floor across K on the 16.8M-token corpus (or,
+    with --wiki, on the corpus shaped like the paper's at its eight K): the
+    token-order draw and the fastest launch shape of the floor probe, and
     (K >= 768) the routed draw, routing built once, and the routed order's
     floor; one JSON line per K, with each draw's fraction of its floor."""
     import torch
-    from paper_1505_03851_amd.inputs import corpus16M_at, make_corpus
-    for K in FLOOR_SWEEP_K:
-        c = make_corpus(corpus16M_at(K))
+    from paper_1505_03851_amd.inputs import WIKI_K, corpus16M_at, make_corpus, wiki_shaped
+    for K in (WIKI_K if args.wiki else FLOOR_SWEEP_K):
+        c = make_corpus(wiki_shaped(K) if args.wiki else corpus16M_at(K))
         dev = upload(c)
         rec = {"workload": c.name, "N": c.N, "V": c.V, "K": K}
         measure(c.name, c, dev, "butterfly", args.steps, args.warmup)  # (untimed pass)
@@ -1188,6 +1189,9 @@ def main() -> int:
     ap.add_argument("--floor-sweep", action="store_true",
                     help="each draw against its own floor on the 16.8M-token "
                          "corpus at K = 256 ... 2048; one JSON line per K")
+    ap.add_argument("--wiki", action="store_true",
+                    help="with --floor-sweep: the corpus shaped like the paper's at "
+                         "its eight K instead")
     ap.add_argument("--ablation", action="store_true",
                     help="time the block-table variants and the offsets form "
                          "of the documents; one JSON line per workload")
