@@ -201,7 +201,8 @@ def _wide_case(K, seed, big):
 
 
 @pytest.mark.parametrize("big,K", [("phi", 1024), ("phi", 256), ("phi", 96), ("phi", 130),
-                                   ("theta", 1024), ("theta", 20)])
+                                   ("phi", 300), ("theta", 1024), ("theta", 20),
+                                   ("theta", 436)])
 def test_tables_past_4_gib(big, K):
     import torch
     import paper_1505_03851_amd as lda
