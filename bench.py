@@ -536,7 +536,9 @@ def floor_sweep(args) -> int:
     floor; one JSON line per K, with each draw's fraction of its floor."""
     import torch
     from paper_1505_03851_amd.inputs import WIKI_K, corpus16M_at, make_corpus, wiki_shaped
-    for K in (WIKI_K if args.wiki else FLOOR_SWEEP_K):
+    ks = [int(k) for k in args.floor_k.split(",")] if args.floor_k else \
+        (WIKI_K if args.wiki else FLOOR_SWEEP_K)
+    for K in ks:
         c = make_corpus(wiki_shaped(K) if args.wiki else corpus16M_at(K))
         dev = upload(c)
         rec = {"workload": c.name, "N": c.N, "V": c.V, "K": K}
@@ -1189,6 +1191,8 @@ def main() -> int:
     ap.add_argument("--floor-sweep", action="store_true",
                     help="each draw against its own floor on the 16.8M-token "
                          "corpus at K = 256 ... 2048; one JSON line per K")
+    ap.add_argument("--floor-k", default=None,
+                    help="with --floor-sweep: the topic counts to sweep (comma-separated)")
     ap.add_argument("--wiki", action="store_true",
                     help="with --floor-sweep: the corpus shaped like the paper's at "
                          "its eight K instead")
