@@ -131,8 +131,8 @@ bool leaf8_for(int64_t N, int32_t K) {
 // N >= 64.  Measured on MI355X against the one-topic kernel: 15-30% faster
 // from K = 144 (K = 144 ... 240 on the paper-shaped corpus), 7% at K = 256,
 // 4% at K = 1024, 5% at K = 2048; 3-4% slower at K = 80 and 112, whose
-// padding fills most of the block.  (The dispatch gives K up to 256 to the
-// leaf-group kernel first.)
+// padding fills most of the block.  (The dispatch gives K up to 256, and
+// most K up to 508, to the leaf-group kernel first.)
 bool eighths_for(int64_t N, int32_t K) {
   return N >= kWave && K % kLeaf == 0 && K >= LDA_EIGHTHS_MIN_K &&
          eighths_blocks(K) <= LDA_EIGHTHS_MAX_BLOCKS;
