@@ -247,7 +247,7 @@ def test_uniforms_just_below_one_with_empty_trailing_topics(K, kernel):
 
 
 @pytest.mark.parametrize("kernel", KERNELS)
-@pytest.mark.parametrize("K", [1, 5, 32, 64, 100, 1000, 1024])
+@pytest.mark.parametrize("K", [1, 5, 32, 64, 100, 300, 508, 1000, 1024])
 def test_degenerate_weights(K, kernel):
     """All-zero documents draw K-1; a one-hot document draws its topic for
     every u (including u = 0 and u = 1 - 2**-24); mixed with normal rows."""
